@@ -1,0 +1,97 @@
+"""Planted mistakes in the oracle must be caught by its pins.
+
+Each case swaps one oracle function for a plausibly wrong variant (on the CPU)
+and checks that at least one pin test then fails.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.prhs_oracle as M
+from tests import test_oracle_pins as P
+
+
+def _wrong_scale_dense(q, K, V, scale=None):
+    return _orig["dense_attention"](q, K, V, 1.0)
+
+
+def _tie_high_index(sigma, n0, k, sink, window):
+    sink_end, win_start = M.region_bounds(n0, sink, window)
+    pos = np.arange(sink_end, win_start)
+    if pos.size == 0 or k <= 0:
+        return np.zeros(0, dtype=np.int64)
+    order = np.lexsort((-pos, -np.asarray(sigma, float)[pos]))
+    return pos[order][:k]
+
+
+def _reuse_without_new_tokens(s_star, m, r, n0, n, sink, window):
+    return _orig["reuse_set"](s_star, m, r, n0, n0, sink, window)
+
+
+def _reuse_no_clip(s_star, m, r, n0, n, sink, window):
+    s_star = np.asarray(s_star, dtype=np.int64)
+    sink_end, win_start = M.region_bounds(n0, sink, window)
+    neigh = (s_star[:m, None] + np.arange(-r, r + 1)[None, :]).ravel()
+    parts = [np.arange(0, sink_end), s_star, neigh, np.arange(win_start, n)]
+    return np.unique(np.concatenate(parts))
+
+
+def _min_over_group(Qg, K):
+    Qg = np.atleast_2d(np.asarray(Qg, float))
+    K = np.asarray(K, float)
+    return (K @ Qg.T).min(axis=1) if K.shape[0] else np.zeros(0)
+
+
+def _window_off_by_one(n0, sink, window):
+    sink_end = min(sink, n0)
+    return sink_end, max(sink_end, n0 - window - 1)
+
+
+def _m_is_k_over_2(k_b, topk_len, dilate_m=-1):
+    m = k_b // 2 if dilate_m < 0 else dilate_m
+    return max(0, min(m, topk_len))
+
+
+def _lse_missing_max(q, K, V, scale=None):
+    y, lse = _orig["dense_attention"](q, K, V, scale)
+    z = M.attention_logits(q, K, scale)
+    return y, (lse - z.max()) if z.size else lse
+
+
+def _schedule_layer_only(step, layer, s, G):
+    return layer % G == 0
+
+
+_orig = {name: getattr(M, name) for name in
+         ["dense_attention", "topk_middle", "reuse_set", "ranking_scores",
+          "region_bounds", "dilation_m", "is_refresh"]}
+
+PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]
+
+MUTANTS = [
+    ("dense_attention", _wrong_scale_dense),
+    ("dense_attention", _lse_missing_max),
+    ("topk_middle", _tie_high_index),
+    ("reuse_set", _reuse_without_new_tokens),
+    ("reuse_set", _reuse_no_clip),
+    ("ranking_scores", _min_over_group),
+    ("region_bounds", _window_off_by_one),
+    ("dilation_m", _m_is_k_over_2),
+    ("is_refresh", _schedule_layer_only),
+]
+
+
+@pytest.mark.parametrize("name,fn", MUTANTS, ids=[f"{n}:{f.__name__}" for n, f in MUTANTS])
+def test_planted_mistake_is_caught(monkeypatch, name, fn):
+    monkeypatch.setattr(M, name, fn)
+    monkeypatch.setattr(O, name, fn)
+    failed = []
+    for pin in PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"no pin caught the mutant {fn.__name__} of {name}"

@@ -1,0 +1,428 @@
+"""Pins of the CPU oracle to facts the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: closed forms,
+brute-force enumeration, an independent library routine, identities proved in
+the paper's appendices, and budgets the paper prints (tests/golden).
+"""
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_budgets.json")
+
+
+def grid(rng, *shape, scale=1.0):
+    """Values on the j/16 grid (|j| <= 255)."""
+    x = rng.standard_normal(shape) * scale
+    return np.clip(np.round(x * 16), -255, 255) / 16
+
+
+# ---------------------------------------------------------------- dense attention
+
+def test_dense_equal_keys_gives_mean_value():
+    # all logits equal => uniform weights => y = mean(V)  (Eq. attn_eq)
+    rng = np.random.default_rng(0)
+    k = rng.standard_normal(16)
+    K = np.tile(k, (9, 1))
+    V = rng.standard_normal((9, 16))
+    q = rng.standard_normal(16)
+    y, lse = O.dense_attention(q, K, V)
+    np.testing.assert_allclose(y, V.mean(0), rtol=0, atol=1e-14)
+    assert lse == pytest.approx(q @ k / 4.0 + math.log(9), abs=1e-12)
+
+
+def test_dense_single_key_returns_its_value():
+    rng = np.random.default_rng(1)
+    q, k, v = rng.standard_normal((3, 8))
+    y, lse = O.dense_attention(q, k[None], v[None])
+    np.testing.assert_array_equal(y, v)
+    assert lse == pytest.approx(q @ k / math.sqrt(8), abs=1e-14)
+
+
+def test_dense_dominant_key():
+    # one logit exceeds every other by 60: its weight is 1 - O(n e^-60)
+    rng = np.random.default_rng(2)
+    d = 4
+    K = np.zeros((7, d))
+    K[3, 0] = 60.0 * math.sqrt(d)
+    q = np.array([1.0, 0, 0, 0])
+    V = rng.standard_normal((7, d))
+    y, _ = O.dense_attention(q, K, V)
+    np.testing.assert_allclose(y, V[3], atol=1e-20 + 7 * math.exp(-60) * np.abs(V).max())
+
+
+def test_dense_matches_torch_sdpa_fp64():
+    rng = np.random.default_rng(3)
+    for n, d in [(1, 8), (5, 64), (300, 128)]:
+        q = rng.standard_normal(d)
+        K = rng.standard_normal((n, d)) * 2
+        V = rng.standard_normal((n, d))
+        y, _ = O.dense_attention(q, K, V)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.tensor(q)[None, None, None], torch.tensor(K)[None, None],
+            torch.tensor(V)[None, None]).numpy()[0, 0, 0]
+        np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_dense_matches_scalar_loop_and_lse():
+    # independent plain-Python evaluation of Eq. attn_eq
+    rng = np.random.default_rng(4)
+    n, d = 11, 6
+    q = rng.standard_normal(d)
+    K = rng.standard_normal((n, d))
+    V = rng.standard_normal((n, d))
+    logits = [sum(q[t] * K[i][t] for t in range(d)) / math.sqrt(d) for i in range(n)]
+    Z = sum(math.exp(z) for z in logits)
+    yref = [sum(math.exp(logits[i]) / Z * V[i][t] for i in range(n)) for t in range(d)]
+    y, lse = O.dense_attention(q, K, V)
+    np.testing.assert_allclose(y, yref, rtol=1e-13, atol=1e-14)
+    assert lse == pytest.approx(math.log(Z), rel=1e-14)
+    A = O.attention_weights(q, K)
+    np.testing.assert_allclose(A, [math.exp(z) / Z for z in logits], rtol=1e-13)
+
+
+def test_empty_set_attention():
+    y, lse = O.sparse_attention(np.ones(4), np.ones((3, 4)), np.ones((3, 4)), [])
+    np.testing.assert_array_equal(y, np.zeros(4))
+    assert lse == -math.inf
+
+
+# ---------------------------------------------------------------- scores and Z1 exactness
+
+def test_ranking_score_is_group_max_of_raw_dot():
+    rng = np.random.default_rng(5)
+    Qg = rng.standard_normal((4, 8))
+    K = rng.standard_normal((10, 8))
+    s = O.ranking_scores(Qg, K)
+    for i in range(10):
+        ref = max(sum(Qg[h][t] * K[i][t] for t in range(8)) for h in range(4))
+        assert s[i] == pytest.approx(ref, abs=1e-12)
+
+
+def test_grid_scores_exact_in_float32_any_order():
+    # The generator's grid makes fp32 dot products exact in every order, so the
+    # GPU's fp32 scores equal the oracle's fp64 scores bit for bit.
+    rng = np.random.default_rng(6)
+    for d in (64, 128):
+        q = grid(rng, d, scale=4.0)
+        K = grid(rng, 200, d, scale=4.0)
+        ref = O.ranking_scores(q, K)
+        seq = np.zeros(200, dtype=np.float32)
+        for t in range(d):
+            seq = (seq + (q[t].astype(np.float32) * K[:, t].astype(np.float32))).astype(np.float32)
+        rev = np.zeros(200, dtype=np.float32)
+        for t in reversed(range(d)):
+            rev = (rev + (q[t].astype(np.float32) * K[:, t].astype(np.float32))).astype(np.float32)
+        pair = (K.astype(np.float32) * q.astype(np.float32)).sum(axis=1, dtype=np.float32)
+        for v in (seq, rev, pair):
+            assert np.array_equal(v.astype(np.float64), ref)
+        # extreme grid values: the worst-case magnitude is still exact
+        qx = np.full(d, 255 / 16)
+        Kx = np.full((1, d), -255 / 16)
+        assert O.ranking_scores(qx, Kx)[0] == np.float32(d * (255 / 16) ** 2) * -1
+
+
+# ---------------------------------------------------------------- top-k oracle
+
+def test_topk_brute_force_max_mass():
+    # the top-k set maximises retained mass over every k-subset of the middle
+    # range (Thm. oracle); checked by enumeration on tiny inputs
+    rng = np.random.default_rng(7)
+    for trial in range(40):
+        n0 = int(rng.integers(1, 13))
+        sink, window = int(rng.integers(0, 3)), int(rng.integers(0, 4))
+        k = int(rng.integers(0, 6))
+        d = 4
+        q = grid(rng, d, scale=2)
+        K = grid(rng, n0, d, scale=2)
+        A = O.attention_weights(q, K)
+        sigma = O.ranking_scores(q, K)
+        S = O.topk_middle(sigma, n0, k, sink, window)
+        best = O.brute_force_topk_mass(A, n0, k, sink, window)
+        sink_end, win_start = O.region_bounds(n0, sink, window)
+        assert len(S) == min(k, max(0, win_start - sink_end))
+        assert O.retained_mass(A, S) == pytest.approx(best, abs=1e-14)
+
+
+def test_topk_order_and_tie_break_lowest_index():
+    # ties on the score resolve to the lower position; output order is
+    # (score desc, position asc); checked against Python's sort of tuples
+    rng = np.random.default_rng(8)
+    for trial in range(50):
+        n0 = int(rng.integers(5, 60))
+        sigma = rng.integers(-3, 4, size=n0).astype(np.float64)  # many ties
+        sink, window = 2, 3
+        k = int(rng.integers(1, n0))
+        S = O.topk_middle(sigma, n0, k, sink, window)
+        mid = [i for i in range(n0) if sink <= i < n0 - window]
+        ref = sorted(mid, key=lambda i: (-sigma[i], i))[:k]
+        assert list(S) == ref
+
+
+def test_topk_negative_zero_ties_positive_zero():
+    sigma = np.array([0.0, -0.0, 0.0, -0.0, -1.0])
+    S = O.topk_middle(sigma, 5, 3, 0, 0)
+    assert list(S) == [0, 1, 2]
+
+
+def test_topk_degenerate_ranges():
+    sigma = np.arange(10, dtype=np.float64)
+    assert list(O.topk_middle(sigma, 10, 0, 2, 2)) == []
+    assert list(O.topk_middle(sigma, 10, 99, 2, 2)) == [7, 6, 5, 4, 3, 2]
+    assert list(O.topk_middle(sigma, 4, 3, 2, 2)) == []   # n0 <= sink + window
+    assert list(O.topk_middle(sigma, 3, 3, 4, 0)) == []   # n0 < sink
+
+
+# ---------------------------------------------------------------- set algebra
+
+def _anchor_by_definition(s_star, n0, sink, window):
+    return sorted({i for i in range(n0) if i < sink} | set(int(x) for x in s_star)
+                  | {i for i in range(n0) if i >= n0 - window})
+
+
+def _reuse_by_definition(s_star, m, r, n0, n, sink, window):
+    out = {i for i in range(n) if i < sink}
+    out |= set(int(x) for x in s_star)
+    for p in list(s_star)[:m]:
+        for j in range(-r, r + 1):
+            if 0 <= p + j < n:
+                out.add(int(p + j))
+    out |= {i for i in range(n) if i >= max(min(sink, n0), n0 - window)}
+    return sorted(out)
+
+
+def test_sets_brute_force_random():
+    rng = np.random.default_rng(9)
+    for trial in range(400):
+        n0 = int(rng.integers(0, 40))
+        n = n0 + int(rng.integers(0, 6))
+        sink = int(rng.integers(0, 6))
+        window = int(rng.integers(0, 8))
+        k = int(rng.integers(0, 12))
+        r = int(rng.integers(0, 3))
+        sigma = rng.integers(-4, 5, size=max(n, 1)).astype(np.float64)
+        S = O.topk_middle(sigma, n0, k, sink, window)
+        m = O.dilation_m(k, len(S), -1 if trial % 2 else int(rng.integers(0, 5)))
+        assert list(O.anchor_set(S, n0, sink, window)) == _anchor_by_definition(S, n0, sink, window)
+        assert list(O.reuse_set(S, m, r, n0, n, sink, window)) == \
+            _reuse_by_definition(S, m, r, n0, n, sink, window)
+
+
+def test_reuse_at_range_edges_and_overlaps():
+    # top-m at the first and last middle positions; neighbours land in the
+    # sink and window (no duplicates) or are clipped
+    sink, window, n0, n = 3, 4, 20, 22
+    S = np.array([3, 15, 9])
+    R = O.reuse_set(S, 2, 1, n0, n, sink, window)
+    assert list(R) == [0, 1, 2, 3, 4, 9, 14, 15, 16, 17, 18, 19, 20, 21]
+    R0 = O.reuse_set(np.array([0]), 1, 2, 1, 1, 0, 0)
+    assert list(R0) == [0]
+
+
+def test_reuse_radius_zero_and_m_zero_equal_plain_sharing():
+    rng = np.random.default_rng(10)
+    sigma = rng.standard_normal(100)
+    S = O.topk_middle(sigma, 90, 20, 4, 8)
+    base = O.reuse_set(S, 0, 1, 90, 95, 4, 8)
+    assert list(base) == list(O.reuse_set(S, 7, 0, 90, 95, 4, 8))
+    expect = sorted(set(range(4)) | set(S.tolist()) | set(range(82, 95)))
+    assert list(base) == expect
+
+
+def test_isolated_dilation_size_closed_form():
+    # isolated top-m winners each add exactly 2r neighbours: |S_hat| = C + 2rm
+    sink, window, n0 = 4, 32, 1000
+    k, r = 30, 1
+    sigma = np.zeros(n0)
+    winners = np.arange(10, 10 + 10 * k, 10)[:k]
+    sigma[winners] = np.linspace(100, 50, k)
+    S = O.topk_middle(sigma, n0, k, sink, window)
+    assert sorted(S.tolist()) == winners.tolist()
+    m = O.dilation_m(k, len(S))
+    assert m == 10
+    C = O.anchor_set(S, n0, sink, window)
+    R = O.reuse_set(S, m, r, n0, n0, sink, window)
+    assert len(C) == sink + k + window
+    assert len(R) == sink + k + window + 2 * r * m
+
+
+# ---------------------------------------------------------------- golden budgets
+
+def test_golden_paper_budgets():
+    g = json.load(open(GOLDEN))
+    gs = g["gsm8k_coqa"]
+    sink = gs["C_t"] - gs["C_local"] - gs["k"]
+    assert sink == 8
+    n0 = 2000
+    sigma = np.zeros(n0)
+    sigma[np.arange(100, 100 + 3 * gs["k"], 3)] = 1.0  # k spread winners
+    S = O.topk_middle(sigma, n0, gs["k"], sink, gs["C_local"])
+    C = O.anchor_set(S, n0, sink, gs["C_local"])
+    assert len(C) == gs["C_t"]                        # C = C_sink + k + C_local
+    m = O.dilation_m(gs["k"], len(S))
+    assert m == 29 and g["defaults"]["r"] == 1
+    R = O.reuse_set(S, m, 1, n0, n0, sink, gs["C_local"])
+    assert gs["C_t"] <= len(R) <= gs["C_t"] + 2 * m
+    lb = g["longbench"]
+    C_lb = lb["C_sink"] + lb["k"] + lb["C_local"]
+    assert C_lb == lb["budget"]
+    m_lb = lb["k"] // 3
+    # the paper's average dilated shared set lies within [C, C + 2 r m]
+    assert C_lb <= lb["avg_shared_set"] <= C_lb + 2 * m_lb
+    C_star = lb["C_sink"] + lb["k_cis_star"] + lb["C_local"]
+    assert C_star <= lb["cis_star_avg_budget"] <= C_star + 2 * (lb["k_cis_star"] // 3)
+
+
+# ---------------------------------------------------------------- invariants of the benchmark spec
+
+def test_full_budget_reproduces_dense():
+    # k >= |middle| (or window >= n) gives R = [0, n): sparse == dense
+    rng = np.random.default_rng(11)
+    for (n0, extra, sink, window, k) in [(50, 3, 4, 8, 1000), (50, 0, 4, 64, 10), (7, 2, 0, 0, 7)]:
+        n = n0 + extra
+        d = 16
+        q = rng.standard_normal(d)
+        K = rng.standard_normal((n, d))
+        V = rng.standard_normal((n, d))
+        sigma = O.ranking_scores(q, K)
+        S = O.topk_middle(sigma, n0, k, sink, window)
+        R = O.reuse_set(S, O.dilation_m(k, len(S)), 1, n0, n, sink, window)
+        assert list(R) == list(range(n))
+        y_s, l_s = O.sparse_attention(q, K, V, R)
+        y_d, l_d = O.dense_attention(q, K, V)
+        np.testing.assert_allclose(y_s, y_d, rtol=0, atol=1e-15)
+        assert l_s == pytest.approx(l_d, abs=1e-15)
+        if extra == 0:
+            C = O.anchor_set(S, n0, sink, window)
+            assert list(C) == list(range(n0))
+
+
+# ---------------------------------------------------------------- mass relations (appendices)
+
+def _random_case(rng, n=200, d=32):
+    q = rng.standard_normal(d)
+    K = rng.standard_normal((n, d)) * 1.5
+    V = rng.standard_normal((n, d))
+    return q, K, V
+
+
+def test_tv_identity_and_kl_identity():
+    # ||A - A~_S||_TV = delta_S (Lemma tv); KL(A~_S || A) = log 1/tau_S (U2)
+    rng = np.random.default_rng(12)
+    for _ in range(20):
+        q, K, V = _random_case(rng)
+        A = O.attention_weights(q, K)
+        S = np.sort(rng.choice(200, size=int(rng.integers(1, 200)), replace=False))
+        At = O.renormalised(A, S)
+        assert O.tv_distance(A, At) == pytest.approx(O.dropped_mass(A, S), abs=1e-14)
+        assert O.kl_divergence(At, A) == pytest.approx(-math.log(O.retained_mass(A, S)), abs=1e-12)
+
+
+def test_output_error_bounded_by_dropped_mass():
+    # |y - y_S|_inf <= 2 delta_S max|v| (from the TV identity)
+    rng = np.random.default_rng(13)
+    for _ in range(30):
+        q, K, V = _random_case(rng)
+        S = np.sort(rng.choice(200, size=int(rng.integers(1, 200)), replace=False))
+        A = O.attention_weights(q, K)
+        y, _ = O.dense_attention(q, K, V)
+        ys, _ = O.sparse_attention(q, K, V, S)
+        assert np.abs(y - ys).max() <= 2 * O.dropped_mass(A, S) * np.abs(V).max() + 1e-13
+
+
+def test_family_best_is_minimal_dropped_mass():
+    # the per-head top-k member of the family beats every random member
+    rng = np.random.default_rng(14)
+    sink, window, k = 4, 16, 20
+    for _ in range(20):
+        q, K, V = _random_case(rng)
+        n = K.shape[0]
+        A = O.attention_weights(q, K)
+        best = O.family_best_dropped(A, n, sink, window, k)
+        S = O.anchor_set(O.topk_middle(O.ranking_scores(q, K), n, k, sink, window), n, sink, window)
+        assert O.dropped_mass(A, S) == pytest.approx(best, abs=1e-14)
+        mid = np.arange(sink, n - window)
+        for _ in range(20):
+            Sr = O.anchor_set(rng.choice(mid, size=k, replace=False), n, sink, window)
+            assert best <= O.dropped_mass(A, Sr) + 1e-15
+
+
+def test_cis_retained_mass_gap():
+    # Prop. cis-beta: on fixed keys, a later query reusing the dilated set of
+    # the reference query keeps tau_pre(q') >= tau*(q') - 2 ||A(q') - A(q)||_1
+    rng = np.random.default_rng(15)
+    sink, window, k, n, d = 4, 16, 24, 300, 32
+    for _ in range(30):
+        K = rng.standard_normal((n, d)) * 1.5
+        q = rng.standard_normal(d)
+        Sq = O.topk_middle(O.ranking_scores(q, K), n, k, sink, window)
+        R = O.reuse_set(Sq, O.dilation_m(k, len(Sq)), 1, n, n, sink, window)
+        qp = q
+        for _ in range(8):
+            qp = 0.9 * qp + math.sqrt(0.19) * rng.standard_normal(d)
+            A_q = O.attention_weights(q, K)
+            A_p = O.attention_weights(qp, K)
+            d_att = np.abs(A_p - A_q).sum()
+            tau_star = 1.0 - O.family_best_dropped(A_p, n, sink, window, k)
+            tau_pre = O.retained_mass(A_p, R)
+            assert tau_pre >= tau_star - 2 * d_att - 1e-13
+
+
+def test_attention_variation_lipschitz_bound():
+    # ||A(q') - A(q)||_1 <= 2 K_max / sqrt(d) * ||q' - q|| (CIS appendix lemmas)
+    rng = np.random.default_rng(16)
+    for _ in range(50):
+        n, d = 100, 16
+        K = rng.standard_normal((n, d))
+        q = rng.standard_normal(d)
+        qp = q + rng.standard_normal(d) * rng.uniform(0.01, 1.0)
+        lhs = np.abs(O.attention_weights(qp, K) - O.attention_weights(q, K)).sum()
+        kmax = np.linalg.norm(K, axis=1).max()
+        assert lhs <= 2 * kmax / math.sqrt(d) * np.linalg.norm(qp - q) + 1e-14
+
+
+def test_mi_bound_monotone_on_restricted_domain():
+    # g is increasing on (0, L/(1+L)] (footnote to Eq. pohs bound)
+    for L in (2, 10, 1000, 131072):
+        xs = np.linspace(1e-9, L / (1 + L), 2000)
+        gs = [O.mi_loss_bound(x, L) for x in xs]
+        assert all(b >= a - 1e-12 for a, b in zip(gs, gs[1:]))
+    assert O.mi_loss_bound(0.0, 100) == 0.0
+
+
+# ---------------------------------------------------------------- schedule
+
+def test_retrieval_ratio_closed_form():
+    # rho_hat = 1 / (s G) when T is a multiple of s and N of G (Sec. 5.1)
+    for s, G, T, N in [(4, 1, 16, 1), (4, 4, 16, 32), (8, 4, 16, 32), (8, 1, 16, 32)]:
+        assert O.retrieval_ratio(T, N, s, G) == pytest.approx(1.0 / (s * G))
+
+
+def test_decode_oracle_schedule_and_anchor_state():
+    rng = np.random.default_rng(17)
+    L, T, g, d, n_ctx = 4, 8, 2, 16, 60
+    sink, window, k, s, G = 2, 4, 6, 4, 2
+    K = [rng.standard_normal((n_ctx + T, d)) for _ in range(L)]
+    Q = [[rng.standard_normal((g, d)) for _ in range(T)] for _ in range(L)]
+    dec = O.DecodeOracle(sink, window, s, G, r=1, k=k)
+    for j in range(T):
+        n = n_ctx + j + 1
+        for l in range(L):
+            S = dec.step_set(l, j, Q[l][j], K[l], n)
+            a = (l // G) * G
+            j0 = (j // s) * s
+            n0 = n_ctx + j0 + 1
+            s_star = O.topk_middle(O.ranking_scores(Q[a][j0], K[a][:n0]), n0, k, sink, window)
+            if l == a and j == j0:
+                expect = O.anchor_set(s_star, n0, sink, window)
+            else:
+                expect = O.reuse_set(s_star, k // 3, 1, n0, n, sink, window)
+            assert list(S) == list(expect)
