@@ -1,0 +1,266 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the PrHS hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+
+A step is one decode step of the whole hot path over every layer of the
+workload: refresh selection (score, top-k, anchor set) where the schedule asks
+for it, the dilated shared set of every layer group, and sparse decode
+attention of every layer.  Inputs are seeded synthetic tensors already
+resident in HBM.  The same steps are timed with dense decode attention for the
+speedup.  Prints one JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+METRIC = ("sparse decode-attn µs/layer-step + effective HBM GB/s (% peak); "
+          "speedup vs dense")
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(run, set_lens, sel_rows):
+    """Bytes the method itself must move, per decode step j (dict j -> dict).
+
+    attention: sum over (b, g) of |R| (2 d e + 4) + q + out/lse per layer;
+    selection: middle keys (d e each) + q + 8 B per key of radix traffic +
+    top-k and set writes, once per refresh of an anchor layer; reuse: top-k
+    read and set write per group."""
+    w = run.w
+    e = 4 if w.dtype == "f32" else 2
+    qbytes = w.batch * w.hq * w.d * e
+    outbytes = w.batch * w.hq * (w.d + 1) * 4
+    per = {}
+    for j in range(w.steps):
+        attn = 0
+        for l in range(run.L):
+            total_set = set_lens[(l, j)]
+            attn += total_set * (2 * w.d * e + 4) + qbytes + outbytes
+        sel = 0
+        if j % w.s == 0:
+            m_rows, k_rows, c_rows = sel_rows[j]
+            sel += m_rows * (w.d * e + 8) + run.groups * qbytes + (k_rows + c_rows) * 4
+        if w.G > 1 or j % w.s != 0:
+            for gi in range(run.groups):
+                sel += set_lens[("shared", gi, j)] * 4 + set_lens[("topk", gi, j)] * 4
+        per[j] = dict(attn=attn, sel=sel)
+    return per
+
+
+def cpu_baseline(run, budget_s):
+    """Times the CPU oracle on a bounded sample of the same workload: every
+    layer-step of the first refresh block of layer group 0, for as many
+    (batch, kv-head) units as fit the time budget; scaled to all units."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+    from paper_2602_08329_amd import synth
+
+    w = run.w
+    inp = run.inp
+    units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
+    layers = list(range(min(w.G, run.L)))
+    steps = list(range(min(w.s, w.steps)))
+    done = 0
+    spent = 0.0
+    with threadpool_limits(limits=1):
+        for (b, g) in units:
+            n_max = w.n_ctx[b] + w.steps
+            cache = {l: synth.gather_unit(inp, l, b, g, n_max) for l in layers}
+            qs = {(l, j): synth.query_group(inp, l, j, b, g) for l in layers for j in steps}
+            dec = O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k, k_num=w.k_num,
+                                 k_den=w.k_den, dilate_m=w.dilate_m)
+            t0 = time.perf_counter()
+            for j in steps:
+                n = w.n_ctx[b] + j + 1
+                for l in layers:
+                    K, V = cache[l]
+                    S = dec.step_set(l, j, qs[(l, j)], K, n)
+                    dec.attend(qs[(l, j)], K[:n], V[:n], S)
+            spent += time.perf_counter() - t0
+            done += 1
+            if spent >= budget_s:
+                break
+    layer_steps = len(layers) * len(steps)
+    us = spent / done * len(units) / layer_steps * 1e6
+    return {"value": round(us, 1), "unit": "us/layer-step", "cores": 1, "kind": "oracle",
+            "sample": (f"{done} of {len(units)} (batch, kv-head) units x {layer_steps} "
+                       f"layer-steps (layers {layers[0]}-{layers[-1]}, steps {steps[0]}-{steps[-1]}); "
+                       f"{spent:.1f} s; scaled to all units"),
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", type=int, default=1, help="workload index 0-4")
+    ap.add_argument("--batch", type=int, default=None, help="workload 4: batch (16 or 64)")
+    ap.add_argument("--nmax", type=int, default=None, help="workload 4: max context")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path has no multi-GPU mode)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2602_08329_amd import binding as B
+    from paper_2602_08329_amd import synth
+    from paper_2602_08329_amd.schedule import DecodeRunner
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    B.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.workload(args.config, batch=args.batch, nmax=args.nmax)
+    T = w.steps
+    K_steps, W_steps = args.steps, args.warmup
+    log(f"workload {w.name}: generating inputs on the GPU")
+    t0 = time.time()
+    inp = synth.generate(w, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.time() - t0:.1f} s; "
+        f"{sum(x.numel() * x.element_size() for x in inp.K + inp.V) / 2**30:.1f} GiB of KV")
+    run = DecodeRunner(inp, dev)
+
+    # one untimed pass over all steps: set sizes for the byte accounting
+    set_lens = {}
+    sel_rows = {}
+    for j in range(T):
+        run.selection_step(j)
+        if j % w.s == 0:
+            mid = 0
+            for b in range(w.batch):
+                n0 = w.n_ctx[b] + j + 1
+                se = min(w.sink, n0)
+                mid += (max(se, n0 - w.window) - se) * w.hkv
+            tl = int(run.topk_len.sum().item())
+            al = int(run.anchor_len.sum().item())
+            sel_rows[j] = (mid * run.groups, tl, al)
+        sh = run.shared_len.sum(dim=(1, 2)).cpu().tolist()
+        tk = run.topk_len.sum(dim=(1, 2)).cpu().tolist()
+        for gi in range(run.groups):
+            set_lens[("shared", gi, j)] = sh[gi]
+            set_lens[("topk", gi, j)] = tk[gi]
+        for l in range(run.L):
+            s_idx, s_len = run.set_for(l, j)
+            set_lens[(l, j)] = int(s_len.sum().item())
+        run.step(j)
+    torch.cuda.synchronize()
+    per = algorithmic_bytes(run, set_lens, sel_rows)
+
+    def timed(fn, label):
+        for i in range(W_steps):
+            fn(i % T)
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        js = [(W_steps + i) % T for i in range(K_steps)]
+        torch.cuda.synchronize()
+        ev0.record()
+        t = time.perf_counter()
+        for j in js:
+            fn(j)
+        ev1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t
+        ms = ev0.elapsed_time(ev1)
+        log(f"{label}: {ms / K_steps:.3f} ms/step (wall {wall * 1e3 / K_steps:.3f} ms/step)")
+        return ms, js
+
+    log(f"timing {K_steps} sparse decode steps after {W_steps} warm-up steps")
+    ms_sparse, js = timed(run.step, "sparse (selection + attention)")
+    ms_sel, _ = timed(run.selection_step, "selection only")
+
+    def attn_only(j):
+        for l in range(run.L):
+            run.attend(l, j)
+    ms_attn, _ = timed(attn_only, "attention only")
+    ms_dense, _ = timed(run.dense_step, "dense attention")
+
+    # dominant kernel: the sparse attention launch, timed per launch with events
+    starts, ends, launch_bytes = [], [], []
+    for j in js:
+        run.selection_step(j)
+        for l in range(run.L):
+            a = torch.cuda.Event(enable_timing=True)
+            z = torch.cuda.Event(enable_timing=True)
+            a.record()
+            run.attend(l, j)
+            z.record()
+            starts.append(a)
+            ends.append(z)
+            e = 4 if w.dtype == "f32" else 2
+            launch_bytes.append(set_lens[(l, j)] * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e
+                                + w.batch * w.hq * (w.d + 1) * 4)
+    torch.cuda.synchronize()
+    durs = [a.elapsed_time(z) * 1e-3 for a, z in zip(starts, ends)]
+    avg_dur = sum(durs) / len(durs)
+    avg_bytes = sum(launch_bytes) / len(launch_bytes)
+    achieved = avg_bytes / avg_dur / 1e9
+
+    L = run.L
+    total_bytes = sum(per[j]["attn"] + per[j]["sel"] for j in js)
+    us_layer_step = ms_sparse * 1e3 / (K_steps * L)
+    eff_gbps = total_bytes / (ms_sparse * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(us_layer_step, 3),
+        "unit": "us/layer-step",
+        "n_gpus": 1,
+        "steps": K_steps,
+        "warmup": W_steps,
+        "ms_per_step": round(ms_sparse / K_steps, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "layers": w.layers, "batch": w.batch, "q_heads": w.hq,
+            "kv_heads": w.hkv, "head_dim": w.d, "context": max(w.n_ctx),
+            "k": w.k if not w.k_den else f"{w.k_num}/{w.k_den} n", "window": w.window,
+            "sink": w.sink, "refresh_every": w.s, "layer_group": w.G, "dilate_r": w.r,
+            "paged": w.paged, "decode_steps_cycled": T,
+        },
+        "effective_gbps": round(eff_gbps, 1),
+        "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),
+        "speedup_vs_dense": round(ms_dense / ms_sparse, 3),
+        "dense_us_per_layer_step": round(ms_dense * 1e3 / (K_steps * L), 3),
+        "selection_us_per_layer_step": round(ms_sel * 1e3 / (K_steps * L), 3),
+        "attention_us_per_layer_step": round(ms_attn * 1e3 / (K_steps * L), 3),
+        "roofline": {
+            "kernel": "attn_split_bf16 (sparse)" if w.dtype != "f32" else "attn_split_f32 (sparse)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None, "avg_launch_us": round(avg_dur * 1e6, 3),
+            "avg_launch_bytes": int(avg_bytes), "launches": len(durs),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle for about {args.cpu_seconds:.0f} s")
+        result["cpu_baseline"] = cpu_baseline(run, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

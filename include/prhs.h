@@ -1,0 +1,214 @@
+/*
+ * prhs.h -- C ABI of libprhs, the MI355X (gfx950) decode hot path of
+ * Pre-hoc Sparsity (PrHS): per-KV-head top-k selection, union with sink and
+ * recency window, reuse of the selection across decode steps (with neighbour
+ * dilation) and across a group of layers, and gather-sparse decode attention.
+ *
+ * Paper: "Near-Oracle KV Selection via Pre-hoc Sparsity for Long-Context
+ * Inference" (arXiv 2602.08329).  Each entry point cites the passage that
+ * defines the operation it computes.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named for tensors (q, k, v, block_table, seq_lens, topk_*, set_*,
+ *   out, lse, ws) are DEVICE pointers.  Descriptor structs (prhs_kv,
+ *   prhs_params) and size outputs are HOST memory.  No ROCm header is needed:
+ *   the stream is passed as void* (a hipStream_t; NULL is the null stream).
+ * - The caller owns every buffer.  The library allocates no device memory and
+ *   keeps no state between calls; calls on different streams with different
+ *   buffers may run concurrently.  Calls sharing a workspace must be ordered.
+ * - Every call is asynchronous on `stream`; results are valid once the stream
+ *   has synchronised.  No call synchronises internally.
+ * - Positions are 0-based.  A sequence of current length n attends keys
+ *   [0, n): the current token's own key/value is already in the cache (the
+ *   sum of Eq. attn_eq runs up to and including the current step).
+ * - Argument validation happens on the host before any device work and
+ *   returns PRHS_E_INVALID / PRHS_E_UNSUPPORTED / PRHS_E_CAPACITY /
+ *   PRHS_E_WORKSPACE; a failed launch returns PRHS_E_DEVICE.  The message of
+ *   the last non-OK status of the calling thread is in prhs_last_error().
+ * - Device-array preconditions the host cannot see: 0 <= seq_lens[b] <=
+ *   max_seq_len, anchor_lens[b] <= seq_lens[b], block-table entries in
+ *   [0, num_pages), set indices < seq_lens[b].  Kernels clamp lengths to the
+ *   host-declared bounds and skip out-of-range rows instead of reading out of
+ *   bounds; results for inputs that break a precondition are unspecified.
+ */
+#ifndef PRHS_H_
+#define PRHS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PRHS_ABI_VERSION 1
+
+typedef enum prhs_status {
+  PRHS_OK = 0,
+  PRHS_E_INVALID = -1,      /* null pointer, negative size, inconsistent shape */
+  PRHS_E_UNSUPPORTED = -2,  /* head_dim, dtype, group size or k outside what is built */
+  PRHS_E_CAPACITY = -3,     /* k_cap or set_cap smaller than the bound the call needs */
+  PRHS_E_WORKSPACE = -4,    /* ws null or smaller than prhs_workspace_size() */
+  PRHS_E_DEVICE = -5        /* kernel launch failed; see prhs_last_error() */
+} prhs_status;
+
+typedef enum prhs_dtype {
+  PRHS_F32 = 0,   /* q, K and V in fp32 */
+  PRHS_BF16 = 1   /* q, K and V in bf16; all outputs stay fp32 */
+} prhs_dtype;
+
+typedef enum prhs_layout {
+  PRHS_KV_CONTIGUOUS = 0,  /* K, V: [batch][num_kv_heads][capacity][head_dim] */
+  PRHS_KV_PAGED = 1        /* K, V: [num_pages][num_kv_heads][page_size][head_dim];
+                              token i of sequence b lives in page
+                              block_table[b * max_pages + i / page_size],
+                              slot i % page_size */
+} prhs_layout;
+
+/* The KV cache of one layer (Sec. 3.1: K^h, V^h in R^{L x d} per head). */
+typedef struct prhs_kv {
+  int32_t batch;          /* B >= 0 */
+  int32_t num_q_heads;    /* Hq >= 1 */
+  int32_t num_kv_heads;   /* Hkv >= 1, Hq % Hkv == 0; query head h reads kv head h / (Hq/Hkv) */
+  int32_t head_dim;       /* d: 64 or 128 */
+  int32_t dtype;          /* prhs_dtype */
+  int32_t layout;         /* prhs_layout */
+  int32_t capacity;       /* contiguous: token stride per (b, kv head); >= max_seq_len */
+  int32_t page_size;      /* paged: tokens per page (>= 1) */
+  int32_t max_pages;      /* paged: row length of block_table; max_pages*page_size >= max_seq_len */
+  int32_t num_pages;      /* paged: physical pages in K and V */
+  const void* k;
+  const void* v;
+  const int32_t* block_table;  /* paged: [batch][max_pages] int32; ignored when contiguous */
+  const int32_t* seq_lens;     /* [batch] current length n_b (includes the current token) */
+  int32_t max_seq_len;         /* host-known bound on seq_lens; < 2^22 */
+} prhs_kv;
+
+/* Selection budget and reuse schedule (Sec. 4.1; defaults of Sec. 5.1). */
+typedef struct prhs_params {
+  int32_t k;              /* middle budget when k_den == 0 */
+  int32_t k_num, k_den;   /* k_den > 0: per-sequence budget k_b = floor(k_num * n0_b / k_den) */
+  int32_t sink;           /* C_sink: positions [0, sink) are always kept */
+  int32_t window;         /* C_local: positions [n0 - window, n0) at the anchor */
+  int32_t dilate_m;       /* top-m winners that are dilated; < 0 means floor(k_b / 3) */
+  int32_t dilate_r;       /* dilation radius r >= 0 */
+  int32_t refresh_every;  /* s >= 1: decode steps j with j % s == 0 refresh */
+  int32_t layer_group;    /* G >= 1: layers l with l % G == 0 anchor their group */
+} prhs_params;
+
+enum {
+  PRHS_OP_SELECT = 0,
+  PRHS_OP_DILATE_REUSE = 1,
+  PRHS_OP_SPARSE_ATTN = 2,
+  PRHS_OP_DENSE_ATTN = 3
+};
+
+enum { PRHS_REUSE = 0, PRHS_REFRESH = 1 };
+
+/* Largest sort buffer of the top-k stage: k_b is clamped to the middle range
+ * length, and the clamped value must not exceed this. */
+#define PRHS_MAX_TOPK 16384
+
+/* ABI version of the loaded library (PRHS_ABI_VERSION). */
+int32_t prhs_abi_version(void);
+
+/* Largest middle budget k_b any sequence of length <= max_seq_len gets, after
+ * clamping to the middle range; the minimum k_cap for prhs_select.  Returns
+ * -1 when params is NULL or inconsistent. */
+int32_t prhs_max_topk(const prhs_params* params, int32_t max_seq_len);
+
+/* Smallest set_cap that holds every index set the schedule produces when each
+ * call's current length exceeds its anchor length by at most
+ * refresh_every - 1: min(max_seq_len, sink + k + 2*r*m + window +
+ * refresh_every - 1) (the dilated-set size of the CIS parameterisation
+ * appendix plus the tokens decoded since the anchor).  -1 on bad arguments. */
+int32_t prhs_set_capacity(const prhs_params* params, int32_t max_seq_len);
+
+/* Device workspace in bytes that entry point `op` (PRHS_OP_*) needs for this
+ * cache shape; set_cap is used by PRHS_OP_SPARSE_ATTN only.  0 bytes is a
+ * valid answer (ws may then be NULL). */
+prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params* params,
+                                int32_t set_cap, size_t* bytes);
+
+/* Block schedule of CIS (Sec. 4.1): PRHS_REFRESH when decode step `step`
+ * opens a block of refresh_every steps and `layer` opens a group of
+ * layer_group layers, else PRHS_REUSE.  -1 on bad arguments. */
+int32_t prhs_schedule(int32_t step, int32_t layer, const prhs_params* params);
+
+/* Refresh: score, top-k and anchor set for one layer (Sec. 4.1 Selection
+ * Criteria; top-k oracle of Sec. 3.3).
+ *
+ * For every (b, kv head g) with anchor length n0 = seq_lens[b]:
+ *   sigma_i = max over the g-th group's query heads h of q[b][h] . k_i (raw
+ *   dot product, computed in fp32) for i in the middle range
+ *   [min(sink, n0), max(min(sink, n0), n0 - window));
+ *   topk_idx[b][g][0 .. topk_len) = the min(k_b, middle length) positions of
+ *   largest sigma, ordered by (sigma descending, position ascending);
+ *   set_idx[b][g][0 .. set_len) = sink U top-k U [n0 - window, n0),
+ *   ascending and without duplicates (the critical set C_t).
+ * q: [batch][num_q_heads][head_dim] in kv->dtype.
+ * topk_idx: [batch][num_kv_heads][k_cap] int32, k_cap >= prhs_max_topk().
+ * topk_len: [batch][num_kv_heads] int32.
+ * set_idx: [batch][num_kv_heads][set_cap] int32, set_cap >= min(max_seq_len,
+ *   sink + prhs_max_topk() + window).  set_len: [batch][num_kv_heads] int32.
+ * ws: >= prhs_workspace_size(PRHS_OP_SELECT) bytes, contents need no
+ *   initialisation and are clobbered.
+ * -0.0 scores rank equal to +0.0; NaN or infinite inputs are a precondition
+ * violation. */
+prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* params,
+                        int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                        int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Reuse: build the dilated shared set of a later step or another layer of the
+ * group (Def. 3.2 key-value sharing; Eq. neighboring).
+ *
+ * For every (b, g), with n0 = anchor_lens[b] (the anchor's length at its
+ * refresh), n = seq_lens[b] >= n0, S* = topk_idx[b][g][0 .. topk_len) as
+ * returned by prhs_select and m = min(dilate_m or floor(k_b / 3), topk_len):
+ *   set = [0, min(sink, n0)) U S* U {p + j : p in first m of S*, |j| <= r,
+ *         0 <= p + j < n} U [max(min(sink, n0), n0 - window), n),
+ * ascending and without duplicates.  The set does not depend on any layer's
+ * K/V, so one call serves every layer that shares the selection.
+ * Writes at most set_cap entries; set_len is clamped to set_cap. */
+prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t num_kv_heads,
+                              const int32_t* topk_idx, const int32_t* topk_len, int32_t k_cap,
+                              const int32_t* anchor_lens, const int32_t* seq_lens,
+                              int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                              void* stream);
+
+/* Token-sparse decode attention (Def. 3.1) over per-kv-head index sets.
+ *
+ * For every (b, query head h) with g = h / (Hq/Hkv) and
+ * S = set_idx[b][g][0 .. min(set_len[b][g], set_cap)):
+ *   out[b][h] = sum_{i in S} softmax_S(scale * q[b][h] . k_i) v_i   (fp32)
+ *   lse[b][h] = log sum_{i in S} exp(scale * q[b][h] . k_i)        (fp32)
+ * i.e. attention renormalised over S (the truncated distribution of the
+ * unified-bounds appendix).  An empty S gives out = 0, lse = -inf.  Indices
+ * outside [0, seq_lens[b]) are skipped.  lse may be NULL.
+ * q: [batch][num_q_heads][head_dim] in kv->dtype.  out: [batch][num_q_heads]
+ * [head_dim] fp32.  ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap)
+ * bytes; its contents need no initialisation and are clobbered. */
+prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q,
+                                    const int32_t* set_idx, const int32_t* set_len,
+                                    int32_t set_cap, float scale, float* out, float* lse,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/* Dense decode attention over every cached key [0, seq_lens[b]) (Eq. attn_eq):
+ * the baseline the sparse path is measured against, and the k = n special
+ * case.  Same outputs and conventions as prhs_sparse_decode_attn.
+ * ws: >= prhs_workspace_size(PRHS_OP_DENSE_ATTN) bytes (no initialisation
+ * needed). */
+prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale,
+                                   float* out, float* lse, void* ws, size_t ws_bytes,
+                                   void* stream);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char* prhs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRHS_H_ */

@@ -1,0 +1,159 @@
+// Internal declarations shared by the libprhs translation units.
+// Device-side views of the C-ABI descriptors, KV row addressing, and the
+// host-side launch functions each kernel file provides.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace prhs {
+
+// Positions are < 2^22, so a position fits the low half of a 64-bit sort key.
+constexpr int kIdxBits = 22;
+constexpr uint32_t kIdxMax = (1u << kIdxBits) - 1u;
+constexpr int kHistBins = 2048;
+
+// Device view of one layer's KV cache.
+struct KvView {
+  const void* k;
+  const void* v;
+  const int32_t* table;
+  const int32_t* seq_lens;
+  int32_t batch, hq, hkv, d;
+  int32_t capacity;   // contiguous token stride
+  int32_t page_size, max_pages, num_pages;
+  int32_t max_seq_len;
+  int32_t paged;
+};
+
+// Element offset of the row holding token `pos` of (b, kv head g), or -1 when
+// the position or its page lies outside the cache.  Contiguous rows are
+// [b][g][pos][d]; paged rows are [page][g][slot][d].
+__device__ __forceinline__ int64_t kv_row_offset(const KvView& kv, int b, int g, int pos) {
+  if (pos < 0) return -1;
+  if (!kv.paged) {
+    if (pos >= kv.capacity) return -1;
+    return ((int64_t)(b * kv.hkv + g) * kv.capacity + pos) * kv.d;
+  }
+  int page = pos / kv.page_size;
+  if (page >= kv.max_pages) return -1;
+  int phys = kv.table[(int64_t)b * kv.max_pages + page];
+  if (phys < 0 || phys >= kv.num_pages) return -1;
+  return (((int64_t)phys * kv.hkv + g) * kv.page_size + (pos - page * kv.page_size)) * kv.d;
+}
+
+// Number of valid cached tokens of sequence b, clamped to what the cache can hold.
+__device__ __forceinline__ int kv_seq_len(const KvView& kv, int b) {
+  int n = kv.seq_lens[b];
+  n = n < 0 ? 0 : n;
+  return n > kv.max_seq_len ? kv.max_seq_len : n;
+}
+
+// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
+// -0.0 is mapped like +0.0.
+__device__ __forceinline__ uint32_t score_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Warp-aggregated append: lanes with pred reserve consecutive slots of
+// *counter (one atomic per wave).  Returns the lane's slot or -1.  Every lane
+// of the wave must call it.
+__device__ __forceinline__ int wave_append(bool pred, uint32_t* counter) {
+  const uint64_t mask = __ballot(pred);
+  const int lane = __lane_id();
+  const int cnt = __popcll(mask);
+  if (cnt == 0) return -1;
+  const int leader = __ffsll((long long)mask) - 1;
+  uint32_t base = 0;
+  if (lane == leader) base = atomicAdd(counter, (uint32_t)cnt);
+  base = __shfl(base, leader);
+  const int off = __popcll(mask & ((1ull << lane) - 1ull));
+  return pred ? (int)(base + off) : -1;
+}
+
+// Exclusive prefix sum over a workgroup of BLOCK threads; `scratch` holds
+// BLOCK/64 + 1 words of LDS.  Returns this thread's exclusive prefix and the
+// block total in *total.  Must be reached by every thread.
+template <int BLOCK>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scratch, uint32_t* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) scratch[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int w = 0; w < BLOCK / 64; ++w) {
+      uint32_t t = scratch[w];
+      scratch[w] = run;
+      run += t;
+    }
+    scratch[BLOCK / 64] = run;
+  }
+  __syncthreads();
+  const uint32_t res = scratch[wave] + x - v;
+  *total = scratch[BLOCK / 64];
+  __syncthreads();
+  return res;
+}
+
+// ---------------------------------------------------------------------------
+// Host launch functions (defined next to their kernels).
+
+struct SelectLaunch {
+  KvView kv;
+  const void* q;
+  int dtype;
+  int k, k_num, k_den, sink, window;
+  int32_t* topk_idx;
+  int32_t* topk_len;
+  int k_cap;
+  int32_t* set_idx;
+  int32_t* set_len;
+  int set_cap;
+  void* ws;
+  int max_topk;   // host bound on the clamped budget (sort size)
+};
+size_t select_workspace_bytes(int rows, int max_seq_len, int max_topk);
+hipError_t launch_select(const SelectLaunch& a, hipStream_t stream);
+
+struct DilateLaunch {
+  int batch, hkv;
+  const int32_t* topk_idx;
+  const int32_t* topk_len;
+  int k_cap;
+  const int32_t* anchor_lens;
+  const int32_t* seq_lens;
+  int32_t* set_idx;
+  int32_t* set_len;
+  int set_cap;
+  int k, k_num, k_den, sink, window, dilate_m, dilate_r;
+};
+hipError_t launch_dilate_reuse(const DilateLaunch& a, hipStream_t stream);
+
+struct AttnLaunch {
+  KvView kv;
+  const void* q;
+  int dtype;
+  const int32_t* set_idx;  // null for dense
+  const int32_t* set_len;
+  int set_cap;
+  float scale;
+  float* out;
+  float* lse;
+  void* ws;
+};
+// Split geometry shared by workspace sizing and launch.
+void attn_split_geometry(int dtype, int batch, int hq, int hkv, int rows_cap, int* chunk, int* nsplit);
+size_t attn_workspace_bytes(int dtype, int batch, int hq, int hkv, int d, int rows_cap);
+hipError_t launch_attention(const AttnLaunch& a, bool dense, hipStream_t stream);
+
+}  // namespace prhs

@@ -1,0 +1,120 @@
+"""Host-side decode schedule over layers and steps (Sec. 4.1 blocks, Def. 3.2
+sharing, layer groups).
+
+For decode step j and layer l:
+  * (l, j) with prhs_schedule == REFRESH (j % s == 0 and l % G == 0) runs
+    prhs_select on its own q and K, then attends its critical set C(n0);
+  * once per (group, step) where some layer reuses, prhs_dilate_reuse builds
+    the dilated shared set R(n) from the group's latest top-k;
+  * every other layer of the group attends R(n) over its own K/V.
+The carried state is the per-group top-k buffer and the anchor lengths n0,
+which are simply the sequence lengths of the refresh step.
+"""
+
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import binding as B
+
+
+class DecodeRunner:
+    """Runs the hot path of a synthetic workload (paper_2602_08329_amd.synth)
+    whose inputs already live on the GPU."""
+
+    def __init__(self, inp, device="cuda", dense=False):
+        w = inp.w
+        self.w = w
+        self.inp = inp
+        self.device = torch.device(device)
+        self.L = len(inp.K)
+        self.groups = (self.L + w.G - 1) // w.G
+        self.scale = 1.0 / math.sqrt(w.d)
+        T, Bsz = w.steps, w.batch
+        lens = torch.tensor([[n + j + 1 for n in w.n_ctx] for j in range(T)], dtype=torch.int32)
+        self.seq_lens = lens.to(self.device)
+        self.max_seq_len = w.capacity
+        self.params = B.params(k=w.k, k_num=w.k_num, k_den=w.k_den, sink=w.sink,
+                               window=w.window, dilate_m=w.dilate_m, dilate_r=w.r,
+                               refresh_every=w.s, layer_group=w.G)
+        table = inp.block_table.to(self.device) if inp.block_table is not None else None
+        # one descriptor per (layer, step): only the lengths pointer differs
+        self.kv = [[B.KV(inp.K[l], inp.V[l], self.seq_lens[j], self.max_seq_len, w.hq, table)
+                    for j in range(T)] for l in range(self.L)]
+        self.k_cap = max(1, B.prhs_max_topk(self.params, self.max_seq_len))
+        self.set_cap = max(1, B.prhs_set_capacity(self.params, self.max_seq_len),
+                           min(self.max_seq_len, w.sink + self.k_cap + w.window))
+        dev = self.device
+        i32 = torch.int32
+        G_ = self.groups
+        self.topk_idx = torch.zeros(G_, Bsz, w.hkv, self.k_cap, dtype=i32, device=dev)
+        self.topk_len = torch.zeros(G_, Bsz, w.hkv, dtype=i32, device=dev)
+        self.anchor_set = torch.zeros(G_, Bsz, w.hkv, self.set_cap, dtype=i32, device=dev)
+        self.anchor_len = torch.zeros(G_, Bsz, w.hkv, dtype=i32, device=dev)
+        self.shared_set = torch.zeros(G_, Bsz, w.hkv, self.set_cap, dtype=i32, device=dev)
+        self.shared_len = torch.zeros(G_, Bsz, w.hkv, dtype=i32, device=dev)
+        self.anchor_step = [None] * G_
+        kv0 = self.kv[0][0]
+        self.ws_select = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv0, self.params), dev)
+        self.ws_attn = B.workspace(
+            B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv0, self.params, self.set_cap), dev)
+        self.ws_dense = B.workspace(B.prhs_workspace_size(B.PRHS_OP_DENSE_ATTN, kv0, self.params), dev)
+        self.out = torch.zeros(Bsz, w.hq, w.d, dtype=torch.float32, device=dev)
+        self.lse = torch.zeros(Bsz, w.hq, dtype=torch.float32, device=dev)
+
+    # -- pieces -------------------------------------------------------------
+    def refresh(self, gi, j):
+        l = gi * self.w.G
+        B.prhs_select(self.kv[l][j], self.inp.q[l, j], self.params, self.topk_idx[gi],
+                      self.topk_len[gi], self.anchor_set[gi], self.anchor_len[gi], self.ws_select)
+        self.anchor_step[gi] = j
+
+    def share(self, gi, j):
+        j0 = self.anchor_step[gi]
+        if j0 is None or j - j0 >= self.w.s or j < j0:
+            raise RuntimeError(f"group {gi} has no anchor for step {j}")
+        B.prhs_dilate_reuse(self.params, self.topk_idx[gi], self.topk_len[gi], self.seq_lens[j0],
+                            self.seq_lens[j], self.shared_set[gi], self.shared_len[gi])
+
+    def set_for(self, l, j):
+        """(set, len) tensors that layer l attends at step j."""
+        gi = l // self.w.G
+        if B.prhs_schedule(j, l, self.params) == B.PRHS_REFRESH:
+            return self.anchor_set[gi], self.anchor_len[gi]
+        return self.shared_set[gi], self.shared_len[gi]
+
+    def attend(self, l, j, out=None, lse=None):
+        s, n = self.set_for(l, j)
+        B.prhs_sparse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.scale,
+                                  self.out if out is None else out,
+                                  self.lse if lse is None else lse, self.ws_attn)
+
+    def dense(self, l, j, out=None, lse=None):
+        B.prhs_dense_decode_attn(self.kv[l][j], self.inp.q[l, j], self.scale,
+                                 self.out if out is None else out,
+                                 self.lse if lse is None else lse, self.ws_dense)
+
+    # -- whole decode steps -------------------------------------------------
+    def selection_step(self, j):
+        """Refresh and reuse-set construction of step j for every group."""
+        w = self.w
+        for gi in range(self.groups):
+            if j % w.s == 0:
+                self.refresh(gi, j)
+            if w.G > 1 or j % w.s != 0:
+                self.share(gi, j)
+
+    def step(self, j, outs=None):
+        """One sparse decode step j over every layer; outs[l] receives layer
+        l's (out, lse) when given."""
+        self.selection_step(j)
+        for l in range(self.L):
+            o = None if outs is None else outs[l]
+            self.attend(l, j, *(o if o is not None else (None, None)))
+
+    def dense_step(self, j, outs=None):
+        for l in range(self.L):
+            o = None if outs is None else outs[l]
+            self.dense(l, j, *(o if o is not None else (None, None)))

@@ -239,7 +239,7 @@ def _to_paged(inp, gen, dev):
             Xp = torch.nn.functional.pad(X, (0, 0, 0, pad)) if pad else X
             Xp = Xp.reshape(B, Hkv, max_pages, ps, d).permute(0, 2, 1, 3, 4)
             Xp = Xp.reshape(P, Hkv, ps, d)
-            phys = torch.empty_like(Xp)
+            phys = torch.empty((P, Hkv, ps, d), dtype=Xp.dtype, device=Xp.device)
             phys[table.reshape(-1).long()] = Xp
             out.append(phys)
         newK.append(out[0])
@@ -271,3 +271,65 @@ def query_group(inp, layer, step, b, h_kv):
     g = inp.w.g
     qg = inp.q[layer, step, b, h_kv * g:(h_kv + 1) * g]
     return qg.float().cpu().numpy().astype(np.float64)
+
+
+def random_inputs(batch, hq, hkv, d, lens, dtype="bf16", paged=False, page_size=16, seed=0,
+                  grid=True, layers=1, steps=1, key_scale=1.0, device="cpu", spare_pages=3):
+    """Unstructured seeded cache for parity tests: N(0, key_scale^2) keys,
+    N(0, 1) values and queries, optionally rounded to the j/16 grid.  Sequence
+    b holds lens[b] valid tokens at step 0 (step j holds lens[b] + j); every
+    cache row beyond the valid tokens, and every unused page, is NaN so that a
+    read past the end shows up in the results."""
+    lens = tuple(int(x) for x in lens)
+    w = Workload(f"random-{seed}", dtype, layers, batch, hq, hkv, d,
+                 tuple(n - 1 for n in lens), steps, k=0, window=0, sink=0, s=1, G=1,
+                 paged=paged, page_size=page_size, seed=seed)
+    dt = torch.float32 if dtype == "f32" else torch.bfloat16
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed)
+    cap = max(max(lens) + steps - 1, 1)
+
+    def draw(*shape, scale=1.0):
+        x = torch.randn(*shape, generator=gen) * scale
+        return _round_grid(x) if grid else x
+
+    q = draw(layers, steps, batch, hq, d).to(dt)
+    valid = torch.zeros(batch, 1, cap, 1, dtype=torch.bool)
+    for b, n in enumerate(lens):
+        valid[b, :, : n + steps - 1] = True
+    Ks, Vs = [], []
+    for _ in range(layers):
+        K = draw(batch, hkv, cap, d, scale=key_scale)
+        V = draw(batch, hkv, cap, d)
+        nan = torch.tensor(float("nan"))
+        Ks.append(torch.where(valid, K, nan).to(dt))
+        Vs.append(torch.where(valid, V, nan).to(dt))
+    inp = Inputs(w.replace(n_ctx=tuple(n - 1 for n in lens)), q, Ks, Vs, n_ctx=tuple(n - 1 for n in lens))
+    if paged:
+        ps = page_size
+        max_pages = (cap + ps - 1) // ps
+        P = batch * max_pages + spare_pages
+        perm = torch.randperm(P, generator=gen)
+        table = perm[: batch * max_pages].reshape(batch, max_pages).to(torch.int32)
+        pad = max_pages * ps - cap
+        newK, newV = [], []
+        for Kc, Vc in zip(inp.K, inp.V):
+            out = []
+            for X in (Kc, Vc):
+                Xp = torch.nn.functional.pad(X.float(), (0, 0, 0, pad), value=float("nan")) if pad else X.float()
+                Xp = Xp.reshape(batch, hkv, max_pages, ps, d).permute(0, 2, 1, 3, 4).reshape(-1, hkv, ps, d)
+                phys = torch.full((P, hkv, ps, d), float("nan"))
+                phys[table.reshape(-1).long()] = Xp
+                out.append(phys.to(dt))
+            newK.append(out[0])
+            newV.append(out[1])
+        inp.K, inp.V = newK, newV
+        inp.block_table = table
+        inp.num_pages = P
+    if device != "cpu":
+        inp.q = inp.q.to(device)
+        inp.K = [x.to(device) for x in inp.K]
+        inp.V = [x.to(device) for x in inp.V]
+        if inp.block_table is not None:
+            inp.block_table = inp.block_table.to(device)
+    return inp

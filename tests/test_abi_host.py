@@ -1,0 +1,211 @@
+"""The C-ABI library on the host: it loads, exports every symbol the header
+declares, its pure host logic matches the oracle's definitions, and every
+validation error returns its status before any device work (so these tests
+need no GPU; no call here reaches a kernel launch)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2602_08329_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "prhs.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2602_08329_amd import build
+        build.build()
+    return B.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(prhs_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_abi_version(L):
+    assert L.prhs_abi_version() == 1
+
+
+def test_schedule_matches_oracle(L):
+    for s in (1, 2, 4, 8):
+        for G in (1, 2, 4):
+            p = B.params(k=8, refresh_every=s, layer_group=G)
+            for j in range(20):
+                for l in range(9):
+                    got = B.prhs_schedule(j, l, p)
+                    assert got == (B.PRHS_REFRESH if O.is_refresh(j, l, s, G) else B.PRHS_REUSE)
+    assert B.prhs_schedule(-1, 0, B.params()) == -1
+    assert B.prhs_schedule(0, 0, B.params(refresh_every=0)) == -1
+
+
+def test_max_topk_matches_oracle_budget(L):
+    rng = np.random.default_rng(0)
+    for _ in range(300):
+        n = int(rng.integers(0, 5000))
+        sink, window = int(rng.integers(0, 20)), int(rng.integers(0, 300))
+        if rng.random() < 0.5:
+            p = B.params(k=int(rng.integers(0, 3000)), sink=sink, window=window)
+            kb = p.k
+        else:
+            num, den = int(rng.integers(0, 5)), int(rng.integers(1, 40))
+            p = B.params(k_num=num, k_den=den, sink=sink, window=window)
+            kb = O.budget_k(n, k_num=num, k_den=den)
+        se, ws = O.region_bounds(n, sink, window)
+        assert B.prhs_max_topk(p, n) == min(kb, ws - se)
+
+
+def test_set_capacity_bounds_every_schedule_set(L):
+    # the capacity covers the largest anchor or shared set the oracle builds
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        n_ctx = int(rng.integers(1, 300))
+        s = int(rng.integers(1, 9))
+        sink, window, k = int(rng.integers(0, 8)), int(rng.integers(0, 40)), int(rng.integers(0, 80))
+        r = int(rng.integers(0, 3))
+        p = B.params(k=k, sink=sink, window=window, dilate_r=r, refresh_every=s)
+        cap = B.prhs_set_capacity(p, n_ctx + s)
+        sigma = rng.integers(-5, 5, size=n_ctx + s).astype(float)
+        for j0 in range(s):
+            n0 = n_ctx + 1
+            S = O.topk_middle(sigma, n0, k, sink, window)
+            m = O.dilation_m(k, len(S))
+            assert len(O.anchor_set(S, n0, sink, window)) <= cap
+            for j in range(s):
+                assert len(O.reuse_set(S, m, r, n0, n0 + j, sink, window)) <= cap
+
+
+def _kv(**over):
+    f = dict(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128, dtype=B.PRHS_BF16,
+             layout=B.PRHS_KV_CONTIGUOUS, capacity=1024, page_size=16, max_pages=64,
+             num_pages=128, k=0x1000, v=0x2000, block_table=None, seq_lens=0x3000,
+             max_seq_len=1000)
+    f.update(over)
+    return B.PrhsKv(**f)
+
+
+def _select(L, kv, p, k_cap=64, set_cap=200, ws_bytes=None, q=0x4000):
+    n = ctypes.c_size_t(0)
+    L.prhs_workspace_size(B.PRHS_OP_SELECT, ctypes.byref(kv), ctypes.byref(p), 0, ctypes.byref(n))
+    wsb = n.value if ws_bytes is None else ws_bytes
+    return L.prhs_select(ctypes.byref(kv), q, ctypes.byref(p), 0x5000, 0x6000, k_cap, 0x7000,
+                         0x8000, set_cap, 0x9000, wsb, None)
+
+
+@pytest.mark.parametrize("over,status,msg", [
+    (dict(num_q_heads=6, num_kv_heads=4), B.PRHS_E_INVALID, "multiple"),
+    (dict(num_q_heads=34, num_kv_heads=2), B.PRHS_E_UNSUPPORTED, "<= 16"),
+    (dict(head_dim=96), B.PRHS_E_UNSUPPORTED, "head_dim"),
+    (dict(dtype=7), B.PRHS_E_UNSUPPORTED, "dtype"),
+    (dict(capacity=10), B.PRHS_E_INVALID, "capacity"),
+    (dict(layout=B.PRHS_KV_PAGED, block_table=None), B.PRHS_E_INVALID, "block_table"),
+    (dict(layout=B.PRHS_KV_PAGED, block_table=0xA000, max_pages=2), B.PRHS_E_INVALID, "max_pages"),
+    (dict(layout=5), B.PRHS_E_UNSUPPORTED, "layout"),
+    (dict(max_seq_len=1 << 22, capacity=1 << 22), B.PRHS_E_UNSUPPORTED, "max_seq_len"),
+    (dict(k=None), B.PRHS_E_INVALID, "NULL"),
+    (dict(seq_lens=None), B.PRHS_E_INVALID, "seq_lens"),
+    (dict(batch=-1), B.PRHS_E_INVALID, "batch"),
+])
+def test_select_shape_validation(L, over, status, msg):
+    st = _select(L, _kv(**over), B.params(k=32, sink=4, window=64))
+    assert st == status
+    assert msg in L.prhs_last_error().decode()
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(k=-1), B.PRHS_E_INVALID),
+    (dict(refresh_every=0), B.PRHS_E_INVALID),
+    (dict(layer_group=0), B.PRHS_E_INVALID),
+    (dict(sink=-2), B.PRHS_E_INVALID),
+    (dict(window=-1), B.PRHS_E_INVALID),
+    (dict(dilate_r=-1), B.PRHS_E_INVALID),
+    (dict(k_num=-1, k_den=20), B.PRHS_E_INVALID),
+])
+def test_select_param_validation(L, over, status):
+    base = dict(k=32, sink=4, window=64)
+    base.update(over)
+    assert _select(L, _kv(), B.params(**base)) == status
+
+
+def test_select_capacity_and_workspace_errors(L):
+    p = B.params(k=32, sink=4, window=64)
+    assert _select(L, _kv(), p, k_cap=31) == B.PRHS_E_CAPACITY
+    assert "k_cap" in L.prhs_last_error().decode()
+    assert _select(L, _kv(), p, set_cap=99) == B.PRHS_E_CAPACITY
+    assert _select(L, _kv(), p, ws_bytes=100) == B.PRHS_E_WORKSPACE
+    assert _select(L, _kv(), p, q=None) == B.PRHS_E_INVALID
+    big = B.params(k=20000, sink=0, window=0)
+    kv = _kv(capacity=30000, max_seq_len=30000)
+    assert _select(L, kv, big, k_cap=20000, set_cap=30000) == B.PRHS_E_UNSUPPORTED
+
+
+def test_attention_validation(L):
+    kv = _kv()
+    n = ctypes.c_size_t(0)
+    assert L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 300,
+                                 ctypes.byref(n)) == 0
+    assert n.value > 0
+    st = L.prhs_sparse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 300, 0.1, 0x4, None, 0x5,
+                                   n.value - 1, None)
+    assert st == B.PRHS_E_WORKSPACE
+    st = L.prhs_sparse_decode_attn(ctypes.byref(kv), 0x1, None, 0x3, 300, 0.1, 0x4, None, 0x5,
+                                   n.value, None)
+    assert st == B.PRHS_E_INVALID
+    st = L.prhs_sparse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 300, float("nan"), 0x4, None,
+                                   0x5, n.value, None)
+    assert st == B.PRHS_E_INVALID
+    st = L.prhs_dense_decode_attn(ctypes.byref(_kv(head_dim=80)), 0x1, 0.1, 0x4, None, 0x5, 1 << 30,
+                                  None)
+    assert st == B.PRHS_E_UNSUPPORTED
+    st = L.prhs_dense_decode_attn(ctypes.byref(kv), None, 0.1, 0x4, None, 0x5, 1 << 30, None)
+    assert st == B.PRHS_E_INVALID
+
+
+def test_dilate_validation_and_empty_batch(L):
+    p = B.params(k=8)
+    assert L.prhs_dilate_reuse(ctypes.byref(p), 2, 0, 1, 1, 8, 1, 1, 1, 1, 8, None) == B.PRHS_E_INVALID
+    assert L.prhs_dilate_reuse(ctypes.byref(p), 2, 2, None, 1, 8, 1, 1, 1, 1, 8, None) == B.PRHS_E_INVALID
+    # an empty batch is a no-op that never touches the device
+    assert L.prhs_dilate_reuse(ctypes.byref(p), 0, 2, None, None, 8, None, None, None, None, 8,
+                               None) == B.PRHS_OK
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert _select(L, kv0, B.params(k=8, window=4), q=None) == B.PRHS_OK
+
+
+def test_workspace_size_errors(L):
+    n = ctypes.c_size_t(7)
+    assert L.prhs_workspace_size(99, None, None, 0, ctypes.byref(n)) == B.PRHS_E_INVALID
+    assert L.prhs_workspace_size(B.PRHS_OP_SELECT, None, None, 0, ctypes.byref(n)) == B.PRHS_E_INVALID
+    assert L.prhs_workspace_size(B.PRHS_OP_DILATE_REUSE, None, None, 0, ctypes.byref(n)) == B.PRHS_OK
+    assert n.value == 0
+
+
+def test_binding_marshalling_checks():
+    # shape and dtype checks of the Python layer run before the C call
+    K = torch.zeros(1, 2, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        B.KV(K, K.float(), torch.zeros(1, dtype=torch.int32), 8, 2)
+    with pytest.raises(ValueError):
+        B.KV(K, K, torch.zeros(2, dtype=torch.int32), 8, 2)
+    kv = B.KV(K, K, torch.zeros(1, dtype=torch.int32), 8, 2)
+    with pytest.raises(ValueError):
+        B.prhs_sparse_decode_attn(kv, torch.zeros(1, 2, 64, dtype=torch.float32),
+                                  torch.zeros(1, 2, 8, dtype=torch.int32),
+                                  torch.zeros(1, 2, dtype=torch.int32), 0.1,
+                                  torch.zeros(1, 2, 64), None, torch.zeros(8, dtype=torch.uint8))

@@ -1,0 +1,302 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Index sets are compared bit for bit (inputs on the j/16 grid make GPU fp32
+scores exact, see the synth module); attention outputs per (batch, query head)
+must satisfy |y_gpu - y_ref|_inf / |y_ref|_inf <= 2e-3 for bf16 inputs and
+1e-5 for fp32 inputs, with y_ref the fp64 oracle over the same set.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2602_08329_amd import binding as B
+from paper_2602_08329_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TOL = {"bf16": 2e-3, "f32": 1e-5}
+LSE_TOL = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def lens_tensor(lens):
+    return torch.tensor(list(lens), dtype=torch.int32, device=DEV)
+
+
+def kv_for(inp, lens, layer=0):
+    t = lens_tensor(lens)
+    table = inp.block_table
+    return B.KV(inp.K[layer], inp.V[layer], t, inp.w.capacity, inp.w.hq, table), t
+
+
+def assert_close(y, lse, y_ref, lse_ref, tol, label):
+    y = np.asarray(y, dtype=np.float64)
+    if not np.isfinite(lse_ref):
+        assert np.all(y == 0.0), f"{label}: empty set must give zeros"
+        assert lse == -math.inf, f"{label}: empty set must give lse=-inf"
+        return
+    den = np.abs(y_ref).max()
+    err = np.abs(y - y_ref).max() / (den if den > 0 else 1.0)
+    assert err <= tol, f"{label}: rel err {err:.3e} > {tol}"
+    assert abs(lse - lse_ref) <= LSE_TOL * max(1.0, abs(lse_ref)), \
+        f"{label}: lse {lse} vs {lse_ref}"
+
+
+def run_dense(inp, lens, layer=0, step=0):
+    kv, _ = kv_for(inp, lens, layer)
+    w = inp.w
+    out = torch.full((w.batch, w.hq, w.d), float("nan"), device=DEV)
+    lse = torch.full((w.batch, w.hq), float("nan"), device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_DENSE_ATTN, kv), DEV)
+    B.prhs_dense_decode_attn(kv, inp.q[layer, step], 1 / math.sqrt(w.d), out, lse, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy()
+
+
+def run_sparse(inp, lens, sets, set_cap, layer=0, step=0):
+    w = inp.w
+    kv, _ = kv_for(inp, lens, layer)
+    idx = torch.zeros(w.batch, w.hkv, set_cap, dtype=torch.int32)
+    ln = torch.zeros(w.batch, w.hkv, dtype=torch.int32)
+    for (b, g), S in sets.items():
+        idx[b, g, : len(S)] = torch.tensor(S, dtype=torch.int32)
+        ln[b, g] = len(S)
+    idx, ln = idx.to(DEV), ln.to(DEV)
+    out = torch.full((w.batch, w.hq, w.d), float("nan"), device=DEV)
+    lse = torch.full((w.batch, w.hq), float("nan"), device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv, None, set_cap), DEV)
+    B.prhs_sparse_decode_attn(kv, inp.q[layer, step], idx, ln, 1 / math.sqrt(w.d), out, lse, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy()
+
+
+DENSE_CASES = [
+    # dtype, d, paged, Hq, Hkv, lens
+    ("bf16", 128, False, 8, 2, (1, 37, 300, 1025)),
+    ("bf16", 64, True, 4, 4, (700, 5, 64)),
+    ("bf16", 128, True, 32, 8, (4100, 129)),
+    ("bf16", 128, False, 16, 1, (2000,)),
+    ("f32", 64, False, 4, 4, (129, 3000)),
+    ("f32", 128, True, 4, 2, (17, 450, 33)),
+]
+
+
+@pytest.mark.parametrize("dtype,d,paged,hq,hkv,lens", DENSE_CASES)
+def test_dense_attention(dtype, d, paged, hq, hkv, lens):
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=11 + d + len(lens), grid=False, key_scale=1.5, device=DEV)
+    y, lse = run_dense(inp, lens)
+    g = hq // hkv
+    for b, n in enumerate(lens):
+        for hk in range(hkv):
+            K, V = synth.gather_unit(inp, 0, b, hk, n)
+            Qg = synth.query_group(inp, 0, 0, b, hk)
+            for j in range(g):
+                h = hk * g + j
+                yr, lr = O.dense_attention(Qg[j], K, V)
+                assert_close(y[b, h], lse[b, h], yr, lr, TOL[dtype], f"b{b} h{h} n{n}")
+
+
+def test_dense_zero_length_gives_empty():
+    inp = synth.random_inputs(2, 4, 2, 128, (50, 70), seed=5, device=DEV)
+    y, lse = run_dense(inp, (0, 70))
+    assert np.all(y[0] == 0) and np.all(lse[0] == -np.inf)
+    assert np.isfinite(y[1]).all()
+
+
+SPARSE_CASES = [
+    ("bf16", 128, False, 8, 2, (900, 77, 2500)),
+    ("bf16", 128, True, 32, 8, (3000, 1200)),
+    ("bf16", 64, False, 4, 4, (500, 640)),
+    ("f32", 64, True, 4, 4, (1000, 40)),
+]
+
+
+@pytest.mark.parametrize("dtype,d,paged,hq,hkv,lens", SPARSE_CASES)
+def test_sparse_attention_oracle_sets(dtype, d, paged, hq, hkv, lens):
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=23 + d, grid=False, key_scale=1.5, device=DEV)
+    rng = np.random.default_rng(7)
+    sets = {}
+    for b, n in enumerate(lens):
+        for g in range(hkv):
+            kind = (b * hkv + g) % 4
+            if kind == 0:
+                S = []                                    # empty set
+            elif kind == 1:
+                S = list(range(n))                        # everything
+            else:
+                size = int(rng.integers(1, n + 1))
+                S = sorted(rng.choice(n, size=size, replace=False).tolist())
+            sets[(b, g)] = S
+    set_cap = max(len(s) for s in sets.values()) + 5
+    y, lse = run_sparse(inp, lens, sets, set_cap)
+    gq = hq // hkv
+    for (b, g), S in sets.items():
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, 0, b, g)
+        for j in range(gq):
+            yr, lr = O.sparse_attention(Qg[j], K, V, S)
+            assert_close(y[b, g * gq + j], lse[b, g * gq + j], yr, lr, TOL[dtype],
+                         f"b{b} g{g} |S|={len(S)}")
+
+
+def test_sparse_full_set_matches_dense_kernel():
+    lens = (1500, 333)
+    inp = synth.random_inputs(2, 8, 2, 128, lens, seed=31, grid=False, device=DEV)
+    sets = {(b, g): list(range(lens[b])) for b in range(2) for g in range(2)}
+    ys, ls = run_sparse(inp, lens, sets, 1600)
+    yd, ld = run_dense(inp, lens)
+    for b in range(2):
+        for h in range(8):
+            den = np.abs(yd[b, h]).max()
+            assert np.abs(ys[b, h] - yd[b, h]).max() / den <= 2e-3
+            assert abs(ls[b, h] - ld[b, h]) <= 1e-4 * max(1, abs(ld[b, h]))
+
+
+# ---------------------------------------------------------------- selection
+
+def run_select(inp, lens, p, layer=0, step=0):
+    w = inp.w
+    kv, _ = kv_for(inp, lens, layer)
+    k_cap = max(1, B.prhs_max_topk(p, w.capacity))
+    set_cap = max(1, min(w.capacity, p.sink + k_cap + p.window))
+    topk = torch.full((w.batch, w.hkv, k_cap), -7, dtype=torch.int32, device=DEV)
+    tlen = torch.full((w.batch, w.hkv), -7, dtype=torch.int32, device=DEV)
+    sidx = torch.full((w.batch, w.hkv, set_cap), -7, dtype=torch.int32, device=DEV)
+    slen = torch.full((w.batch, w.hkv), -7, dtype=torch.int32, device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv, p), DEV)
+    ws.fill_(0xAB)   # the workspace needs no initialisation
+    B.prhs_select(kv, inp.q[layer, step], p, topk, tlen, sidx, slen, ws)
+    torch.cuda.synchronize()
+    return topk.cpu().numpy(), tlen.cpu().numpy(), sidx.cpu().numpy(), slen.cpu().numpy()
+
+
+def oracle_select(inp, lens, p, layer=0, step=0):
+    res = {}
+    for b, n0 in enumerate(lens):
+        for g in range(inp.w.hkv):
+            K, _ = synth.gather_unit(inp, layer, b, g, n0)
+            Qg = synth.query_group(inp, layer, step, b, g)
+            kb = O.budget_k(n0, p.k, p.k_num, p.k_den)
+            S = O.topk_middle(O.ranking_scores(Qg, K), n0, kb, p.sink, p.window)
+            res[(b, g)] = (S, O.anchor_set(S, n0, p.sink, p.window))
+    return res
+
+
+def check_select(inp, lens, p, layer=0, step=0):
+    topk, tlen, sidx, slen = run_select(inp, lens, p, layer, step)
+    ref = oracle_select(inp, lens, p, layer, step)
+    for (b, g), (S, C) in ref.items():
+        assert tlen[b, g] == len(S), f"b{b} g{g}: topk_len {tlen[b, g]} != {len(S)}"
+        assert np.array_equal(topk[b, g, : len(S)], S), f"b{b} g{g}: top-k order differs"
+        assert slen[b, g] == len(C), f"b{b} g{g}: set_len {slen[b, g]} != {len(C)}"
+        assert np.array_equal(sidx[b, g, : len(C)], C), f"b{b} g{g}: anchor set differs"
+    return topk, tlen
+
+
+SELECT_CASES = [
+    # name, dtype, d, paged, hq, hkv, lens, params
+    ("ragged-gqa", "bf16", 128, False, 8, 2, (5000, 2100, 70), dict(k=300, sink=4, window=64)),
+    ("mha-d64-paged", "bf16", 64, True, 4, 4, (3000, 1500), dict(k=100, sink=4, window=32)),
+    ("g8", "bf16", 128, False, 16, 2, (4500,), dict(k=64, sink=0, window=0)),
+    ("k-ge-middle", "bf16", 128, False, 4, 2, (400, 900), dict(k=2000, sink=4, window=16)),
+    ("k-zero", "bf16", 128, False, 4, 2, (400, 900), dict(k=0, sink=4, window=16)),
+    ("short-seqs", "bf16", 128, False, 4, 2, (3, 20, 21, 22), dict(k=5, sink=4, window=16)),
+    ("ratio", "bf16", 128, True, 8, 2, (9000, 4100), dict(k_num=1, k_den=20, sink=4, window=128)),
+    ("f32", "f32", 64, False, 4, 4, (1025, 300), dict(k=64, sink=4, window=32)),
+    ("f32-paged-gqa", "f32", 128, True, 8, 2, (2000,), dict(k=50, sink=2, window=8)),
+    ("big-k", "bf16", 128, False, 4, 1, (20000,), dict(k=9000, sink=4, window=64)),
+]
+
+
+@pytest.mark.parametrize("name,dtype,d,paged,hq,hkv,lens,pk", SELECT_CASES,
+                         ids=[c[0] for c in SELECT_CASES])
+def test_select_bit_exact(name, dtype, d, paged, hq, hkv, lens, pk):
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=41 + len(name), grid=True, device=DEV)
+    check_select(inp, lens, B.params(**pk))
+
+
+def test_select_all_ties_lowest_positions():
+    # every key equal: each score ties, so the top-k are the lowest middle positions
+    lens = (3000, 1800)
+    inp = synth.random_inputs(2, 8, 2, 128, lens, seed=3, grid=True, device=DEV)
+    for K in inp.K:
+        K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, 0.25)))
+    p = B.params(k=200, sink=4, window=64)
+    topk, tlen = check_select(inp, lens, p)
+    assert list(topk[0, 0, :5]) == [4, 5, 6, 7, 8]
+
+
+def test_select_coarse_grid_many_ties():
+    # values in {-1/16, 0, 1/16}: very many exact ties at the threshold
+    lens = (6000, 2500)
+    inp = synth.random_inputs(2, 8, 2, 128, lens, seed=4, grid=True, device=DEV)
+    for t in inp.K + [inp.q]:
+        t.copy_(torch.where(torch.isnan(t), t, torch.clamp(torch.round(t.float()), -1, 1).to(t.dtype) / 16))
+    check_select(inp, lens, B.params(k=500, sink=4, window=64))
+
+
+def test_select_negative_zero_scores():
+    # scores of exactly +0 and -0 rank equal; ties break to the lower position
+    lens = (600,)
+    inp = synth.random_inputs(1, 2, 1, 64, lens, dtype="f32", seed=6, grid=True, device=DEV)
+    q = inp.q
+    q.zero_()
+    q[0, 0, 0, 0, 0] = 1.0
+    q[0, 0, 0, 1, 0] = -1.0      # second head of the group: scores are -k
+    K = inp.K[0]
+    K[0, 0, :600, 0] = 0.0       # every key scores +0 on head 0 and -0 on head 1
+    K[0, 0, 100, 0] = -0.0
+    check_select(inp, lens, B.params(k=10, sink=4, window=8))
+
+
+def test_select_reuses_workspace_across_calls():
+    lens = (3000, 1000)
+    inp = synth.random_inputs(2, 8, 2, 128, lens, seed=8, grid=True, layers=2, device=DEV)
+    p = B.params(k=120, sink=4, window=32)
+    for layer in (0, 1, 0):
+        check_select(inp, lens, p, layer=layer)
+
+
+# ---------------------------------------------------------------- dilation / reuse
+
+def test_dilate_reuse_bit_exact():
+    lens0 = (5000, 2000, 30)
+    steps = 6
+    inp = synth.random_inputs(3, 8, 2, 128, lens0, seed=9, grid=True, steps=steps, device=DEV)
+    for pk in (dict(k=300, sink=4, window=64, dilate_r=1),
+               dict(k=90, sink=0, window=0, dilate_r=2, dilate_m=40),
+               dict(k=300, sink=4, window=64, dilate_r=0),
+               dict(k_num=1, k_den=20, sink=4, window=16, dilate_r=1)):
+        p = B.params(refresh_every=steps, **pk)
+        topk, tlen, _, _ = run_select(inp, lens0, p)
+        ref = oracle_select(inp, lens0, p)
+        topk_d = torch.tensor(topk, device=DEV)
+        tlen_d = torch.tensor(tlen, device=DEV)
+        set_cap = B.prhs_set_capacity(p, inp.w.capacity)
+        anchor = lens_tensor(lens0)
+        for j in range(steps):
+            lens = tuple(n + j for n in lens0)
+            sidx = torch.full((3, 2, set_cap), -7, dtype=torch.int32, device=DEV)
+            slen = torch.full((3, 2), -7, dtype=torch.int32, device=DEV)
+            B.prhs_dilate_reuse(p, topk_d, tlen_d, anchor, lens_tensor(lens), sidx, slen)
+            torch.cuda.synchronize()
+            sidx, slen = sidx.cpu().numpy(), slen.cpu().numpy()
+            for (b, g), (S, _) in ref.items():
+                kb = O.budget_k(lens0[b], p.k, p.k_num, p.k_den)
+                m = O.dilation_m(kb, len(S), p.dilate_m)
+                R = O.reuse_set(S, m, p.dilate_r, lens0[b], lens[b], p.sink, p.window)
+                assert slen[b, g] == len(R), f"step {j} b{b} g{g}"
+                assert np.array_equal(sidx[b, g, : len(R)], R), f"step {j} b{b} g{g}"

@@ -1,0 +1,173 @@
+"""GPU parity of the whole decode schedule (refresh, reuse across steps and
+layer groups, sparse attention) against the oracle's DecodeOracle, on the
+paper-shaped synthetic workloads: cut-down versions over every (layer, step),
+and the full-size shapes (the launch configuration the benchmark times) on
+refresh and reuse steps with every set compared and sampled outputs."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2602_08329_amd import binding as B
+from paper_2602_08329_amd import synth
+from paper_2602_08329_amd.schedule import DecodeRunner
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TOL = {"bf16": 2e-3, "f32": 1e-5}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def rel_err(y, yr):
+    den = np.abs(yr).max()
+    return np.abs(np.asarray(y, np.float64) - yr).max() / (den if den > 0 else 1.0)
+
+
+class UnitCache:
+    """fp64 host copies of the (layer, unit) caches that outputs are checked on."""
+
+    def __init__(self, inp):
+        self.inp = inp
+        self.c = {}
+
+    def get(self, l, b, g):
+        key = (l, b, g)
+        if key not in self.c:
+            n = self.inp.w.n_ctx[b] + self.inp.w.steps
+            self.c[key] = synth.gather_unit(self.inp, l, b, g, n)
+        return self.c[key]
+
+
+def run_schedule(w, steps, units_out, units_set=None, layers=None):
+    """Runs the runner and the oracle side by side; compares the sets of
+    units_set (default: all units) and the outputs of units_out at every
+    (layer, step).  The oracle reads a unit's keys only where the schedule
+    refreshes."""
+    inp = synth.generate(w, device=DEV, layers=layers)
+    L = len(inp.K)
+    run = DecodeRunner(inp, DEV)
+    cache = UnitCache(inp)
+    all_units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
+    units_set = all_units if units_set is None else units_set
+    dec = {u: O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k, k_num=w.k_num,
+                             k_den=w.k_den, dilate_m=w.dilate_m) for u in units_set}
+    out = torch.empty(w.batch, w.hq, w.d, device=DEV)
+    lse = torch.empty(w.batch, w.hq, device=DEV)
+    worst = 0.0
+    for j in steps:
+        run.selection_step(j)
+        for l in range(L):
+            out.fill_(float("nan"))
+            run.attend(l, j, out, lse)
+            s_idx, s_len = run.set_for(l, j)
+            torch.cuda.synchronize()
+            s_idx, s_len = s_idx.cpu().numpy(), s_len.cpu().numpy()
+            y, ls = out.cpu().numpy(), lse.cpu().numpy()
+            refresh = O.is_refresh(j, l, w.s, w.G)
+            for (b, g) in units_set:
+                n = w.n_ctx[b] + j + 1
+                Qg = synth.query_group(inp, l, j, b, g)
+                K_sel = synth.gather_unit(inp, l, b, g, n)[0] if refresh else None
+                S = dec[(b, g)].step_set(l, j, Qg, K_sel, n)
+                assert s_len[b, g] == len(S), f"l{l} j{j} b{b} g{g}: |set| {s_len[b, g]} != {len(S)}"
+                assert np.array_equal(s_idx[b, g, : len(S)], S), f"l{l} j{j} b{b} g{g}: set differs"
+                if (b, g) in units_out:
+                    K, V = cache.get(l, b, g)
+                    for i in range(w.g):
+                        h = g * w.g + i
+                        yr, lr = O.sparse_attention(Qg[i], K[:n], V[:n], S)
+                        e = rel_err(y[b, h], yr)
+                        worst = max(worst, e)
+                        assert e <= TOL[w.dtype], f"l{l} j{j} b{b} h{h}: rel err {e:.3e}"
+                        assert abs(ls[b, h] - lr) <= 1e-4 * max(1, abs(lr))
+    print(f"{w.name}: worst relative error {worst:.3e}")
+    return worst
+
+
+def test_config0_full_schedule():
+    w = synth.workload(0)
+    units = {(0, g) for g in range(w.hkv)}
+    run_schedule(w, range(w.steps), units)
+
+
+def test_config1_cut_schedule():
+    w = synth.workload(1).replace(layers=8, batch=2, n_ctx=(2048, 1500))
+    units = {(b, g) for b in range(2) for g in (0, 17, 31)}
+    run_schedule(w, range(w.steps), units)
+
+
+def test_config2_cut_schedule():
+    w = synth.workload(2).replace(layers=8, batch=2, n_ctx=(5000, 7777))
+    units = {(b, g) for b in range(2) for g in range(8)}
+    run_schedule(w, range(w.steps), units)
+
+
+def test_config3_cut_schedule_paged():
+    w = synth.workload(3).replace(layers=2, n_ctx=(20000,), heavy=100)
+    units = {(0, g) for g in range(8)}
+    run_schedule(w, range(w.steps), units)
+
+
+def test_config4_cut_schedule_ragged():
+    w = synth.workload(4, batch=4, nmax=4096).replace(layers=2)
+    units = {(b, g) for b in range(4) for g in (0, 5)}
+    run_schedule(w, range(w.steps), units)
+
+
+# Full-size shapes: the benchmark's launch configuration per layer; a refresh
+# step, a reuse step and the last step of a refresh block.
+
+def test_config1_full_size():
+    w = synth.workload(1)
+    units = {(0, 0), (3, 9), (7, 31)}
+    run_schedule(w, (0, 1, 3), units, layers=4)
+
+
+def test_config2_full_size():
+    w = synth.workload(2)
+    units = {(0, 0), (2, 5), (3, 7)}
+    run_schedule(w, (0, 1, 7), units, layers=4)
+
+
+def test_config3_full_size_paged():
+    w = synth.workload(3)
+    units = {(0, 0), (0, 7)}
+    run_schedule(w, (0, 1, 7), units, layers=1)
+
+
+@pytest.mark.parametrize("batch,nmax", [(16, 16384), (64, 8192)])
+def test_config4_full_size(batch, nmax):
+    w = synth.workload(4, batch=batch, nmax=nmax)
+    units = {(0, 0), (batch - 1, 7)}
+    sets = [(b, g) for b in range(0, batch, max(1, batch // 8)) for g in (0, 3, 7)]
+    run_schedule(w, (0, 1, 3), units, units_set=sorted(set(sets) | units), layers=1)
+
+
+def test_dense_full_size_config2_sampled():
+    # the dense baseline at 32k context: sampled (batch, head) outputs
+    w = synth.workload(2)
+    inp = synth.generate(w, device=DEV, layers=1)
+    run = DecodeRunner(inp, DEV)
+    out = torch.empty(w.batch, w.hq, w.d, device=DEV)
+    lse = torch.empty(w.batch, w.hq, device=DEV)
+    j = 5
+    run.dense(0, j, out, lse)
+    torch.cuda.synchronize()
+    y, ls = out.cpu().numpy(), lse.cpu().numpy()
+    for (b, h) in [(0, 0), (1, 13), (3, 31)]:
+        g = h // w.g
+        n = w.n_ctx[b] + j + 1
+        K, V = synth.gather_unit(inp, 0, b, g, n)
+        q = synth.query_group(inp, 0, j, b, g)[h % w.g]
+        yr, lr = O.dense_attention(q, K, V)
+        assert rel_err(y[b, h], yr) <= TOL["bf16"]
+        assert abs(ls[b, h] - lr) <= 1e-4 * max(1, abs(lr))
