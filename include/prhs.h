@@ -143,8 +143,12 @@ int32_t prhs_schedule(int32_t step, int32_t layer, const prhs_params* params);
  *   sigma_i = max over the g-th group's query heads h of q[b][h] . k_i (raw
  *   dot product, computed in fp32) for i in the middle range
  *   [min(sink, n0), max(min(sink, n0), n0 - window));
- *   topk_idx[b][g][0 .. topk_len) = the min(k_b, middle length) positions of
- *   largest sigma, ordered by (sigma descending, position ascending);
+ *   S* = the min(k_b, middle length) positions of largest sigma, ties going
+ *   to the lower position (total order: sigma descending, position
+ *   ascending); with m = min(dilate_m or floor(k_b / 3), |S*|),
+ *   topk_idx[b][g][0 .. m) = the m highest-ranked members of S* and
+ *   topk_idx[b][g][m .. topk_len) = the others, each part in ascending
+ *   position order (only the set of the top m matters to the dilation);
  *   set_idx[b][g][0 .. set_len) = sink U top-k U [n0 - window, n0),
  *   ascending and without duplicates (the critical set C_t).
  * q: [batch][num_q_heads][head_dim] in kv->dtype.
@@ -166,7 +170,8 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
  *
  * For every (b, g), with n0 = anchor_lens[b] (the anchor's length at its
  * refresh), n = seq_lens[b] >= n0, S* = topk_idx[b][g][0 .. topk_len) as
- * returned by prhs_select and m = min(dilate_m or floor(k_b / 3), topk_len):
+ * returned by prhs_select with the same params, whose first
+ * m = min(dilate_m or floor(k_b / 3), topk_len) entries are the top m:
  *   set = [0, min(sink, n0)) U S* U {p + j : p in first m of S*, |j| <= r,
  *         0 <= p + j < n} U [max(min(sink, n0), n0 - window), n),
  * ascending and without duplicates.  The set does not depend on any layer's

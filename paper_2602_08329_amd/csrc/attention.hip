@@ -14,6 +14,14 @@
 // device-scope fences, which on this chip write back and invalidate a whole
 // L2 slice per workgroup.
 //
+// Latency: the workgroup first resolves every list entry of its chunk to a
+// physical row id (index load, and block-table load for paged caches, each
+// issued for the whole chunk at once) and stages the ids in LDS.  Waves then
+// walk 32-row tiles with two register buffers: the 16 K/V loads of the next
+// tile are in flight while the current tile is multiplied.  Loads are issued
+// unconditionally (a missing row reads row 0) and invalid rows are masked
+// afterwards, so no load waits on a branch.
+//
 // bf16 inputs use MFMA for both products of a wave's 32-row tile:
 //   S^T (32 keys x 16 heads) = K_tile . Q^T  (v_mfma_f32_16x16x32_bf16, two 16-row halves)
 //   O^T (d x 16 heads)      += V_tile^T . P^T, P split into bf16 hi + lo parts so
@@ -35,6 +43,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kRowsPerThread = 8;   // staged list entries per thread
+constexpr int kMaxSplits = 4096;
 
 struct AttnArgs {
   KvView kv;
@@ -58,15 +68,41 @@ __device__ __forceinline__ int unit_rows(const AttnArgs& a, int b, int u) {
   return L > a.set_cap ? a.set_cap : L;
 }
 
-// Element offset of the cached row at list position r, or -1 if r is past the
-// list end or names a position outside [0, nb) or outside the cache.
-template <bool DENSE>
-__device__ __forceinline__ int64_t list_row(const AttnArgs& a, const int32_t* idx, int r, int end,
-                                            int nb, int b, int g) {
-  if (r >= end) return -1;
-  const int pos = DENSE ? r : idx[r];
+// Row id (element offset / d) of position pos of (b, kv head g), or -1 when
+// the position lies outside [0, nb) or outside the cache.
+template <bool PAGED>
+__device__ __forceinline__ int32_t phys_row(const KvView& kv, int b, int g, int pos, int nb) {
   if (pos < 0 || pos >= nb) return -1;
-  return kv_row_offset(a.kv, b, g, pos);
+  if (!PAGED) {
+    if (pos >= kv.capacity) return -1;
+    return (b * kv.hkv + g) * kv.capacity + pos;
+  }
+  const int page = pos / kv.page_size;
+  if (page >= kv.max_pages) return -1;
+  const int phys = kv.table[(int64_t)b * kv.max_pages + page];
+  if (phys < 0 || phys >= kv.num_pages) return -1;
+  return (phys * kv.hkv + g) * kv.page_size + (pos - page * kv.page_size);
+}
+
+// Resolves list entries [start, start + n) of the unit to row ids in s_row.
+// All index loads of a thread are issued before any is used, then all table
+// loads: two memory latencies for the whole chunk.  n <= blockDim * 8.
+template <bool DENSE, bool PAGED>
+__device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t* idx, int start, int n,
+                                           int nb, int b, int g, int32_t* s_row) {
+  int pos[kRowsPerThread];
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    const int r = threadIdx.x + k * blockDim.x;
+    pos[k] = -1;
+    if (r < n) pos[k] = DENSE ? start + r : idx[start + r];
+  }
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    const int r = threadIdx.x + k * blockDim.x;
+    if (r < n) s_row[r] = phys_row<PAGED>(a.kv, b, g, pos[k], nb);
+  }
+  __syncthreads();
 }
 
 __device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
@@ -104,28 +140,144 @@ __device__ __forceinline__ uint32_t vrow_elem(const VRow<DB>& v, int e) {
   return (e & 1) ? (w >> 16) : (w & 0xFFFFu);
 }
 
-template <int D, bool DENSE>
-__global__ __launch_bounds__(256) void attn_split_bf16(AttnArgs a) {
+// Registers of one wave's 32-row tile: K operand rows (16s + col), V rows
+// (16s + 4 grp + j) and the validity of the V rows, which are also the rows
+// of the lane's logits.
+template <int D>
+struct Tile {
+  static constexpr int KS = D / 32;
+  static constexpr int DB = D / 16;
+  bf16x8_t kf[2][KS];
+  VRow<DB> vf[2][4];
+  uint32_t ok;
+};
+
+template <int D>
+__device__ __forceinline__ void load_tile(Tile<D>& T, const int32_t* s_row, int r0, int n,
+                                          const __bf16* kb, const __bf16* vb, int col, int grp) {
   constexpr int KS = D / 32;
   constexpr int DB = D / 16;
-  __shared__ float sm_m[4][16];
-  __shared__ float sm_l[4][16];
-  __shared__ float sm_o[4][16][D + 1];
+  T.ok = 0u;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int rk = r0 + 16 * s + col;
+    const int row = rk < n ? s_row[rk] : -1;
+    const uint4* kp = (const uint4*)(kb + (int64_t)(row < 0 ? 0 : row) * D + grp * (D / 4));
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) T.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[kk]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int rv = r0 + 16 * s + grp * 4 + j;
+      const int vrow = rv < n ? s_row[rv] : -1;
+      T.vf[s][j] = load_vrow<DB>(vb + (int64_t)(vrow < 0 ? 0 : vrow) * D + col * DB);
+      if (vrow >= 0) T.ok |= 1u << (s * 4 + j);
+    }
+  }
+}
+
+// Online-softmax state of one wave: lane (col, grp) owns query head col and
+// output dims grp * d/4 .. (grp + 1) * d/4 - 1 via the o[] accumulators.
+template <int D>
+struct WaveState {
+  float m, l;
+  f32x4_t o[D / 16];
+};
+
+template <int D>
+__device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const bf16x8_t* qf,
+                                             float scale_log2) {
+  constexpr int KS = D / 32;
+  constexpr int DB = D / 16;
+  float x[2][4];
+  float mt = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T.kf[s][kk], qf[kk], acc, 0, 0, 0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = (T.ok >> (s * 4 + e)) & 1u;
+      x[s][e] = ok ? acc[e] * scale_log2 : -INFINITY;
+      mt = fmaxf(mt, x[s][e]);
+      if (!ok) {
+#pragma unroll
+        for (int w = 0; w < DB / 2; ++w) T.vf[s][e].w[w] = 0u;
+      }
+    }
+  }
+  mt = fmaxf(mt, __shfl_xor(mt, 16));
+  mt = fmaxf(mt, __shfl_xor(mt, 32));
+  const float m_new = fmaxf(st.m, mt);
+  float alpha = 1.f, psum = 0.f;
+  uint32_t hi[4], lo[4];
+  if (m_new == -INFINITY) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) hi[w] = lo[w] = 0u;
+  } else {
+    alpha = exp2f(st.m - m_new);
+    uint32_t hb[8], lb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float p = exp2f(x[j >> 2][j & 3] - m_new);
+      psum += p;
+      hb[j] = bf16_bits_rne(p);
+      lb[j] = bf16_bits_rne(p - __uint_as_float(hb[j] << 16));
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
+      lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+    }
+  }
+  st.l = st.l * alpha + psum;
+  st.m = m_new;
+  const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+  const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+#pragma unroll
+  for (int blk = 0; blk < DB; ++blk) {
+    st.o[blk] *= alpha;
+    uint32_t aw[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int j0 = 2 * w, j1 = 2 * w + 1;
+      aw[w] = vrow_elem<DB>(T.vf[j0 >> 2][j0 & 3], blk) |
+              (vrow_elem<DB>(T.vf[j1 >> 2][j1 & 3], blk) << 16);
+    }
+    const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
+    st.o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, st.o[blk], 0, 0, 0);
+    st.o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, st.o[blk], 0, 0, 0);
+  }
+}
+
+// Writes out/lse of query head bh from (M, sum, unnormalised numerator).
+__device__ __forceinline__ void write_final(const AttnArgs& a, size_t bh, int D, int dim, float M,
+                                            float num, float den) {
+  a.out[bh * D + dim] = den > 0.f ? num / den : 0.f;
+  if (a.lse && dim == 0) a.lse[bh] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+}
+
+template <int D, bool DENSE, bool PAGED>
+__global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
+  constexpr int KS = D / 32;
+  constexpr int DB = D / 16;
+  extern __shared__ float dyn[];  // [nwaves][G][D + 1] wave outputs
+  __shared__ float sm_m[8][16];
+  __shared__ float sm_l[8][16];
+  __shared__ int32_t s_row[512 * kRowsPerThread];
   const int split = blockIdx.x, u = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = u / hkv, g = u % hkv;
   const int L = unit_rows<DENSE>(a, b, u);
   const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
-    for (int e = threadIdx.x; e < G * D; e += blockDim.x) {
-      const size_t bh = (size_t)b * hq + g * G + e / D;
-      a.out[bh * D + e % D] = 0.f;
-      if (a.lse && e % D == 0) a.lse[bh] = -INFINITY;
-    }
+    for (int e = threadIdx.x; e < G * D; e += blockDim.x)
+      write_final(a, (size_t)b * hq + g * G + e / D, D, e % D, -INFINITY, 0.f, 0.f);
     return;
   }
   if (start >= L) return;
-  const int end = min(L, start + a.chunk);
+  const int n = min(L, start + a.chunk) - start;
   const int nb = kv_seq_len(a.kv, b);
   const int nwaves = blockDim.x >> 6;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -135,116 +287,64 @@ __global__ __launch_bounds__(256) void attn_split_bf16(AttnArgs a) {
   bf16x8_t qf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    if (col < G) {
-      const uint4* qp = (const uint4*)(qb + ((size_t)b * hq + g * G + col) * D + grp * (D / 4));
-      qf[kk] = __builtin_bit_cast(bf16x8_t, qp[kk]);
-    } else {
-      qf[kk] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
-    }
+    const int qh = col < G ? col : 0;
+    const uint4* qp = (const uint4*)(qb + ((size_t)b * hq + g * G + qh) * D + grp * (D / 4));
+    const uint4 v = qp[kk];
+    qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
+  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
+  stage_rows<DENSE, PAGED>(a, idx, start, n, nb, b, g, s_row);
+
   const __bf16* kb = (const __bf16*)a.kv.k;
   const __bf16* vb = (const __bf16*)a.kv.v;
-  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
+  WaveState<D> st;
+  st.m = -INFINITY;
+  st.l = 0.f;
+#pragma unroll
+  for (int i = 0; i < DB; ++i) st.o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t o[DB];
-#pragma unroll
-  for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int t = start + wave * 32; t < end; t += 32 * nwaves) {
-    bf16x8_t kf[2][KS];
-    VRow<DB> vf[2][4];
-    bool vok[2][4];
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int64_t off = list_row<DENSE>(a, idx, t + 16 * s + col, end, nb, b, g);
-      const uint4* kp = (const uint4*)(kb + (off < 0 ? 0 : off) + grp * (D / 4));
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        kf[s][kk] = __builtin_bit_cast(bf16x8_t, off < 0 ? make_uint4(0, 0, 0, 0) : kp[kk]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t vo = list_row<DENSE>(a, idx, t + 16 * s + grp * 4 + j, end, nb, b, g);
-        vok[s][j] = vo >= 0;
-        if (vo >= 0) {
-          vf[s][j] = load_vrow<DB>(vb + vo + col * DB);
-        } else {
-#pragma unroll
-          for (int w = 0; w < DB / 2; ++w) vf[s][j].w[w] = 0u;
-        }
-      }
+  // this wave's tiles: wave, wave + nwaves, ...; the steady-state body always
+  // has a next tile, so its prefetch is unconditional and the compiler can
+  // wait for the current buffer only
+  const int ntiles = (n + 31) >> 5;
+  const int iters = wave < ntiles ? (ntiles - wave + nwaves - 1) / nwaves : 0;
+  if (iters > 0) {
+    Tile<D> A, B;
+    const int step = 32 * nwaves;
+    int r0 = wave * 32;
+    load_tile<D>(A, s_row, r0, n, kb, vb, col, grp);
+    int i = 0;
+    for (; i + 2 < iters; i += 2) {
+      load_tile<D>(B, s_row, r0 + step, n, kb, vb, col, grp);
+      consume_tile<D>(A, st, qf, a.scale_log2);
+      load_tile<D>(A, s_row, r0 + 2 * step, n, kb, vb, col, grp);
+      consume_tile<D>(B, st, qf, a.scale_log2);
+      r0 += 2 * step;
     }
-    float x[2][4];
-    float mt = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s][kk], qf[kk], acc, 0, 0, 0);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[s][e] = vok[s][e] ? acc[e] * a.scale_log2 : -INFINITY;
-        mt = fmaxf(mt, x[s][e]);
-      }
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    float alpha = 1.f, psum = 0.f;
-    uint32_t hi[4], lo[4];
-    if (m_new == -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) hi[w] = lo[w] = 0u;
+    if (i + 1 < iters) {
+      load_tile<D>(B, s_row, r0 + step, n, kb, vb, col, grp);
+      consume_tile<D>(A, st, qf, a.scale_log2);
+      consume_tile<D>(B, st, qf, a.scale_log2);
     } else {
-      alpha = exp2f(m_run - m_new);
-      uint32_t hb[8], lb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p = exp2f(x[j >> 2][j & 3] - m_new);
-        psum += p;
-        hb[j] = bf16_bits_rne(p);
-        lb[j] = bf16_bits_rne(p - __uint_as_float(hb[j] << 16));
-      }
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
-        lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
-      }
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-    const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-#pragma unroll
-    for (int blk = 0; blk < DB; ++blk) {
-      o[blk] *= alpha;
-      uint32_t aw[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const int j0 = 2 * w, j1 = 2 * w + 1;
-        aw[w] = vrow_elem<DB>(vf[j0 >> 2][j0 & 3], blk) | (vrow_elem<DB>(vf[j1 >> 2][j1 & 3], blk) << 16);
-      }
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
-      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
-      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
+      consume_tile<D>(A, st, qf, a.scale_log2);
     }
   }
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
+
+  st.l += __shfl_xor(st.l, 16);
+  st.l += __shfl_xor(st.l, 32);
   if (grp == 0) {
-    sm_m[wave][col] = m_run;
-    sm_l[wave][col] = l_run;
+    sm_m[wave][col] = st.m;
+    sm_l[wave][col] = st.l;
   }
   if (col < G) {
+    float* wo = dyn + ((size_t)wave * G + col) * (D + 1);
 #pragma unroll
     for (int blk = 0; blk < DB; ++blk)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sm_o[wave][col][(grp * 4 + i) * DB + blk] = o[blk][i];
+      for (int i = 0; i < 4; ++i) wo[(grp * 4 + i) * DB + blk] = st.o[blk][i];
   }
   __syncthreads();
   const int nsp = (L + a.chunk - 1) / a.chunk;
-  const bool direct = nsp == 1;
   for (int e = threadIdx.x; e < G * D; e += blockDim.x) {
     const int h = e / D, dim = e - h * D;
     float M = -INFINITY;
@@ -253,14 +353,13 @@ __global__ __launch_bounds__(256) void attn_split_bf16(AttnArgs a) {
     if (M != -INFINITY) {
       for (int w = 0; w < nwaves; ++w) {
         const float f = exp2f(sm_m[w][h] - M);
-        num += f * sm_o[w][h][dim];
+        num += f * dyn[((size_t)w * G + h) * (D + 1) + dim];
         den += f * sm_l[w][h];
       }
     }
     const size_t bh = (size_t)b * hq + g * G + h;
-    if (direct) {
-      a.out[bh * D + dim] = den > 0.f ? num / den : 0.f;
-      if (a.lse && dim == 0) a.lse[bh] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+    if (nsp == 1) {
+      write_final(a, bh, D, dim, M, num, den);
     } else {
       const size_t pidx = bh * a.nsplit + split;
       a.part_o[pidx * D + dim] = num;
@@ -272,23 +371,24 @@ __global__ __launch_bounds__(256) void attn_split_bf16(AttnArgs a) {
   }
 }
 
-template <int D, bool DENSE>
+template <int D, bool DENSE, bool PAGED>
 __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   constexpr int DPL = D / 16;
   __shared__ float sm_m[4], sm_l[4];
   __shared__ float sm_o[4][D];
+  __shared__ int32_t s_row[256 * kRowsPerThread];
   const int split = blockIdx.x, bh = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, g = h / G, u = b * hkv + g;
   const int L = unit_rows<DENSE>(a, b, u);
   const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
-    for (int dim = threadIdx.x; dim < D; dim += blockDim.x) a.out[(size_t)bh * D + dim] = 0.f;
-    if (a.lse && threadIdx.x == 0) a.lse[bh] = -INFINITY;
+    for (int dim = threadIdx.x; dim < D; dim += blockDim.x)
+      write_final(a, bh, D, dim, -INFINITY, 0.f, 0.f);
     return;
   }
   if (start >= L) return;
-  const int end = min(L, start + a.chunk);
+  const int n = min(L, start + a.chunk) - start;
   const int nb = kv_seq_len(a.kv, b);
   const int nwaves = blockDim.x >> 6;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -297,37 +397,41 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   float qv[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) qv[i] = qp[i];
+  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
+  stage_rows<DENSE, PAGED>(a, idx, start, n, nb, b, g, s_row);
   const float* kb = (const float*)a.kv.k;
   const float* vb = (const float*)a.kv.v;
-  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
   float m_run = -INFINITY, l_run = 0.f, o[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) o[i] = 0.f;
-  for (int t = start + wave * 4; t < end; t += 4 * nwaves) {
-    const int64_t off = list_row<DENSE>(a, idx, t + rg, end, nb, b, g);
+  for (int t = wave * 4; t < n; t += 4 * nwaves) {
+    const int r = t + rg;
+    const int row = r < n ? s_row[r] : -1;
+    const float* kp = kb + (int64_t)(row < 0 ? 0 : row) * D + c * DPL;
+    const float* vp = vb + (int64_t)(row < 0 ? 0 : row) * D + c * DPL;
     float kx[DPL], vx[DPL];
 #pragma unroll
     for (int i = 0; i < DPL; ++i) {
-      kx[i] = off >= 0 ? kb[off + c * DPL + i] : 0.f;
-      vx[i] = off >= 0 ? vb[off + c * DPL + i] : 0.f;
+      kx[i] = kp[i];
+      vx[i] = vp[i];
     }
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < DPL; ++i) s = fmaf(qv[i], kx[i], s);
 #pragma unroll
     for (int w = 1; w < 16; w <<= 1) s += __shfl_xor(s, w, 16);
-    const float x = off >= 0 ? s * a.scale_log2 : -INFINITY;
+    const float x = row >= 0 ? s * a.scale_log2 : -INFINITY;
     float mt = fmaxf(x, __shfl_xor(x, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     float alpha = 1.f, p = 0.f;
     if (m_new != -INFINITY) {
       alpha = exp2f(m_run - m_new);
-      p = exp2f(x - m_new);
+      p = row >= 0 ? exp2f(x - m_new) : 0.f;
     }
     l_run = l_run * alpha + p;
 #pragma unroll
-    for (int i = 0; i < DPL; ++i) o[i] = o[i] * alpha + p * vx[i];
+    for (int i = 0; i < DPL; ++i) o[i] = o[i] * alpha + (row >= 0 ? p * vx[i] : 0.f);
     m_run = m_new;
   }
 #pragma unroll
@@ -347,7 +451,6 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   }
   __syncthreads();
   const int nsp = (L + a.chunk - 1) / a.chunk;
-  const bool direct = nsp == 1;
   for (int dim = threadIdx.x; dim < D; dim += blockDim.x) {
     float M = -INFINITY;
     for (int w = 0; w < nwaves; ++w) M = fmaxf(M, sm_m[w]);
@@ -359,9 +462,8 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
         den += f * sm_l[w];
       }
     }
-    if (direct) {
-      a.out[(size_t)bh * D + dim] = den > 0.f ? num / den : 0.f;
-      if (a.lse && dim == 0) a.lse[bh] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+    if (nsp == 1) {
+      write_final(a, bh, D, dim, M, num, den);
     } else {
       const size_t pidx = (size_t)bh * a.nsplit + split;
       a.part_o[pidx * D + dim] = num;
@@ -374,64 +476,121 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
 }
 
 // Combines the split partials of one query head (grid: batch * num_q_heads,
-// block: d threads).  Units that fit one split were written by the split
-// kernel and are skipped.
+// 256 threads).  Split weights are computed once into LDS; the numerator sum
+// is spread over 256 / d split groups whose loads are all in flight at once.
+// Units that fit one split were written by the split kernel and are skipped.
 template <int D, bool DENSE>
-__global__ __launch_bounds__(D) void attn_merge(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
+  constexpr int SG = 256 / D;
+  extern __shared__ float s_w[];  // [nsplit] split weights
+  __shared__ float s_red[SG][D];
+  __shared__ float s_part[4];
   const int bh = blockIdx.x;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, u = b * hkv + h / G;
   const int L = unit_rows<DENSE>(a, b, u);
   const int nsp = (L + a.chunk - 1) / a.chunk;
   if (nsp <= 1) return;
-  const int dim = threadIdx.x;
   const float* ml = a.part_ml + (size_t)bh * a.nsplit * 2;
   const float* po = a.part_o + (size_t)bh * a.nsplit * D;
-  float M = -INFINITY;
-  for (int s = 0; s < nsp; ++s) M = fmaxf(M, ml[2 * s]);
-  float num = 0.f, den = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < nsp; ++s) {
-      const float f = exp2f(ml[2 * s] - M);
-      num += f * po[(size_t)s * D + dim];
-      den += f * ml[2 * s + 1];
-    }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // M = max_s m_s
+  float mx = -INFINITY;
+  for (int s = tid; s < nsp; s += 256) mx = fmaxf(mx, ml[2 * s]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  if (lane == 0) s_part[wave] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(s_part[0], s_part[1]), fmaxf(s_part[2], s_part[3]));
+  __syncthreads();
+  // weights and denominator
+  float den = 0.f;
+  for (int s = tid; s < nsp; s += 256) {
+    const float f = M == -INFINITY ? 0.f : exp2f(ml[2 * s] - M);
+    s_w[s] = f;
+    den += f * ml[2 * s + 1];
   }
-  a.out[(size_t)bh * D + dim] = den > 0.f ? num / den : 0.f;
-  if (a.lse && dim == 0) a.lse[bh] = den > 0.f ? (M + log2f(den)) * kLn2 : -INFINITY;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) den += __shfl_xor(den, off);
+  if (lane == 0) s_part[wave] = den;
+  __syncthreads();
+  den = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+  const int sg = tid / D, dim = tid - sg * D;
+  float num = 0.f;
+  for (int s0 = sg; s0 < nsp; s0 += 4 * SG) {
+    float v[4], w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int s = s0 + k * SG;
+      v[k] = s < nsp ? po[(size_t)s * D + dim] : 0.f;
+      w[k] = s < nsp ? s_w[s] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) num += w[k] * v[k];
+  }
+  s_red[sg][dim] = num;
+  __syncthreads();
+  if (sg == 0) {
+    float tot = 0.f;
+#pragma unroll
+    for (int k = 0; k < SG; ++k) tot += s_red[k][dim];
+    write_final(a, bh, D, dim, M, tot, den);
+  }
 }
 
-constexpr int kDefaultTargetGroups = 1024;
+// Workgroups the split geometry aims for: few for the sparse path (one
+// split per unit avoids the merge launch whenever the units alone fill the
+// chip), many for the dense stream.  PRHS_ATTN_GROUPS and
+// PRHS_ATTN_DENSE_GROUPS override them (tuning knobs, read once per process).
+int env_int(const char* name, int dflt) {
+  const char* e = getenv(name);
+  const int x = e ? atoi(e) : 0;
+  return x > 0 ? x : dflt;
+}
 
-// Workgroups the split geometry aims for; PRHS_ATTN_GROUPS overrides it (a
-// tuning knob, read once per process).
-int target_groups() {
+int target_groups(bool dense) {
+  static const int sparse_v = env_int("PRHS_ATTN_GROUPS", 256);
+  static const int dense_v = env_int("PRHS_ATTN_DENSE_GROUPS", 1024);
+  return dense ? dense_v : sparse_v;
+}
+
+// Waves per bf16 workgroup: PRHS_ATTN_WAVES overrides the default of 4.
+int wave_limit() {
   static int v = [] {
-    const char* e = getenv("PRHS_ATTN_GROUPS");
+    const char* e = getenv("PRHS_ATTN_WAVES");
     const int x = e ? atoi(e) : 0;
-    return x > 0 ? x : kDefaultTargetGroups;
+    return x >= 1 && x <= 8 ? x : 4;
   }();
   return v;
 }
 
-template <int D, bool DENSE>
-void launch_typed(const AttnArgs& a, int dtype, int units, int waves, hipStream_t stream) {
+template <int D, bool DENSE, bool PAGED>
+hipError_t launch_typed(const AttnArgs& a, int dtype, int units, int waves, hipStream_t stream) {
   if (dtype == 1) {
-    hipLaunchKernelGGL((attn_split_bf16<D, DENSE>), dim3(a.nsplit, units), dim3(64 * waves), 0,
-                       stream, a);
+    const int G = a.kv.hq / a.kv.hkv;
+    const size_t dyn = (size_t)waves * G * (D + 1) * sizeof(float);
+    if (dyn > 65536) {
+      const hipError_t e = hipFuncSetAttribute((const void*)attn_split_bf16<D, DENSE, PAGED>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((attn_split_bf16<D, DENSE, PAGED>), dim3(a.nsplit, units), dim3(64 * waves),
+                       dyn, stream, a);
   } else {
-    hipLaunchKernelGGL((attn_split_f32<D, DENSE>), dim3(a.nsplit, units), dim3(64 * waves), 0,
+    hipLaunchKernelGGL((attn_split_f32<D, DENSE, PAGED>), dim3(a.nsplit, units), dim3(256), 0,
                        stream, a);
   }
   if (a.nsplit > 1)
-    hipLaunchKernelGGL((attn_merge<D, DENSE>), dim3(a.kv.batch * a.kv.hq), dim3(D), 0, stream, a);
+    hipLaunchKernelGGL((attn_merge<D, DENSE>), dim3(a.kv.batch * a.kv.hq), dim3(256),
+                       (size_t)a.nsplit * sizeof(float), stream, a);
+  return hipGetLastError();
 }
 
 struct AttnLayout {
   size_t part_o, part_ml, total;
 };
 
-AttnLayout attn_layout(int dtype, int batch, int hq, int hkv, int d, int nsplit) {
+AttnLayout attn_layout(int batch, int hq, int d, int nsplit) {
   const size_t parts = (size_t)batch * hq * nsplit;
   AttnLayout L;
   size_t off = 0;
@@ -441,29 +600,45 @@ AttnLayout attn_layout(int dtype, int batch, int hq, int hkv, int d, int nsplit)
   return L;
 }
 
+int waves_for(int dtype, int chunk) {
+  if (dtype != 1) return 4;
+  int w = chunk / 32;
+  const int lim = wave_limit();
+  return w < 1 ? 1 : (w > lim ? lim : w);
+}
+
 }  // namespace
 
 // Rows per workgroup: a multiple of the per-wave tile (32 rows for bf16, 16
 // rows for fp32), sized so about target_groups() workgroups cover the
-// largest unit, with up to 4 waves per workgroup.
-void attn_split_geometry(int dtype, int batch, int hq, int hkv, int rows_cap, int* chunk,
-                         int* nsplit) {
+// largest unit, at most 8 staged rows per thread, at most kMaxSplits splits,
+// and balanced so the splits of a full unit differ by at most one tile.
+void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int rows_cap,
+                         int* chunk, int* nsplit) {
   const int gran = dtype == 1 ? 32 : 16;
   const long long units = dtype == 1 ? (long long)batch * hkv : (long long)batch * hq;
   const long long rows = rows_cap > 0 ? rows_cap : 1;
-  const long long tg = target_groups();
+  const long long tg = target_groups(dense);
   long long c = (rows * (units > 0 ? units : 1) + tg - 1) / tg;
-  c = ((c + gran - 1) / gran) * gran;
+  const long long cmin = (rows + kMaxSplits - 1) / kMaxSplits;
+  if (c < cmin) c = cmin;
+  const long long threads = dtype == 1 ? 64LL * wave_limit() : 256;
+  const long long cmax = threads * kRowsPerThread;
+  if (c > cmax) c = cmax;
   if (c < gran) c = gran;
-  if (c > rows) c = ((rows + gran - 1) / gran) * gran;
+  const long long ns = (rows + c - 1) / c;
+  c = (rows + ns - 1) / ns;
+  c = ((c + gran - 1) / gran) * gran;
+  if (c > cmax) c = cmax;
   *chunk = (int)c;
   *nsplit = (int)((rows + c - 1) / c);
 }
 
-size_t attn_workspace_bytes(int dtype, int batch, int hq, int hkv, int d, int rows_cap) {
+size_t attn_workspace_bytes(int dtype, bool dense, int batch, int hq, int hkv, int d,
+                            int rows_cap) {
   int chunk, nsplit;
-  attn_split_geometry(dtype, batch, hq, hkv, rows_cap, &chunk, &nsplit);
-  return attn_layout(dtype, batch, hq, hkv, d, nsplit).total;
+  attn_split_geometry(dtype, dense, batch, hq, hkv, rows_cap, &chunk, &nsplit);
+  return attn_layout(batch, hq, d, nsplit).total;
 }
 
 hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream) {
@@ -476,25 +651,29 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.set_cap = s.set_cap;
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   const int rows_cap = dense ? s.kv.max_seq_len : s.set_cap;
-  attn_split_geometry(s.dtype, s.kv.batch, s.kv.hq, s.kv.hkv, rows_cap, &a.chunk, &a.nsplit);
-  const AttnLayout L = attn_layout(s.dtype, s.kv.batch, s.kv.hq, s.kv.hkv, s.kv.d, a.nsplit);
+  attn_split_geometry(s.dtype, dense, s.kv.batch, s.kv.hq, s.kv.hkv, rows_cap, &a.chunk,
+                      &a.nsplit);
+  const AttnLayout L = attn_layout(s.kv.batch, s.kv.hq, s.kv.d, a.nsplit);
   char* ws = (char*)s.ws;
   a.part_o = (float*)(ws + L.part_o);
   a.part_ml = (float*)(ws + L.part_ml);
   a.out = s.out;
   a.lse = s.lse;
-  const int gran = s.dtype == 1 ? 32 : 16;
-  int waves = s.dtype == 1 ? a.chunk / gran : 4;
-  waves = waves < 1 ? 1 : (waves > 4 ? 4 : waves);
+  const int waves = waves_for(s.dtype, a.chunk);
   const int units = s.dtype == 1 ? s.kv.batch * s.kv.hkv : s.kv.batch * s.kv.hq;
+  const bool paged = s.kv.paged != 0;
+#define PRHS_ATTN_DISPATCH(DV)                                                          \
+  if (dense) {                                                                          \
+    return paged ? launch_typed<DV, true, true>(a, s.dtype, units, waves, stream)       \
+                 : launch_typed<DV, true, false>(a, s.dtype, units, waves, stream);     \
+  }                                                                                     \
+  return paged ? launch_typed<DV, false, true>(a, s.dtype, units, waves, stream)        \
+               : launch_typed<DV, false, false>(a, s.dtype, units, waves, stream);
   if (s.kv.d == 128) {
-    if (dense) launch_typed<128, true>(a, s.dtype, units, waves, stream);
-    else launch_typed<128, false>(a, s.dtype, units, waves, stream);
-  } else {
-    if (dense) launch_typed<64, true>(a, s.dtype, units, waves, stream);
-    else launch_typed<64, false>(a, s.dtype, units, waves, stream);
+    PRHS_ATTN_DISPATCH(128)
   }
-  return hipGetLastError();
+  PRHS_ATTN_DISPATCH(64)
+#undef PRHS_ATTN_DISPATCH
 }
 
 }  // namespace prhs

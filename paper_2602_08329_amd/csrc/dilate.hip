@@ -9,7 +9,7 @@
 namespace prhs {
 namespace {
 
-constexpr int kDilateBlock = 256;
+constexpr int kDilateBlock = 1024;
 
 __global__ __launch_bounds__(kDilateBlock) void dilate_reuse_kernel(DilateLaunch a) {
   __shared__ uint32_t bm[kSegWords];
@@ -22,16 +22,17 @@ __global__ __launch_bounds__(kDilateBlock) void dilate_reuse_kernel(DilateLaunch
   n0 = n0 < 0 ? 0 : (n0 > n ? n : n0);
   const int sink_end = min(a.sink, n0);
   const int win_start = max(sink_end, n0 - a.window);
-  const int mid = win_start - sink_end;
+  // m = floor(k_b / 3) of the budget before clamping to the middle range
+  // (or dilate_m), then clamped to the selected count
   long long kb = a.k_den > 0 ? ((long long)a.k_num * n0) / a.k_den : (long long)a.k;
-  kb = kb < 0 ? 0 : (kb > mid ? mid : kb);
+  kb = kb < 0 ? 0 : kb;
   int klen = a.topk_len[row];
   klen = klen < 0 ? 0 : (klen > a.k_cap ? a.k_cap : klen);
   long long m = a.dilate_m < 0 ? kb / 3 : a.dilate_m;
   m = m > klen ? klen : m;
   build_index_set<kDilateBlock>(a.topk_idx + (size_t)row * a.k_cap, klen, (int)m, a.dilate_r,
                                 sink_end, win_start, n, a.set_idx + (size_t)row * a.set_cap,
-                                a.set_cap, a.set_len + row, bm, scan);
+                                a.set_cap, a.set_len + row, bm, scan, kSegBits);
 }
 
 }  // namespace

@@ -55,14 +55,20 @@ prhs_status check_kv_shape(const prhs_kv* kv) {
     return fail(PRHS_E_UNSUPPORTED, "dtype must be PRHS_F32 or PRHS_BF16");
   if (kv->max_seq_len < 0 || kv->max_seq_len >= (1 << prhs::kIdxBits))
     return fail(PRHS_E_UNSUPPORTED, "max_seq_len must be in [0, 2^22)");
+  // kernels address rows by 32-bit row ids
+  const long long kRowLimit = 1LL << 31;
   if (kv->layout == PRHS_KV_CONTIGUOUS) {
     if (kv->capacity < kv->max_seq_len)
       return fail(PRHS_E_INVALID, "capacity (%d) < max_seq_len (%d)", kv->capacity, kv->max_seq_len);
+    if ((long long)kv->batch * kv->num_kv_heads * kv->capacity >= kRowLimit)
+      return fail(PRHS_E_UNSUPPORTED, "batch * num_kv_heads * capacity must be < 2^31");
   } else if (kv->layout == PRHS_KV_PAGED) {
     if (kv->page_size < 1) return fail(PRHS_E_INVALID, "page_size must be >= 1");
     if (kv->max_pages < 0 || (long long)kv->max_pages * kv->page_size < kv->max_seq_len)
       return fail(PRHS_E_INVALID, "max_pages * page_size < max_seq_len");
     if (kv->num_pages < 1) return fail(PRHS_E_INVALID, "num_pages must be >= 1");
+    if ((long long)kv->num_pages * kv->num_kv_heads * kv->page_size >= kRowLimit)
+      return fail(PRHS_E_UNSUPPORTED, "num_pages * num_kv_heads * page_size must be < 2^31");
   } else {
     return fail(PRHS_E_UNSUPPORTED, "unknown layout %d", kv->layout);
   }
@@ -161,15 +167,15 @@ prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params
       prhs_status st = check_kv_shape(kv);
       if (st != PRHS_OK) return st;
       if (set_cap < 0) return fail(PRHS_E_INVALID, "set_cap must be >= 0");
-      *bytes = prhs::attn_workspace_bytes(kv->dtype, kv->batch, kv->num_q_heads, kv->num_kv_heads,
-                                          kv->head_dim, set_cap);
+      *bytes = prhs::attn_workspace_bytes(kv->dtype, false, kv->batch, kv->num_q_heads,
+                                          kv->num_kv_heads, kv->head_dim, set_cap);
       return PRHS_OK;
     }
     case PRHS_OP_DENSE_ATTN: {
       prhs_status st = check_kv_shape(kv);
       if (st != PRHS_OK) return st;
-      *bytes = prhs::attn_workspace_bytes(kv->dtype, kv->batch, kv->num_q_heads, kv->num_kv_heads,
-                                          kv->head_dim, kv->max_seq_len);
+      *bytes = prhs::attn_workspace_bytes(kv->dtype, true, kv->batch, kv->num_q_heads,
+                                          kv->num_kv_heads, kv->head_dim, kv->max_seq_len);
       return PRHS_OK;
     }
     default:
@@ -209,6 +215,7 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
   a.k_den = params->k_den;
   a.sink = params->sink;
   a.window = params->window;
+  a.dilate_m = params->dilate_m;
   a.topk_idx = topk_idx;
   a.topk_len = topk_len;
   a.k_cap = k_cap;
@@ -266,7 +273,7 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   }
   if (!(scale == scale)) return fail(PRHS_E_INVALID, "scale is NaN");
   const int rows_cap = dense ? kv->max_seq_len : set_cap;
-  const size_t wsz = prhs::attn_workspace_bytes(kv->dtype, kv->batch, kv->num_q_heads,
+  const size_t wsz = prhs::attn_workspace_bytes(kv->dtype, dense, kv->batch, kv->num_q_heads,
                                                 kv->num_kv_heads, kv->head_dim, rows_cap);
   if (kv->batch > 0 && (!ws || ws_bytes < wsz))
     return fail(PRHS_E_WORKSPACE, "workspace of %zu bytes needed (got %zu)", wsz, ws_bytes);

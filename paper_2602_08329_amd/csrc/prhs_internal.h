@@ -112,7 +112,7 @@ struct SelectLaunch {
   KvView kv;
   const void* q;
   int dtype;
-  int k, k_num, k_den, sink, window;
+  int k, k_num, k_den, sink, window, dilate_m;
   int32_t* topk_idx;
   int32_t* topk_len;
   int k_cap;
@@ -152,8 +152,10 @@ struct AttnLaunch {
   void* ws;
 };
 // Split geometry shared by workspace sizing and launch.
-void attn_split_geometry(int dtype, int batch, int hq, int hkv, int rows_cap, int* chunk, int* nsplit);
-size_t attn_workspace_bytes(int dtype, int batch, int hq, int hkv, int d, int rows_cap);
+void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int rows_cap,
+                         int* chunk, int* nsplit);
+size_t attn_workspace_bytes(int dtype, bool dense, int batch, int hq, int hkv, int d,
+                            int rows_cap);
 hipError_t launch_attention(const AttnLaunch& a, bool dense, hipStream_t stream);
 
 }  // namespace prhs

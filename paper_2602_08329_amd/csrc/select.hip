@@ -14,6 +14,7 @@
 //                  composite (key, kIdxMax - pos) making every key distinct so
 //                  ties go to the lower position; bitonic sort of the k
 //                  winners in LDS; ordered compaction of the anchor set.
+#include "prhs.h"
 #include "prhs_internal.h"
 #include "setops.cuh"
 
@@ -26,14 +27,19 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kScoreBlock = 256;
 constexpr int kScoreChunk = 1024;   // keys per score workgroup
 constexpr int kFilterBlock = 256;
-constexpr int kFilterChunk = 4096;  // keys per filter workgroup
+constexpr int kFilterPerThread = 16;
+constexpr int kFilterChunk = kFilterBlock * kFilterPerThread;
 constexpr int kFinishBlock = 1024;
+constexpr int kFinishPerThread = 8;  // candidates per thread per pass
+constexpr int kFinishTies = 4096;    // level-1 ties the finish kernel keeps in LDS
+constexpr int kFinishSegBits = 65536; // bitmap segment of the finish kernel (8 KB)
 
 struct SelArgs {
   KvView kv;
   const void* q;
-  int k, k_num, k_den, sink, window;
+  int k, k_num, k_den, sink, window, dilate_m;
   int mcap, selcap;
+  int sortcap;         // LDS sort buffer entries of select_finish (power of two)
   uint32_t* keys;      // [rows][mcap]
   uint32_t* hist0;     // [rows][2048]
   uint32_t* hist1;     // [rows][2048]
@@ -66,6 +72,9 @@ __device__ __forceinline__ RowGeom row_geom(const SelArgs& a, int b) {
   return r;
 }
 
+// Radix digits of the 64-bit composite (score key, kIdxMax - position), most
+// significant first: 11 + 11 + 10 bits of the score key, then 11 + 11 bits
+// of the reversed position (positions are < 2^22).
 __device__ __forceinline__ uint32_t level_digit(uint2 e, int level) {
   const uint32_t rp = kIdxMax - e.y;
   switch (level) {
@@ -75,6 +84,16 @@ __device__ __forceinline__ uint32_t level_digit(uint2 e, int level) {
     case 3: return (rp >> 11) & 0x7FFu;
     default: return rp & 0x7FFu;
   }
+}
+
+// 54-bit composite of a (score key, position) pair: larger score first,
+// lower position first among equal scores; every value is distinct.
+__device__ __forceinline__ uint64_t composite(uint2 e) {
+  return ((uint64_t)e.x << kIdxBits) | (uint64_t)(kIdxMax - e.y);
+}
+
+__device__ __forceinline__ int composite_pos(uint64_t c) {
+  return (int)(kIdxMax - (uint32_t)(c & kIdxMax));
 }
 
 // Finds the bin holding the kk-th largest element of histogram h (LDS,
@@ -124,12 +143,74 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
 // with the group's g <= 16 query heads in the columns (unused columns zero).
 // Lane l loads d/2 contiguous bytes of key l%16; the contraction runs over a
 // permutation of d shared by both operands.  Products of bf16 values are exact
-// in fp32 and the accumulation is fp32.
+// in fp32 and the accumulation is fp32.  Each wave handles 64 keys per step
+// and prefetches its next step's 16 loads while multiplying the current one.
 template <int D>
+struct ScoreStep {
+  bf16x8_t kf[4][D / 32];
+};
+
+template <int D, bool PAGED>
+__device__ __forceinline__ int32_t score_row(const SelArgs& a, const RowGeom& rg, int b, int g,
+                                             int i, int end, int p0, const int32_t* s_page) {
+  if (i >= end) return -1;
+  const int pos = rg.sink_end + i;
+  if (!PAGED) return (b * a.kv.hkv + g) * a.kv.capacity + pos;
+  const int phys = s_page[pos / a.kv.page_size - p0];
+  if (phys < 0) return -1;
+  return (phys * a.kv.hkv + g) * a.kv.page_size + pos % a.kv.page_size;
+}
+
+template <int D, bool PAGED>
+__device__ __forceinline__ void score_load(ScoreStep<D>& S, const SelArgs& a, const RowGeom& rg,
+                                           int b, int g, int t, int end, int p0,
+                                           const int32_t* s_page, int col, int grp) {
+  const __bf16* kbase = (const __bf16*)a.kv.k;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int32_t row = score_row<D, PAGED>(a, rg, b, g, t + s * 16 + col, end, p0, s_page);
+    const uint4* kp = (const uint4*)(kbase + (int64_t)(row < 0 ? 0 : row) * D + grp * (D / 4));
+#pragma unroll
+    for (int kk = 0; kk < D / 32; ++kk) S.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[kk]);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void score_consume(const ScoreStep<D>& S, const bf16x8_t* qf, int G,
+                                              int gp, int t, int end, int col, int grp,
+                                              uint32_t* keys, uint32_t* hist) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < D / 32; ++kk)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(S.kf[s][kk], qf[kk], acc, 0, 0, 0);
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = col < G ? acc[e] : -INFINITY;
+    for (int off = 1; off < gp; off <<= 1) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], __shfl_xor(v[e], off, 16));
+    }
+    if (col == 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = t + s * 16 + grp * 4 + e;
+        if (i < end) {
+          const uint32_t key = score_key(v[e]);
+          keys[i] = key;
+          atomicAdd(&hist[key >> 21], 1u);
+        }
+      }
+    }
+  }
+}
+
+template <int D, bool PAGED>
 __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
-  constexpr int KS = D / 32;  // MFMA k-steps
-  constexpr int SUB = 4;      // 16-key sub-tiles per wave iteration
+  constexpr int KS = D / 32;
   __shared__ uint32_t hist[kHistBins];
+  __shared__ int32_t s_page[kScoreChunk + 1];
   const int row = blockIdx.y;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
@@ -137,63 +218,57 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
   if (base >= rg.m || rg.kb <= 0) return;
   const int end = min(rg.m, base + kScoreChunk);
   for (int i = threadIdx.x; i < kHistBins; i += kScoreBlock) hist[i] = 0u;
+  int p0 = 0;
+  if (PAGED) {
+    // the chunk's pages, resolved once
+    const int ps = a.kv.page_size;
+    p0 = (rg.sink_end + base) / ps;
+    const int np = (rg.sink_end + end - 1) / ps - p0 + 1;
+    for (int i = threadIdx.x; i < np; i += kScoreBlock) {
+      const int page = p0 + i;
+      int phys = -1;
+      if (page < a.kv.max_pages) phys = a.kv.table[(int64_t)b * a.kv.max_pages + page];
+      s_page[i] = (phys >= 0 && phys < a.kv.num_pages) ? phys : -1;
+    }
+  }
   __syncthreads();
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   const int G = a.kv.hq / a.kv.hkv;
   const __bf16* q = (const __bf16*)a.q;
-  const __bf16* kbase = (const __bf16*)a.kv.k;
   bf16x8_t qf[KS];
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
-    if (col < G) {
-      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + col) * D + grp * (D / 4));
-      qf[kk] = __builtin_bit_cast(bf16x8_t, qp[kk]);
-    } else {
-      qf[kk] = __builtin_bit_cast(bf16x8_t, make_uint4(0, 0, 0, 0));
-    }
+    const int qh = col < G ? col : 0;
+    const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * (D / 4));
+    const uint4 v = qp[kk];
+    qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
   int gp = 1;
   while (gp < G) gp <<= 1;
-
   uint32_t* keys = a.keys + (size_t)row * a.mcap;
-  for (int t = base + wave * 16 * SUB; t < end; t += 4 * 16 * SUB) {
-    bf16x8_t kf[SUB][KS];
-#pragma unroll
-    for (int s = 0; s < SUB; ++s) {
-      const int i = t + s * 16 + col;
-      int64_t off = -1;
-      if (i < end) off = kv_row_offset(a.kv, b, g, rg.sink_end + i);
-      const uint4* kp = (const uint4*)(kbase + (off < 0 ? 0 : off) + grp * (D / 4));
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        kf[s][kk] = __builtin_bit_cast(bf16x8_t, off < 0 ? make_uint4(0, 0, 0, 0) : kp[kk]);
+
+  const int t0 = base + wave * 64;
+  const int iters = t0 < end ? (end - t0 + 255) / 256 : 0;
+  if (iters > 0) {
+    ScoreStep<D> A, B;
+    int t = t0;
+    score_load<D, PAGED>(A, a, rg, b, g, t, end, p0, s_page, col, grp);
+    int i = 0;
+    for (; i + 2 < iters; i += 2) {
+      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, col, grp);
+      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
+      score_load<D, PAGED>(A, a, rg, b, g, t + 512, end, p0, s_page, col, grp);
+      score_consume<D>(B, qf, G, gp, t + 256, end, col, grp, keys, hist);
+      t += 512;
     }
-#pragma unroll
-    for (int s = 0; s < SUB; ++s) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s][kk], qf[kk], acc, 0, 0, 0);
-      float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = col < G ? acc[e] : -INFINITY;
-      for (int off = 1; off < gp; off <<= 1) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], __shfl_xor(v[e], off, 16));
-      }
-      if (col == 0) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int i = t + s * 16 + grp * 4 + e;
-          if (i < end) {
-            const uint32_t key = score_key(v[e]);
-            keys[i] = key;
-            atomicAdd(&hist[key >> 21], 1u);
-          }
-        }
-      }
+    if (i + 1 < iters) {
+      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, col, grp);
+      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
+      score_consume<D>(B, qf, G, gp, t + 256, end, col, grp, keys, hist);
+    } else {
+      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
     }
   }
   __syncthreads();
@@ -246,11 +321,16 @@ __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
   flush_hist(hist, a.hist0 + (size_t)row * kHistBins);
 }
 
+// Level-0 split of a chunk of keys: keys above the threshold bin are
+// selected, keys inside it become candidates (with the level-1 histogram).
+// Each thread holds 16 keys; one workgroup prefix sum and one atomic per
+// output list place them.
 __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFilterBlock / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt;
+  __shared__ uint32_t s_base[2];
   const int row = blockIdx.y;
   const int b = row / a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
@@ -258,44 +338,59 @@ __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   if (base >= rg.m || rg.kb <= 0) return;
   const int end = min(rg.m, base + kFilterChunk);
   const bool all = rg.kb >= rg.m;
+  const int tid = threadIdx.x;
+  const uint32_t* keys = a.keys + (size_t)row * a.mcap;
+  uint32_t key[kFilterPerThread];
+#pragma unroll
+  for (int k = 0; k < kFilterPerThread; ++k) {
+    const int i = base + tid + k * kFilterBlock;
+    key[k] = i < end ? keys[i] : 0u;
+  }
   int bin = 0;
   bool resolved = true;
   if (!all) {
-    for (int i = threadIdx.x; i < kHistBins; i += kFilterBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
+    for (int i = tid; i < kHistBins; i += kFilterBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
     __syncthreads();
     find_threshold<kFilterBlock>(h, (uint32_t)rg.kb, scan, &s_bin, &s_krem, &s_cnt);
     bin = s_bin;
     resolved = (s_cnt == s_krem);
     __syncthreads();
-    for (int i = threadIdx.x; i < kHistBins; i += kFilterBlock) h[i] = 0u;
-    __syncthreads();
+    for (int i = tid; i < kHistBins; i += kFilterBlock) h[i] = 0u;
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t* keys = a.keys + (size_t)row * a.mcap;
+  uint32_t tmask = 0, kmask = 0;
+#pragma unroll
+  for (int k = 0; k < kFilterPerThread; ++k) {
+    const int i = base + tid + k * kFilterBlock;
+    const int d0 = (int)(key[k] >> 21);
+    const bool valid = i < end;
+    const bool take = valid && (all || d0 > bin || (resolved && d0 == bin));
+    const bool keep = valid && !all && !resolved && d0 == bin;
+    tmask |= (take ? 1u : 0u) << k;
+    kmask |= (keep ? 1u : 0u) << k;
+  }
+  const uint32_t packed = ((uint32_t)__popc(tmask) << 16) | (uint32_t)__popc(kmask);
+  uint32_t total;
+  const uint32_t pre = block_exclusive_scan<kFilterBlock>(packed, scan, &total);
   uint32_t* cnt = a.counters + row * 4;
+  if (tid == 0) {
+    s_base[0] = (total >> 16) ? atomicAdd(&cnt[0], total >> 16) : 0u;
+    s_base[1] = (total & 0xFFFFu) ? atomicAdd(&cnt[1], total & 0xFFFFu) : 0u;
+  }
+  __syncthreads();
+  uint32_t ot = s_base[0] + (pre >> 16), ok = s_base[1] + (pre & 0xFFFFu);
   uint2* sel = a.sel + (size_t)row * a.selcap;
   uint2* cand = a.cand + (size_t)row * a.mcap;
-  for (int i0 = base + wave * 64; i0 < end; i0 += kFilterBlock) {
-    const int i = i0 + lane;
-    const bool valid = i < end;
-    uint2 e = make_uint2(0u, 0u);
-    bool take = false, keep = false;
-    if (valid) {
-      e = make_uint2(keys[i], (uint32_t)(rg.sink_end + i));
-      if (all) {
-        take = true;
-      } else {
-        const int d0 = (int)(e.x >> 21);
-        take = d0 > bin || (resolved && d0 == bin);
-        keep = !resolved && d0 == bin;
-      }
+#pragma unroll
+  for (int k = 0; k < kFilterPerThread; ++k) {
+    const uint2 e = make_uint2(key[k], (uint32_t)(rg.sink_end + base + tid + k * kFilterBlock));
+    if ((tmask >> k) & 1u) {
+      if (ot < (uint32_t)a.selcap) sel[ot] = e;
+      ++ot;
     }
-    const int slot = wave_append(take, &cnt[0]);
-    if (slot >= 0 && slot < a.selcap) sel[slot] = e;
-    const int slot2 = wave_append(keep, &cnt[1]);
-    if (slot2 >= 0 && slot2 < a.mcap) {
-      cand[slot2] = e;
+    if ((kmask >> k) & 1u) {
+      if (ok < (uint32_t)a.mcap) cand[ok] = e;
       atomicAdd(&h[(e.x >> 10) & 0x7FFu], 1u);
+      ++ok;
     }
   }
   if (!all && !resolved) {
@@ -316,104 +411,223 @@ __device__ __forceinline__ void block_publish() {
   __threadfence_block();
 }
 
+// Splits `count` candidates of src by radix digit `level` against bin bl:
+// digit above bl (or equal, when the bin is taken whole) goes to the output
+// list sel; digit equal to bl is kept, either as a 64-bit composite in the LDS
+// buffer `keep_lds` or in the global list `keep_glb`.  Returns the number
+// kept.  Every thread of the workgroup must call it.
+__device__ uint32_t split_candidates(const SelArgs& a, uint32_t* cnt, uint2* sel, const uint2* src,
+                                     uint32_t count, int level, uint32_t bl, bool resolved,
+                                     uint64_t* keep_lds, uint2* keep_glb, uint32_t* scan,
+                                     uint32_t* s_base) {
+  const int tid = threadIdx.x;
+  uint32_t kept = 0;
+  for (uint32_t e0 = 0; e0 < count; e0 += kFinishBlock * kFinishPerThread) {
+    uint2 x[kFinishPerThread];
+    uint32_t tmask = 0, kmask = 0;
+#pragma unroll
+    for (int k = 0; k < kFinishPerThread; ++k) {
+      const uint32_t e = e0 + tid + k * kFinishBlock;
+      x[k] = e < count ? src[e] : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int k = 0; k < kFinishPerThread; ++k) {
+      const bool valid = e0 + tid + k * kFinishBlock < count;
+      const uint32_t dg = level_digit(x[k], level);
+      tmask |= (valid && (dg > bl || (resolved && dg == bl)) ? 1u : 0u) << k;
+      kmask |= (valid && !resolved && dg == bl ? 1u : 0u) << k;
+    }
+    const uint32_t packed = ((uint32_t)__popc(tmask) << 16) | (uint32_t)__popc(kmask);
+    uint32_t total;
+    const uint32_t pre = block_exclusive_scan<kFinishBlock>(packed, scan, &total);
+    if (tid == 0) *s_base = (total >> 16) ? atomicAdd(&cnt[0], total >> 16) : 0u;
+    __syncthreads();
+    uint32_t ot = *s_base + (pre >> 16), ok = kept + (pre & 0xFFFFu);
+#pragma unroll
+    for (int k = 0; k < kFinishPerThread; ++k) {
+      if ((tmask >> k) & 1u) {
+        if (ot < (uint32_t)a.selcap) sel[ot] = x[k];
+        ++ot;
+      }
+      if ((kmask >> k) & 1u) {
+        if (keep_lds) keep_lds[ok] = composite(x[k]);
+        else if (ok < (uint32_t)a.mcap) keep_glb[ok] = x[k];
+        ++ok;
+      }
+    }
+    kept += total & 0xFFFFu;
+    __syncthreads();
+  }
+  return kept;
+}
+
+// Radix select to the end inside the global candidate lists (levels from
+// `level` to 4), for the rare rows whose ties do not fit LDS.
+__device__ void radix_global(const SelArgs& a, uint32_t* cnt, uint2* sel, uint2* src, uint2* dst,
+                             uint32_t count, uint32_t krem, int level, uint32_t* h, uint32_t* scan,
+                             int* s_bin, uint32_t* s_krem, uint32_t* s_cnt, uint32_t* s_base) {
+  const int tid = threadIdx.x;
+  for (; level <= 4; ++level) {
+    __syncthreads();
+    for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+    __syncthreads();
+    for (uint32_t e0 = 0; e0 < count; e0 += kFinishBlock * kFinishPerThread) {
+      uint2 x[kFinishPerThread];
+#pragma unroll
+      for (int k = 0; k < kFinishPerThread; ++k) {
+        const uint32_t e = e0 + tid + k * kFinishBlock;
+        x[k] = e < count ? src[e] : make_uint2(0u, 0u);
+      }
+#pragma unroll
+      for (int k = 0; k < kFinishPerThread; ++k)
+        if (e0 + tid + k * kFinishBlock < count) atomicAdd(&h[level_digit(x[k], level)], 1u);
+    }
+    __syncthreads();
+    find_threshold<kFinishBlock>(h, krem, scan, s_bin, s_krem, s_cnt);
+    const uint32_t bl = (uint32_t)*s_bin;
+    const bool resolved = *s_cnt == *s_krem;
+    const uint32_t krem_next = *s_krem;
+    const uint32_t kept = split_candidates(a, cnt, sel, src, count, level, bl, resolved, nullptr,
+                                           dst, scan, s_base);
+    block_publish();
+    if (resolved) break;
+    count = kept < (uint32_t)a.mcap ? kept : (uint32_t)a.mcap;
+    krem = krem_next;
+    uint2* tmp = src;
+    src = dst;
+    dst = tmp;
+  }
+}
+
+// Threshold T with exactly k of the n distinct composites in LDS buffer `buf`
+// at or above it (1 <= k <= n): radix select over 11-bit digits of the 54-bit
+// values, stopping as soon as a whole bin is taken.  Every thread must call it.
+__device__ uint64_t lds_kth_largest(const uint64_t* buf, uint32_t n, uint32_t k, uint32_t* h,
+                                    uint32_t* scan, int* s_bin, uint32_t* s_krem, uint32_t* s_cnt) {
+  const int tid = threadIdx.x;
+  uint64_t prefix = 0, pmask = 0;
+  uint32_t krem = k;
+  for (int lv = 0; lv < 5; ++lv) {
+    const int sh = lv < 4 ? 43 - 11 * lv : 0;
+    const uint64_t dmask = lv < 4 ? 0x7FFull : 0x3FFull;
+    for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+    __syncthreads();
+    for (uint32_t i = tid; i < n; i += kFinishBlock) {
+      const uint64_t x = buf[i];
+      if ((x & pmask) == prefix) atomicAdd(&h[(uint32_t)((x >> sh) & dmask)], 1u);
+    }
+    __syncthreads();
+    find_threshold<kFinishBlock>(h, krem, scan, s_bin, s_krem, s_cnt);
+    const uint32_t bin = (uint32_t)*s_bin, krem2 = *s_krem, cnt = *s_cnt;
+    prefix |= (uint64_t)bin << sh;
+    pmask |= dmask << sh;
+    if (cnt == krem2) break;
+    krem = krem2;
+  }
+  return prefix;
+}
+
+// Appends the positions of the LDS composites in [lo, hi), ascending, to out.
+__device__ int compact_range(const uint64_t* comp, uint32_t n, uint64_t lo, uint64_t hi,
+                             int mid_lo, int mid_hi, int32_t* out, int cap, int pos,
+                             uint32_t* bm, uint32_t* scan, int seg_bits) {
+  const int tid = threadIdx.x;
+  auto mark = [&](int seg_lo, int seg_hi, uint32_t* b) {
+    for (uint32_t i = tid; i < n; i += kFinishBlock) {
+      const uint64_t x = comp[i];
+      if (x >= lo && x < hi) {
+        const int p = composite_pos(x);
+        if (p >= seg_lo && p < seg_hi) mark_bit(b, seg_lo, p);
+      }
+    }
+  };
+  return compact_marked<kFinishBlock>(mid_lo, mid_hi, seg_bits, mark, out, cap, pos, bm, scan);
+}
+
+// Finishes the selection of one row (one workgroup per row): the level-0 and
+// level-1 thresholds come from the histograms of the score and filter
+// kernels; one pass over the level-0 candidates moves the level-1 winners to
+// the output list and stages the level-1 ties in LDS.  Winners and staged
+// ties, as distinct 54-bit composites in LDS, then give the exact k_b-th and
+// m-th largest by LDS radix select; ordered bitmap compactions write the top
+// m, the other winners and the anchor set, each ascending by position.
 __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
-  extern __shared__ uint64_t dyn[];
+  extern __shared__ uint64_t dyn[];  // sort buffer: a.sortcap entries
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFinishBlock / 64 + 1];
   __shared__ int s_bin;
-  __shared__ uint32_t s_krem, s_cnt, s_dst;
+  __shared__ uint32_t s_krem, s_cnt, s_base;
   const int row = blockIdx.x;
   const int b = row / a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x;
   uint32_t* cnt = a.counters + row * 4;
   uint2* sel = a.sel + (size_t)row * a.selcap;
+  uint32_t n_lds = 0;  // staged ties in dyn[0, n_lds)
 
   if (rg.kb > 0 && rg.kb < rg.m) {
     for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
     __syncthreads();
     find_threshold<kFinishBlock>(h, (uint32_t)rg.kb, scan, &s_bin, &s_krem, &s_cnt);
     if (s_cnt != s_krem) {
-      uint2* src = a.cand + (size_t)row * a.mcap;
-      uint2* dst = a.cand2 + (size_t)row * a.mcap;
-      uint32_t count = min(coherent_load(&cnt[1]), (uint32_t)a.mcap);
-      uint32_t krem = s_krem;
-      for (int level = 1; level <= 4; ++level) {
-        __syncthreads();
-        if (level == 1) {
-          for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist1[(size_t)row * kHistBins + i];
-        } else {
-          for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
-          __syncthreads();
-          for (uint32_t e = tid; e < count; e += kFinishBlock) atomicAdd(&h[level_digit(src[e], level)], 1u);
-        }
-        if (tid == 0) s_dst = 0u;
-        __syncthreads();
-        find_threshold<kFinishBlock>(h, krem, scan, &s_bin, &s_krem, &s_cnt);
-        const uint32_t bl = (uint32_t)s_bin;
-        const bool resolved = s_cnt == s_krem;
-        for (uint32_t e0 = wave * 64; e0 < count; e0 += kFinishBlock) {
-          const uint32_t e = e0 + lane;
-          const bool valid = e < count;
-          const uint2 x = valid ? src[e] : make_uint2(0u, 0u);
-          const uint32_t dg = level_digit(x, level);
-          const bool take = valid && (dg > bl || (resolved && dg == bl));
-          const bool keep = valid && !resolved && dg == bl;
-          const int slot = wave_append(take, &cnt[0]);
-          if (slot >= 0 && slot < a.selcap) sel[slot] = x;
-          const int slot2 = wave_append(keep, &s_dst);
-          if (slot2 >= 0 && slot2 < a.mcap) dst[slot2] = x;
-        }
-        block_publish();
-        if (resolved) break;
-        count = s_dst;
-        krem = s_krem;
-        uint2* tmp = src;
-        src = dst;
-        dst = tmp;
+      const uint32_t krem0 = s_krem;
+      __syncthreads();
+      for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist1[(size_t)row * kHistBins + i];
+      __syncthreads();
+      find_threshold<kFinishBlock>(h, krem0, scan, &s_bin, &s_krem, &s_cnt);
+      const uint32_t b1 = (uint32_t)s_bin, krem1 = s_krem, c1 = s_cnt;
+      const bool resolved1 = c1 == krem1;
+      const bool in_lds = !resolved1 && c1 + (uint32_t)rg.kb <= (uint32_t)a.sortcap;
+      const uint32_t count0 = min(coherent_load(&cnt[1]), (uint32_t)a.mcap);
+      uint2* cand2 = a.cand2 + (size_t)row * a.mcap;
+      const uint32_t kept = split_candidates(a, cnt, sel, a.cand + (size_t)row * a.mcap, count0, 1,
+                                             b1, resolved1, in_lds ? dyn : nullptr, cand2, scan,
+                                             &s_base);
+      block_publish();
+      if (in_lds) {
+        n_lds = kept;
+      } else if (!resolved1) {
+        radix_global(a, cnt, sel, cand2, a.cand + (size_t)row * a.mcap,
+                     min(kept, (uint32_t)a.mcap), krem1, 2, h, scan, &s_bin, &s_krem, &s_cnt,
+                     &s_base);
       }
     }
   }
   block_publish();
 
-  uint32_t total = 0;
-  if (rg.kb > 0) total = min(coherent_load(&cnt[0]), (uint32_t)min(rg.kb, a.selcap));
-  uint32_t P = 1;
-  while (P < total) P <<= 1;
-  for (uint32_t i = tid; i < P; i += kFinishBlock) {
-    uint64_t c = 0;
-    if (i < total) {
-      const uint2 e = sel[i];
-      c = ((uint64_t)e.x << 32) | (uint64_t)(kIdxMax - e.y);
-    }
-    dyn[i] = c;
-  }
+  const uint32_t n_sel = rg.kb > 0 ? min(coherent_load(&cnt[0]), (uint32_t)a.selcap) : 0u;
+  const uint32_t total = n_sel + n_lds;
+  for (uint32_t i = n_lds + tid; i < total; i += kFinishBlock) dyn[i] = composite(sel[i - n_lds]);
   __syncthreads();
-  // bitonic sort, descending by the composite key
-  for (uint32_t kk = 2; kk <= P; kk <<= 1) {
-    for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = tid; i < P; i += kFinishBlock) {
-        const uint32_t ixj = i ^ j;
-        if (ixj > i) {
-          const uint64_t x = dyn[i], y = dyn[ixj];
-          const bool desc = (i & kk) == 0;
-          if (desc ? (x < y) : (x > y)) {
-            dyn[i] = y;
-            dyn[ixj] = x;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
+  // winners: the kout largest composites; top: the m largest of them
+  const uint32_t kout = min(total, (uint32_t)(rg.kb > 0 ? rg.kb : 0));
+  // m from the budget before clamping to the middle range, then clamped to
+  // the winners (floor(k_b / 3) by default)
+  const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
+  long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
+  const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
+  const uint64_t c_k = kout < total ? lds_kth_largest(dyn, total, kout, h, scan, &s_bin, &s_krem, &s_cnt)
+                                    : 0ull;
+  const uint64_t c_m = m > 0 ? lds_kth_largest(dyn, total, m, h, scan, &s_bin, &s_krem, &s_cnt)
+                             : ~0ull;
+  uint32_t* bm = (uint32_t*)(dyn + a.sortcap);
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
-  for (uint32_t i = tid; i < total; i += kFinishBlock)
-    topk[i] = (int32_t)(kIdxMax - (uint32_t)(dyn[i] & 0xFFFFFFFFull));
-  if (tid == 0) a.topk_len[row] = (int32_t)total;
-  block_publish();
-  build_index_set<kFinishBlock>(topk, (int)total, 0, 0, rg.sink_end, rg.win_start, rg.n0,
-                                a.set_idx + (size_t)row * a.set_cap, a.set_cap, a.set_len + row,
-                                (uint32_t*)dyn, scan);
+  compact_range(dyn, total, c_m, ~0ull, rg.sink_end, rg.win_start, topk, a.k_cap, 0, bm, scan,
+                kFinishSegBits);
+  compact_range(dyn, total, c_k, c_m, rg.sink_end, rg.win_start, topk, a.k_cap, (int)m, bm, scan,
+                kFinishSegBits);
+  if (tid == 0) a.topk_len[row] = (int32_t)kout;
+  // anchor set: sink, winners, window
+  int32_t* out = a.set_idx + (size_t)row * a.set_cap;
+  for (int i = tid; i < rg.sink_end; i += kFinishBlock)
+    if (i < a.set_cap) out[i] = i;
+  int pos = compact_range(dyn, total, c_k, ~0ull, rg.sink_end, rg.win_start, out, a.set_cap,
+                          rg.sink_end, bm, scan, kFinishSegBits);
+  const int nw = rg.n0 - rg.win_start;
+  for (int i = tid; i < nw; i += kFinishBlock)
+    if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
+  if (nw > 0) pos += nw;
+  if (tid == 0) a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -455,6 +669,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.k_den = s.k_den;
   a.sink = s.sink;
   a.window = s.window;
+  a.dilate_m = s.dilate_m;
   a.mcap = s.kv.max_seq_len > 0 ? s.kv.max_seq_len : 1;
   a.selcap = s.max_topk > 0 ? s.max_topk : 1;
   const SelLayout L = select_layout(rows, a.mcap, a.selcap);
@@ -478,18 +693,27 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   hipLaunchKernelGGL(select_clear, dim3(rows), dim3(256), 0, stream, a);
   const dim3 sgrid((mid_max + kScoreChunk - 1) / kScoreChunk, rows);
   if (s.dtype == 1) {
-    if (s.kv.d == 128) hipLaunchKernelGGL(score_bf16<128>, sgrid, dim3(kScoreBlock), 0, stream, a);
-    else hipLaunchKernelGGL(score_bf16<64>, sgrid, dim3(kScoreBlock), 0, stream, a);
+    const bool paged = s.kv.paged != 0;
+    if (s.kv.d == 128) {
+      if (paged) hipLaunchKernelGGL((score_bf16<128, true>), sgrid, dim3(kScoreBlock), 0, stream, a);
+      else hipLaunchKernelGGL((score_bf16<128, false>), sgrid, dim3(kScoreBlock), 0, stream, a);
+    } else {
+      if (paged) hipLaunchKernelGGL((score_bf16<64, true>), sgrid, dim3(kScoreBlock), 0, stream, a);
+      else hipLaunchKernelGGL((score_bf16<64, false>), sgrid, dim3(kScoreBlock), 0, stream, a);
+    }
   } else {
     if (s.kv.d == 128) hipLaunchKernelGGL(score_f32<128>, sgrid, dim3(kScoreBlock), 0, stream, a);
     else hipLaunchKernelGGL(score_f32<64>, sgrid, dim3(kScoreBlock), 0, stream, a);
   }
   const dim3 fgrid((mid_max + kFilterChunk - 1) / kFilterChunk, rows);
   hipLaunchKernelGGL(select_filter, fgrid, dim3(kFilterBlock), 0, stream, a);
-  uint32_t P = 1;
-  while ((int)P < a.selcap) P <<= 1;
-  size_t dyn = (size_t)P * 8;
-  if (dyn < (size_t)kSegWords * 4) dyn = (size_t)kSegWords * 4;
+  // LDS buffer: the k winners plus up to kFinishTies level-1 ties, then the
+  // bitmap segment
+  long long cap = (long long)a.selcap + kFinishTies;
+  if (cap > PRHS_MAX_TOPK) cap = PRHS_MAX_TOPK;
+  if (cap < a.selcap) cap = a.selcap;
+  a.sortcap = (int)cap;
+  const size_t dyn = (size_t)a.sortcap * 8 + kFinishSegBits / 8;
   if (dyn > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)select_finish,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);

@@ -199,7 +199,9 @@ def check_select(inp, lens, p, layer=0, step=0):
     ref = oracle_select(inp, lens, p, layer, step)
     for (b, g), (S, C) in ref.items():
         assert tlen[b, g] == len(S), f"b{b} g{g}: topk_len {tlen[b, g]} != {len(S)}"
-        assert np.array_equal(topk[b, g, : len(S)], S), f"b{b} g{g}: top-k order differs"
+        kb = O.budget_k(lens[b], p.k, p.k_num, p.k_den)
+        expect = O.topk_layout(S, O.dilation_m(kb, len(S), p.dilate_m))
+        assert np.array_equal(topk[b, g, : len(S)], expect), f"b{b} g{g}: top-k differs"
         assert slen[b, g] == len(C), f"b{b} g{g}: set_len {slen[b, g]} != {len(C)}"
         assert np.array_equal(sidx[b, g, : len(C)], C), f"b{b} g{g}: anchor set differs"
     return topk, tlen
@@ -236,7 +238,18 @@ def test_select_all_ties_lowest_positions():
         K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, 0.25)))
     p = B.params(k=200, sink=4, window=64)
     topk, tlen = check_select(inp, lens, p)
-    assert list(topk[0, 0, :5]) == [4, 5, 6, 7, 8]
+    assert list(topk[0, 0, :5]) == [4, 5, 6, 7, 8]   # the top m = the lowest positions
+
+
+def test_select_all_ties_beyond_lds_budget():
+    # every score equal on a row longer than the finish kernel's LDS tie buffer:
+    # the tie-break runs through the global radix levels over positions
+    lens = (14000,)
+    inp = synth.random_inputs(1, 4, 1, 128, lens, seed=12, grid=True, device=DEV)
+    for K in inp.K:
+        K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, -0.5)))
+    topk, tlen = check_select(inp, lens, B.params(k=300, sink=4, window=64))
+    assert list(topk[0, 0, :3]) == [4, 5, 6]
 
 
 def test_select_coarse_grid_many_ties():
@@ -279,7 +292,8 @@ def test_dilate_reuse_bit_exact():
     for pk in (dict(k=300, sink=4, window=64, dilate_r=1),
                dict(k=90, sink=0, window=0, dilate_r=2, dilate_m=40),
                dict(k=300, sink=4, window=64, dilate_r=0),
-               dict(k_num=1, k_den=20, sink=4, window=16, dilate_r=1)):
+               dict(k_num=1, k_den=20, sink=4, window=16, dilate_r=1),
+               dict(k=9000, sink=4, window=64, dilate_r=1)):
         p = B.params(refresh_every=steps, **pk)
         topk, tlen, _, _ = run_select(inp, lens0, p)
         ref = oracle_select(inp, lens0, p)

@@ -426,3 +426,16 @@ def test_decode_oracle_schedule_and_anchor_state():
             else:
                 expect = O.reuse_set(s_star, k // 3, 1, n0, n, sink, window)
             assert list(S) == list(expect)
+
+
+def test_topk_layout_partitions_by_rank_then_position():
+    # the library's layout of S*: its m top-ranked members, then the rest, each
+    # part ascending; the set and the top-m set are those of the ranked S*
+    rng = np.random.default_rng(18)
+    sigma = rng.integers(-5, 6, size=300).astype(float)
+    S = O.topk_middle(sigma, 300, 40, 4, 16)
+    for m in (0, 1, 13, 40):
+        lay = O.topk_layout(S, m)
+        assert sorted(lay.tolist()) == sorted(S.tolist())
+        assert set(lay[:m].tolist()) == set(S[:m].tolist())
+        assert list(lay[:m]) == sorted(lay[:m]) and list(lay[m:]) == sorted(lay[m:])
