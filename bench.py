@@ -59,9 +59,11 @@ def algorithmic_bytes(run, set_lens, sel_rows):
 
 
 def cpu_baseline(run, budget_s):
-    """Times the CPU oracle on a bounded sample of the same workload: every
-    layer-step of the first refresh block of layer group 0, for as many
-    (batch, kv-head) units as fit the time budget; scaled to all units."""
+    """Times the CPU oracle on a bounded sample of the same workload: whole
+    layer groups (every (batch, kv-head) unit, every decode step of the
+    cycle, in schedule order), group after group until the time budget is
+    spent; scaled to all layers.  Only the oracle calls are timed; copying the
+    caches to the host is not."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
@@ -71,35 +73,90 @@ def cpu_baseline(run, budget_s):
     w = run.w
     inp = run.inp
     units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
-    layers = list(range(min(w.G, run.L)))
-    steps = list(range(min(w.s, w.steps)))
-    done = 0
     spent = 0.0
+    layer_steps = 0
     with threadpool_limits(limits=1):
-        for (b, g) in units:
-            n_max = w.n_ctx[b] + w.steps
-            cache = {l: synth.gather_unit(inp, l, b, g, n_max) for l in layers}
-            qs = {(l, j): synth.query_group(inp, l, j, b, g) for l in layers for j in steps}
-            dec = O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k, k_num=w.k_num,
-                                 k_den=w.k_den, dilate_m=w.dilate_m)
+        for g0 in range(0, run.L, w.G):
+            layers = list(range(g0, min(g0 + w.G, run.L)))
+            caches = {}
+            for l in layers:
+                for (b, g) in units:
+                    caches[(l, b, g)] = synth.gather_unit(inp, l, b, g, w.n_ctx[b] + w.steps)
+            qs = {}
+            for l in layers:
+                qh = inp.q[l].float().cpu().numpy().astype(np.float64)
+                for j in range(w.steps):
+                    for (b, g) in units:
+                        qs[(l, j, b, g)] = qh[j, b, g * w.g:(g + 1) * w.g]
+            decs = {u: O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k, k_num=w.k_num,
+                                      k_den=w.k_den, dilate_m=w.dilate_m) for u in units}
             t0 = time.perf_counter()
-            for j in steps:
-                n = w.n_ctx[b] + j + 1
+            for j in range(w.steps):
                 for l in layers:
-                    K, V = cache[l]
-                    S = dec.step_set(l, j, qs[(l, j)], K, n)
-                    dec.attend(qs[(l, j)], K[:n], V[:n], S)
+                    for (b, g) in units:
+                        n = w.n_ctx[b] + j + 1
+                        K, V = caches[(l, b, g)]
+                        Qg = qs[(l, j, b, g)]
+                        S = decs[(b, g)].step_set(l, j, Qg, K, n)
+                        decs[(b, g)].attend(Qg, K[:n], V[:n], S)
             spent += time.perf_counter() - t0
-            done += 1
+            layer_steps += len(layers) * w.steps
+            del caches
             if spent >= budget_s:
                 break
-    layer_steps = len(layers) * len(steps)
-    us = spent / done * len(units) / layer_steps * 1e6
+    us = spent / layer_steps * 1e6
     return {"value": round(us, 1), "unit": "us/layer-step", "cores": 1, "kind": "oracle",
-            "sample": (f"{done} of {len(units)} (batch, kv-head) units x {layer_steps} "
-                       f"layer-steps (layers {layers[0]}-{layers[-1]}, steps {steps[0]}-{steps[-1]}); "
-                       f"{spent:.1f} s; scaled to all units"),
+            "sample": (f"{layer_steps // w.steps} of {run.L} layers x {w.steps} decode steps x all "
+                       f"{len(units)} (batch, kv-head) units; {spent:.1f} s of oracle time; "
+                       "per layer-step"),
             "cpu": platform.processor() or platform.machine()}
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+
+def committed_traffic(workload):
+    """HBM bytes per sparse-attention launch measured with rocprofv3 counters
+    (FETCH_SIZE and WRITE_SIZE, scaled by a plain-copy calibration) and
+    recorded in profiles/; None when there is no record for this workload or
+    the attention kernel source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_split_bf16_{workload}_pmc.md")
+    src = os.path.join(ROOT, "paper_2602_08329_amd", "csrc", "attention.hip")
+    if not os.path.exists(path) or not os.path.exists(src):
+        return None
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("attention.hip sha256") != digest:
+        return None
+    try:
+        return int(fields["traffic bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """A plain device-to-device copy of 1 GiB, repeated 5 times: the kernel of
+    known size against which FETCH_SIZE and WRITE_SIZE are scaled."""
+    import torch
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": round(ms, 4),
+                      "gbps": round(2 * n / ms / 1e6, 1)}), flush=True)
 
 
 def main():
@@ -112,7 +169,12 @@ def main():
     ap.add_argument("--nmax", type=int, default=None, help="workload 4: max context")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
@@ -197,27 +259,17 @@ def main():
     ms_attn, _ = timed(attn_only, "attention only")
     ms_dense, _ = timed(run.dense_step, "dense attention")
 
-    # dominant kernel: the sparse attention launch, timed per launch with events
-    starts, ends, launch_bytes = [], [], []
-    for j in js:
-        run.selection_step(j)
-        for l in range(run.L):
-            a = torch.cuda.Event(enable_timing=True)
-            z = torch.cuda.Event(enable_timing=True)
-            a.record()
-            run.attend(l, j)
-            z.record()
-            starts.append(a)
-            ends.append(z)
-            e = 4 if w.dtype == "f32" else 2
-            launch_bytes.append(set_lens[(l, j)] * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e
-                                + w.batch * w.hq * (w.d + 1) * 4)
-    torch.cuda.synchronize()
-    durs = [a.elapsed_time(z) * 1e-3 for a, z in zip(starts, ends)]
-    avg_dur = sum(durs) / len(durs)
+    # dominant kernel: the sparse attention launch.  Its average duration is
+    # the back-to-back attention-only loop above (HIP events on the launch
+    # stream, over the timed region); its bytes are the per-launch algorithmic
+    # bytes averaged over the same launches.
+    e = 4 if w.dtype == "f32" else 2
+    launch_bytes = [set_lens[(l, j)] * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e
+                    + w.batch * w.hq * (w.d + 1) * 4 for j in js for l in range(run.L)]
     avg_bytes = sum(launch_bytes) / len(launch_bytes)
+    avg_dur = ms_attn * 1e-3 / (K_steps * run.L)
     achieved = avg_bytes / avg_dur / 1e9
-
+    traffic = committed_traffic(w.name)
     L = run.L
     total_bytes = sum(per[j]["attn"] + per[j]["sel"] for j in js)
     us_layer_step = ms_sparse * 1e3 / (K_steps * L)
@@ -252,8 +304,8 @@ def main():
             "kernel": "attn_split_bf16 (sparse)" if w.dtype != "f32" else "attn_split_f32 (sparse)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None, "avg_launch_us": round(avg_dur * 1e6, 3),
-            "avg_launch_bytes": int(avg_bytes), "launches": len(durs),
+            "traffic": traffic, "avg_launch_us": round(avg_dur * 1e6, 3),
+            "avg_launch_bytes": int(avg_bytes), "launches": len(launch_bytes),
         },
     }
     if not args.no_cpu_baseline:

@@ -66,7 +66,7 @@ typedef enum prhs_layout {
                               slot i % page_size */
 } prhs_layout;
 
-/* The KV cache of one layer (Sec. 3.1: K^h, V^h in R^{L x d} per head). */
+/* The KV cache of one layer (Sec. 2.1: K^h, V^h in R^{L x d} per head). */
 typedef struct prhs_kv {
   int32_t batch;          /* B >= 0 */
   int32_t num_q_heads;    /* Hq >= 1 */
@@ -137,7 +137,7 @@ prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params
 int32_t prhs_schedule(int32_t step, int32_t layer, const prhs_params* params);
 
 /* Refresh: score, top-k and anchor set for one layer (Sec. 4.1 Selection
- * Criteria; top-k oracle of Sec. 3.3).
+ * Criteria; top-k oracle of Sec. 2.3).
  *
  * For every (b, kv head g) with anchor length n0 = seq_lens[b]:
  *   sigma_i = max over the g-th group's query heads h of q[b][h] . k_i (raw
@@ -166,7 +166,7 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
                         void* ws, size_t ws_bytes, void* stream);
 
 /* Reuse: build the dilated shared set of a later step or another layer of the
- * group (Def. 3.2 key-value sharing; Eq. neighboring).
+ * group (Def. 3.2 key-value sharing, Sec. 2.2; Eq. neighboring).
  *
  * For every (b, g), with n0 = anchor_lens[b] (the anchor's length at its
  * refresh), n = seq_lens[b] >= n0, S* = topk_idx[b][g][0 .. topk_len) as
@@ -183,7 +183,7 @@ prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t 
                               int32_t* set_idx, int32_t* set_len, int32_t set_cap,
                               void* stream);
 
-/* Token-sparse decode attention (Def. 3.1) over per-kv-head index sets.
+/* Token-sparse decode attention (Def. 3.1, Sec. 2.2) over per-kv-head index sets.
  *
  * For every (b, query head h) with g = h / (Hq/Hkv) and
  * S = set_idx[b][g][0 .. min(set_len[b][g], set_cap)):

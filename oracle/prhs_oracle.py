@@ -10,7 +10,7 @@ explicit ordering wherever order matters.  Token positions are 0-based; the
 paper counts from 1.  Each function names the passage of the paper it follows
 ("Near-Oracle KV Selection via Pre-hoc Sparsity for Long-Context Inference").
 
-Readings of passages that the paper leaves open (all listed in the design doc):
+Readings of passages that the paper leaves open:
 
 * Positions are 0-based and ranges half-open.  The current decode token is
   already in the cache, so a query at context length ``n`` attends ``[0, n)``
@@ -67,7 +67,7 @@ __all__ = [
 
 
 # ---------------------------------------------------------------------------
-# Attention (Sec. 3.1, Eq. attn_eq)
+# Attention (Sec. 2.1, Eq. attn_eq)
 # ---------------------------------------------------------------------------
 
 def _f64(x):
@@ -114,7 +114,7 @@ def dense_attention(q, K, V, scale=None):
 
 
 def sparse_attention(q, K, V, S, scale=None):
-    """Token-sparse attention restricted to the index set S (Def. 3.1).
+    """Token-sparse attention restricted to the index set S (Def. 3.1, Sec. 2.2).
 
     The weights are the softmax over S only, i.e. the renormalised distribution
     A_i / tau_S of the unified-bounds appendix.  Returns (y, lse); an empty S
@@ -127,7 +127,7 @@ def sparse_attention(q, K, V, S, scale=None):
 
 
 # ---------------------------------------------------------------------------
-# Selection (Sec. 4.1, Selection Criteria; top-k oracle of Sec. 3.3)
+# Selection (Sec. 4.1, Selection Criteria; top-k oracle of Sec. 2.3)
 # ---------------------------------------------------------------------------
 
 def ranking_scores(Qg, K):
@@ -245,7 +245,7 @@ def retrieval_ratio(T, num_layers, s, G):
 
 
 # ---------------------------------------------------------------------------
-# Mass accounting (Sec. 3.3 and the unified-bounds appendix)
+# Mass accounting (Sec. 2.3 and the unified-bounds appendix)
 # ---------------------------------------------------------------------------
 
 def retained_mass(A, S):
@@ -281,7 +281,7 @@ def kl_divergence(P, Q):
 
 def family_best_dropped(A, n, sink, window, k):
     """Smallest dropped mass over the family sink U window U (any k middle
-    positions): the per-head top-k oracle of Sec. 3.3 restricted to the
+    positions): the per-head top-k oracle of Sec. 2.3 restricted to the
     middle range, with the current length as anchor length."""
     A = _f64(A)
     sink_end, win_start = region_bounds(n, sink, window)
@@ -317,7 +317,7 @@ class DecodeOracle:
 
     The anchor layer of a group at a refresh step attends its undilated
     critical set C(n0); every other (layer, step) attends the dilated shared
-    set built from the group's latest anchor top-k (Sec. 4.1 and Def. 3.2).
+    set built from the group's latest anchor top-k (Sec. 4.1 and Def. 3.2, Sec. 2.2).
     """
 
     def __init__(self, sink, window, s, G, r=1, k=None, k_num=0, k_den=0,

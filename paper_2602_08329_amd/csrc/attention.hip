@@ -476,15 +476,18 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
 }
 
 // Combines the split partials of one query head (grid: batch * num_q_heads,
-// 256 threads).  Split weights are computed once into LDS; the numerator sum
-// is spread over 256 / d split groups whose loads are all in flight at once.
+// 256 threads).  Every thread first loads all it needs (its splits' m, l and
+// numerators, for 256 / d split groups), so the kernel costs one memory
+// latency; the max, the weights and the sums follow in registers and LDS.
 // Units that fit one split were written by the split kernel and are skipped.
+constexpr int kMergePerThread = 16;
+
 template <int D, bool DENSE>
 __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   constexpr int SG = 256 / D;
-  extern __shared__ float s_w[];  // [nsplit] split weights
   __shared__ float s_red[SG][D];
-  __shared__ float s_part[4];
+  __shared__ float s_den[SG];
+  __shared__ float s_max[4];
   const int bh = blockIdx.x;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, u = b * hkv + h / G;
@@ -494,47 +497,54 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   const float* ml = a.part_ml + (size_t)bh * a.nsplit * 2;
   const float* po = a.part_o + (size_t)bh * a.nsplit * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // M = max_s m_s
-  float mx = -INFINITY;
-  for (int s = tid; s < nsp; s += 256) mx = fmaxf(mx, ml[2 * s]);
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-  if (lane == 0) s_part[wave] = mx;
-  __syncthreads();
-  const float M = fmaxf(fmaxf(s_part[0], s_part[1]), fmaxf(s_part[2], s_part[3]));
-  __syncthreads();
-  // weights and denominator
-  float den = 0.f;
-  for (int s = tid; s < nsp; s += 256) {
-    const float f = M == -INFINITY ? 0.f : exp2f(ml[2 * s] - M);
-    s_w[s] = f;
-    den += f * ml[2 * s + 1];
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) den += __shfl_xor(den, off);
-  if (lane == 0) s_part[wave] = den;
-  __syncthreads();
-  den = s_part[0] + s_part[1] + s_part[2] + s_part[3];
   const int sg = tid / D, dim = tid - sg * D;
-  float num = 0.f;
-  for (int s0 = sg; s0 < nsp; s0 += 4 * SG) {
-    float v[4], w[4];
+  float mx = -INFINITY, num = 0.f, den = 0.f;
+  for (int s0 = sg; s0 < nsp; s0 += SG * kMergePerThread) {
+    float m[kMergePerThread], l[kMergePerThread], o[kMergePerThread];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < kMergePerThread; ++k) {
       const int s = s0 + k * SG;
-      v[k] = s < nsp ? po[(size_t)s * D + dim] : 0.f;
-      w[k] = s < nsp ? s_w[s] : 0.f;
+      const bool ok = s < nsp;
+      m[k] = ok ? ml[2 * s] : -INFINITY;
+      l[k] = ok ? ml[2 * s + 1] : 0.f;
+      o[k] = ok ? po[(size_t)s * D + dim] : 0.f;
     }
+    // rescale the running sums to the new maximum of this thread
+    float bm = mx;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) num += w[k] * v[k];
+    for (int k = 0; k < kMergePerThread; ++k) bm = fmaxf(bm, m[k]);
+    if (bm != -INFINITY) {
+      const float r = exp2f(mx - bm);
+      num *= r;
+      den *= r;
+#pragma unroll
+      for (int k = 0; k < kMergePerThread; ++k) {
+        const float f = exp2f(m[k] - bm);
+        num += f * o[k];
+        den += f * l[k];
+      }
+      mx = bm;
+    }
   }
-  s_red[sg][dim] = num;
+  // block-wide maximum
+  float wm = mx;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
+  if (lane == 0) s_max[wave] = wm;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
+  const float f = (mx == -INFINITY || M == -INFINITY) ? 0.f : exp2f(mx - M);
+  s_red[sg][dim] = num * f;
+  if (dim == 0) s_den[sg] = den * f;
   __syncthreads();
   if (sg == 0) {
-    float tot = 0.f;
+    float tot = 0.f, dt = 0.f;
 #pragma unroll
-    for (int k = 0; k < SG; ++k) tot += s_red[k][dim];
-    write_final(a, bh, D, dim, M, tot, den);
+    for (int k = 0; k < SG; ++k) {
+      tot += s_red[k][dim];
+      dt += s_den[k];
+    }
+    write_final(a, bh, D, dim, M, tot, dt);
   }
 }
 
@@ -581,8 +591,8 @@ hipError_t launch_typed(const AttnArgs& a, int dtype, int units, int waves, hipS
                        stream, a);
   }
   if (a.nsplit > 1)
-    hipLaunchKernelGGL((attn_merge<D, DENSE>), dim3(a.kv.batch * a.kv.hq), dim3(256),
-                       (size_t)a.nsplit * sizeof(float), stream, a);
+    hipLaunchKernelGGL((attn_merge<D, DENSE>), dim3(a.kv.batch * a.kv.hq), dim3(256), 0, stream,
+                       a);
   return hipGetLastError();
 }
 

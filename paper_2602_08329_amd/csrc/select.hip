@@ -1,7 +1,7 @@
 // Refresh-step selection for one layer: ranking scores over the middle range,
 // exact top-k by multi-level radix select, ordering by (score desc, position
 // asc), and the critical set sink U top-k U window (Sec. 4.1 Selection
-// Criteria; top-k oracle of Sec. 3.3).
+// Criteria; top-k oracle of Sec. 2.3).
 //
 // Pipeline (one launch each, all on the caller's stream):
 //   select_clear   zero the per-row histograms and counters
@@ -14,6 +14,8 @@
 //                  composite (key, kIdxMax - pos) making every key distinct so
 //                  ties go to the lower position; bitonic sort of the k
 //                  winners in LDS; ordered compaction of the anchor set.
+#include <stdlib.h>
+
 #include "prhs.h"
 #include "prhs_internal.h"
 #include "setops.cuh"
@@ -145,9 +147,10 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
 // permutation of d shared by both operands.  Products of bf16 values are exact
 // in fp32 and the accumulation is fp32.  Each wave handles 64 keys per step
 // and prefetches its next step's 16 loads while multiplying the current one.
-template <int D>
+template <int D, int SUB = 4>
 struct ScoreStep {
-  bf16x8_t kf[4][D / 32];
+  static constexpr int kSub = SUB;  // 16-key sub-tiles per step
+  bf16x8_t kf[SUB][D / 32];
 };
 
 template <int D, bool PAGED>
@@ -161,13 +164,13 @@ __device__ __forceinline__ int32_t score_row(const SelArgs& a, const RowGeom& rg
   return (phys * a.kv.hkv + g) * a.kv.page_size + pos % a.kv.page_size;
 }
 
-template <int D, bool PAGED>
-__device__ __forceinline__ void score_load(ScoreStep<D>& S, const SelArgs& a, const RowGeom& rg,
+template <int D, bool PAGED, int SUB>
+__device__ __forceinline__ void score_load(ScoreStep<D, SUB>& S, const SelArgs& a, const RowGeom& rg,
                                            int b, int g, int t, int end, int p0,
                                            const int32_t* s_page, int col, int grp) {
   const __bf16* kbase = (const __bf16*)a.kv.k;
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < SUB; ++s) {
     const int32_t row = score_row<D, PAGED>(a, rg, b, g, t + s * 16 + col, end, p0, s_page);
     const uint4* kp = (const uint4*)(kbase + (int64_t)(row < 0 ? 0 : row) * D + grp * (D / 4));
 #pragma unroll
@@ -175,12 +178,12 @@ __device__ __forceinline__ void score_load(ScoreStep<D>& S, const SelArgs& a, co
   }
 }
 
-template <int D>
-__device__ __forceinline__ void score_consume(const ScoreStep<D>& S, const bf16x8_t* qf, int G,
+template <int D, int SUB>
+__device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const bf16x8_t* qf, int G,
                                               int gp, int t, int end, int col, int grp,
                                               uint32_t* keys, uint32_t* hist) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  for (int s = 0; s < SUB; ++s) {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk)
@@ -499,11 +502,13 @@ __device__ void radix_global(const SelArgs& a, uint32_t* cnt, uint2* sel, uint2*
   }
 }
 
-// Threshold T with exactly k of the n distinct composites in LDS buffer `buf`
-// at or above it (1 <= k <= n): radix select over 11-bit digits of the 54-bit
-// values, stopping as soon as a whole bin is taken.  Every thread must call it.
-__device__ uint64_t lds_kth_largest(const uint64_t* buf, uint32_t n, uint32_t k, uint32_t* h,
-                                    uint32_t* scan, int* s_bin, uint32_t* s_krem, uint32_t* s_cnt) {
+// Threshold T with exactly k of the n distinct composites get(0..n-1) at or
+// above it (1 <= k <= n): radix select over 11-bit digits of the 54-bit
+// values, stopping as soon as a whole bin is taken.  The values must be
+// readable from LDS.  Every thread must call it.
+template <typename Get>
+__device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, uint32_t* h, uint32_t* scan,
+                                    int* s_bin, uint32_t* s_krem, uint32_t* s_cnt) {
   const int tid = threadIdx.x;
   uint64_t prefix = 0, pmask = 0;
   uint32_t krem = k;
@@ -513,7 +518,7 @@ __device__ uint64_t lds_kth_largest(const uint64_t* buf, uint32_t n, uint32_t k,
     for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
     __syncthreads();
     for (uint32_t i = tid; i < n; i += kFinishBlock) {
-      const uint64_t x = buf[i];
+      const uint64_t x = get(i);
       if ((x & pmask) == prefix) atomicAdd(&h[(uint32_t)((x >> sh) & dmask)], 1u);
     }
     __syncthreads();
@@ -606,9 +611,10 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
   long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
   const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
-  const uint64_t c_k = kout < total ? lds_kth_largest(dyn, total, kout, h, scan, &s_bin, &s_krem, &s_cnt)
+  auto get = [&](uint32_t i) { return dyn[i]; };
+  const uint64_t c_k = kout < total ? lds_kth_largest(get, total, kout, h, scan, &s_bin, &s_krem, &s_cnt)
                                     : 0ull;
-  const uint64_t c_m = m > 0 ? lds_kth_largest(dyn, total, m, h, scan, &s_bin, &s_krem, &s_cnt)
+  const uint64_t c_m = m > 0 ? lds_kth_largest(get, total, m, h, scan, &s_bin, &s_krem, &s_cnt)
                              : ~0ull;
   uint32_t* bm = (uint32_t*)(dyn + a.sortcap);
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
@@ -630,7 +636,143 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   if (tid == 0) a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
 }
 
+// Whole refresh of one row in one workgroup, for many short rows: MFMA
+// scores of the middle range into LDS as order-preserving keys, the exact
+// k_b-th and m-th largest composite (key, position) by LDS radix select, and
+// ordered compactions in position order (the key array is already in
+// position order): top m, other winners, anchor set.  Contiguous bf16 caches
+// whose middle range fits LDS.
+template <int D>
+__global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
+  constexpr int KS = D / 32;
+  extern __shared__ uint32_t s_keys[];  // [middle length]
+  __shared__ uint32_t h[kHistBins];
+  __shared__ uint32_t scan[kFinishBlock / 64 + 1];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_krem, s_cnt;
+  const int row = blockIdx.x;
+  const int b = row / a.kv.hkv, g = row % a.kv.hkv;
+  const RowGeom rg = row_geom(a, b);
+  const int tid = threadIdx.x;
+  const int M = rg.m;
+  if (rg.kb > 0) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int G = a.kv.hq / a.kv.hkv;
+    const __bf16* q = (const __bf16*)a.q;
+    bf16x8_t qf[KS];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int qh = col < G ? col : 0;
+      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * (D / 4));
+      const uint4 v = qp[kk];
+      qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
+    }
+    int gp = 1;
+    while (gp < G) gp <<= 1;
+    constexpr int kStride = 32 * (kFinishBlock / 64);
+    const int t0 = wave * 32;
+    const int iters = t0 < M ? (M - t0 + kStride - 1) / kStride : 0;
+    if (iters > 0) {
+      ScoreStep<D, 2> A, B;
+      int t = t0;
+      score_load<D, false>(A, a, rg, b, g, t, M, 0, nullptr, col, grp);
+      int i = 0;
+      for (; i + 2 < iters; i += 2) {
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, col, grp);
+        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
+        score_load<D, false>(A, a, rg, b, g, t + 2 * kStride, M, 0, nullptr, col, grp);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, col, grp, s_keys, h);
+        t += 2 * kStride;
+      }
+      if (i + 1 < iters) {
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, col, grp);
+        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, col, grp, s_keys, h);
+      } else {
+        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
+      }
+    }
+  }
+  __syncthreads();
+  const int se = rg.sink_end;
+  auto get = [&](uint32_t i) {
+    return ((uint64_t)s_keys[i] << kIdxBits) | (uint64_t)(kIdxMax - (uint32_t)(se + (int)i));
+  };
+  const uint32_t kout = (uint32_t)rg.kb;
+  const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
+  long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
+  const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
+  const uint64_t c_k = kout > 0 && kout < (uint32_t)M
+                           ? lds_kth_largest(get, M, kout, h, scan, &s_bin, &s_krem, &s_cnt)
+                           : (kout > 0 ? 0ull : ~0ull);
+  const uint64_t c_m = m > 0 ? lds_kth_largest(get, M, m, h, scan, &s_bin, &s_krem, &s_cnt) : ~0ull;
+  // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept)
+  const int ept = (M + kFinishBlock - 1) / kFinishBlock;
+  const int i_begin = min(M, tid * ept), i_end = min(M, i_begin + ept);
+  uint32_t na = 0, nbk = 0;
+  if (kout > 0) {
+    for (int i = i_begin; i < i_end; ++i) {
+      const uint64_t x = get(i);
+      na += x >= c_m ? 1u : 0u;
+      nbk += (x >= c_k && x < c_m) ? 1u : 0u;
+    }
+  }
+  uint32_t tot;
+  const uint32_t pre = block_exclusive_scan<kFinishBlock>((na << 16) | nbk, scan, &tot);
+  int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
+  int32_t* out = a.set_idx + (size_t)row * a.set_cap;
+  uint32_t oa = pre >> 16, ob = m + (pre & 0xFFFFu), os = se + (pre >> 16) + (pre & 0xFFFFu);
+  if (kout > 0) {
+    for (int i = i_begin; i < i_end; ++i) {
+      const uint64_t x = get(i);
+      const int p = se + i;
+      if (x >= c_m) {
+        if (oa < (uint32_t)a.k_cap) topk[oa] = p;
+        ++oa;
+      } else if (x >= c_k) {
+        if (ob < (uint32_t)a.k_cap) topk[ob] = p;
+        ++ob;
+      }
+      if (x >= c_k) {
+        if (os < (uint32_t)a.set_cap) out[os] = p;
+        ++os;
+      }
+    }
+  }
+  for (int i = tid; i < se; i += kFinishBlock)
+    if (i < a.set_cap) out[i] = i;
+  int pos = se + (int)(tot >> 16) + (int)(tot & 0xFFFFu);
+  const int nw = rg.n0 - rg.win_start;
+  for (int i = tid; i < nw; i += kFinishBlock)
+    if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
+  if (nw > 0) pos += nw;
+  if (tid == 0) {
+    a.topk_len[row] = (int32_t)kout;
+    a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
+  }
+}
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
+constexpr int kFusedMinRows = 128;    // enough rows to occupy the chip one per CU
+
+// The fused path: bf16, contiguous, many rows, middle range within LDS.
+// PRHS_SELECT_PATH=fused|split overrides the choice (a tuning knob, read once
+// per process; the fused path still needs a contiguous bf16 cache that fits).
+bool use_fused_select(int dtype, bool paged, int rows, int mcap) {
+  static const int force = [] {
+    const char* e = getenv("PRHS_SELECT_PATH");
+    if (!e) return 0;
+    if (e[0] == 'f') return 1;
+    if (e[0] == 's') return -1;
+    return 0;
+  }();
+  if (dtype != 1 || paged || mcap > kFusedMaxKeys) return false;
+  if (force != 0) return force > 0;
+  return rows >= kFusedMinRows;
+}
 
 struct SelLayout {
   size_t keys, hist0, hist1, counters, sel, cand, cand2, total;
@@ -688,6 +830,25 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.set_len = s.set_len;
   a.set_cap = s.set_cap;
 
+  // many short contiguous bf16 rows: the whole refresh in one launch
+  if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {
+    const size_t dyn = (size_t)a.mcap * 4;
+    hipError_t e = hipSuccess;
+    if (s.kv.d == 128) {
+      if (dyn > 65536)
+        e = hipFuncSetAttribute((const void*)select_fused<128>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+      if (e == hipSuccess)
+        hipLaunchKernelGGL(select_fused<128>, dim3(rows), dim3(kFinishBlock), dyn, stream, a);
+    } else {
+      if (dyn > 65536)
+        e = hipFuncSetAttribute((const void*)select_fused<64>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+      if (e == hipSuccess)
+        hipLaunchKernelGGL(select_fused<64>, dim3(rows), dim3(kFinishBlock), dyn, stream, a);
+    }
+    return e != hipSuccess ? e : hipGetLastError();
+  }
   // the middle range is shorter than max_seq_len; size grids by max_seq_len
   const int mid_max = a.mcap;
   hipLaunchKernelGGL(select_clear, dim3(rows), dim3(256), 0, stream, a);

@@ -219,6 +219,17 @@ SELECT_CASES = [
     ("f32", "f32", 64, False, 4, 4, (1025, 300), dict(k=64, sink=4, window=32)),
     ("f32-paged-gqa", "f32", 128, True, 8, 2, (2000,), dict(k=50, sink=2, window=8)),
     ("big-k", "bf16", 128, False, 4, 1, (20000,), dict(k=9000, sink=4, window=64)),
+    # 16 sequences x 8 kv heads = 128 rows: the single-launch refresh path
+    ("fused-ragged", "bf16", 128, False, 32, 8,
+     (3000, 2100, 70, 1500, 999, 2048, 300, 2999, 1200, 640, 77, 2500, 1800, 33, 2222, 1024),
+     dict(k=150, sink=4, window=32)),
+    ("fused-mha-d64", "bf16", 64, False, 8, 8, (900, 1300) * 8, dict(k=60, sink=2, window=16)),
+    ("fused-k-ge-middle", "bf16", 128, False, 16, 8, (400, 150) * 8, dict(k=5000, sink=4, window=16)),
+    ("fused-k-zero", "bf16", 128, False, 16, 8, (400, 900) * 8, dict(k=0, sink=4, window=16)),
+    ("fused-short", "bf16", 128, False, 8, 8, (3, 20, 21, 22, 40, 60, 5, 1) * 2,
+     dict(k=5, sink=4, window=16)),
+    ("fused-ratio", "bf16", 128, False, 32, 8, (9000, 4100) * 8,
+     dict(k_num=1, k_den=20, sink=4, window=128)),
 ]
 
 
@@ -239,6 +250,16 @@ def test_select_all_ties_lowest_positions():
     p = B.params(k=200, sink=4, window=64)
     topk, tlen = check_select(inp, lens, p)
     assert list(topk[0, 0, :5]) == [4, 5, 6, 7, 8]   # the top m = the lowest positions
+
+
+def test_select_fused_all_ties():
+    # all scores equal on the single-launch path: ties go to the lower positions
+    lens = (2500, 1700) * 8
+    inp = synth.random_inputs(16, 8, 8, 128, lens, seed=14, grid=True, device=DEV)
+    for K in inp.K:
+        K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, 0.75)))
+    topk, tlen = check_select(inp, lens, B.params(k=120, sink=4, window=32))
+    assert list(topk[0, 0, :3]) == [4, 5, 6]
 
 
 def test_select_all_ties_beyond_lds_budget():
