@@ -5,7 +5,8 @@
 
 A step is one decode step of the whole hot path over every layer of the
 workload: refresh selection (score, top-k, anchor set) where the schedule asks
-for it, the dilated shared set of every layer group, and sparse decode
+for it, the dilated shared set of every layer group (built once per refresh;
+later steps attend it plus the tokens decoded since), and sparse decode
 attention of every layer.  Inputs are seeded synthetic tensors already
 resident in HBM.  The same steps are timed with dense decode attention for the
 speedup.  Prints one JSON line on stdout; progress goes to stderr.
@@ -36,7 +37,7 @@ def algorithmic_bytes(run, set_lens, sel_rows):
     attention: sum over (b, g) of |R| (2 d e + 4) + q + out/lse per layer;
     selection: middle keys (d e each) + q + 8 B per key of radix traffic +
     top-k and set writes, once per refresh of an anchor layer; reuse: top-k
-    read and set write per group."""
+    read and set write per shared-set build."""
     w = run.w
     e = 4 if w.dtype == "f32" else 2
     qbytes = w.batch * w.hq * w.d * e
@@ -51,9 +52,8 @@ def algorithmic_bytes(run, set_lens, sel_rows):
         if j % w.s == 0:
             m_rows, k_rows, c_rows = sel_rows[j]
             sel += m_rows * (w.d * e + 8) + run.groups * qbytes + (k_rows + c_rows) * 4
-        if w.G > 1 or j % w.s != 0:
-            for gi in range(run.groups):
-                sel += set_lens[("shared", gi, j)] * 4 + set_lens[("topk", gi, j)] * 4
+        for gi in run.shares_at(j):
+            sel += set_lens[("shared", gi, j)] * 4 + set_lens[("topk", gi, j)] * 4
         per[j] = dict(attn=attn, sel=sel)
     return per
 
@@ -169,6 +169,8 @@ def main():
     ap.add_argument("--nmax", type=int, default=None, help="workload 4: max context")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-step-sets", action="store_true",
+                    help="rebuild the dilated shared set at every step instead of once per refresh")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -202,7 +204,7 @@ def main():
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f} s; "
         f"{sum(x.numel() * x.element_size() for x in inp.K + inp.V) / 2**30:.1f} GiB of KV")
-    run = DecodeRunner(inp, dev)
+    run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets)
 
     # one untimed pass over all steps: set sizes for the byte accounting
     set_lens = {}
@@ -224,19 +226,23 @@ def main():
             set_lens[("shared", gi, j)] = sh[gi]
             set_lens[("topk", gi, j)] = tk[gi]
         for l in range(run.L):
-            s_idx, s_len = run.set_for(l, j)
-            set_lens[(l, j)] = int(s_len.sum().item())
+            s_idx, s_len, tail = run.set_for(l, j)
+            rows = int(s_len.sum().item())
+            if tail is not None:   # rows [n0_b, n_b) of every kv head follow the set
+                rows += int((run.seq_lens[j] - tail).sum().item()) * w.hkv
+            set_lens[(l, j)] = rows
         run.step(j)
     torch.cuda.synchronize()
     per = algorithmic_bytes(run, set_lens, sel_rows)
 
-    def timed(fn, label):
+    def timed(fn, label, order=None):
+        order = order or (lambda i: i % T)
         for i in range(W_steps):
-            fn(i % T)
+            fn(order(i))
         torch.cuda.synchronize()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
-        js = [(W_steps + i) % T for i in range(K_steps)]
+        js = [order(W_steps + i) for i in range(K_steps)]
         torch.cuda.synchronize()
         ev0.record()
         t = time.perf_counter()
@@ -253,10 +259,20 @@ def main():
     ms_sparse, js = timed(run.step, "sparse (selection + attention)")
     ms_sel, _ = timed(run.selection_step, "selection only")
 
+    # attention alone: the steps of the last refresh block, cycled, over the
+    # sets that block's selection produced (its sets and tails are exactly
+    # those of the byte accounting)
+    j_blk = ((T - 1) // w.s) * w.s
+    run.selection_step(j_blk)
+    if args.per_step_sets:   # the shared set is then rebuilt per step; keep the last one
+        for j in range(j_blk + 1, T):
+            run.selection_step(j)
+
     def attn_only(j):
         for l in range(run.L):
             run.attend(l, j)
-    ms_attn, _ = timed(attn_only, "attention only")
+    ms_attn, js_attn = timed(attn_only, "attention only",
+                             order=lambda i: j_blk + i % (T - j_blk))
     ms_dense, _ = timed(run.dense_step, "dense attention")
 
     # dominant kernel: the sparse attention launch.  Its average duration is
@@ -265,7 +281,7 @@ def main():
     # bytes averaged over the same launches.
     e = 4 if w.dtype == "f32" else 2
     launch_bytes = [set_lens[(l, j)] * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e
-                    + w.batch * w.hq * (w.d + 1) * 4 for j in js for l in range(run.L)]
+                    + w.batch * w.hq * (w.d + 1) * 4 for j in js_attn for l in range(run.L)]
     avg_bytes = sum(launch_bytes) / len(launch_bytes)
     avg_dur = ms_attn * 1e-3 / (K_steps * run.L)
     achieved = avg_bytes / avg_dur / 1e9
@@ -293,6 +309,7 @@ def main():
             "k": w.k if not w.k_den else f"{w.k_num}/{w.k_den} n", "window": w.window,
             "sink": w.sink, "refresh_every": w.s, "layer_group": w.G, "dilate_r": w.r,
             "paged": w.paged, "decode_steps_cycled": T,
+            "shared_sets": "per step" if args.per_step_sets else "per refresh + decoded tail",
         },
         "effective_gbps": round(eff_gbps, 1),
         "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),

@@ -200,6 +200,29 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q,
                                     int32_t set_cap, float scale, float* out, float* lse,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* Token-sparse decode attention over a reused set (Def. 3.2 key-value sharing,
+ * Sec. 2.2; Eq. neighboring): the shared set of a later decode step without
+ * rebuilding it.
+ *
+ * For n >= n0 the dilated shared set at length n is the one at the anchor
+ * length n0 followed by the positions decoded since, [n0, n): neighbours of
+ * the middle range never pass n0 - window + 1, and every position in [n0, n)
+ * lies in the recency window.  So one prhs_dilate_reuse call at
+ * seq_lens = anchor_lens serves every step of the block, and this call
+ * attends, for every (b, query head h) with g = h / (Hq/Hkv),
+ *   S = {i in set_idx[b][g][0 .. min(set_len[b][g], set_cap)) : i < n0}
+ *       U [n0, seq_lens[b]),   n0 = clamp(anchor_lens[b], 0, seq_lens[b]),
+ * with the same outputs as prhs_sparse_decode_attn over S.
+ * anchor_lens: [batch] int32 device array.  Precondition:
+ * set_len[b][g] + seq_lens[b] - n0 <= set_cap (prhs_set_capacity with this
+ * refresh period guarantees it); rows beyond set_cap are not attended.
+ * ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
+prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
+                                   const int32_t* set_idx, const int32_t* set_len,
+                                   int32_t set_cap, const int32_t* anchor_lens, float scale,
+                                   float* out, float* lse, void* ws, size_t ws_bytes,
+                                   void* stream);
+
 /* Dense decode attention over every cached key [0, seq_lens[b]) (Eq. attn_eq):
  * the baseline the sparse path is measured against, and the k = n special
  * case.  Same outputs and conventions as prhs_sparse_decode_attn.

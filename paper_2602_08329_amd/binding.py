@@ -39,7 +39,7 @@ PRHS_MAX_TOPK = 16384
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
-    "prhs_dense_decode_attn", "prhs_last_error",
+    "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_last_error",
 ]
 
 
@@ -101,6 +101,9 @@ def lib():
         L.prhs_sparse_decode_attn.restype = i32
         L.prhs_sparse_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, ctypes.c_float, vp, vp,
                                               vp, sz, vp]
+        L.prhs_reuse_decode_attn.restype = i32
+        L.prhs_reuse_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, vp, ctypes.c_float, vp,
+                                             vp, vp, sz, vp]
         L.prhs_dense_decode_attn.restype = i32
         L.prhs_dense_decode_attn.argtypes = [P(PrhsKv), vp, ctypes.c_float, vp, vp, vp, sz, vp]
         L.prhs_last_error.restype = ctypes.c_char_p
@@ -243,6 +246,24 @@ def prhs_sparse_decode_attn(kv, q, set_idx, set_len, scale, out, lse, ws, stream
     check(lib().prhs_sparse_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx), _ptr(set_len),
                                         set_idx.shape[-1], float(scale), _ptr(out), _ptr(lse),
                                         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def prhs_reuse_decode_attn(kv, q, set_idx, set_len, anchor_lens, scale, out, lse, ws,
+                           stream=None):
+    """Attention over set U [anchor_lens[b], n_b): the reused set of a later
+    step, with the set built once at the anchor length."""
+    _q_dtype(kv, q)
+    _need(set_idx, torch.int32, "set_idx", 3)
+    _need(set_len, torch.int32, "set_len", 2)
+    _need(anchor_lens, torch.int32, "anchor_lens", 1)
+    _need(out, torch.float32, "out", 3)
+    if lse is not None:
+        _need(lse, torch.float32, "lse", 2)
+    _need(ws, torch.uint8, "ws")
+    check(lib().prhs_reuse_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx), _ptr(set_len),
+                                       set_idx.shape[-1], _ptr(anchor_lens), float(scale),
+                                       _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
+                                       _stream(stream)))
 
 
 def prhs_dense_decode_attn(kv, q, scale, out, lse, ws, stream=None):

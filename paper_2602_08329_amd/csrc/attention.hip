@@ -51,6 +51,7 @@ struct AttnArgs {
   const void* q;
   const int32_t* set_idx;
   const int32_t* set_len;
+  const int32_t* tail_start;  // [B] or null: rows also cover [tail_start[b], n_b)
   int set_cap;
   float scale_log2;
   int chunk, nsplit;
@@ -60,12 +61,34 @@ struct AttnArgs {
   float* lse;
 };
 
+// The rows a unit attends, in order: the first `base` come from its index
+// set (entries at or beyond t0 are skipped), then the tail positions
+// [t0, t0 + L - base).  Dense: rows are the positions [0, n_b).  Without a
+// tail t0 = n_b.  L never exceeds set_cap, the bound the split geometry uses.
+struct UnitSpan {
+  int L, base, t0;
+};
+
 template <bool DENSE>
-__device__ __forceinline__ int unit_rows(const AttnArgs& a, int b, int u) {
-  if (DENSE) return kv_seq_len(a.kv, b);
+__device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, int nb) {
+  UnitSpan sp;
+  sp.t0 = nb;
+  if (DENSE) {
+    sp.L = sp.base = nb;
+    return sp;
+  }
   int L = a.set_len[u];
-  L = L < 0 ? 0 : L;
-  return L > a.set_cap ? a.set_cap : L;
+  L = L < 0 ? 0 : (L > a.set_cap ? a.set_cap : L);
+  sp.base = L;
+  if (a.tail_start) {
+    int t0 = a.tail_start[b];
+    t0 = t0 < 0 ? 0 : (t0 > nb ? nb : t0);
+    sp.t0 = t0;
+    L += nb - t0;
+    L = L > a.set_cap ? a.set_cap : L;
+  }
+  sp.L = L;
+  return sp;
 }
 
 // Row id (element offset / d) of position pos of (b, kv head g), or -1 when
@@ -89,13 +112,24 @@ __device__ __forceinline__ int32_t phys_row(const KvView& kv, int b, int g, int 
 // loads: two memory latencies for the whole chunk.  n <= blockDim * 8.
 template <bool DENSE, bool PAGED>
 __device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t* idx, int start, int n,
-                                           int nb, int b, int g, int32_t* s_row) {
+                                           const UnitSpan& sp, int nb, int b, int g,
+                                           int32_t* s_row) {
   int pos[kRowsPerThread];
 #pragma unroll
   for (int k = 0; k < kRowsPerThread; ++k) {
     const int r = threadIdx.x + k * blockDim.x;
+    const int t = start + r;
     pos[k] = -1;
-    if (r < n) pos[k] = DENSE ? start + r : idx[start + r];
+    if (r < n) {
+      if (DENSE) {
+        pos[k] = t;
+      } else if (t < sp.base) {
+        const int p = idx[t];
+        pos[k] = p < sp.t0 ? p : -1;
+      } else {
+        pos[k] = sp.t0 + (t - sp.base);
+      }
+    }
   }
 #pragma unroll
   for (int k = 0; k < kRowsPerThread; ++k) {
@@ -269,7 +303,9 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   const int split = blockIdx.x, u = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = u / hkv, g = u % hkv;
-  const int L = unit_rows<DENSE>(a, b, u);
+  const int nb = kv_seq_len(a.kv, b);
+  const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
+  const int L = sp.L;
   const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
     for (int e = threadIdx.x; e < G * D; e += blockDim.x)
@@ -278,7 +314,6 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   }
   if (start >= L) return;
   const int n = min(L, start + a.chunk) - start;
-  const int nb = kv_seq_len(a.kv, b);
   const int nwaves = blockDim.x >> 6;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
@@ -293,7 +328,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
   const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
-  stage_rows<DENSE, PAGED>(a, idx, start, n, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, idx, start, n, sp, nb, b, g, s_row);
 
   const __bf16* kb = (const __bf16*)a.kv.k;
   const __bf16* vb = (const __bf16*)a.kv.v;
@@ -380,7 +415,9 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   const int split = blockIdx.x, bh = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, g = h / G, u = b * hkv + g;
-  const int L = unit_rows<DENSE>(a, b, u);
+  const int nb = kv_seq_len(a.kv, b);
+  const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
+  const int L = sp.L;
   const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
     for (int dim = threadIdx.x; dim < D; dim += blockDim.x)
@@ -389,7 +426,6 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   }
   if (start >= L) return;
   const int n = min(L, start + a.chunk) - start;
-  const int nb = kv_seq_len(a.kv, b);
   const int nwaves = blockDim.x >> 6;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rg = lane >> 4, c = lane & 15;
@@ -398,7 +434,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < DPL; ++i) qv[i] = qp[i];
   const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
-  stage_rows<DENSE, PAGED>(a, idx, start, n, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, idx, start, n, sp, nb, b, g, s_row);
   const float* kb = (const float*)a.kv.k;
   const float* vb = (const float*)a.kv.v;
   float m_run = -INFINITY, l_run = 0.f, o[DPL];
@@ -491,7 +527,7 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   const int bh = blockIdx.x;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, u = b * hkv + h / G;
-  const int L = unit_rows<DENSE>(a, b, u);
+  const int L = unit_span<DENSE>(a, u, b, kv_seq_len(a.kv, b)).L;
   const int nsp = (L + a.chunk - 1) / a.chunk;
   if (nsp <= 1) return;
   const float* ml = a.part_ml + (size_t)bh * a.nsplit * 2;
@@ -658,6 +694,7 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.q = s.q;
   a.set_idx = s.set_idx;
   a.set_len = s.set_len;
+  a.tail_start = dense ? nullptr : s.tail_start;
   a.set_cap = s.set_cap;
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   const int rows_cap = dense ? s.kv.max_seq_len : s.set_cap;

@@ -260,8 +260,10 @@ prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t 
 }
 
 static prhs_status attention_common(const prhs_kv* kv, const void* q, const int32_t* set_idx,
-                                    const int32_t* set_len, int32_t set_cap, float scale, float* out,
-                                    float* lse, void* ws, size_t ws_bytes, void* stream, bool dense) {
+                                    const int32_t* set_len, int32_t set_cap,
+                                    const int32_t* tail_start, float scale, float* out, float* lse,
+                                    void* ws, size_t ws_bytes, void* stream, bool dense,
+                                    const char* name) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_kv_data(kv)) != PRHS_OK) return st;
@@ -284,26 +286,37 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   a.dtype = kv->dtype;
   a.set_idx = set_idx;
   a.set_len = set_len;
+  a.tail_start = tail_start;
   a.set_cap = set_cap;
   a.scale = scale;
   a.out = out;
   a.lse = lse;
   a.ws = ws;
-  return device_status(prhs::launch_attention(a, dense, (hipStream_t)stream),
-                       dense ? "prhs_dense_decode_attn launch" : "prhs_sparse_decode_attn launch");
+  return device_status(prhs::launch_attention(a, dense, (hipStream_t)stream), name);
 }
 
 prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int32_t* set_idx,
                                     const int32_t* set_len, int32_t set_cap, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream) {
-  return attention_common(kv, q, set_idx, set_len, set_cap, scale, out, lse, ws, ws_bytes, stream,
-                          false);
+  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, scale, out, lse, ws, ws_bytes,
+                          stream, false, "prhs_sparse_decode_attn launch");
+}
+
+prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32_t* set_idx,
+                                   const int32_t* set_len, int32_t set_cap,
+                                   const int32_t* anchor_lens, float scale, float* out, float* lse,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  if (kv && kv->batch > 0 && !anchor_lens)
+    return fail(PRHS_E_INVALID, "anchor_lens must be non-NULL");
+  return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, scale, out, lse, ws,
+                          ws_bytes, stream, false, "prhs_reuse_decode_attn launch");
 }
 
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return attention_common(kv, q, nullptr, nullptr, 0, scale, out, lse, ws, ws_bytes, stream, true);
+  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, scale, out, lse, ws, ws_bytes,
+                          stream, true, "prhs_dense_decode_attn launch");
 }
 
 }  // extern "C"

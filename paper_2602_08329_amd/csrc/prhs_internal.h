@@ -145,6 +145,7 @@ struct AttnLaunch {
   int dtype;
   const int32_t* set_idx;  // null for dense
   const int32_t* set_len;
+  const int32_t* tail_start;  // [B] or null (reuse attention: set U [tail_start, n))
   int set_cap;
   float scale;
   float* out;

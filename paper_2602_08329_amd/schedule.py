@@ -4,11 +4,16 @@ sharing, layer groups).
 For decode step j and layer l:
   * (l, j) with prhs_schedule == REFRESH (j % s == 0 and l % G == 0) runs
     prhs_select on its own q and K, then attends its critical set C(n0);
-  * once per (group, step) where some layer reuses, prhs_dilate_reuse builds
-    the dilated shared set R(n) from the group's latest top-k;
-  * every other layer of the group attends R(n) over its own K/V.
-The carried state is the per-group top-k buffer and the anchor lengths n0,
-which are simply the sequence lengths of the refresh step.
+  * every other layer of the group attends the dilated shared set R(n) over
+    its own K/V.
+R(n) is R(n0) followed by the positions decoded since the anchor, [n0, n)
+(dilated neighbours of the middle range stay below n0 and [n0, n) lies in the
+recency window).  By default prhs_dilate_reuse therefore runs once per
+refresh, at n = n0, and later steps attend R(n0) plus that tail through
+prhs_reuse_decode_attn.  With per_step_sets=True it instead builds R(n) at
+every step and attends it with prhs_sparse_decode_attn.
+The carried state is the per-group top-k buffer, the shared set and the anchor
+lengths n0, which are simply the sequence lengths of the refresh step.
 """
 
 from __future__ import annotations
@@ -24,8 +29,9 @@ class DecodeRunner:
     """Runs the hot path of a synthetic workload (paper_2602_08329_amd.synth)
     whose inputs already live on the GPU."""
 
-    def __init__(self, inp, device="cuda", dense=False):
+    def __init__(self, inp, device="cuda", per_step_sets=False):
         w = inp.w
+        self.per_step_sets = per_step_sets
         self.w = w
         self.inp = inp
         self.device = torch.device(device)
@@ -71,25 +77,45 @@ class DecodeRunner:
                       self.topk_len[gi], self.anchor_set[gi], self.anchor_len[gi], self.ws_select)
         self.anchor_step[gi] = j
 
-    def share(self, gi, j):
+    def _anchor(self, gi, j):
         j0 = self.anchor_step[gi]
         if j0 is None or j - j0 >= self.w.s or j < j0:
             raise RuntimeError(f"group {gi} has no anchor for step {j}")
+        return j0
+
+    def share(self, gi, j):
+        j0 = self._anchor(gi, j)
+        n = self.seq_lens[j] if self.per_step_sets else self.seq_lens[j0]
         B.prhs_dilate_reuse(self.params, self.topk_idx[gi], self.topk_len[gi], self.seq_lens[j0],
-                            self.seq_lens[j], self.shared_set[gi], self.shared_len[gi])
+                            n, self.shared_set[gi], self.shared_len[gi])
+
+    def shares_at(self, j):
+        """Groups whose shared set is (re)built at step j."""
+        w = self.w
+        if self.per_step_sets:
+            return list(range(self.groups)) if (w.G > 1 or j % w.s != 0) else []
+        return list(range(self.groups)) if (j % w.s == 0 and (w.G > 1 or w.s > 1)) else []
 
     def set_for(self, l, j):
-        """(set, len) tensors that layer l attends at step j."""
+        """(set, len, tail_start) that layer l attends at step j: the rows are
+        set[:len], then [tail_start[b], n_b) when tail_start is not None."""
         gi = l // self.w.G
         if B.prhs_schedule(j, l, self.params) == B.PRHS_REFRESH:
-            return self.anchor_set[gi], self.anchor_len[gi]
-        return self.shared_set[gi], self.shared_len[gi]
+            return self.anchor_set[gi], self.anchor_len[gi], None
+        j0 = self._anchor(gi, j)
+        tail = None if self.per_step_sets else self.seq_lens[j0]
+        return self.shared_set[gi], self.shared_len[gi], tail
 
     def attend(self, l, j, out=None, lse=None):
-        s, n = self.set_for(l, j)
-        B.prhs_sparse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.scale,
-                                  self.out if out is None else out,
-                                  self.lse if lse is None else lse, self.ws_attn)
+        s, n, tail = self.set_for(l, j)
+        out = self.out if out is None else out
+        lse = self.lse if lse is None else lse
+        if tail is None:
+            B.prhs_sparse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.scale, out, lse,
+                                      self.ws_attn)
+        else:
+            B.prhs_reuse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, tail, self.scale, out,
+                                     lse, self.ws_attn)
 
     def dense(self, l, j, out=None, lse=None):
         B.prhs_dense_decode_attn(self.kv[l][j], self.inp.q[l, j], self.scale,
@@ -100,10 +126,11 @@ class DecodeRunner:
     def selection_step(self, j):
         """Refresh and reuse-set construction of step j for every group."""
         w = self.w
+        shares = set(self.shares_at(j))
         for gi in range(self.groups):
             if j % w.s == 0:
                 self.refresh(gi, j)
-            if w.G > 1 or j % w.s != 0:
+            if gi in shares:
                 self.share(gi, j)
 
     def step(self, j, outs=None):

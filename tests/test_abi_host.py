@@ -170,6 +170,20 @@ def test_attention_validation(L):
     st = L.prhs_sparse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 300, float("nan"), 0x4, None,
                                    0x5, n.value, None)
     assert st == B.PRHS_E_INVALID
+    # the reuse variant: same checks plus its anchor lengths
+    st = L.prhs_reuse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 300, None, 0.1, 0x4, None, 0x5,
+                                  n.value, None)
+    assert st == B.PRHS_E_INVALID
+    assert b"anchor_lens" in L.prhs_last_error()
+    st = L.prhs_reuse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 300, 0x6, 0.1, 0x4, None, 0x5,
+                                  n.value - 1, None)
+    assert st == B.PRHS_E_WORKSPACE
+    st = L.prhs_reuse_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, -1, 0x6, 0.1, 0x4, None, 0x5,
+                                  n.value, None)
+    assert st == B.PRHS_E_INVALID
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert L.prhs_reuse_decode_attn(ctypes.byref(kv0), None, None, None, 8, None, 0.1, None, None,
+                                    None, 0, None) == B.PRHS_OK
     st = L.prhs_dense_decode_attn(ctypes.byref(_kv(head_dim=80)), 0x1, 0.1, 0x4, None, 0x5, 1 << 30,
                                   None)
     assert st == B.PRHS_E_UNSUPPORTED

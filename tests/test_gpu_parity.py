@@ -335,3 +335,104 @@ def test_dilate_reuse_bit_exact():
                 R = O.reuse_set(S, m, p.dilate_r, lens0[b], lens[b], p.sink, p.window)
                 assert slen[b, g] == len(R), f"step {j} b{b} g{g}"
                 assert np.array_equal(sidx[b, g, : len(R)], R), f"step {j} b{b} g{g}"
+
+
+def run_reuse(inp, lens, idx, ln, anchor, layer=0, step=0):
+    w = inp.w
+    kv, _ = kv_for(inp, lens, layer)
+    out = torch.full((w.batch, w.hq, w.d), float("nan"), device=DEV)
+    lse = torch.full((w.batch, w.hq), float("nan"), device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv, None, idx.shape[-1]), DEV)
+    B.prhs_reuse_decode_attn(kv, inp.q[layer, step], idx, ln, lens_tensor(anchor),
+                             1 / math.sqrt(w.d), out, lse, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype,d,paged,hq,hkv", [("bf16", 128, False, 8, 2),
+                                                  ("bf16", 128, True, 32, 8),
+                                                  ("f32", 64, False, 4, 4)])
+def test_reuse_attention_equals_per_step_set(dtype, d, paged, hq, hkv):
+    # set built once at the anchor length, attended at later lengths with the
+    # tail [n0, n): same rows, same outputs as the oracle over R(n)
+    lens0 = (3000, 700, 40)
+    steps = 8
+    inp = synth.random_inputs(3, hq, hkv, d, lens0, dtype=dtype, paged=paged, seed=41 + d,
+                              grid=True, steps=steps, device=DEV)
+    p = B.params(k=150, sink=4, window=32, dilate_r=1, refresh_every=steps)
+    topk, tlen, _, _ = run_select(inp, lens0, p)
+    ref = oracle_select(inp, lens0, p)
+    set_cap = B.prhs_set_capacity(p, inp.w.capacity)
+    sidx = torch.zeros(3, hkv, set_cap, dtype=torch.int32, device=DEV)
+    slen = torch.zeros(3, hkv, dtype=torch.int32, device=DEV)
+    anchor = lens_tensor(lens0)
+    B.prhs_dilate_reuse(p, torch.tensor(topk, device=DEV), torch.tensor(tlen, device=DEV),
+                        anchor, anchor, sidx, slen)
+    gq = hq // hkv
+    for j in (0, 1, steps - 1):
+        lens = tuple(n + j for n in lens0)
+        y, lse = run_reuse(inp, lens, sidx, slen, lens0, step=j)
+        for (b, g), (S, _) in ref.items():
+            kb = O.budget_k(lens0[b], p.k, p.k_num, p.k_den)
+            R = O.reuse_set(S, O.dilation_m(kb, len(S)), 1, lens0[b], lens[b], 4, 32)
+            K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+            Qg = synth.query_group(inp, 0, j, b, g)
+            for i in range(gq):
+                yr, lr = O.sparse_attention(Qg[i], K, V, R)
+                assert_close(y[b, g * gq + i], lse[b, g * gq + i], yr, lr, TOL[dtype],
+                             f"step {j} b{b} g{g}")
+
+
+def test_reuse_attention_skips_set_entries_past_anchor():
+    # set entries at or beyond n0 are covered by the tail and not attended
+    # twice; an anchor length of 0 leaves only the tail [0, n): dense attention;
+    # an anchor length past n is clamped to n (no tail)
+    lens = (900, 260, 50)
+    inp = synth.random_inputs(3, 8, 2, 128, lens, seed=43, grid=False, device=DEV)
+    cap = 1000
+    sets = {(0, 0): list(range(0, 900, 3)), (0, 1): list(range(850, 900)),
+            (1, 0): list(range(260)), (1, 1): [5, 100, 259],
+            (2, 0): [0, 1, 2], (2, 1): []}
+    anchor = (600, 0, 70)
+    idx = torch.zeros(3, 2, cap, dtype=torch.int32)
+    ln = torch.zeros(3, 2, dtype=torch.int32)
+    for (b, g), S in sets.items():
+        idx[b, g, : len(S)] = torch.tensor(S, dtype=torch.int32)
+        ln[b, g] = len(S)
+    y, lse = run_reuse(inp, lens, idx.to(DEV), ln.to(DEV), anchor)
+    for (b, g), S in sets.items():
+        n0 = min(max(anchor[b], 0), lens[b])
+        R = sorted(set(i for i in S if i < n0) | set(range(n0, lens[b])))
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, 0, b, g)
+        for i in range(4):
+            yr, lr = O.sparse_attention(Qg[i], K, V, R)
+            assert_close(y[b, g * 4 + i], lse[b, g * 4 + i], yr, lr, TOL["bf16"], f"b{b} g{g}")
+    yd, ld = run_dense(inp, lens)
+    assert np.abs(y[1] - yd[1]).max() <= 2e-3 * np.abs(yd[1]).max()
+
+
+def test_reuse_attention_many_splits_ragged():
+    # several splits per unit and a tail crossing split boundaries
+    lens0 = (20000, 9000)
+    inp = synth.random_inputs(2, 32, 8, 128, lens0, seed=47, grid=True, steps=8, device=DEV)
+    p = B.params(k=1500, sink=4, window=128, dilate_r=1, refresh_every=8)
+    topk, tlen, _, _ = run_select(inp, lens0, p)
+    ref = oracle_select(inp, lens0, p)
+    set_cap = B.prhs_set_capacity(p, inp.w.capacity)
+    sidx = torch.zeros(2, 8, set_cap, dtype=torch.int32, device=DEV)
+    slen = torch.zeros(2, 8, dtype=torch.int32, device=DEV)
+    anchor = lens_tensor(lens0)
+    B.prhs_dilate_reuse(p, torch.tensor(topk, device=DEV), torch.tensor(tlen, device=DEV),
+                        anchor, anchor, sidx, slen)
+    j = 7
+    lens = tuple(n + j for n in lens0)
+    y, lse = run_reuse(inp, lens, sidx, slen, lens0, step=j)
+    for (b, g) in [(0, 0), (0, 7), (1, 3)]:
+        S = ref[(b, g)][0]
+        R = O.reuse_set(S, O.dilation_m(1500, len(S)), 1, lens0[b], lens[b], 4, 128)
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, j, b, g)
+        for i in range(4):
+            yr, lr = O.sparse_attention(Qg[i], K, V, R)
+            assert_close(y[b, g * 4 + i], lse[b, g * 4 + i], yr, lr, TOL["bf16"], f"b{b} g{g}")

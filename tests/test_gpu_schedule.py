@@ -47,14 +47,15 @@ class UnitCache:
         return self.c[key]
 
 
-def run_schedule(w, steps, units_out, units_set=None, layers=None):
+def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets=False):
     """Runs the runner and the oracle side by side; compares the sets of
     units_set (default: all units) and the outputs of units_out at every
     (layer, step).  The oracle reads a unit's keys only where the schedule
-    refreshes."""
+    refreshes.  A reused set attended with a tail is compared as the stored
+    set followed by the tail positions."""
     inp = synth.generate(w, device=DEV, layers=layers)
     L = len(inp.K)
-    run = DecodeRunner(inp, DEV)
+    run = DecodeRunner(inp, DEV, per_step_sets=per_step_sets)
     cache = UnitCache(inp)
     all_units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
     units_set = all_units if units_set is None else units_set
@@ -68,9 +69,10 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None):
         for l in range(L):
             out.fill_(float("nan"))
             run.attend(l, j, out, lse)
-            s_idx, s_len = run.set_for(l, j)
+            s_idx, s_len, tail = run.set_for(l, j)
             torch.cuda.synchronize()
             s_idx, s_len = s_idx.cpu().numpy(), s_len.cpu().numpy()
+            tail = None if tail is None else tail.cpu().numpy()
             y, ls = out.cpu().numpy(), lse.cpu().numpy()
             refresh = O.is_refresh(j, l, w.s, w.G)
             for (b, g) in units_set:
@@ -78,8 +80,12 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None):
                 Qg = synth.query_group(inp, l, j, b, g)
                 K_sel = synth.gather_unit(inp, l, b, g, n)[0] if refresh else None
                 S = dec[(b, g)].step_set(l, j, Qg, K_sel, n)
-                assert s_len[b, g] == len(S), f"l{l} j{j} b{b} g{g}: |set| {s_len[b, g]} != {len(S)}"
-                assert np.array_equal(s_idx[b, g, : len(S)], S), f"l{l} j{j} b{b} g{g}: set differs"
+                got = s_idx[b, g, : s_len[b, g]]
+                if tail is not None:
+                    assert tail[b] <= n and np.all(got < tail[b])
+                    got = np.concatenate([got, np.arange(tail[b], n)])
+                assert len(got) == len(S), f"l{l} j{j} b{b} g{g}: |set| {len(got)} != {len(S)}"
+                assert np.array_equal(got, S), f"l{l} j{j} b{b} g{g}: set differs"
                 if (b, g) in units_out:
                     K, V = cache.get(l, b, g)
                     for i in range(w.g):
@@ -99,10 +105,11 @@ def test_config0_full_schedule():
     run_schedule(w, range(w.steps), units)
 
 
-def test_config1_cut_schedule():
+@pytest.mark.parametrize("per_step_sets", [False, True])
+def test_config1_cut_schedule(per_step_sets):
     w = synth.workload(1).replace(layers=8, batch=2, n_ctx=(2048, 1500))
     units = {(b, g) for b in range(2) for g in (0, 17, 31)}
-    run_schedule(w, range(w.steps), units)
+    run_schedule(w, range(w.steps), units, per_step_sets=per_step_sets)
 
 
 def test_config2_cut_schedule():
@@ -117,10 +124,11 @@ def test_config3_cut_schedule_paged():
     run_schedule(w, range(w.steps), units)
 
 
-def test_config4_cut_schedule_ragged():
+@pytest.mark.parametrize("per_step_sets", [False, True])
+def test_config4_cut_schedule_ragged(per_step_sets):
     w = synth.workload(4, batch=4, nmax=4096).replace(layers=2)
     units = {(b, g) for b in range(4) for g in (0, 5)}
-    run_schedule(w, range(w.steps), units)
+    run_schedule(w, range(w.steps), units, per_step_sets=per_step_sets)
 
 
 # Full-size shapes: the benchmark's launch configuration per layer; a refresh

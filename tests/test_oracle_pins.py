@@ -216,6 +216,26 @@ def test_sets_brute_force_random():
             _reuse_by_definition(S, m, r, n0, n, sink, window)
 
 
+def test_reuse_set_grows_by_the_decoded_tail():
+    # R(n) = R(n0) followed by [n0, n) for every n >= n0: dilated neighbours of
+    # middle positions stay below n0 and [n0, n) lies in the window.  Checked
+    # against the set-by-definition, including window 0 and wide radii.
+    rng = np.random.default_rng(12)
+    for trial in range(400):
+        n0 = int(rng.integers(0, 40))
+        sink = int(rng.integers(0, 6))
+        window = int(rng.integers(0, 8))
+        k = int(rng.integers(0, 12))
+        r = int(rng.integers(0, 4))
+        sigma = rng.integers(-4, 5, size=max(n0, 1)).astype(np.float64)
+        S = O.topk_middle(sigma, n0, k, sink, window)
+        m = O.dilation_m(k, len(S))
+        base = _reuse_by_definition(S, m, r, n0, n0, sink, window)
+        assert all(i < n0 for i in base)
+        for n in range(n0, n0 + 6):
+            assert list(O.reuse_set(S, m, r, n0, n, sink, window)) == base + list(range(n0, n))
+
+
 def test_reuse_at_range_edges_and_overlaps():
     # top-m at the first and last middle positions; neighbours land in the
     # sink and window (no duplicates) or are clipped
