@@ -202,8 +202,8 @@ def prhs_workspace_size(op, kv=None, p=None, set_cap=0):
 
 
 def workspace(nbytes, device):
-    """A zero-filled device workspace (the attention entry points need zeros
-    before first use)."""
+    """A zero-filled device workspace.  No entry point needs its workspace
+    initialised; zeros keep runs reproducible."""
     return torch.zeros(max(1, nbytes), dtype=torch.uint8, device=device)
 
 

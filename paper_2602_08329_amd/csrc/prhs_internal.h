@@ -75,31 +75,33 @@ __device__ __forceinline__ int wave_append(bool pred, uint32_t* counter) {
 }
 
 // Exclusive prefix sum over a workgroup of BLOCK threads; `scratch` holds
-// BLOCK/64 + 1 words of LDS.  Returns this thread's exclusive prefix and the
-// block total in *total.  Must be reached by every thread.
-template <int BLOCK>
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scratch, uint32_t* total) {
+// BLOCK/64 + 1 elements of LDS.  Returns this thread's exclusive prefix and
+// the block total in *total.  Must be reached by every thread.  With T =
+// uint64_t, several narrow counters packed into one word scan together as
+// long as no field overflows.
+template <int BLOCK, typename T = uint32_t>
+__device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  uint32_t x = v;
+  T x = v;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    uint32_t y = __shfl_up(x, off);
+    T y = __shfl_up(x, off);
     if (lane >= off) x += y;
   }
   if (lane == 63) scratch[wave] = x;
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t run = 0;
+    T run = 0;
     for (int w = 0; w < BLOCK / 64; ++w) {
-      uint32_t t = scratch[w];
+      T t = scratch[w];
       scratch[w] = run;
       run += t;
     }
     scratch[BLOCK / 64] = run;
   }
   __syncthreads();
-  const uint32_t res = scratch[wave] + x - v;
+  const T res = scratch[wave] + x - v;
   *total = scratch[BLOCK / 64];
   __syncthreads();
   return res;

@@ -636,18 +636,72 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   if (tid == 0) a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
 }
 
+// Exact threshold of one selection target over the LDS key array: a key
+// with (key >> sh) > p is selected, and so are the first `take` keys (in
+// position order) with (key >> sh) == p.  take = 0xFFFFFFFF selects them
+// all.  Because ties go to the lower position, this is the same set as the
+// k largest (key, -position) composites.
+struct KeyThreshold {
+  int sh;
+  uint32_t p, take;
+};
+
+// Radix levels over the 32-bit key: bits [31:21], [20:10], [9:0].
+__device__ __forceinline__ int key_level_shift(int lv) { return lv == 0 ? 21 : (lv == 1 ? 10 : 0); }
+
+// Threshold for the kk largest of the n LDS keys (kk = 0 selects nothing,
+// kk >= n everything).  h0 holds the level-0 histogram (key >> 21) of all n
+// keys; h (which may be h0) is overwritten when a deeper level is needed.
+// Reached by every thread.
+__device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t kk,
+                                      const uint32_t* h0, uint32_t* h, uint32_t* scan, int* s_bin,
+                                      uint32_t* s_krem, uint32_t* s_cnt) {
+  if (kk == 0) return {0, 0xFFFFFFFFu, 0u};        // nothing: key > max never holds
+  if (kk >= n) return {0, 0u, 0xFFFFFFFFu};        // everything
+  const int tid = threadIdx.x;
+  KeyThreshold t = {21, 0u, 0u};
+  for (int lv = 0; lv < 3; ++lv) {
+    const int sh = key_level_shift(lv);
+    if (lv > 0) {
+      // histogram of the next digit over the keys that share the prefix
+      const int psh = key_level_shift(lv - 1);
+      const uint32_t dmask = lv == 1 ? 0x7FFu : 0x3FFu;
+      for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+      __syncthreads();
+      for (uint32_t i = tid; i < n; i += kFinishBlock) {
+        const uint32_t key = keys[i];
+        if ((key >> psh) == t.p) atomicAdd(&h[(key >> sh) & dmask], 1u);
+      }
+      __syncthreads();
+    }
+    find_threshold<kFinishBlock>(lv == 0 ? h0 : h, kk, scan, s_bin, s_krem, s_cnt);
+    const uint32_t bin = (uint32_t)*s_bin, krem = *s_krem, cnt = *s_cnt;
+    __syncthreads();
+    t.p = lv == 0 ? bin : ((t.p << (key_level_shift(lv - 1) - sh)) | bin);
+    t.sh = sh;
+    if (cnt == krem) {  // the whole bin is taken
+      t.take = 0xFFFFFFFFu;
+      return t;
+    }
+    kk = krem;
+  }
+  t.take = kk;  // the first kk keys equal to the full 32-bit threshold
+  return t;
+}
+
 // Whole refresh of one row in one workgroup, for many short rows: MFMA
-// scores of the middle range into LDS as order-preserving keys, the exact
-// k_b-th and m-th largest composite (key, position) by LDS radix select, and
-// ordered compactions in position order (the key array is already in
-// position order): top m, other winners, anchor set.  Contiguous bf16 caches
-// whose middle range fits LDS.
+// scores of the middle range into LDS as order-preserving keys with their
+// level-0 histogram, exact thresholds for the k_b and m largest, and one
+// ordered compaction in position order (the key array is already in position
+// order, which also settles ties): top m, other winners, anchor set.
+// Contiguous bf16 caches whose middle range fits LDS.
 template <int D>
 __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   constexpr int KS = D / 32;
   extern __shared__ uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFinishBlock / 64 + 1];
+  __shared__ uint64_t scan64[kFinishBlock / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt;
   const int row = blockIdx.x;
@@ -655,6 +709,8 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
   const int M = rg.m;
+  for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+  __syncthreads();
   if (rg.kb > 0) {
     const int lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -696,53 +752,67 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   }
   __syncthreads();
   const int se = rg.sink_end;
-  auto get = [&](uint32_t i) {
-    return ((uint64_t)s_keys[i] << kIdxBits) | (uint64_t)(kIdxMax - (uint32_t)(se + (int)i));
-  };
   const uint32_t kout = (uint32_t)rg.kb;
   const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
   long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
   const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
-  const uint64_t c_k = kout > 0 && kout < (uint32_t)M
-                           ? lds_kth_largest(get, M, kout, h, scan, &s_bin, &s_krem, &s_cnt)
-                           : (kout > 0 ? 0ull : ~0ull);
-  const uint64_t c_m = m > 0 ? lds_kth_largest(get, M, m, h, scan, &s_bin, &s_krem, &s_cnt) : ~0ull;
-  // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept)
+  // both searches start from the scoring histogram; each thread keeps its
+  // two bins in registers while the first search reuses h
+  static_assert(kHistBins == 2 * kFinishBlock, "two histogram bins per thread");
+  const uint32_t h_lo = h[tid], h_hi = h[tid + kFinishBlock];
+  const KeyThreshold tm = key_threshold(s_keys, (uint32_t)M, m, h, h, scan, &s_bin, &s_krem, &s_cnt);
+  h[tid] = h_lo;
+  h[tid + kFinishBlock] = h_hi;
+  __syncthreads();
+  const KeyThreshold tk = key_threshold(s_keys, (uint32_t)M, kout, h, h, scan, &s_bin, &s_krem, &s_cnt);
+  // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept); one
+  // scan of four 16-bit counts gives every thread its output offsets (the
+  // middle range is below 2^16 keys here)
   const int ept = (M + kFinishBlock - 1) / kFinishBlock;
   const int i_begin = min(M, tid * ept), i_end = min(M, i_begin + ept);
-  uint32_t na = 0, nbk = 0;
-  if (kout > 0) {
-    for (int i = i_begin; i < i_end; ++i) {
-      const uint64_t x = get(i);
-      na += x >= c_m ? 1u : 0u;
-      nbk += (x >= c_k && x < c_m) ? 1u : 0u;
-    }
+  uint32_t gm = 0, em = 0, gk = 0, ek = 0;
+  for (int i = i_begin; i < i_end; ++i) {
+    const uint32_t xm = s_keys[i] >> tm.sh, xk = s_keys[i] >> tk.sh;
+    gm += xm > tm.p ? 1u : 0u;
+    em += xm == tm.p ? 1u : 0u;
+    gk += xk > tk.p ? 1u : 0u;
+    ek += xk == tk.p ? 1u : 0u;
   }
-  uint32_t tot;
-  const uint32_t pre = block_exclusive_scan<kFinishBlock>((na << 16) | nbk, scan, &tot);
+  uint64_t tot;
+  const uint64_t pre = block_exclusive_scan<kFinishBlock, uint64_t>(
+      (uint64_t)gm | ((uint64_t)em << 16) | ((uint64_t)gk << 32) | ((uint64_t)ek << 48), scan64,
+      &tot);
+  uint32_t rm = (uint32_t)(pre >> 16) & 0xFFFFu, rk = (uint32_t)(pre >> 48) & 0xFFFFu;
+  // winners before this thread's range: strictly above plus the earlier ties taken
+  const uint32_t before_m = ((uint32_t)pre & 0xFFFFu) + min(rm, tm.take);
+  const uint32_t before_k = ((uint32_t)(pre >> 32) & 0xFFFFu) + min(rk, tk.take);
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
-  uint32_t oa = pre >> 16, ob = m + (pre & 0xFFFFu), os = se + (pre >> 16) + (pre & 0xFFFFu);
-  if (kout > 0) {
-    for (int i = i_begin; i < i_end; ++i) {
-      const uint64_t x = get(i);
-      const int p = se + i;
-      if (x >= c_m) {
-        if (oa < (uint32_t)a.k_cap) topk[oa] = p;
-        ++oa;
-      } else if (x >= c_k) {
-        if (ob < (uint32_t)a.k_cap) topk[ob] = p;
-        ++ob;
-      }
-      if (x >= c_k) {
-        if (os < (uint32_t)a.set_cap) out[os] = p;
-        ++os;
-      }
+  uint32_t oa = before_m, ob = m + (before_k - before_m), os = se + before_k;
+  for (int i = i_begin; i < i_end; ++i) {
+    const uint32_t key = s_keys[i];
+    const uint32_t xm = key >> tm.sh, xk = key >> tk.sh;
+    const bool in_m = xm > tm.p || (xm == tm.p && rm < tm.take);
+    const bool in_k = xk > tk.p || (xk == tk.p && rk < tk.take);
+    rm += xm == tm.p ? 1u : 0u;
+    rk += xk == tk.p ? 1u : 0u;
+    const int p = se + i;
+    if (in_m) {
+      if (oa < (uint32_t)a.k_cap) topk[oa] = p;
+      ++oa;
+    } else if (in_k) {
+      if (ob < (uint32_t)a.k_cap) topk[ob] = p;
+      ++ob;
+    }
+    if (in_k) {
+      if (os < (uint32_t)a.set_cap) out[os] = p;
+      ++os;
     }
   }
+  const uint32_t total_k = ((uint32_t)(tot >> 32) & 0xFFFFu) + min((uint32_t)(tot >> 48) & 0xFFFFu, tk.take);
   for (int i = tid; i < se; i += kFinishBlock)
     if (i < a.set_cap) out[i] = i;
-  int pos = se + (int)(tot >> 16) + (int)(tot & 0xFFFFu);
+  int pos = se + (int)total_k;
   const int nw = rg.n0 - rg.win_start;
   for (int i = tid; i < nw; i += kFinishBlock)
     if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;

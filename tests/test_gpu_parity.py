@@ -436,3 +436,41 @@ def test_reuse_attention_many_splits_ragged():
         for i in range(4):
             yr, lr = O.sparse_attention(Qg[i], K, V, R)
             assert_close(y[b, g * 4 + i], lse[b, g * 4 + i], yr, lr, TOL["bf16"], f"b{b} g{g}")
+
+
+def test_split_merge_workspace_reused_across_calls():
+    # one attention workspace for consecutive calls whose units split a
+    # different number of ways (including one split and empty units): the
+    # merge of every call is complete and the workspace is left reusable.
+    inp = synth.random_inputs(2, 32, 8, 128, (9000, 3000), seed=53, grid=False, device=DEV)
+    rng = np.random.default_rng(53)
+    cap = 8200
+    kv, _ = kv_for(inp, (9000, 3000))
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv, None, cap), DEV)
+    for call in range(4):
+        lens = (9000 - 1000 * call, 3000 - 700 * call)
+        sets = {}
+        for b in range(2):
+            for g in range(8):
+                size = 0 if (b + g + call) % 7 == 0 else int(rng.integers(1, min(cap, lens[b]) + 1))
+                sets[(b, g)] = sorted(rng.choice(lens[b], size=size, replace=False).tolist())
+        kv, _ = kv_for(inp, lens)
+        idx = torch.zeros(2, 8, cap, dtype=torch.int32)
+        ln = torch.zeros(2, 8, dtype=torch.int32)
+        for (b, g), S in sets.items():
+            idx[b, g, : len(S)] = torch.tensor(S, dtype=torch.int32)
+            ln[b, g] = len(S)
+        out = torch.full((2, 32, 128), float("nan"), device=DEV)
+        lse = torch.full((2, 32), float("nan"), device=DEV)
+        B.prhs_sparse_decode_attn(kv, inp.q[0, 0], idx.to(DEV), ln.to(DEV), 1 / math.sqrt(128),
+                                  out, lse, ws)
+        torch.cuda.synchronize()
+        y, ls = out.cpu().numpy(), lse.cpu().numpy()
+        assert not np.isnan(y).any(), f"call {call}: unmerged heads"
+        for (b, g) in [(0, 0), (0, 5), (1, 2), (1, 7), ((call + 1) % 2, (call * 3) % 8)]:
+            K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+            Qg = synth.query_group(inp, 0, 0, b, g)
+            for i in range(4):
+                yr, lr = O.sparse_attention(Qg[i], K, V, sets[(b, g)])
+                assert_close(y[b, g * 4 + i], ls[b, g * 4 + i], yr, lr, TOL["bf16"],
+                             f"call {call} b{b} g{g}")
