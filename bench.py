@@ -35,9 +35,10 @@ def algorithmic_bytes(run, set_lens, sel_rows):
     """Bytes the method itself must move, per decode step j (dict j -> dict).
 
     attention: sum over (b, g) of |R| (2 d e + 4) + q + out/lse per layer;
-    selection: middle keys (d e each) + q + 8 B per key of radix traffic +
-    top-k and set writes, once per refresh of an anchor layer; reuse: top-k
-    read and set write per shared-set build."""
+    selection: middle keys (d e each) + q +
+    top-k, anchor-set and (when the refresh writes it) shared-set writes, once
+    per refresh of an anchor layer; a separate shared-set build reads the
+    top-k and writes the set."""
     w = run.w
     e = 4 if w.dtype == "f32" else 2
     qbytes = w.batch * w.hq * w.d * e
@@ -50,8 +51,8 @@ def algorithmic_bytes(run, set_lens, sel_rows):
             attn += total_set * (2 * w.d * e + 4) + qbytes + outbytes
         sel = 0
         if j % w.s == 0:
-            m_rows, k_rows, c_rows = sel_rows[j]
-            sel += m_rows * (w.d * e + 8) + run.groups * qbytes + (k_rows + c_rows) * 4
+            m_rows, k_rows, c_rows, s_rows = sel_rows[j]
+            sel += m_rows * w.d * e + run.groups * qbytes + (k_rows + c_rows + s_rows) * 4
         for gi in run.shares_at(j):
             sel += set_lens[("shared", gi, j)] * 4 + set_lens[("topk", gi, j)] * 4
         per[j] = dict(attn=attn, sel=sel)
@@ -219,7 +220,8 @@ def main():
                 mid += (max(se, n0 - w.window) - se) * w.hkv
             tl = int(run.topk_len.sum().item())
             al = int(run.anchor_len.sum().item())
-            sel_rows[j] = (mid * run.groups, tl, al)
+            sl = int(run.shared_len.sum().item()) if (run.reuses and not run.per_step_sets) else 0
+            sel_rows[j] = (mid * run.groups, tl, al, sl)
         sh = run.shared_len.sum(dim=(1, 2)).cpu().tolist()
         tk = run.topk_len.sum(dim=(1, 2)).cpu().tolist()
         for gi in range(run.groups):

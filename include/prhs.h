@@ -165,6 +165,25 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
                         int32_t* set_idx, int32_t* set_len, int32_t set_cap,
                         void* ws, size_t ws_bytes, void* stream);
 
+/* Refresh that also caches the dilated shared set (Sec. 4.4: the critical
+ * sets of shared heads are known ahead and can be prepared; Eq. neighboring).
+ *
+ * Same as prhs_select, and in the same launch also writes, for every (b, g),
+ *   shared_idx[b][g][0 .. shared_len) = the set prhs_dilate_reuse returns
+ *   for these params with anchor_lens = seq_lens = n0,
+ * i.e. [0, min(sink, n0)) U S* U {p + j : p in the top m, |j| <= r} U
+ * [n0 - window, n0) clipped to [0, n0), ascending and without duplicates.
+ * With prhs_reuse_decode_attn it serves every later step of the block and
+ * every other layer of the group, so no separate dilation call is needed.
+ * shared_idx: [batch][num_kv_heads][set_cap] int32, shared_len:
+ * [batch][num_kv_heads] int32.  set_cap (for both sets) must be at least
+ * prhs_set_capacity(params, max_seq_len). */
+prhs_status prhs_select_shared(const prhs_kv* kv, const void* q, const prhs_params* params,
+                               int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                               int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                               int32_t* shared_idx, int32_t* shared_len, void* ws,
+                               size_t ws_bytes, void* stream);
+
 /* Reuse: build the dilated shared set of a later step or another layer of the
  * group (Def. 3.2 key-value sharing, Sec. 2.2; Eq. neighboring).
  *

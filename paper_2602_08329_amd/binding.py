@@ -38,7 +38,7 @@ PRHS_MAX_TOPK = 16384
 
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
-    "prhs_schedule", "prhs_select", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
+    "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
     "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_last_error",
 ]
 
@@ -96,6 +96,9 @@ def lib():
         L.prhs_schedule.argtypes = [i32, i32, P(PrhsParams)]
         L.prhs_select.restype = i32
         L.prhs_select.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, i32, vp, vp, i32, vp, sz, vp]
+        L.prhs_select_shared.restype = i32
+        L.prhs_select_shared.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, i32, vp, vp, i32,
+                                         vp, vp, vp, sz, vp]
         L.prhs_dilate_reuse.restype = i32
         L.prhs_dilate_reuse.argtypes = [P(PrhsParams), i32, i32, vp, vp, i32, vp, vp, vp, vp, i32, vp]
         L.prhs_sparse_decode_attn.restype = i32
@@ -222,6 +225,24 @@ def prhs_select(kv, q, p, topk_idx, topk_len, set_idx, set_len, ws, stream=None)
     check(lib().prhs_select(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(topk_idx),
                             _ptr(topk_len), topk_idx.shape[-1], _ptr(set_idx), _ptr(set_len),
                             set_idx.shape[-1], _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def prhs_select_shared(kv, q, p, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len, ws,
+                       stream=None):
+    """prhs_select that also writes the dilated shared set at the anchor
+    length (shared_idx has the same capacity as set_idx)."""
+    _q_dtype(kv, q)
+    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
+                       (set_idx, "set_idx", 3), (set_len, "set_len", 2),
+                       (shared_idx, "shared_idx", 3), (shared_len, "shared_len", 2)):
+        _need(t, torch.int32, n, dims)
+    if shared_idx.shape != set_idx.shape:
+        raise ValueError("shared_idx must have the shape of set_idx")
+    _need(ws, torch.uint8, "ws")
+    check(lib().prhs_select_shared(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(topk_idx),
+                                   _ptr(topk_len), topk_idx.shape[-1], _ptr(set_idx),
+                                   _ptr(set_len), set_idx.shape[-1], _ptr(shared_idx),
+                                   _ptr(shared_len), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def prhs_dilate_reuse(p, topk_idx, topk_len, anchor_lens, seq_lens, set_idx, set_len, stream=None):

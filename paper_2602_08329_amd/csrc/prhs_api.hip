@@ -183,16 +183,19 @@ prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params
   }
 }
 
-prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* params,
-                        int32_t* topk_idx, int32_t* topk_len, int32_t k_cap, int32_t* set_idx,
-                        int32_t* set_len, int32_t set_cap, void* ws, size_t ws_bytes,
-                        void* stream) {
+static prhs_status select_common(const prhs_kv* kv, const void* q, const prhs_params* params,
+                                 int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                                 int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                                 int32_t* shared_idx, int32_t* shared_len, bool shared, void* ws,
+                                 size_t ws_bytes, void* stream, const char* name) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_params(params)) != PRHS_OK) return st;
   if ((st = check_kv_data(kv)) != PRHS_OK) return st;
   if (kv->batch > 0 && (!q || !topk_idx || !topk_len || !set_idx || !set_len))
     return fail(PRHS_E_INVALID, "q, topk_idx, topk_len, set_idx and set_len must be non-NULL");
+  if (shared && kv->batch > 0 && (!shared_idx || !shared_len))
+    return fail(PRHS_E_INVALID, "shared_idx and shared_len must be non-NULL");
   const int32_t kmax = prhs_max_topk(params, kv->max_seq_len);
   if (kmax > PRHS_MAX_TOPK)
     return fail(PRHS_E_UNSUPPORTED, "top-k of %d exceeds the sort limit %d", kmax, PRHS_MAX_TOPK);
@@ -200,8 +203,10 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
     return fail(PRHS_E_CAPACITY, "k_cap (%d) < largest top-k (%d)", k_cap, kmax);
   long long need = (long long)params->sink + kmax + params->window;
   if (need > kv->max_seq_len) need = kv->max_seq_len;
+  if (shared) need = prhs_set_capacity(params, kv->max_seq_len);
   if (set_cap < need || set_cap < 0)
-    return fail(PRHS_E_CAPACITY, "set_cap (%d) < anchor set bound (%lld)", set_cap, need);
+    return fail(PRHS_E_CAPACITY, "set_cap (%d) < %s bound (%lld)", set_cap,
+                shared ? "shared set" : "anchor set", need);
   const size_t wsz = prhs::select_workspace_bytes(kv->batch * kv->num_kv_heads, kv->max_seq_len, kmax);
   if (kv->batch > 0 && (!ws || ws_bytes < wsz))
     return fail(PRHS_E_WORKSPACE, "workspace of %zu bytes needed (got %zu)", wsz, ws_bytes);
@@ -222,9 +227,30 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
   a.set_idx = set_idx;
   a.set_len = set_len;
   a.set_cap = set_cap;
+  a.dilate_r = params->dilate_r;
+  a.shared_idx = shared ? shared_idx : nullptr;
+  a.shared_len = shared ? shared_len : nullptr;
   a.ws = ws;
   a.max_topk = kmax;
-  return device_status(prhs::launch_select(a, (hipStream_t)stream), "prhs_select launch");
+  return device_status(prhs::launch_select(a, (hipStream_t)stream), name);
+}
+
+prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* params,
+                        int32_t* topk_idx, int32_t* topk_len, int32_t k_cap, int32_t* set_idx,
+                        int32_t* set_len, int32_t set_cap, void* ws, size_t ws_bytes,
+                        void* stream) {
+  return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
+                       nullptr, nullptr, false, ws, ws_bytes, stream, "prhs_select launch");
+}
+
+prhs_status prhs_select_shared(const prhs_kv* kv, const void* q, const prhs_params* params,
+                               int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                               int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                               int32_t* shared_idx, int32_t* shared_len, void* ws,
+                               size_t ws_bytes, void* stream) {
+  return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
+                       shared_idx, shared_len, true, ws, ws_bytes, stream,
+                       "prhs_select_shared launch");
 }
 
 prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t num_kv_heads,

@@ -121,6 +121,9 @@ struct SelectLaunch {
   int32_t* set_idx;
   int32_t* set_len;
   int set_cap;
+  int dilate_r;
+  int32_t* shared_idx;  // optional: dilated shared set at the anchor length
+  int32_t* shared_len;
   void* ws;
   int max_topk;   // host bound on the clamped budget (sort size)
 };

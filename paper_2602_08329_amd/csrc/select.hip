@@ -55,6 +55,9 @@ struct SelArgs {
   int32_t* set_idx;
   int32_t* set_len;
   int set_cap;
+  int dilate_r;
+  int32_t* shared_idx;  // optional [rows][set_cap]: the dilated shared set at n0
+  int32_t* shared_len;
 };
 
 struct RowGeom {
@@ -634,6 +637,31 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
   if (nw > 0) pos += nw;
   if (tid == 0) a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
+  if (a.shared_idx) {
+    // dilated shared set at n0: the winners, the +-r neighbours of the top m
+    // inside the middle range (the others fall in the sink, the window or
+    // outside [0, n0)), then sink and window as above
+    int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
+    for (int i = tid; i < rg.sink_end; i += kFinishBlock)
+      if (i < a.set_cap) sh[i] = i;
+    const int r = a.dilate_r;
+    auto mark = [&](int seg_lo, int seg_hi, uint32_t* bmap) {
+      for (uint32_t i = tid; i < total; i += kFinishBlock) {
+        const uint64_t x = dyn[i];
+        if (x < c_k) continue;
+        const int p = composite_pos(x);
+        const int lo = max(x >= c_m ? p - r : p, seg_lo);
+        const int hi = min(x >= c_m ? p + r : p, seg_hi - 1);
+        for (int q = lo; q <= hi; ++q) mark_bit(bmap, seg_lo, q);
+      }
+    };
+    int pos2 = compact_marked<kFinishBlock>(rg.sink_end, rg.win_start, kFinishSegBits, mark, sh,
+                                            a.set_cap, rg.sink_end, bm, scan);
+    for (int i = tid; i < nw; i += kFinishBlock)
+      if (pos2 + i < a.set_cap) sh[pos2 + i] = rg.win_start + i;
+    if (nw > 0) pos2 += nw;
+    if (tid == 0) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
+  }
 }
 
 // Exact threshold of one selection target over the LDS key array: a key
@@ -765,6 +793,12 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   h[tid + kFinishBlock] = h_hi;
   __syncthreads();
   const KeyThreshold tk = key_threshold(s_keys, (uint32_t)M, kout, h, h, scan, &s_bin, &s_krem, &s_cnt);
+  // h becomes the bitmap of the dilated shared set over the middle indices
+  // (M <= 32 * kHistBins); the scan below orders the clearing before marking
+  const bool shared = a.shared_idx != nullptr;
+  const int mwords = (M + 31) >> 5;
+  if (shared)
+    for (int i = tid; i < mwords; i += kFinishBlock) h[i] = 0u;
   // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept); one
   // scan of four 16-bit counts gives every thread its output offsets (the
   // middle range is below 2^16 keys here)
@@ -808,6 +842,12 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
       if (os < (uint32_t)a.set_cap) out[os] = p;
       ++os;
     }
+    if (shared && in_k) {
+      // a top-m winner brings its +-r neighbours that stay in the middle range
+      const int lo = in_m ? max(0, i - a.dilate_r) : i;
+      const int hi = in_m ? min(M - 1, i + a.dilate_r) : i;
+      for (int j = lo; j <= hi; ++j) atomicOr(&h[j >> 5], 1u << (j & 31));
+    }
   }
   const uint32_t total_k = ((uint32_t)(tot >> 32) & 0xFFFFu) + min((uint32_t)(tot >> 48) & 0xFFFFu, tk.take);
   for (int i = tid; i < se; i += kFinishBlock)
@@ -821,11 +861,23 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
     a.topk_len[row] = (int32_t)kout;
     a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
   }
+  if (shared) {
+    __syncthreads();
+    int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
+    for (int i = tid; i < se; i += kFinishBlock)
+      if (i < a.set_cap) sh[i] = i;
+    int pos2 = compact_bitmap<kFinishBlock>(h, mwords, se, sh, a.set_cap, se, scan);
+    for (int i = tid; i < nw; i += kFinishBlock)
+      if (pos2 + i < a.set_cap) sh[pos2 + i] = rg.win_start + i;
+    if (nw > 0) pos2 += nw;
+    if (tid == 0) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
+  }
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
+static_assert(kFusedMaxKeys <= 32 * kHistBins, "the shared-set bitmap reuses the histogram");
 constexpr int kFusedMinRows = 128;    // enough rows to occupy the chip one per CU
 
 // The fused path: bf16, contiguous, many rows, middle range within LDS.
@@ -899,6 +951,9 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.set_idx = s.set_idx;
   a.set_len = s.set_len;
   a.set_cap = s.set_cap;
+  a.dilate_r = s.dilate_r;
+  a.shared_idx = s.shared_idx;
+  a.shared_len = s.shared_len;
 
   // many short contiguous bf16 rows: the whole refresh in one launch
   if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {

@@ -21,6 +21,36 @@ namespace prhs {
 constexpr int kSegBits = 262144;
 constexpr int kSegWords = kSegBits / 32;
 
+// Writes base + b for every set bit b of the LDS bitmap bm[0, nwords), in
+// ascending order, to out[pos ...] (entries at or past cap are dropped) and
+// returns pos plus the number of set bits.  `scan` holds BLOCK/64 + 1 words.
+// Every thread of the workgroup must call it; bm must be complete (a barrier
+// after the last mark).
+template <int BLOCK>
+__device__ int compact_bitmap(const uint32_t* bm, int nwords, int base, int32_t* out, int cap,
+                              int pos, uint32_t* scan) {
+  const int tid = threadIdx.x;
+  // thread t owns words [t*wpt, (t+1)*wpt)
+  const int wpt = (nwords + BLOCK - 1) / BLOCK;
+  const int w_begin = min(nwords, tid * wpt);
+  const int w_end = min(nwords, w_begin + wpt);
+  uint32_t cnt = 0;
+  for (int w = w_begin; w < w_end; ++w) cnt += __popc(bm[w]);
+  uint32_t total = 0;
+  const uint32_t off = block_exclusive_scan<BLOCK>(cnt, scan, &total);
+  int o = pos + (int)off;
+  for (int w = w_begin; w < w_end; ++w) {
+    uint32_t bits = bm[w];
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      bits &= bits - 1u;
+      if (o < cap) out[o] = base + (w << 5) + bit;
+      ++o;
+    }
+  }
+  return pos + (int)total;
+}
+
 // `bm` holds seg_bits / 32 words of LDS, `scan` BLOCK/64 + 1 words.  Writes
 // out[pos ...] (entries at or past cap are dropped) and returns the new pos.
 // Every thread of the workgroup must call it.
@@ -35,25 +65,7 @@ __device__ int compact_marked(int lo, int hi, int seg_bits, Mark mark, int32_t* 
     __syncthreads();
     mark(seg_lo, seg_hi, bm);
     __syncthreads();
-    // ordered compaction: thread t owns words [t*wpt, (t+1)*wpt)
-    const int wpt = (nwords + BLOCK - 1) / BLOCK;
-    const int w_begin = min(nwords, tid * wpt);
-    const int w_end = min(nwords, w_begin + wpt);
-    uint32_t cnt = 0;
-    for (int w = w_begin; w < w_end; ++w) cnt += __popc(bm[w]);
-    uint32_t total = 0;
-    const uint32_t off = block_exclusive_scan<BLOCK>(cnt, scan, &total);
-    int o = pos + (int)off;
-    for (int w = w_begin; w < w_end; ++w) {
-      uint32_t bits = bm[w];
-      while (bits) {
-        const int bit = __ffs(bits) - 1;
-        bits &= bits - 1u;
-        if (o < cap) out[o] = seg_lo + (w << 5) + bit;
-        ++o;
-      }
-    }
-    pos += (int)total;
+    pos = compact_bitmap<BLOCK>(bm, nwords, seg_lo, out, cap, pos, scan);
     __syncthreads();
   }
   return pos;

@@ -8,10 +8,10 @@ For decode step j and layer l:
     its own K/V.
 R(n) is R(n0) followed by the positions decoded since the anchor, [n0, n)
 (dilated neighbours of the middle range stay below n0 and [n0, n) lies in the
-recency window).  By default prhs_dilate_reuse therefore runs once per
-refresh, at n = n0, and later steps attend R(n0) plus that tail through
-prhs_reuse_decode_attn.  With per_step_sets=True it instead builds R(n) at
-every step and attends it with prhs_sparse_decode_attn.
+recency window).  By default the refresh therefore writes R(n0) in the same
+launch (prhs_select_shared), and later steps attend R(n0) plus that tail
+through prhs_reuse_decode_attn.  With per_step_sets=True, prhs_dilate_reuse
+instead builds R(n) at every step and prhs_sparse_decode_attn attends it.
 The carried state is the per-group top-k buffer, the shared set and the anchor
 lengths n0, which are simply the sequence lengths of the refresh step.
 """
@@ -32,6 +32,7 @@ class DecodeRunner:
     def __init__(self, inp, device="cuda", per_step_sets=False):
         w = inp.w
         self.per_step_sets = per_step_sets
+        self.reuses = w.G > 1 or w.s > 1   # some layer-step attends a shared set
         self.w = w
         self.inp = inp
         self.device = torch.device(device)
@@ -73,8 +74,14 @@ class DecodeRunner:
     # -- pieces -------------------------------------------------------------
     def refresh(self, gi, j):
         l = gi * self.w.G
-        B.prhs_select(self.kv[l][j], self.inp.q[l, j], self.params, self.topk_idx[gi],
-                      self.topk_len[gi], self.anchor_set[gi], self.anchor_len[gi], self.ws_select)
+        if self.per_step_sets or not self.reuses:
+            B.prhs_select(self.kv[l][j], self.inp.q[l, j], self.params, self.topk_idx[gi],
+                          self.topk_len[gi], self.anchor_set[gi], self.anchor_len[gi],
+                          self.ws_select)
+        else:
+            B.prhs_select_shared(self.kv[l][j], self.inp.q[l, j], self.params, self.topk_idx[gi],
+                                 self.topk_len[gi], self.anchor_set[gi], self.anchor_len[gi],
+                                 self.shared_set[gi], self.shared_len[gi], self.ws_select)
         self.anchor_step[gi] = j
 
     def _anchor(self, gi, j):
@@ -90,11 +97,12 @@ class DecodeRunner:
                             n, self.shared_set[gi], self.shared_len[gi])
 
     def shares_at(self, j):
-        """Groups whose shared set is (re)built at step j."""
+        """Groups whose shared set prhs_dilate_reuse (re)builds at step j (in
+        the default mode the refresh writes it)."""
         w = self.w
         if self.per_step_sets:
             return list(range(self.groups)) if (w.G > 1 or j % w.s != 0) else []
-        return list(range(self.groups)) if (j % w.s == 0 and (w.G > 1 or w.s > 1)) else []
+        return []
 
     def set_for(self, l, j):
         """(set, len, tail_start) that layer l attends at step j: the rows are

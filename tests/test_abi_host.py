@@ -191,6 +191,24 @@ def test_attention_validation(L):
     assert st == B.PRHS_E_INVALID
 
 
+def test_select_shared_validation(L):
+    kv = _kv()
+    p = B.params(k=8, window=4, refresh_every=4)
+    cap = L.prhs_set_capacity(ctypes.byref(p), kv.max_seq_len)
+    n = ctypes.c_size_t(0)
+    assert L.prhs_workspace_size(B.PRHS_OP_SELECT, ctypes.byref(kv), ctypes.byref(p), 0,
+                                 ctypes.byref(n)) == 0
+    args = lambda shared, set_cap: (ctypes.byref(kv), 0x1, ctypes.byref(p), 0x2, 0x3, 64, 0x4, 0x5,
+                                    set_cap, shared, 0x7, 0x8, n.value, None)
+    assert L.prhs_select_shared(*args(None, cap)) == B.PRHS_E_INVALID
+    # the shared set needs room for the dilation as well (prhs_set_capacity)
+    assert L.prhs_select_shared(*args(0x6, cap - 1)) == B.PRHS_E_CAPACITY
+    assert b"shared set" in L.prhs_last_error()
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert L.prhs_select_shared(ctypes.byref(kv0), None, ctypes.byref(p), None, None, 8, None, None,
+                                cap, None, None, None, 0, None) == B.PRHS_OK
+
+
 def test_dilate_validation_and_empty_batch(L):
     p = B.params(k=8)
     assert L.prhs_dilate_reuse(ctypes.byref(p), 2, 0, 1, 1, 8, 1, 1, 1, 1, 8, None) == B.PRHS_E_INVALID

@@ -241,6 +241,61 @@ def test_select_bit_exact(name, dtype, d, paged, hq, hkv, lens, pk):
     check_select(inp, lens, B.params(**pk))
 
 
+def check_select_shared(inp, lens, p):
+    """prhs_select_shared: top-k and anchor set as prhs_select, plus the
+    dilated shared set at the anchor length equal to the oracle's R(n0)."""
+    w = inp.w
+    kv, _ = kv_for(inp, lens)
+    k_cap = max(1, B.prhs_max_topk(p, w.capacity))
+    set_cap = max(1, B.prhs_set_capacity(p, w.capacity))
+    shape = (w.batch, w.hkv)
+    topk = torch.full(shape + (k_cap,), -7, dtype=torch.int32, device=DEV)
+    tlen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    sidx = torch.full(shape + (set_cap,), -7, dtype=torch.int32, device=DEV)
+    slen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    hidx = torch.full(shape + (set_cap,), -7, dtype=torch.int32, device=DEV)
+    hlen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv, p), DEV)
+    ws.fill_(0xCD)
+    B.prhs_select_shared(kv, inp.q[0, 0], p, topk, tlen, sidx, slen, hidx, hlen, ws)
+    torch.cuda.synchronize()
+    topk, tlen, sidx, slen = (t.cpu().numpy() for t in (topk, tlen, sidx, slen))
+    hidx, hlen = hidx.cpu().numpy(), hlen.cpu().numpy()
+    for (b, g), (S, C) in oracle_select(inp, lens, p).items():
+        kb = O.budget_k(lens[b], p.k, p.k_num, p.k_den)
+        m = O.dilation_m(kb, len(S), p.dilate_m)
+        assert tlen[b, g] == len(S) and np.array_equal(topk[b, g, : len(S)], O.topk_layout(S, m))
+        assert slen[b, g] == len(C) and np.array_equal(sidx[b, g, : len(C)], C)
+        R = O.reuse_set(S, m, p.dilate_r, lens[b], lens[b], p.sink, p.window)
+        assert hlen[b, g] == len(R), f"b{b} g{g}: shared_len {hlen[b, g]} != {len(R)}"
+        assert np.array_equal(hidx[b, g, : len(R)], R), f"b{b} g{g}: shared set differs"
+
+
+SHARED_VARIANTS = [dict(dilate_r=1), dict(dilate_r=2, dilate_m=7), dict(dilate_r=0)]
+
+
+@pytest.mark.parametrize("name,dtype,d,paged,hq,hkv,lens,pk", SELECT_CASES,
+                         ids=[c[0] for c in SELECT_CASES])
+def test_select_shared_bit_exact(name, dtype, d, paged, hq, hkv, lens, pk):
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=43 + len(name), grid=True, device=DEV)
+    for var in SHARED_VARIANTS:
+        check_select_shared(inp, lens, B.params(refresh_every=4, **pk, **var))
+
+
+def test_select_shared_window_zero_edges():
+    # no window: a top-m winner at the last middle position has its right
+    # neighbour at n0, outside [0, n0); a winner at the first has its left
+    # neighbour in the sink; coarse grid, many ties
+    for lens in ((600, 1500, 9), (700,) * 16):
+        hkv = 8 if len(lens) == 16 else 2
+        inp = synth.random_inputs(len(lens), 2 * hkv, hkv, 128, lens, seed=59, grid=True,
+                                  device=DEV)
+        for K in inp.K:
+            K.copy_(torch.where(torch.isnan(K), K, torch.clamp(torch.round(K.float()), -1, 1).to(K.dtype) / 16))
+        check_select_shared(inp, lens, B.params(k=40, sink=3, window=0, dilate_r=3))
+
+
 def test_select_all_ties_lowest_positions():
     # every key equal: each score ties, so the top-k are the lowest middle positions
     lens = (3000, 1800)
