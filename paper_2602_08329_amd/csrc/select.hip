@@ -58,6 +58,7 @@ struct SelArgs {
   int dilate_r;
   int32_t* shared_idx;  // optional [rows][set_cap]: the dilated shared set at n0
   int32_t* shared_len;
+  int balance_cus;      // fused refresh: > 0 = CU count to balance rows over, 0 = off
 };
 
 struct RowGeom {
@@ -681,6 +682,7 @@ __device__ __forceinline__ int key_level_shift(int lv) { return lv == 0 ? 21 : (
 // kk >= n everything).  h0 holds the level-0 histogram (key >> 21) of all n
 // keys; h (which may be h0) is overwritten when a deeper level is needed.
 // Reached by every thread.
+template <int BLOCK>
 __device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t kk,
                                       const uint32_t* h0, uint32_t* h, uint32_t* scan, int* s_bin,
                                       uint32_t* s_krem, uint32_t* s_cnt) {
@@ -694,15 +696,15 @@ __device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t
       // histogram of the next digit over the keys that share the prefix
       const int psh = key_level_shift(lv - 1);
       const uint32_t dmask = lv == 1 ? 0x7FFu : 0x3FFu;
-      for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+      for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
       __syncthreads();
-      for (uint32_t i = tid; i < n; i += kFinishBlock) {
+      for (uint32_t i = tid; i < n; i += BLOCK) {
         const uint32_t key = keys[i];
         if ((key >> psh) == t.p) atomicAdd(&h[(key >> sh) & dmask], 1u);
       }
       __syncthreads();
     }
-    find_threshold<kFinishBlock>(lv == 0 ? h0 : h, kk, scan, s_bin, s_krem, s_cnt);
+    find_threshold<BLOCK>(lv == 0 ? h0 : h, kk, scan, s_bin, s_krem, s_cnt);
     const uint32_t bin = (uint32_t)*s_bin, krem = *s_krem, cnt = *s_cnt;
     __syncthreads();
     t.p = lv == 0 ? bin : ((t.p << (key_level_shift(lv - 1) - sh)) | bin);
@@ -723,21 +725,51 @@ __device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t
 // ordered compaction in position order (the key array is already in position
 // order, which also settles ties): top m, other winners, anchor set.
 // Contiguous bf16 caches whose middle range fits LDS.
-template <int D>
-__global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
+// Row of fused-refresh workgroup w when there are more rows than CUs: rows
+// in order of decreasing length, so the workgroups that start last, as
+// earlier ones finish, carry the shortest rows (longest-first scheduling).
+// Sequences rank by length, ties by index; all kv heads of a sequence have
+// its length.  A mapping only: every row is taken exactly once.
+constexpr int kBalanceMaxBatch = 256;
+
+__device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
+  const int ncu = a.balance_cus;
+  const int B = a.kv.batch, H = a.kv.hkv, rows = B * H;
+  if (ncu <= 0 || rows <= ncu || B > kBalanceMaxBatch) return w;
+  const int t = w;  // target length rank
+  const int tb = t / H;
+  for (int b = threadIdx.x; b < B; b += blockDim.x) s_len[b] = kv_seq_len(a.kv, b);
+  __syncthreads();
+  for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    const int nb = s_len[b];
+    int r = 0;
+    for (int b2 = 0; b2 < B; ++b2) {
+      const int n2 = s_len[b2];
+      r += (n2 > nb || (n2 == nb && b2 < b)) ? 1 : 0;
+    }
+    if (r == tb) *s_row = b * H + (t - tb * H);
+  }
+  __syncthreads();
+  return *s_row;
+}
+
+template <int D, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   constexpr int KS = D / 32;
   extern __shared__ uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
-  __shared__ uint32_t scan[kFinishBlock / 64 + 1];
-  __shared__ uint64_t scan64[kFinishBlock / 64 + 1];
+  __shared__ uint32_t scan[BLOCK / 64 + 1];
+  __shared__ uint64_t scan64[BLOCK / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt;
-  const int row = blockIdx.x;
+  __shared__ int s_len[kBalanceMaxBatch];
+  __shared__ int s_row;
+  const int row = fused_row(a, blockIdx.x, s_len, &s_row);
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
   const int M = rg.m;
-  for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+  for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
   __syncthreads();
   if (rg.kb > 0) {
     const int lane = tid & 63, wave = tid >> 6;
@@ -754,7 +786,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
     }
     int gp = 1;
     while (gp < G) gp <<= 1;
-    constexpr int kStride = 32 * (kFinishBlock / 64);
+    constexpr int kStride = 32 * (BLOCK / 64);
     const int t0 = wave * 32;
     const int iters = t0 < M ? (M - t0 + kStride - 1) / kStride : 0;
     if (iters > 0) {
@@ -785,24 +817,29 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
   const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
   // both searches start from the scoring histogram; each thread keeps its
-  // two bins in registers while the first search reuses h
-  static_assert(kHistBins == 2 * kFinishBlock, "two histogram bins per thread");
-  const uint32_t h_lo = h[tid], h_hi = h[tid + kFinishBlock];
-  const KeyThreshold tm = key_threshold(s_keys, (uint32_t)M, m, h, h, scan, &s_bin, &s_krem, &s_cnt);
-  h[tid] = h_lo;
-  h[tid + kFinishBlock] = h_hi;
+  // bins in registers while the first search reuses h
+  constexpr int kBinsPerThread = kHistBins / BLOCK;
+  static_assert(kHistBins % BLOCK == 0, "whole histogram bins per thread");
+  uint32_t h_keep[kBinsPerThread];
+#pragma unroll
+  for (int j = 0; j < kBinsPerThread; ++j) h_keep[j] = h[tid + j * BLOCK];
+  const KeyThreshold tm =
+      key_threshold<BLOCK>(s_keys, (uint32_t)M, m, h, h, scan, &s_bin, &s_krem, &s_cnt);
+#pragma unroll
+  for (int j = 0; j < kBinsPerThread; ++j) h[tid + j * BLOCK] = h_keep[j];
   __syncthreads();
-  const KeyThreshold tk = key_threshold(s_keys, (uint32_t)M, kout, h, h, scan, &s_bin, &s_krem, &s_cnt);
+  const KeyThreshold tk =
+      key_threshold<BLOCK>(s_keys, (uint32_t)M, kout, h, h, scan, &s_bin, &s_krem, &s_cnt);
   // h becomes the bitmap of the dilated shared set over the middle indices
   // (M <= 32 * kHistBins); the scan below orders the clearing before marking
   const bool shared = a.shared_idx != nullptr;
   const int mwords = (M + 31) >> 5;
   if (shared)
-    for (int i = tid; i < mwords; i += kFinishBlock) h[i] = 0u;
+    for (int i = tid; i < mwords; i += BLOCK) h[i] = 0u;
   // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept); one
   // scan of four 16-bit counts gives every thread its output offsets (the
   // middle range is below 2^16 keys here)
-  const int ept = (M + kFinishBlock - 1) / kFinishBlock;
+  const int ept = (M + BLOCK - 1) / BLOCK;
   const int i_begin = min(M, tid * ept), i_end = min(M, i_begin + ept);
   uint32_t gm = 0, em = 0, gk = 0, ek = 0;
   for (int i = i_begin; i < i_end; ++i) {
@@ -813,7 +850,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
     ek += xk == tk.p ? 1u : 0u;
   }
   uint64_t tot;
-  const uint64_t pre = block_exclusive_scan<kFinishBlock, uint64_t>(
+  const uint64_t pre = block_exclusive_scan<BLOCK, uint64_t>(
       (uint64_t)gm | ((uint64_t)em << 16) | ((uint64_t)gk << 32) | ((uint64_t)ek << 48), scan64,
       &tot);
   uint32_t rm = (uint32_t)(pre >> 16) & 0xFFFFu, rk = (uint32_t)(pre >> 48) & 0xFFFFu;
@@ -850,11 +887,11 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
     }
   }
   const uint32_t total_k = ((uint32_t)(tot >> 32) & 0xFFFFu) + min((uint32_t)(tot >> 48) & 0xFFFFu, tk.take);
-  for (int i = tid; i < se; i += kFinishBlock)
+  for (int i = tid; i < se; i += BLOCK)
     if (i < a.set_cap) out[i] = i;
   int pos = se + (int)total_k;
   const int nw = rg.n0 - rg.win_start;
-  for (int i = tid; i < nw; i += kFinishBlock)
+  for (int i = tid; i < nw; i += BLOCK)
     if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
   if (nw > 0) pos += nw;
   if (tid == 0) {
@@ -864,10 +901,10 @@ __global__ __launch_bounds__(kFinishBlock) void select_fused(SelArgs a) {
   if (shared) {
     __syncthreads();
     int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
-    for (int i = tid; i < se; i += kFinishBlock)
+    for (int i = tid; i < se; i += BLOCK)
       if (i < a.set_cap) sh[i] = i;
-    int pos2 = compact_bitmap<kFinishBlock>(h, mwords, se, sh, a.set_cap, se, scan);
-    for (int i = tid; i < nw; i += kFinishBlock)
+    int pos2 = compact_bitmap<BLOCK>(h, mwords, se, sh, a.set_cap, se, scan);
+    for (int i = tid; i < nw; i += BLOCK)
       if (pos2 + i < a.set_cap) sh[pos2 + i] = rg.win_start + i;
     if (nw > 0) pos2 += nw;
     if (tid == 0) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
@@ -894,6 +931,26 @@ bool use_fused_select(int dtype, bool paged, int rows, int mcap) {
   if (dtype != 1 || paged || mcap > kFusedMaxKeys) return false;
   if (force != 0) return force > 0;
   return rows >= kFusedMinRows;
+}
+
+// CUs of the current device, for the fused refresh's row balancing (0 when
+// unknown or when PRHS_SELECT_BALANCE=0).
+int balance_cus() {
+  static const int enabled = [] {
+    const char* e = getenv("PRHS_SELECT_BALANCE");
+    return e ? atoi(e) : 1;
+  }();
+  if (!enabled) return 0;
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    cus[dev] = n > 0 ? n : -1;
+  }
+  return cus[dev] > 0 ? cus[dev] : 0;
 }
 
 struct SelLayout {
@@ -954,24 +1011,31 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.dilate_r = s.dilate_r;
   a.shared_idx = s.shared_idx;
   a.shared_len = s.shared_len;
+  a.balance_cus = 0;
 
   // many short contiguous bf16 rows: the whole refresh in one launch
   if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {
     const size_t dyn = (size_t)a.mcap * 4;
+    a.balance_cus = balance_cus();
+    // one 1024-thread workgroup per CU while the rows fit the CUs; beyond,
+    // 512-thread workgroups so that two share a CU and one's selection
+    // overlaps the other's scoring
+    const bool wide = a.balance_cus <= 0 || rows <= a.balance_cus;
     hipError_t e = hipSuccess;
+#define PRHS_FUSED_LAUNCH(DV, BL)                                                           \
+  {                                                                                         \
+    if (dyn > 65536)                                                                        \
+      e = hipFuncSetAttribute((const void*)select_fused<DV, BL>,                             \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);        \
+    if (e == hipSuccess)                                                                    \
+      hipLaunchKernelGGL((select_fused<DV, BL>), dim3(rows), dim3(BL), dyn, stream, a);     \
+  }
     if (s.kv.d == 128) {
-      if (dyn > 65536)
-        e = hipFuncSetAttribute((const void*)select_fused<128>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-      if (e == hipSuccess)
-        hipLaunchKernelGGL(select_fused<128>, dim3(rows), dim3(kFinishBlock), dyn, stream, a);
+      if (wide) PRHS_FUSED_LAUNCH(128, 1024) else PRHS_FUSED_LAUNCH(128, 512)
     } else {
-      if (dyn > 65536)
-        e = hipFuncSetAttribute((const void*)select_fused<64>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-      if (e == hipSuccess)
-        hipLaunchKernelGGL(select_fused<64>, dim3(rows), dim3(kFinishBlock), dyn, stream, a);
+      if (wide) PRHS_FUSED_LAUNCH(64, 1024) else PRHS_FUSED_LAUNCH(64, 512)
     }
+#undef PRHS_FUSED_LAUNCH
     return e != hipSuccess ? e : hipGetLastError();
   }
   // the middle range is shorter than max_seq_len; size grids by max_seq_len

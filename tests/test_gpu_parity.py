@@ -230,6 +230,12 @@ SELECT_CASES = [
      dict(k=5, sink=4, window=16)),
     ("fused-ratio", "bf16", 128, False, 32, 8, (9000, 4100) * 8,
      dict(k_num=1, k_den=20, sink=4, window=128)),
+    # 40 x 8 = 320 rows, more than the CUs: workgroups take rows by length rank
+    ("fused-balanced", "bf16", 128, False, 16, 8,
+     tuple(300 + (i * 389) % 2700 for i in range(38)) + (1500, 1500),
+     dict(k=100, sink=4, window=32)),
+    ("fused-balanced-d64", "bf16", 64, False, 8, 8,
+     tuple(40 + (i * 577) % 3000 for i in range(40)), dict(k=70, sink=2, window=16)),
 ]
 
 
