@@ -34,7 +34,7 @@ constexpr int kFilterChunk = kFilterBlock * kFilterPerThread;
 constexpr int kFinishBlock = 1024;
 constexpr int kFinishPerThread = 8;  // candidates per thread per pass
 constexpr int kFinishTies = 4096;    // level-1 ties the finish kernel keeps in LDS
-constexpr int kFinishSegBits = 65536; // bitmap segment of the finish kernel (8 KB)
+constexpr int kFinishSegBits = 32768; // positions per bitmap segment of the finish kernel (3 x 4 KB)
 
 struct SelArgs {
   KvView kv;
@@ -536,34 +536,19 @@ __device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, uint32_t* h
   return prefix;
 }
 
-// Appends the positions of the LDS composites in [lo, hi), ascending, to out.
-__device__ int compact_range(const uint64_t* comp, uint32_t n, uint64_t lo, uint64_t hi,
-                             int mid_lo, int mid_hi, int32_t* out, int cap, int pos,
-                             uint32_t* bm, uint32_t* scan, int seg_bits) {
-  const int tid = threadIdx.x;
-  auto mark = [&](int seg_lo, int seg_hi, uint32_t* b) {
-    for (uint32_t i = tid; i < n; i += kFinishBlock) {
-      const uint64_t x = comp[i];
-      if (x >= lo && x < hi) {
-        const int p = composite_pos(x);
-        if (p >= seg_lo && p < seg_hi) mark_bit(b, seg_lo, p);
-      }
-    }
-  };
-  return compact_marked<kFinishBlock>(mid_lo, mid_hi, seg_bits, mark, out, cap, pos, bm, scan);
-}
-
 // Finishes the selection of one row (one workgroup per row): the level-0 and
 // level-1 thresholds come from the histograms of the score and filter
 // kernels; one pass over the level-0 candidates moves the level-1 winners to
 // the output list and stages the level-1 ties in LDS.  Winners and staged
 // ties, as distinct 54-bit composites in LDS, then give the exact k_b-th and
-// m-th largest by LDS radix select; ordered bitmap compactions write the top
-// m, the other winners and the anchor set, each ascending by position.
+// m-th largest by LDS radix select; one segmented bitmap pass writes the top
+// m, the other winners, the anchor set and the shared set, each ascending by
+// position.
 __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   extern __shared__ uint64_t dyn[];  // sort buffer: a.sortcap entries
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFinishBlock / 64 + 1];
+  __shared__ uint64_t scan64[kFinishBlock / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt, s_base;
   const int row = blockIdx.x;
@@ -620,48 +605,113 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
                                     : 0ull;
   const uint64_t c_m = m > 0 ? lds_kth_largest(get, total, m, h, scan, &s_bin, &s_krem, &s_cnt)
                              : ~0ull;
-  uint32_t* bm = (uint32_t*)(dyn + a.sortcap);
+  // One ordered pass over the middle range writes all outputs: per bitmap
+  // segment the winners W (x >= c_k), the top m T (x >= c_m) and the +-r
+  // neighbours D of T are marked together, and one scan of four packed counts
+  // gives each thread its offsets into the top m, the other winners, the
+  // anchor set (W) and the shared set (W | D).  Neighbours outside the middle
+  // range fall in the sink, the window or outside [0, n0).
+  const bool shared = a.shared_idx != nullptr;
+  const int r = a.dilate_r;
+  const int seg_bits = kFinishSegBits;
+  constexpr int kSegW = kFinishSegBits / 32;
+  uint32_t* bw = (uint32_t*)(dyn + a.sortcap);
+  uint32_t* bt = bw + kSegW;
+  uint32_t* bd = bt + kSegW;
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
-  compact_range(dyn, total, c_m, ~0ull, rg.sink_end, rg.win_start, topk, a.k_cap, 0, bm, scan,
-                kFinishSegBits);
-  compact_range(dyn, total, c_k, c_m, rg.sink_end, rg.win_start, topk, a.k_cap, (int)m, bm, scan,
-                kFinishSegBits);
-  if (tid == 0) a.topk_len[row] = (int32_t)kout;
-  // anchor set: sink, winners, window
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
-  for (int i = tid; i < rg.sink_end; i += kFinishBlock)
-    if (i < a.set_cap) out[i] = i;
-  int pos = compact_range(dyn, total, c_k, ~0ull, rg.sink_end, rg.win_start, out, a.set_cap,
-                          rg.sink_end, bm, scan, kFinishSegBits);
-  const int nw = rg.n0 - rg.win_start;
-  for (int i = tid; i < nw; i += kFinishBlock)
-    if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
-  if (nw > 0) pos += nw;
-  if (tid == 0) a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
-  if (a.shared_idx) {
-    // dilated shared set at n0: the winners, the +-r neighbours of the top m
-    // inside the middle range (the others fall in the sink, the window or
-    // outside [0, n0)), then sink and window as above
-    int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
-    for (int i = tid; i < rg.sink_end; i += kFinishBlock)
-      if (i < a.set_cap) sh[i] = i;
-    const int r = a.dilate_r;
-    auto mark = [&](int seg_lo, int seg_hi, uint32_t* bmap) {
-      for (uint32_t i = tid; i < total; i += kFinishBlock) {
-        const uint64_t x = dyn[i];
-        if (x < c_k) continue;
-        const int p = composite_pos(x);
-        const int lo = max(x >= c_m ? p - r : p, seg_lo);
-        const int hi = min(x >= c_m ? p + r : p, seg_hi - 1);
-        for (int q = lo; q <= hi; ++q) mark_bit(bmap, seg_lo, q);
+  int32_t* sh = shared ? a.shared_idx + (size_t)row * a.set_cap : nullptr;
+  for (int i = tid; i < rg.sink_end; i += kFinishBlock) {
+    if (i < a.set_cap) {
+      out[i] = i;
+      if (shared) sh[i] = i;
+    }
+  }
+  int pos_t = 0, pos_r = (int)m, pos_w = rg.sink_end, pos_s = rg.sink_end;
+  for (int seg_lo = rg.sink_end; seg_lo < rg.win_start; seg_lo += seg_bits) {
+    const int seg_hi = min(rg.win_start, seg_lo + seg_bits);
+    const int nwords = (seg_hi - seg_lo + 31) >> 5;
+    for (int w = tid; w < nwords; w += kFinishBlock) {
+      bw[w] = 0u;
+      bt[w] = 0u;
+      bd[w] = 0u;
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < total; i += kFinishBlock) {
+      const uint64_t x = dyn[i];
+      if (x < c_k) continue;
+      const int p = composite_pos(x);
+      const bool top = x >= c_m;
+      if (p >= seg_lo && p < seg_hi) {
+        mark_bit(bw, seg_lo, p);
+        if (top) mark_bit(bt, seg_lo, p);
       }
-    };
-    int pos2 = compact_marked<kFinishBlock>(rg.sink_end, rg.win_start, kFinishSegBits, mark, sh,
-                                            a.set_cap, rg.sink_end, bm, scan);
-    for (int i = tid; i < nw; i += kFinishBlock)
-      if (pos2 + i < a.set_cap) sh[pos2 + i] = rg.win_start + i;
-    if (nw > 0) pos2 += nw;
-    if (tid == 0) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
+      if (shared && top) {
+        const int lo = max(p - r, seg_lo), hi = min(p + r, seg_hi - 1);
+        for (int q = lo; q <= hi; ++q) mark_bit(bd, seg_lo, q);
+      }
+    }
+    __syncthreads();
+    // thread t owns words [t*wpt, (t+1)*wpt); a segment holds at most 2^15
+    // positions, so each packed 16-bit count fits
+    const int wpt = (nwords + kFinishBlock - 1) / kFinishBlock;
+    const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
+    uint64_t cnt = 0;
+    for (int w = w_begin; w < w_end; ++w) {
+      const uint32_t W = bw[w], T = bt[w], S = W | bd[w];
+      cnt += (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
+             ((uint64_t)__popc(W) << 32) | ((uint64_t)__popc(S) << 48);
+    }
+    uint64_t tot;
+    const uint64_t off = block_exclusive_scan<kFinishBlock, uint64_t>(cnt, scan64, &tot);
+    int ot = pos_t + (int)(off & 0xFFFFu), orr = pos_r + (int)((off >> 16) & 0xFFFFu);
+    int ow = pos_w + (int)((off >> 32) & 0xFFFFu), os = pos_s + (int)(off >> 48);
+    for (int w = w_begin; w < w_end; ++w) {
+      const uint32_t W = bw[w], T = bt[w];
+      uint32_t bits = shared ? (W | bd[w]) : W;
+      const int base = seg_lo + (w << 5);
+      while (bits) {
+        const int bit = __ffs(bits) - 1;
+        const uint32_t one = 1u << bit;
+        bits &= bits - 1u;
+        const int p = base + bit;
+        if (W & one) {
+          if (T & one) {
+            if (ot < a.k_cap) topk[ot] = p;
+            ++ot;
+          } else {
+            if (orr < a.k_cap) topk[orr] = p;
+            ++orr;
+          }
+          if (ow < a.set_cap) out[ow] = p;
+          ++ow;
+        }
+        if (shared) {
+          if (os < a.set_cap) sh[os] = p;
+          ++os;
+        }
+      }
+    }
+    pos_t += (int)(tot & 0xFFFFu);
+    pos_r += (int)((tot >> 16) & 0xFFFFu);
+    pos_w += (int)((tot >> 32) & 0xFFFFu);
+    pos_s += (int)(tot >> 48);
+    __syncthreads();
+  }
+  if (tid == 0) a.topk_len[row] = (int32_t)kout;
+  // then the window, after the winners (and after the dilated middle)
+  const int nw = rg.n0 - rg.win_start;
+  for (int i = tid; i < nw; i += kFinishBlock) {
+    if (pos_w + i < a.set_cap) out[pos_w + i] = rg.win_start + i;
+    if (shared && pos_s + i < a.set_cap) sh[pos_s + i] = rg.win_start + i;
+  }
+  if (nw > 0) {
+    pos_w += nw;
+    pos_s += nw;
+  }
+  if (tid == 0) {
+    a.set_len[row] = pos_w < a.set_cap ? pos_w : a.set_cap;
+    if (shared) a.shared_len[row] = pos_s < a.set_cap ? pos_s : a.set_cap;
   }
 }
 
@@ -1063,7 +1113,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   if (cap > PRHS_MAX_TOPK) cap = PRHS_MAX_TOPK;
   if (cap < a.selcap) cap = a.selcap;
   a.sortcap = (int)cap;
-  const size_t dyn = (size_t)a.sortcap * 8 + kFinishSegBits / 8;
+  const size_t dyn = (size_t)a.sortcap * 8 + 3 * kFinishSegBits / 8;
   if (dyn > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)select_finish,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
