@@ -63,6 +63,10 @@ __all__ = [
     "kl_divergence",
     "renormalised",
     "DecodeOracle",
+    "query_similar",
+    "group_similar",
+    "gate_choice",
+    "GatedDecodeOracle",
 ]
 
 
@@ -352,6 +356,119 @@ class DecodeOracle:
             _, c = self.refresh(layer, Qg, K, n)
             return c
         return self.shared(layer, n)
+
+    def attend(self, Qg, K, V, S):
+        """Sparse attention of every query head of the group over S."""
+        Qg = np.atleast_2d(_f64(Qg))
+        outs = [sparse_attention(Qg[h], K, V, S, self.scale) for h in range(Qg.shape[0])]
+        return np.stack([o[0] for o in outs]), np.array([o[1] for o in outs])
+
+
+# ---------------------------------------------------------------------------
+# Similarity gate (Sec. 4.1, Similarity Criteria; Eq. cos_sim)
+# ---------------------------------------------------------------------------
+
+def query_similar(q_now, q_ref, tau):
+    """Whether sim(q_now, q_ref) = q_now . q_ref / (|q_now| |q_ref|) exceeds
+    tau, for 0 <= tau <= 1 (Eq. cos_sim).
+
+    Decided without a square root or a division: sim > tau holds exactly when
+    the dot product is positive and dot^2 > tau^2 |q_now|^2 |q_ref|^2.  The
+    three sums are formed in float64 and the comparison is evaluated as
+    dot * dot > (tau * tau) * n_now * n_ref in that order, so that any
+    implementation computing the same exact sums takes the same decision.
+    A zero query is similar to nothing."""
+    a = _f64(q_now).ravel()
+    b = _f64(q_ref).ravel()
+    dot = float(np.dot(a, b))
+    n_now = float(np.dot(a, a))
+    n_ref = float(np.dot(b, b))
+    t = float(tau)
+    return dot > 0.0 and dot * dot > (t * t) * n_now * n_ref
+
+
+def group_similar(Qg_now, Qg_ref, tau):
+    """A kv head's group shares only when every one of its query heads is
+    similar to the same head of the reference step (the paper gates each
+    head; a grouped-query kv head serves all of its query heads)."""
+    Qn = np.atleast_2d(_f64(Qg_now))
+    Qr = np.atleast_2d(_f64(Qg_ref))
+    return all(query_similar(Qn[h], Qr[h], tau) for h in range(Qn.shape[0]))
+
+
+def gate_choice(Qg_now, anchors, tau):
+    """Sec. 4.1: a later query shares when an earlier query of its block is
+    similar, choosing the most recent such query.  `anchors` lists the
+    block's earlier retrieving steps as (step, Qg) in step order; returns the
+    chosen step, or None when the query must retrieve."""
+    for step, Qg_ref in reversed(list(anchors)):
+        if group_similar(Qg_now, Qg_ref, tau):
+            return step
+    return None
+
+
+class GatedDecodeOracle:
+    """The schedule with the similarity gate, for one (batch, kv-head) unit.
+
+    Blocks of s decode steps restrict sharing to adjacent queries.  At the
+    anchor layer of each group of G layers, the block's first step retrieves;
+    a later step shares the selection of the most recent earlier retrieving
+    step of the block whose queries are similar (gate_choice), else it
+    retrieves and becomes a reference itself.  A retrieving step attends its
+    undilated critical set C(n); every other (layer, step) attends the
+    dilated shared set of the selection it uses, grown by the tokens decoded
+    since that selection (Sec. 4.1; Def. 3.2, Sec. 2.2).  The retrieval ratio
+    is the fraction of (anchor layer, step) pairs that retrieve."""
+
+    def __init__(self, sink, window, s, G, tau, r=1, k=None, k_num=0, k_den=0,
+                 dilate_m=-1, scale=None):
+        self.sink = sink
+        self.window = window
+        self.s = s
+        self.G = G
+        self.tau = tau
+        self.r = r
+        self.k = k
+        self.k_num = k_num
+        self.k_den = k_den
+        self.dilate_m = dilate_m
+        self.scale = scale
+        self.anchors = {}    # anchor layer -> [(step, Qg, s_star, n0, k_b)] of the block
+        self.decision = {}   # (anchor layer, step) -> step whose selection is used
+        self.retrievals = 0
+        self.decisions = 0
+
+    def _retrieve(self, layer, step, Qg, K, n):
+        k_b = budget_k(n, self.k, self.k_num, self.k_den)
+        sigma = ranking_scores(Qg, _f64(K)[:n])
+        s_star = topk_middle(sigma, n, k_b, self.sink, self.window)
+        self.anchors[layer].append((step, np.atleast_2d(_f64(Qg)).copy(), s_star, n, k_b))
+        return s_star
+
+    def _shared_of(self, layer, src, n):
+        for step, _, s_star, n0, k_b in self.anchors[layer]:
+            if step == src:
+                m = dilation_m(k_b, len(s_star), self.dilate_m)
+                return reuse_set(s_star, m, self.r, n0, n, self.sink, self.window)
+        raise KeyError(src)
+
+    def step_set(self, layer, step, Qg, K, n):
+        """Index set that (layer, step) attends at current length n.  K is
+        read only where the anchor layer retrieves."""
+        a = anchor_layer(layer, self.G)
+        if layer == a:
+            if step % self.s == 0:
+                self.anchors[a] = []
+            src = gate_choice(Qg, [(st, q) for st, q, *_ in self.anchors[a]], self.tau)
+            self.decisions += 1
+            if src is None:
+                self.retrievals += 1
+                s_star = self._retrieve(a, step, Qg, K, n)
+                self.decision[(a, step)] = step
+                return anchor_set(s_star, n, self.sink, self.window)
+            self.decision[(a, step)] = src
+            return self._shared_of(a, src, n)
+        return self._shared_of(a, self.decision[(a, step)], n)
 
     def attend(self, Qg, K, V, S):
         """Sparse attention of every query head of the group over S."""

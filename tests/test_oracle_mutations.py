@@ -65,6 +65,24 @@ def _schedule_layer_only(step, layer, s, G):
     return layer % G == 0
 
 
+def _similar_ignoring_sign(q_now, q_ref, tau):
+    a, b = np.ravel(q_now).astype(float), np.ravel(q_ref).astype(float)
+    dot = float(a @ b)
+    return dot * dot > tau * tau * float(a @ a) * float(b @ b)
+
+
+def _gate_oldest_first(Qg_now, anchors, tau):
+    for step, Qg_ref in list(anchors):
+        if M.group_similar(Qg_now, Qg_ref, tau):
+            return step
+    return None
+
+
+def _group_any_head(Qg_now, Qg_ref, tau):
+    Qn, Qr = np.atleast_2d(Qg_now), np.atleast_2d(Qg_ref)
+    return any(M.query_similar(Qn[h], Qr[h], tau) for h in range(Qn.shape[0]))
+
+
 _orig = {name: getattr(M, name) for name in
          ["dense_attention", "topk_middle", "reuse_set", "ranking_scores",
           "region_bounds", "dilation_m", "is_refresh"]}
@@ -81,6 +99,9 @@ MUTANTS = [
     ("region_bounds", _window_off_by_one),
     ("dilation_m", _m_is_k_over_2),
     ("is_refresh", _schedule_layer_only),
+    ("query_similar", _similar_ignoring_sign),
+    ("gate_choice", _gate_oldest_first),
+    ("group_similar", _group_any_head),
 ]
 
 

@@ -459,3 +459,114 @@ def test_topk_layout_partitions_by_rank_then_position():
         assert sorted(lay.tolist()) == sorted(S.tolist())
         assert set(lay[:m].tolist()) == set(S[:m].tolist())
         assert list(lay[:m]) == sorted(lay[:m]) and list(lay[m:]) == sorted(lay[m:])
+
+
+# ---------------------------------------------------------------- similarity gate
+
+def test_query_similarity_closed_forms():
+    # Eq. cos_sim on vectors of known angle
+    e = np.zeros(8)
+    e[0] = 1.0
+    assert O.query_similar(e, 3 * e, 0.99)                  # same direction, any length
+    assert not O.query_similar(e, e, 1.0)                   # cos = 1 is not > 1
+    f = np.zeros(8)
+    f[1] = 2.0
+    assert not O.query_similar(e, f, 0.0)                   # orthogonal
+    assert not O.query_similar(e, -e, 0.0)                  # opposite
+    assert not O.query_similar(np.zeros(8), e, 0.0)         # zero query
+    for deg, tau, want in ((30, 0.8, True), (30, 0.9, False), (40, 0.76, True), (40, 0.77, False)):
+        th = math.radians(deg)
+        v = np.zeros(8)
+        v[0], v[1] = math.cos(th), math.sin(th)
+        assert O.query_similar(e, 5 * v, tau) == want, (deg, tau)
+
+
+def test_group_similarity_needs_every_head():
+    rng = np.random.default_rng(21)
+    Q = rng.standard_normal((4, 16))
+    R = Q + 0.01 * rng.standard_normal((4, 16))
+    assert O.group_similar(Q, R, 0.9)
+    R[2] = -R[2]
+    assert not O.group_similar(Q, R, 0.9)
+
+
+def test_gate_chooses_most_recent_similar_anchor():
+    e0, e1 = np.eye(2)
+    q = np.array([[1.0, 0.2]])
+    anchors = [(0, np.array([[1.0, 0.0]])), (1, np.array([[0.0, 1.0]])), (2, np.array([[1.0, 0.1]]))]
+    assert O.gate_choice(q, anchors, 0.8) == 2
+    assert O.gate_choice(q, anchors[:2], 0.8) == 0
+    assert O.gate_choice(q, anchors[1:2], 0.8) is None
+    assert O.gate_choice(q, [], 0.0) is None
+
+
+def _on_grid(x):
+    return np.clip(np.round(x * 16), -255, 255) / 16
+
+
+def _run_schedule(dec, Qs, K, n_ctx, L, T):
+    sets = {}
+    for j in range(T):
+        for l in range(L):
+            sets[(l, j)] = dec.step_set(l, j, Qs[l][j], K[l], n_ctx + j + 1)
+    return sets
+
+
+def _gate_inputs(seed, L=4, T=8, g=2, d=16, n=220):
+    rng = np.random.default_rng(seed)
+    K = [grid(rng, n + T, d) for _ in range(L)]
+    base = rng.standard_normal((L, g, d))
+    Qs = [[_on_grid(base[l] + 0.3 * rng.standard_normal((g, d))) for _ in range(T)] for l in range(L)]
+    return K, Qs, n
+
+
+def test_gate_tau_one_retrieves_every_step():
+    # cos > 1 never holds: every anchor-layer step retrieves, which is the
+    # fixed schedule with a refresh at every step
+    K, Qs, n = _gate_inputs(3)
+    kw = dict(sink=4, window=16, G=2, r=1, k=24)
+    gated = O.GatedDecodeOracle(s=4, tau=1.0, **kw)
+    fixed = O.DecodeOracle(s=1, **kw)
+    a = _run_schedule(gated, Qs, K, n, 4, 8)
+    b = _run_schedule(fixed, Qs, K, n, 4, 8)
+    assert all(np.array_equal(a[x], b[x]) for x in a)
+    assert gated.retrievals == gated.decisions
+
+
+def test_gate_tau_zero_positive_queries_is_the_block_schedule():
+    # queries with positive dot products share from the block's first step:
+    # the fixed schedule with refresh every s steps, retrieval ratio 1/s
+    K, Qs, n = _gate_inputs(4)
+    Qs = [[np.abs(q) for q in row] for row in Qs]
+    kw = dict(sink=4, window=16, G=2, r=1, k=24)
+    gated = O.GatedDecodeOracle(s=4, tau=0.0, **kw)
+    fixed = O.DecodeOracle(s=4, **kw)
+    a = _run_schedule(gated, Qs, K, n, 4, 8)
+    b = _run_schedule(fixed, Qs, K, n, 4, 8)
+    assert all(np.array_equal(a[x], b[x]) for x in a)
+    assert gated.retrievals * 4 == gated.decisions
+
+
+def test_gate_mixed_decisions_follow_the_rule():
+    # step 2 is unlike step 0 and retrieves; step 3 resembles both and uses
+    # the more recent step 2; non-anchor layers follow their anchor's choice
+    d, n = 16, 200
+    rng = np.random.default_rng(5)
+    K = [grid(rng, n + 4, d) for _ in range(2)]
+    u = np.zeros(d)
+    u[:4] = 1.0
+    w = np.zeros(d)
+    w[4:8] = 1.0                 # orthogonal to u
+    q = {0: u, 1: u, 2: w, 3: u + w}
+    Qs = [[q[j][None, :] for j in range(4)] for _ in range(2)]
+    dec = O.GatedDecodeOracle(sink=2, window=8, s=4, G=2, tau=0.5, k=10)
+    sets = _run_schedule(dec, Qs, K, n, 2, 4)
+    assert [dec.decision[(0, j)] for j in range(4)] == [0, 0, 2, 2]
+    assert dec.retrievals == 2
+    S0 = O.topk_middle(O.ranking_scores(q[0][None, :], K[0][: n + 1]), n + 1, 10, 2, 8)
+    S2 = O.topk_middle(O.ranking_scores(q[2][None, :], K[0][: n + 3]), n + 3, 10, 2, 8)
+    m = O.dilation_m(10, 10)
+    assert np.array_equal(sets[(0, 1)], O.reuse_set(S0, m, 1, n + 1, n + 2, 2, 8))
+    assert np.array_equal(sets[(0, 2)], O.anchor_set(S2, n + 3, 2, 8))
+    assert np.array_equal(sets[(1, 2)], O.reuse_set(S2, m, 1, n + 3, n + 3, 2, 8))
+    assert np.array_equal(sets[(0, 3)], O.reuse_set(S2, m, 1, n + 3, n + 4, 2, 8))
