@@ -31,32 +31,70 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(run, set_lens, sel_rows):
-    """Bytes the method itself must move, per decode step j (dict j -> dict).
+def attention_bytes(w, rows):
+    """Algorithmic bytes of one sparse attention launch over `rows` gathered
+    (batch, kv-head) rows in total: K and V rows plus their indices, the
+    queries, and the outputs y and lse."""
+    e = 4 if w.dtype == "f32" else 2
+    return rows * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e + w.batch * w.hq * (w.d + 1) * 4
 
-    attention: sum over (b, g) of |R| (2 d e + 4) + q + out/lse per layer;
-    selection: middle keys (d e each) + q +
-    top-k, anchor-set and (when the refresh writes it) shared-set writes, once
-    per refresh of an anchor layer; a separate shared-set build reads the
-    top-k and writes the set."""
+
+def middle_len(w, n0):
+    se = min(w.sink, n0)
+    return max(se, n0 - w.window) - se
+
+
+def record_step(run, j, gated):
+    """Runs the selection of decode step j (untimed) and returns the set rows
+    each layer attends and the step's algorithmic selection bytes: middle
+    keys read by the refreshing rows (d e each), their queries, the top-k,
+    critical-set and shared-set entries written; for the gate, the queries it
+    reads and records; for a separate shared-set build, top-k read and set
+    written."""
+    import torch
     w = run.w
     e = 4 if w.dtype == "f32" else 2
     qbytes = w.batch * w.hq * w.d * e
-    outbytes = w.batch * w.hq * (w.d + 1) * 4
-    per = {}
-    for j in range(w.steps):
-        attn = 0
-        for l in range(run.L):
-            total_set = set_lens[(l, j)]
-            attn += total_set * (2 * w.d * e + 4) + qbytes + outbytes
-        sel = 0
+    run.selection_step(j)
+    torch.cuda.synchronize()
+    sel = 0
+    lens_j = [w.n_ctx[b] + j + 1 for b in range(w.batch)]
+    if gated:
+        slot = j % w.s
+        choice = run.choice.view(run.groups, w.batch, w.hkv).cpu()
+        retr = choice < 0
+        mid = sum(middle_len(w, lens_j[b]) * int(retr[:, b].sum()) for b in range(w.batch))
+        written = 0
+        for gi in range(run.groups):
+            r = retr[gi].to(run.topk_len.device)
+            written += int(run.topk_len[gi][r].sum() + run.pool_len[gi, 0, slot][r].sum()
+                           + run.pool_len[gi, 1, slot][r].sum())
+        sel += run.groups * qbytes * (2 + slot) + mid * w.d * e + written * 4
+        if bool(retr.any()):
+            sel += run.groups * qbytes
+    else:
         if j % w.s == 0:
-            m_rows, k_rows, c_rows, s_rows = sel_rows[j]
-            sel += m_rows * w.d * e + run.groups * qbytes + (k_rows + c_rows + s_rows) * 4
+            mid = sum(middle_len(w, n0) for n0 in lens_j) * w.hkv * run.groups
+            written = int(run.topk_len.sum() + run.anchor_len.sum())
+            if run.reuses and not run.per_step_sets:
+                written += int(run.shared_len.sum())
+            sel += mid * w.d * e + run.groups * qbytes + written * 4
         for gi in run.shares_at(j):
-            sel += set_lens[("shared", gi, j)] * 4 + set_lens[("topk", gi, j)] * 4
-        per[j] = dict(attn=attn, sel=sel)
-    return per
+            sel += int(run.shared_len[gi].sum() + run.topk_len[gi].sum()) * 4
+    rows = {}
+    seq = run.seq_lens[j].view(w.batch, 1).expand(w.batch, w.hkv).reshape(-1)
+    for l in range(run.L):
+        if gated:
+            pool, plen, urow, utail = run.set_for(l, j)
+            rows[l] = int((plen.reshape(-1)[urow.long()] + (seq - utail)).sum())
+        else:
+            s_idx, s_len, tail = run.set_for(l, j)
+            r = int(s_len.sum())
+            if tail is not None:   # rows [n0_b, n_b) of every kv head follow the set
+                r += int((run.seq_lens[j] - tail).sum()) * w.hkv
+            rows[l] = r
+        run.attend(l, j)
+    return rows, sel
 
 
 def cpu_baseline(run, budget_s):
@@ -89,8 +127,14 @@ def cpu_baseline(run, budget_s):
                 for j in range(w.steps):
                     for (b, g) in units:
                         qs[(l, j, b, g)] = qh[j, b, g * w.g:(g + 1) * w.g]
-            decs = {u: O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k, k_num=w.k_num,
-                                      k_den=w.k_den, dilate_m=w.dilate_m) for u in units}
+            if hasattr(run, "tau"):
+                decs = {u: O.GatedDecodeOracle(w.sink, w.window, w.s, w.G, run.tau, r=w.r, k=w.k,
+                                               k_num=w.k_num, k_den=w.k_den,
+                                               dilate_m=w.dilate_m) for u in units}
+            else:
+                decs = {u: O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k,
+                                          k_num=w.k_num, k_den=w.k_den, dilate_m=w.dilate_m)
+                        for u in units}
             t0 = time.perf_counter()
             for j in range(w.steps):
                 for l in layers:
@@ -172,6 +216,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-step-sets", action="store_true",
                     help="rebuild the dilated shared set at every step instead of once per refresh")
+    ap.add_argument("--gate", type=float, default=None, metavar="TAU",
+                    help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
+                         "fixed refresh period (blocks of refresh_every steps)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -188,7 +235,7 @@ def main():
 
     from paper_2602_08329_amd import binding as B
     from paper_2602_08329_amd import synth
-    from paper_2602_08329_amd.schedule import DecodeRunner
+    from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -205,37 +252,27 @@ def main():
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f} s; "
         f"{sum(x.numel() * x.element_size() for x in inp.K + inp.V) / 2**30:.1f} GiB of KV")
-    run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets)
+    gated = args.gate is not None
+    if gated and args.per_step_sets:
+        print("--gate and --per-step-sets exclude each other", file=sys.stderr)
+        sys.exit(2)
+    if gated:
+        run = GatedDecodeRunner(inp, dev, tau=args.gate)
+    else:
+        run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets)
 
-    # one untimed pass over all steps: set sizes for the byte accounting
+    # one untimed pass over all steps: set sizes and selection bytes
     set_lens = {}
-    sel_rows = {}
+    per = {}
+    retrieving = 0
     for j in range(T):
-        run.selection_step(j)
-        if j % w.s == 0:
-            mid = 0
-            for b in range(w.batch):
-                n0 = w.n_ctx[b] + j + 1
-                se = min(w.sink, n0)
-                mid += (max(se, n0 - w.window) - se) * w.hkv
-            tl = int(run.topk_len.sum().item())
-            al = int(run.anchor_len.sum().item())
-            sl = int(run.shared_len.sum().item()) if (run.reuses and not run.per_step_sets) else 0
-            sel_rows[j] = (mid * run.groups, tl, al, sl)
-        sh = run.shared_len.sum(dim=(1, 2)).cpu().tolist()
-        tk = run.topk_len.sum(dim=(1, 2)).cpu().tolist()
-        for gi in range(run.groups):
-            set_lens[("shared", gi, j)] = sh[gi]
-            set_lens[("topk", gi, j)] = tk[gi]
-        for l in range(run.L):
-            s_idx, s_len, tail = run.set_for(l, j)
-            rows = int(s_len.sum().item())
-            if tail is not None:   # rows [n0_b, n_b) of every kv head follow the set
-                rows += int((run.seq_lens[j] - tail).sum().item()) * w.hkv
-            set_lens[(l, j)] = rows
-        run.step(j)
+        rows, sel = record_step(run, j, gated)
+        if gated:
+            retrieving += run.retrieving_units()
+        for l, r in rows.items():
+            set_lens[(l, j)] = r
+        per[j] = dict(attn=sum(attention_bytes(w, r) for r in rows.values()), sel=sel)
     torch.cuda.synchronize()
-    per = algorithmic_bytes(run, set_lens, sel_rows)
 
     def timed(fn, label, order=None):
         order = order or (lambda i: i % T)
@@ -263,27 +300,31 @@ def main():
 
     # attention alone: the steps of the last refresh block, cycled, over the
     # sets that block's selection produced (its sets and tails are exactly
-    # those of the byte accounting)
+    # those of the byte accounting); with the gate, whose decisions are per
+    # step, the block's last step repeated
     j_blk = ((T - 1) // w.s) * w.s
-    run.selection_step(j_blk)
-    if args.per_step_sets:   # the shared set is then rebuilt per step; keep the last one
-        for j in range(j_blk + 1, T):
+    if gated:
+        for j in range(j_blk, T):
             run.selection_step(j)
+        order = lambda i: T - 1  # noqa: E731
+    else:
+        run.selection_step(j_blk)
+        if args.per_step_sets:   # the shared set is then rebuilt per step; keep the last one
+            for j in range(j_blk + 1, T):
+                run.selection_step(j)
+        order = lambda i: j_blk + i % (T - j_blk)  # noqa: E731
 
     def attn_only(j):
         for l in range(run.L):
             run.attend(l, j)
-    ms_attn, js_attn = timed(attn_only, "attention only",
-                             order=lambda i: j_blk + i % (T - j_blk))
+    ms_attn, js_attn = timed(attn_only, "attention only", order=order)
     ms_dense, _ = timed(run.dense_step, "dense attention")
 
     # dominant kernel: the sparse attention launch.  Its average duration is
     # the back-to-back attention-only loop above (HIP events on the launch
     # stream, over the timed region); its bytes are the per-launch algorithmic
     # bytes averaged over the same launches.
-    e = 4 if w.dtype == "f32" else 2
-    launch_bytes = [set_lens[(l, j)] * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e
-                    + w.batch * w.hq * (w.d + 1) * 4 for j in js_attn for l in range(run.L)]
+    launch_bytes = [attention_bytes(w, set_lens[(l, j)]) for j in js_attn for l in range(run.L)]
     avg_bytes = sum(launch_bytes) / len(launch_bytes)
     avg_dur = ms_attn * 1e-3 / (K_steps * run.L)
     achieved = avg_bytes / avg_dur / 1e9
@@ -311,7 +352,8 @@ def main():
             "k": w.k if not w.k_den else f"{w.k_num}/{w.k_den} n", "window": w.window,
             "sink": w.sink, "refresh_every": w.s, "layer_group": w.G, "dilate_r": w.r,
             "paged": w.paged, "decode_steps_cycled": T,
-            "shared_sets": "per step" if args.per_step_sets else "per refresh + decoded tail",
+            "shared_sets": ("similarity gate" if gated else
+                            "per step" if args.per_step_sets else "per refresh + decoded tail"),
         },
         "effective_gbps": round(eff_gbps, 1),
         "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),
@@ -327,6 +369,11 @@ def main():
             "avg_launch_bytes": int(avg_bytes), "launches": len(launch_bytes),
         },
     }
+    if gated:
+        result["gate"] = {"tau": args.gate,
+                          "retrieval_ratio": round(retrieving / (run.groups * w.batch * w.hkv * T), 4),
+                          "note": "retrieving (anchor layer, kv head) units over all of them, "
+                                  "measured over the decode-step cycle"}
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle for about {args.cpu_seconds:.0f} s")
         result["cpu_baseline"] = cpu_baseline(run, args.cpu_seconds)

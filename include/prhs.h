@@ -251,6 +251,71 @@ prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale
                                    float* out, float* lse, void* ws, size_t ws_bytes,
                                    void* stream);
 
+/* ---- Similarity-gated sharing (Sec. 4.1, Similarity Criteria; Eq. cos_sim) ----
+ *
+ * Instead of a fixed refresh every refresh_every steps, a later step of a
+ * block of num_slots steps shares the selection of an earlier step of the
+ * block only when their queries are similar.  Per anchor layer of a layer
+ * group the caller keeps, for the block's steps 0 .. num_slots-1 ("slots"):
+ * the reference queries ref_q [num_slots][B][Hq][d] (dtype of q), the flags
+ * ref_valid [num_slots][B*Hkv] (unit retrieved at that slot), the lengths
+ * slot_lens [num_slots][B], and a set pool [2][num_slots][B*Hkv][set_cap] of
+ * int32 with lengths [2][num_slots][B*Hkv]: kind 0 holds each retrieving
+ * step's critical set, kind 1 its dilated shared set.  prhs_gate is called
+ * at every step of the block in order, then prhs_select_gated on the
+ * retrieving units (writing kind 0 and 1 of the current slot), then one
+ * prhs_pool_decode_attn per layer of the group. */
+
+/* Gate for block step `slot` (0 <= slot < num_slots), one decision per
+ * (b, kv head g).  Slot 0 always retrieves.  Otherwise the unit shares the
+ * most recent earlier slot j with ref_valid[j][u] != 0 for which every query
+ * head h of the group satisfies sim(q[b][h], ref_q[j][b][h]) > tau, where
+ * sim is the cosine similarity; it is decided exactly as
+ *   dot > 0 and dot * dot > ((tau * tau) * |q|^2) * |q_j|^2
+ * in binary64 from fp32 sums, which is exact when the inputs are on a grid
+ * coarse enough for the fp32 sums to be exact.  0 <= tau <= 1.
+ * Writes: choice[u] = j, or -1 when the unit retrieves now;
+ *   ref_q[slot] = q; ref_valid[slot][u] = (choice[u] < 0);
+ *   slot_lens[slot][b] = seq_lens[b];
+ *   row_anchor[u] = pool row the group's anchor layer attends: the current
+ *     slot's critical set when retrieving, else slot j's shared set;
+ *   row_other[u] = pool row the group's other layers attend: the shared set
+ *     of the current slot or of slot j;
+ *   tail[u] = first position of the decoded tail to append: seq_lens[b]
+ *     (none) when retrieving, else slot_lens[j][b].
+ * Pool rows are numbered (kind * num_slots + slot) * (B*Hkv) + u. */
+prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t dtype, const void* q, const int32_t* seq_lens, double tau,
+                      int32_t num_slots, int32_t slot, void* ref_q, int32_t* ref_valid,
+                      int32_t* slot_lens, int32_t* choice, int32_t* row_anchor,
+                      int32_t* row_other, int32_t* tail, void* stream);
+
+/* prhs_select_shared for the units the gate sends to retrieval only:
+ * (b, g) with choice[b][g] >= 0 are left untouched, the others get their
+ * top-k, critical set and dilated shared set exactly as prhs_select_shared
+ * computes them.  Pass the current slot's rows of the pool as set_idx
+ * (kind 0) and shared_idx (kind 1). */
+prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_params* params,
+                              const int32_t* choice, int32_t* topk_idx, int32_t* topk_len,
+                              int32_t k_cap, int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                              int32_t* shared_idx, int32_t* shared_len, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Token-sparse decode attention where every (b, kv head g) attends its own
+ * row of a set pool plus a decoded tail (Def. 3.1 and 3.2, Sec. 2.2): with
+ * r = unit_row[u], n = seq_lens[b] and t0 = clamp(unit_tail[u], 0, n),
+ *   S = {i in pool_idx[r][0 .. min(pool_len[r], set_cap)) : i < t0} U [t0, n),
+ * and the outputs of prhs_sparse_decode_attn over S.  A row outside
+ * [0, pool_rows) gives an empty set.  pool_idx: [pool_rows][set_cap] int32;
+ * unit_row, unit_tail: [B*Hkv] int32 (prhs_gate's row_anchor or row_other,
+ * and tail).  Precondition: pool_len[r] + n - t0 <= set_cap.
+ * ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
+prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
+                                  const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
+                                  const int32_t* unit_row, const int32_t* unit_tail, float scale,
+                                  float* out, float* lse, void* ws, size_t ws_bytes,
+                                  void* stream);
+
 /* Message for the last non-OK status returned on the calling thread. */
 const char* prhs_last_error(void);
 

@@ -39,7 +39,8 @@ PRHS_MAX_TOPK = 16384
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
-    "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_last_error",
+    "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_select_gated",
+    "prhs_pool_decode_attn", "prhs_last_error",
 ]
 
 
@@ -109,6 +110,15 @@ def lib():
                                              vp, vp, sz, vp]
         L.prhs_dense_decode_attn.restype = i32
         L.prhs_dense_decode_attn.argtypes = [P(PrhsKv), vp, ctypes.c_float, vp, vp, vp, sz, vp]
+        L.prhs_gate.restype = i32
+        L.prhs_gate.argtypes = [i32, i32, i32, i32, i32, vp, vp, ctypes.c_double, i32, i32, vp, vp,
+                                vp, vp, vp, vp, vp, vp]
+        L.prhs_select_gated.restype = i32
+        L.prhs_select_gated.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, vp, i32, vp, vp, i32,
+                                        vp, vp, vp, sz, vp]
+        L.prhs_pool_decode_attn.restype = i32
+        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, ctypes.c_float,
+                                            vp, vp, vp, sz, vp]
         L.prhs_last_error.restype = ctypes.c_char_p
         L.prhs_last_error.argtypes = []
         _lib = L
@@ -285,6 +295,75 @@ def prhs_reuse_decode_attn(kv, q, set_idx, set_len, anchor_lens, scale, out, lse
                                        set_idx.shape[-1], _ptr(anchor_lens), float(scale),
                                        _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
                                        _stream(stream)))
+
+
+def prhs_gate(q, seq_lens, tau, slot, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other,
+              tail, num_kv_heads, stream=None):
+    """Similarity gate for block step `slot`: q [B][Hq][d]; ref_q
+    [S][B][Hq][d] (dtype of q); ref_valid [S][B*Hkv]; slot_lens [S][B];
+    choice, row_anchor, row_other, tail [B*Hkv] int32 outputs."""
+    if q.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("q must be bf16 or fp32")
+    _need(q, q.dtype, "q", 3)
+    _need(ref_q, q.dtype, "ref_q", 4)
+    B, Hq, d = q.shape
+    S = ref_q.shape[0]
+    if tuple(ref_q.shape[1:]) != (B, Hq, d):
+        raise ValueError("ref_q must be [S][B][Hq][d]")
+    for t, n, shape in ((seq_lens, "seq_lens", (B,)), (ref_valid, "ref_valid", (S, B * num_kv_heads)),
+                        (slot_lens, "slot_lens", (S, B)), (choice, "choice", (B * num_kv_heads,)),
+                        (row_anchor, "row_anchor", (B * num_kv_heads,)),
+                        (row_other, "row_other", (B * num_kv_heads,)),
+                        (tail, "tail", (B * num_kv_heads,))):
+        _need(t, torch.int32, n)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{n} must have shape {shape}, got {tuple(t.shape)}")
+    dt = PRHS_BF16 if q.dtype == torch.bfloat16 else PRHS_F32
+    check(lib().prhs_gate(B, Hq, num_kv_heads, d, dt, _ptr(q), _ptr(seq_lens), float(tau), S,
+                          int(slot), _ptr(ref_q), _ptr(ref_valid), _ptr(slot_lens), _ptr(choice),
+                          _ptr(row_anchor), _ptr(row_other), _ptr(tail), _stream(stream)))
+
+
+def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len,
+                      ws, stream=None):
+    """prhs_select_shared for the units with choice < 0 only."""
+    _q_dtype(kv, q)
+    _need(choice, torch.int32, "choice")
+    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
+                       (set_idx, "set_idx", 3), (set_len, "set_len", 2),
+                       (shared_idx, "shared_idx", 3), (shared_len, "shared_len", 2)):
+        _need(t, torch.int32, n, dims)
+    if shared_idx.shape != set_idx.shape:
+        raise ValueError("shared_idx must have the shape of set_idx")
+    _need(ws, torch.uint8, "ws")
+    check(lib().prhs_select_gated(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(choice),
+                                  _ptr(topk_idx), _ptr(topk_len), topk_idx.shape[-1],
+                                  _ptr(set_idx), _ptr(set_len), set_idx.shape[-1],
+                                  _ptr(shared_idx), _ptr(shared_len), _ptr(ws), ws.numel(),
+                                  _stream(stream)))
+
+
+def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale, out, lse, ws,
+                          stream=None):
+    """Attention where unit u attends pool row unit_row[u] plus the tail
+    [unit_tail[u], n_b).  pool_idx [..][set_cap] (any leading dims, flattened
+    to rows), pool_len with the same leading dims."""
+    _q_dtype(kv, q)
+    _need(pool_idx, torch.int32, "pool_idx")
+    _need(pool_len, torch.int32, "pool_len")
+    cap = pool_idx.shape[-1]
+    rows = pool_idx.numel() // max(cap, 1)
+    if pool_len.numel() != rows:
+        raise ValueError("pool_len must have one entry per pool row")
+    _need(unit_row, torch.int32, "unit_row")
+    _need(unit_tail, torch.int32, "unit_tail")
+    _need(out, torch.float32, "out", 3)
+    if lse is not None:
+        _need(lse, torch.float32, "lse", 2)
+    _need(ws, torch.uint8, "ws")
+    check(lib().prhs_pool_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(pool_idx), _ptr(pool_len),
+                                      rows, cap, _ptr(unit_row), _ptr(unit_tail), float(scale),
+                                      _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def prhs_dense_decode_attn(kv, q, scale, out, lse, ws, stream=None):

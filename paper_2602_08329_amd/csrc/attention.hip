@@ -52,6 +52,9 @@ struct AttnArgs {
   const int32_t* set_idx;
   const int32_t* set_len;
   const int32_t* tail_start;  // [B] or null: rows also cover [tail_start[b], n_b)
+  const int32_t* unit_row;    // [units] or null: pool row of set_idx each unit attends
+  const int32_t* unit_tail;   // [units] with unit_row: first position of the unit's tail
+  int pool_rows;
   int set_cap;
   float scale_log2;
   int chunk, nsplit;
@@ -62,26 +65,45 @@ struct AttnArgs {
 };
 
 // The rows a unit attends, in order: the first `base` come from its index
-// set (entries at or beyond t0 are skipped), then the tail positions
+// set `idx` (entries at or beyond t0 are skipped), then the tail positions
 // [t0, t0 + L - base).  Dense: rows are the positions [0, n_b).  Without a
 // tail t0 = n_b.  L never exceeds set_cap, the bound the split geometry uses.
+// The set is row u of set_idx, or with a pool the row unit_row[u] (a row
+// outside the pool gives an empty set) and the tail from unit_tail[u].
 struct UnitSpan {
   int L, base, t0;
+  const int32_t* idx;
 };
 
 template <bool DENSE>
 __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, int nb) {
   UnitSpan sp;
   sp.t0 = nb;
+  sp.idx = nullptr;
   if (DENSE) {
     sp.L = sp.base = nb;
     return sp;
   }
-  int L = a.set_len[u];
+  int row = u, t0 = nb;
+  bool tail = false;
+  if (a.unit_row) {
+    row = a.unit_row[u];
+    t0 = a.unit_tail[u];
+    tail = true;
+    if (row < 0 || row >= a.pool_rows) {
+      sp.L = sp.base = 0;
+      sp.idx = a.set_idx;
+      return sp;
+    }
+  } else if (a.tail_start) {
+    t0 = a.tail_start[b];
+    tail = true;
+  }
+  sp.idx = a.set_idx + (size_t)row * a.set_cap;
+  int L = a.set_len[row];
   L = L < 0 ? 0 : (L > a.set_cap ? a.set_cap : L);
   sp.base = L;
-  if (a.tail_start) {
-    int t0 = a.tail_start[b];
+  if (tail) {
     t0 = t0 < 0 ? 0 : (t0 > nb ? nb : t0);
     sp.t0 = t0;
     L += nb - t0;
@@ -327,8 +349,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     const uint4 v = qp[kk];
     qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
-  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
-  stage_rows<DENSE, PAGED>(a, idx, start, n, sp, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, sp.idx, start, n, sp, nb, b, g, s_row);
 
   const __bf16* kb = (const __bf16*)a.kv.k;
   const __bf16* vb = (const __bf16*)a.kv.v;
@@ -433,8 +454,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   float qv[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) qv[i] = qp[i];
-  const int32_t* idx = DENSE ? nullptr : a.set_idx + (size_t)u * a.set_cap;
-  stage_rows<DENSE, PAGED>(a, idx, start, n, sp, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, sp.idx, start, n, sp, nb, b, g, s_row);
   const float* kb = (const float*)a.kv.k;
   const float* vb = (const float*)a.kv.v;
   float m_run = -INFINITY, l_run = 0.f, o[DPL];
@@ -695,6 +715,9 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.set_idx = s.set_idx;
   a.set_len = s.set_len;
   a.tail_start = dense ? nullptr : s.tail_start;
+  a.unit_row = dense ? nullptr : s.unit_row;
+  a.unit_tail = dense ? nullptr : s.unit_tail;
+  a.pool_rows = s.pool_rows;
   a.set_cap = s.set_cap;
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   const int rows_cap = dense ? s.kv.max_seq_len : s.set_cap;

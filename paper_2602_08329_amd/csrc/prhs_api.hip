@@ -186,8 +186,9 @@ prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params
 static prhs_status select_common(const prhs_kv* kv, const void* q, const prhs_params* params,
                                  int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
                                  int32_t* set_idx, int32_t* set_len, int32_t set_cap,
-                                 int32_t* shared_idx, int32_t* shared_len, bool shared, void* ws,
-                                 size_t ws_bytes, void* stream, const char* name) {
+                                 int32_t* shared_idx, int32_t* shared_len, bool shared,
+                                 const int32_t* row_choice, void* ws, size_t ws_bytes,
+                                 void* stream, const char* name) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_params(params)) != PRHS_OK) return st;
@@ -230,6 +231,7 @@ static prhs_status select_common(const prhs_kv* kv, const void* q, const prhs_pa
   a.dilate_r = params->dilate_r;
   a.shared_idx = shared ? shared_idx : nullptr;
   a.shared_len = shared ? shared_len : nullptr;
+  a.row_choice = row_choice;
   a.ws = ws;
   a.max_topk = kmax;
   return device_status(prhs::launch_select(a, (hipStream_t)stream), name);
@@ -240,7 +242,8 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
                         int32_t* set_len, int32_t set_cap, void* ws, size_t ws_bytes,
                         void* stream) {
   return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
-                       nullptr, nullptr, false, ws, ws_bytes, stream, "prhs_select launch");
+                       nullptr, nullptr, false, nullptr, ws, ws_bytes, stream,
+                       "prhs_select launch");
 }
 
 prhs_status prhs_select_shared(const prhs_kv* kv, const void* q, const prhs_params* params,
@@ -249,8 +252,19 @@ prhs_status prhs_select_shared(const prhs_kv* kv, const void* q, const prhs_para
                                int32_t* shared_idx, int32_t* shared_len, void* ws,
                                size_t ws_bytes, void* stream) {
   return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
-                       shared_idx, shared_len, true, ws, ws_bytes, stream,
+                       shared_idx, shared_len, true, nullptr, ws, ws_bytes, stream,
                        "prhs_select_shared launch");
+}
+
+prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_params* params,
+                              const int32_t* choice, int32_t* topk_idx, int32_t* topk_len,
+                              int32_t k_cap, int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                              int32_t* shared_idx, int32_t* shared_len, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (kv && kv->batch > 0 && !choice) return fail(PRHS_E_INVALID, "choice must be non-NULL");
+  return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
+                       shared_idx, shared_len, true, choice, ws, ws_bytes, stream,
+                       "prhs_select_gated launch");
 }
 
 prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t num_kv_heads,
@@ -287,9 +301,10 @@ prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t 
 
 static prhs_status attention_common(const prhs_kv* kv, const void* q, const int32_t* set_idx,
                                     const int32_t* set_len, int32_t set_cap,
-                                    const int32_t* tail_start, float scale, float* out, float* lse,
-                                    void* ws, size_t ws_bytes, void* stream, bool dense,
-                                    const char* name) {
+                                    const int32_t* tail_start, const int32_t* unit_row,
+                                    const int32_t* unit_tail, int32_t pool_rows, float scale,
+                                    float* out, float* lse, void* ws, size_t ws_bytes,
+                                    void* stream, bool dense, const char* name) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_kv_data(kv)) != PRHS_OK) return st;
@@ -313,6 +328,9 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   a.set_idx = set_idx;
   a.set_len = set_len;
   a.tail_start = tail_start;
+  a.unit_row = unit_row;
+  a.unit_tail = unit_tail;
+  a.pool_rows = pool_rows;
   a.set_cap = set_cap;
   a.scale = scale;
   a.out = out;
@@ -325,8 +343,8 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int3
                                     const int32_t* set_len, int32_t set_cap, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream) {
-  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, scale, out, lse, ws, ws_bytes,
-                          stream, false, "prhs_sparse_decode_attn launch");
+  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, scale,
+                          out, lse, ws, ws_bytes, stream, false, "prhs_sparse_decode_attn launch");
 }
 
 prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32_t* set_idx,
@@ -335,14 +353,68 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32
                                    void* ws, size_t ws_bytes, void* stream) {
   if (kv && kv->batch > 0 && !anchor_lens)
     return fail(PRHS_E_INVALID, "anchor_lens must be non-NULL");
-  return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, scale, out, lse, ws,
-                          ws_bytes, stream, false, "prhs_reuse_decode_attn launch");
+  return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, nullptr, nullptr, 0,
+                          scale, out, lse, ws, ws_bytes, stream, false,
+                          "prhs_reuse_decode_attn launch");
+}
+
+prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
+                                  const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
+                                  const int32_t* unit_row, const int32_t* unit_tail, float scale,
+                                  float* out, float* lse, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  if (pool_rows < 0) return fail(PRHS_E_INVALID, "pool_rows must be >= 0");
+  if (kv && kv->batch > 0 && (!unit_row || !unit_tail))
+    return fail(PRHS_E_INVALID, "unit_row and unit_tail must be non-NULL");
+  return attention_common(kv, q, pool_idx, pool_len, set_cap, nullptr, unit_row, unit_tail,
+                          pool_rows, scale, out, lse, ws, ws_bytes, stream, false,
+                          "prhs_pool_decode_attn launch");
+}
+
+prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t dtype, const void* q, const int32_t* seq_lens, double tau,
+                      int32_t num_slots, int32_t slot, void* ref_q, int32_t* ref_valid,
+                      int32_t* slot_lens, int32_t* choice, int32_t* row_anchor,
+                      int32_t* row_other, int32_t* tail, void* stream) {
+  if (batch < 0) return fail(PRHS_E_INVALID, "batch must be >= 0");
+  if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
+    return fail(PRHS_E_INVALID, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (head_dim < 1) return fail(PRHS_E_INVALID, "head_dim must be >= 1");
+  if (dtype != PRHS_F32 && dtype != PRHS_BF16) return fail(PRHS_E_UNSUPPORTED, "dtype %d", dtype);
+  if (!(tau >= 0.0 && tau <= 1.0)) return fail(PRHS_E_INVALID, "tau must lie in [0, 1]");
+  if (num_slots < 1 || slot < 0 || slot >= num_slots)
+    return fail(PRHS_E_INVALID, "slot (%d) must lie in [0, num_slots = %d)", slot, num_slots);
+  if ((long long)2 * num_slots * batch * num_kv_heads >= (1LL << 31))
+    return fail(PRHS_E_UNSUPPORTED, "set pool rows exceed 32-bit indices");
+  if (batch > 0 && (!q || !seq_lens || !ref_q || !ref_valid || !slot_lens || !choice ||
+                    !row_anchor || !row_other || !tail))
+    return fail(PRHS_E_INVALID, "device arrays must be non-NULL");
+  if (batch == 0) return PRHS_OK;
+  prhs::GateLaunch a;
+  a.batch = batch;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.d = head_dim;
+  a.dtype = dtype;
+  a.q = q;
+  a.seq_lens = seq_lens;
+  a.tau = tau;
+  a.num_slots = num_slots;
+  a.slot = slot;
+  a.ref_q = ref_q;
+  a.ref_valid = ref_valid;
+  a.slot_lens = slot_lens;
+  a.choice = choice;
+  a.row_anchor = row_anchor;
+  a.row_other = row_other;
+  a.tail = tail;
+  return device_status(prhs::launch_gate(a, (hipStream_t)stream), "prhs_gate launch");
 }
 
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, scale, out, lse, ws, ws_bytes,
-                          stream, true, "prhs_dense_decode_attn launch");
+  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, scale, out,
+                          lse, ws, ws_bytes, stream, true, "prhs_dense_decode_attn launch");
 }
 
 }  // extern "C"

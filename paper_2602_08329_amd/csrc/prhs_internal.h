@@ -124,6 +124,7 @@ struct SelectLaunch {
   int dilate_r;
   int32_t* shared_idx;  // optional: dilated shared set at the anchor length
   int32_t* shared_len;
+  const int32_t* row_choice;  // optional [rows]: only rows with a negative entry are selected
   void* ws;
   int max_topk;   // host bound on the clamped budget (sort size)
 };
@@ -151,6 +152,9 @@ struct AttnLaunch {
   const int32_t* set_idx;  // null for dense
   const int32_t* set_len;
   const int32_t* tail_start;  // [B] or null (reuse attention: set U [tail_start, n))
+  const int32_t* unit_row;    // [B*Hkv] or null: pool row each unit attends
+  const int32_t* unit_tail;   // [B*Hkv] with unit_row: first position of the unit's tail
+  int pool_rows;              // rows of set_idx when unit_row is given
   int set_cap;
   float scale;
   float* out;
@@ -163,5 +167,21 @@ void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int 
 size_t attn_workspace_bytes(int dtype, bool dense, int batch, int hq, int hkv, int d,
                             int rows_cap);
 hipError_t launch_attention(const AttnLaunch& a, bool dense, hipStream_t stream);
+
+struct GateLaunch {
+  int batch, hq, hkv, d, dtype;
+  const void* q;
+  const int32_t* seq_lens;
+  double tau;
+  int num_slots, slot;
+  void* ref_q;          // [num_slots][B][Hq][d]
+  int32_t* ref_valid;   // [num_slots][B*Hkv]
+  int32_t* slot_lens;   // [num_slots][B]
+  int32_t* choice;      // [B*Hkv]
+  int32_t* row_anchor;  // [B*Hkv]
+  int32_t* row_other;   // [B*Hkv]
+  int32_t* tail;        // [B*Hkv]
+};
+hipError_t launch_gate(const GateLaunch& a, hipStream_t stream);
 
 }  // namespace prhs

@@ -59,7 +59,13 @@ struct SelArgs {
   int32_t* shared_idx;  // optional [rows][set_cap]: the dilated shared set at n0
   int32_t* shared_len;
   int balance_cus;      // fused refresh: > 0 = CU count to balance rows over, 0 = off
+  const int32_t* row_choice;  // optional [rows]: rows with an entry >= 0 are left untouched
 };
+
+// Rows the similarity gate lets share are not selected again.
+__device__ __forceinline__ bool row_skipped(const SelArgs& a, int row) {
+  return a.row_choice != nullptr && a.row_choice[row] >= 0;
+}
 
 struct RowGeom {
   int n0, sink_end, win_start, m, kb;
@@ -131,6 +137,7 @@ __device__ void find_threshold(const uint32_t* h, uint32_t kk, uint32_t* scan, i
 
 __global__ __launch_bounds__(256) void select_clear(SelArgs a) {
   const int row = blockIdx.x;
+  if (row_skipped(a, row)) return;
   for (int i = threadIdx.x; i < kHistBins; i += 256) {
     a.hist0[(size_t)row * kHistBins + i] = 0u;
     a.hist1[(size_t)row * kHistBins + i] = 0u;
@@ -219,6 +226,7 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
   __shared__ uint32_t hist[kHistBins];
   __shared__ int32_t s_page[kScoreChunk + 1];
   const int row = blockIdx.y;
+  if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int base = blockIdx.x * kScoreChunk;
@@ -289,6 +297,7 @@ __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
   __shared__ uint32_t hist[kHistBins];
   __shared__ float qs[16 * D];
   const int row = blockIdx.y;
+  if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int base = blockIdx.x * kScoreChunk;
@@ -339,6 +348,7 @@ __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   __shared__ uint32_t s_krem, s_cnt;
   __shared__ uint32_t s_base[2];
   const int row = blockIdx.y;
+  if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int base = blockIdx.x * kFilterChunk;
@@ -552,6 +562,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt, s_base;
   const int row = blockIdx.x;
+  if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
@@ -815,6 +826,7 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   __shared__ int s_len[kBalanceMaxBatch];
   __shared__ int s_row;
   const int row = fused_row(a, blockIdx.x, s_len, &s_row);
+  if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
@@ -1062,6 +1074,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.shared_idx = s.shared_idx;
   a.shared_len = s.shared_len;
   a.balance_cus = 0;
+  a.row_choice = s.row_choice;
 
   // many short contiguous bf16 rows: the whole refresh in one launch
   if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {

@@ -153,3 +153,65 @@ class DecodeRunner:
         for l in range(self.L):
             o = None if outs is None else outs[l]
             self.dense(l, j, *(o if o is not None else (None, None)))
+
+
+class GatedDecodeRunner(DecodeRunner):
+    """The decode schedule with the similarity gate (Sec. 4.1, Similarity
+    Criteria): blocks of s steps; at every step each group's anchor layer
+    runs prhs_gate, the units it sends to retrieval run prhs_select_gated,
+    and every layer attends its pool row plus the decoded tail through
+    prhs_pool_decode_attn.  Per group the state is the block's reference
+    queries, retrieval flags and lengths per slot, and the set pool
+    [2][s][B][Hkv][set_cap] (kind 0 critical sets, kind 1 shared sets)."""
+
+    def __init__(self, inp, device="cuda", tau=0.8):
+        super().__init__(inp, device)
+        w = self.w
+        self.tau = float(tau)
+        dev, i32 = self.device, torch.int32
+        G_, S, U = self.groups, w.s, w.batch * w.hkv
+        q = inp.q
+        self.ref_q = torch.zeros((G_, S) + tuple(q.shape[2:]), dtype=q.dtype, device=dev)
+        self.ref_valid = torch.zeros(G_, S, U, dtype=i32, device=dev)
+        self.slot_lens = torch.zeros(G_, S, w.batch, dtype=i32, device=dev)
+        self.pool = torch.zeros(G_, 2, S, w.batch, w.hkv, self.set_cap, dtype=i32, device=dev)
+        self.pool_len = torch.zeros(G_, 2, S, w.batch, w.hkv, dtype=i32, device=dev)
+        self.choice = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.row_anchor = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.row_other = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.tail = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.gated_step = [None] * G_
+
+    def selection_step(self, j):
+        w = self.w
+        slot = j % w.s
+        for gi in range(self.groups):
+            if slot != 0 and self.gated_step[gi] != j - 1:
+                raise RuntimeError(f"group {gi}: the gate runs at every step of a block in order")
+            l = gi * w.G
+            B.prhs_gate(self.inp.q[l, j], self.seq_lens[j], self.tau, slot, self.ref_q[gi],
+                        self.ref_valid[gi], self.slot_lens[gi], self.choice[gi],
+                        self.row_anchor[gi], self.row_other[gi], self.tail[gi], w.hkv)
+            B.prhs_select_gated(self.kv[l][j], self.inp.q[l, j], self.params, self.choice[gi],
+                                self.topk_idx[gi], self.topk_len[gi], self.pool[gi, 0, slot],
+                                self.pool_len[gi, 0, slot], self.pool[gi, 1, slot],
+                                self.pool_len[gi, 1, slot], self.ws_select)
+            self.gated_step[gi] = j
+
+    def set_for(self, l, j):
+        """(pool, pool_len, unit_row, unit_tail) that layer l attends at step j."""
+        gi = l // self.w.G
+        if self.gated_step[gi] != j:
+            raise RuntimeError(f"group {gi} has not been gated at step {j}")
+        rows = self.row_anchor[gi] if l % self.w.G == 0 else self.row_other[gi]
+        return self.pool[gi], self.pool_len[gi], rows, self.tail[gi]
+
+    def attend(self, l, j, out=None, lse=None):
+        pool, plen, rows, tail = self.set_for(l, j)
+        B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], pool, plen, rows, tail,
+                                self.scale, self.out if out is None else out,
+                                self.lse if lse is None else lse, self.ws_attn)
+
+    def retrieving_units(self):
+        """Units of every group that retrieved at the last gated step."""
+        return int((self.choice < 0).sum().item())

@@ -209,6 +209,45 @@ def test_select_shared_validation(L):
                                 cap, None, None, None, 0, None) == B.PRHS_OK
 
 
+def test_gate_validation(L):
+    def gate(batch=2, hq=8, hkv=2, d=128, dtype=B.PRHS_BF16, tau=0.8, S=4, slot=1, ptr=0x10):
+        return L.prhs_gate(batch, hq, hkv, d, dtype, ptr, ptr, tau, S, slot, ptr, ptr, ptr, ptr, ptr,
+                           ptr, ptr, None)
+    assert gate(tau=1.5) == B.PRHS_E_INVALID
+    assert gate(tau=-0.1) == B.PRHS_E_INVALID
+    assert gate(tau=float("nan")) == B.PRHS_E_INVALID
+    assert gate(slot=4) == B.PRHS_E_INVALID and b"slot" in L.prhs_last_error()
+    assert gate(slot=-1) == B.PRHS_E_INVALID
+    assert gate(hq=6, hkv=4) == B.PRHS_E_INVALID
+    assert gate(dtype=7) == B.PRHS_E_UNSUPPORTED
+    assert gate(ptr=None) == B.PRHS_E_INVALID
+    assert gate(batch=0, ptr=None) == B.PRHS_OK      # nothing to do, no device work
+
+
+def test_select_gated_and_pool_attention_validation(L):
+    kv = _kv()
+    p = B.params(k=8, window=4, refresh_every=4)
+    cap = L.prhs_set_capacity(ctypes.byref(p), kv.max_seq_len)
+    n = ctypes.c_size_t(0)
+    L.prhs_workspace_size(B.PRHS_OP_SELECT, ctypes.byref(kv), ctypes.byref(p), 0, ctypes.byref(n))
+    st = L.prhs_select_gated(ctypes.byref(kv), 0x1, ctypes.byref(p), None, 0x2, 0x3, 64, 0x4, 0x5,
+                             cap, 0x6, 0x7, 0x8, n.value, None)
+    assert st == B.PRHS_E_INVALID and b"choice" in L.prhs_last_error()
+    st = L.prhs_select_gated(ctypes.byref(kv), 0x1, ctypes.byref(p), 0x9, 0x2, 0x3, 64, 0x4, 0x5,
+                             cap - 1, 0x6, 0x7, 0x8, n.value, None)
+    assert st == B.PRHS_E_CAPACITY
+    L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 300, ctypes.byref(n))
+    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, -1, 300, 0x4, 0x5, 0.1, 0x6, None,
+                                 0x7, n.value, None)
+    assert st == B.PRHS_E_INVALID
+    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 8, 300, None, 0x5, 0.1, 0x6, None,
+                                 0x7, n.value, None)
+    assert st == B.PRHS_E_INVALID
+    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 8, 300, 0x4, 0x5, 0.1, 0x6, None,
+                                 0x7, n.value - 1, None)
+    assert st == B.PRHS_E_WORKSPACE
+
+
 def test_dilate_validation_and_empty_batch(L):
     p = B.params(k=8)
     assert L.prhs_dilate_reuse(ctypes.byref(p), 2, 0, 1, 1, 8, 1, 1, 1, 1, 8, None) == B.PRHS_E_INVALID
