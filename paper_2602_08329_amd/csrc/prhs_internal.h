@@ -58,22 +58,6 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Warp-aggregated append: lanes with pred reserve consecutive slots of
-// *counter (one atomic per wave).  Returns the lane's slot or -1.  Every lane
-// of the wave must call it.
-__device__ __forceinline__ int wave_append(bool pred, uint32_t* counter) {
-  const uint64_t mask = __ballot(pred);
-  const int lane = __lane_id();
-  const int cnt = __popcll(mask);
-  if (cnt == 0) return -1;
-  const int leader = __ffsll((long long)mask) - 1;
-  uint32_t base = 0;
-  if (lane == leader) base = atomicAdd(counter, (uint32_t)cnt);
-  base = __shfl(base, leader);
-  const int off = __popcll(mask & ((1ull << lane) - 1ull));
-  return pred ? (int)(base + off) : -1;
-}
-
 // Exclusive prefix sum over a workgroup of BLOCK threads; `scratch` holds
 // BLOCK/64 + 1 elements of LDS.  Returns this thread's exclusive prefix and
 // the block total in *total.  Must be reached by every thread.  With T =

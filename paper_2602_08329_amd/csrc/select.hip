@@ -1,19 +1,26 @@
 // Refresh-step selection for one layer: ranking scores over the middle range,
-// exact top-k by multi-level radix select, ordering by (score desc, position
-// asc), and the critical set sink U top-k U window (Sec. 4.1 Selection
-// Criteria; top-k oracle of Sec. 2.3).
+// the exact top-k under the order (score desc, position asc), and the
+// critical set sink U top-k U window (Sec. 4.1 Selection Criteria; top-k
+// oracle of Sec. 2.3); optionally also the dilated shared set at the anchor
+// length (Eq. neighboring), and optionally only for the rows a similarity
+// gate sends to retrieval.
 //
-// Pipeline (one launch each, all on the caller's stream):
-//   select_clear   zero the per-row histograms and counters
-//   score_*        sigma_i = max_h q_h . k_i (raw, fp32) -> order-preserving
-//                  u32 key; fused histogram of the top 11 key bits
-//   select_filter  locate the threshold bin of level 0; keys above it are
-//                  selected, keys in it become candidates (with the level-1
-//                  histogram fused)
-//   select_finish  remaining radix levels over the candidates, the 64-bit
-//                  composite (key, kIdxMax - pos) making every key distinct so
-//                  ties go to the lower position; bitonic sort of the k
-//                  winners in LDS; ordered compaction of the anchor set.
+// Two paths, both on the caller's stream:
+//   select_fused   many short contiguous bf16 rows: one workgroup per row
+//                  scores into LDS, takes exact thresholds for k and m over
+//                  the 32-bit keys and compacts in position order (which
+//                  settles ties) -- one launch;
+//   radix path     otherwise, one launch each:
+//     select_clear   zero the per-row histograms and counters
+//     score_*        sigma_i = max_h q_h . k_i (raw, fp32) -> order-preserving
+//                    u32 key; fused histogram of the top 11 key bits
+//     select_filter  locate the threshold bin of level 0; keys above it are
+//                    selected, keys in it become candidates (with the level-1
+//                    histogram fused)
+//     select_finish  the remaining radix levels over the candidates as 64-bit
+//                    composites (key, kIdxMax - pos), distinct, so ties go to
+//                    the lower position; one segmented bitmap pass writes the
+//                    ordered outputs.
 #include <stdlib.h>
 
 #include "prhs.h"
