@@ -67,6 +67,9 @@ __all__ = [
     "group_similar",
     "gate_choice",
     "GatedDecodeOracle",
+    "psaw_boundary",
+    "psaw_visible_start",
+    "psaw_restrict",
 ]
 
 
@@ -322,10 +325,13 @@ class DecodeOracle:
     The anchor layer of a group at a refresh step attends its undilated
     critical set C(n0); every other (layer, step) attends the dilated shared
     set built from the group's latest anchor top-k (Sec. 4.1 and Def. 3.2, Sec. 2.2).
+    With psaw = (n_layers, l_s, phi, alpha) every attended set is further
+    restricted to the layer's PSAW-visible positions (CPE, Sec. 4.2 and 4.4);
+    the selection itself is unchanged.
     """
 
     def __init__(self, sink, window, s, G, r=1, k=None, k_num=0, k_den=0,
-                 dilate_m=-1, scale=None):
+                 dilate_m=-1, scale=None, psaw=None):
         self.sink = sink
         self.window = window
         self.s = s
@@ -336,6 +342,7 @@ class DecodeOracle:
         self.k_den = k_den
         self.dilate_m = dilate_m
         self.scale = scale
+        self.psaw = psaw
         self.state = {}  # anchor layer -> (s_star, n0, k_b)
 
     def refresh(self, layer, Qg, K, n0):
@@ -353,15 +360,49 @@ class DecodeOracle:
     def step_set(self, layer, step, Qg, K, n):
         """Index set that (layer, step) attends at current length n."""
         if is_refresh(step, layer, self.s, self.G):
-            _, c = self.refresh(layer, Qg, K, n)
-            return c
-        return self.shared(layer, n)
+            _, S = self.refresh(layer, Qg, K, n)
+        else:
+            S = self.shared(layer, n)
+        return _psaw_apply(self.psaw, S, layer, n, self.sink)
 
     def attend(self, Qg, K, V, S):
         """Sparse attention of every query head of the group over S."""
         Qg = np.atleast_2d(_f64(Qg))
         outs = [sparse_attention(Qg[h], K, V, S, self.scale) for h in range(Qg.shape[0])]
         return np.stack([o[0] for o in outs]), np.array([o[1] for o in outs])
+
+
+# ---------------------------------------------------------------------------
+# Progressive sliding attention window (Sec. 4.2, Eq. psaw)
+# ---------------------------------------------------------------------------
+
+def psaw_boundary(layer, n_layers, t, l_s, phi, alpha):
+    """P_l(t) of Eq. psaw for 1-based layer `layer` of `n_layers` at 1-based
+    step t: 0 below the pruning depth l_s, else floor((1 - phi^(alpha (l -
+    l_s) / (N - l_s))) t)."""
+    if layer < l_s:
+        return 0
+    e = alpha * (layer - l_s) / (n_layers - l_s)
+    return int(math.floor((1.0 - phi ** e) * t))
+
+
+def psaw_visible_start(layer0, n_layers, n, sink, l_s, phi, alpha):
+    """First visible non-sink 0-based position for 0-based layer `layer0` at
+    current length n.  Eq. psaw masks the 1-based positions strictly between
+    C_sink and P_l(t) (layer l = layer0 + 1, t = n); in 0-based terms the
+    masked range is [C_sink, P - 1), so the visible set is [0, C_sink) U
+    [max(C_sink, P - 1), n)."""
+    P = psaw_boundary(layer0 + 1, n_layers, n, l_s, phi, alpha)
+    sink_end = min(sink, n)
+    return max(sink_end, P - 1)
+
+
+def psaw_restrict(S, start, sink, n):
+    """Index set S intersected with the PSAW-visible positions [0, C_sink) U
+    [start, n) (CPE: the CIS set under the PSAW mask, Sec. 4.4)."""
+    S = np.asarray(S, dtype=np.int64)
+    sink_end = min(sink, n)
+    return S[(S < sink_end) | ((S >= start) & (S < n))]
 
 
 # ---------------------------------------------------------------------------
@@ -418,10 +459,11 @@ class GatedDecodeOracle:
     undilated critical set C(n); every other (layer, step) attends the
     dilated shared set of the selection it uses, grown by the tokens decoded
     since that selection (Sec. 4.1; Def. 3.2, Sec. 2.2).  The retrieval ratio
-    is the fraction of (anchor layer, step) pairs that retrieve."""
+    is the fraction of (anchor layer, step) pairs that retrieve.  psaw as in
+    DecodeOracle."""
 
     def __init__(self, sink, window, s, G, tau, r=1, k=None, k_num=0, k_den=0,
-                 dilate_m=-1, scale=None):
+                 dilate_m=-1, scale=None, psaw=None):
         self.sink = sink
         self.window = window
         self.s = s
@@ -433,6 +475,7 @@ class GatedDecodeOracle:
         self.k_den = k_den
         self.dilate_m = dilate_m
         self.scale = scale
+        self.psaw = psaw
         self.anchors = {}    # anchor layer -> [(step, Qg, s_star, n0, k_b)] of the block
         self.decision = {}   # (anchor layer, step) -> step whose selection is used
         self.retrievals = 0
@@ -455,6 +498,9 @@ class GatedDecodeOracle:
     def step_set(self, layer, step, Qg, K, n):
         """Index set that (layer, step) attends at current length n.  K is
         read only where the anchor layer retrieves."""
+        return _psaw_apply(self.psaw, self._step_set(layer, step, Qg, K, n), layer, n, self.sink)
+
+    def _step_set(self, layer, step, Qg, K, n):
         a = anchor_layer(layer, self.G)
         if layer == a:
             if step % self.s == 0:
@@ -475,6 +521,14 @@ class GatedDecodeOracle:
         Qg = np.atleast_2d(_f64(Qg))
         outs = [sparse_attention(Qg[h], K, V, S, self.scale) for h in range(Qg.shape[0])]
         return np.stack([o[0] for o in outs]), np.array([o[1] for o in outs])
+
+
+def _psaw_apply(psaw, S, layer, n, sink):
+    if psaw is None:
+        return S
+    n_layers, l_s, phi, alpha = psaw
+    start = psaw_visible_start(layer, n_layers, n, sink, l_s, phi, alpha)
+    return psaw_restrict(S, start, sink, n)
 
 
 def brute_force_topk_mass(A, n0, k, sink, window):

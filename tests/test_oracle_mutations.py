@@ -83,6 +83,18 @@ def _group_any_head(Qg_now, Qg_ref, tau):
     return any(M.query_similar(Qn[h], Qr[h], tau) for h in range(Qn.shape[0]))
 
 
+def _psaw_start_p_not_p_minus_1(layer0, n_layers, n, sink, l_s, phi, alpha):
+    P = M.psaw_boundary(layer0 + 1, n_layers, n, l_s, phi, alpha)
+    return max(min(sink, n), P)
+
+
+def _psaw_zero_based_layer(layer, n_layers, t, l_s, phi, alpha):
+    if layer - 1 < l_s:
+        return 0
+    e = alpha * (layer - 1 - l_s) / (n_layers - l_s)
+    return int(math.floor((1.0 - phi ** e) * t))
+
+
 _orig = {name: getattr(M, name) for name in
          ["dense_attention", "topk_middle", "reuse_set", "ranking_scores",
           "region_bounds", "dilation_m", "is_refresh"]}
@@ -102,6 +114,8 @@ MUTANTS = [
     ("query_similar", _similar_ignoring_sign),
     ("gate_choice", _gate_oldest_first),
     ("group_similar", _group_any_head),
+    ("psaw_visible_start", _psaw_start_p_not_p_minus_1),
+    ("psaw_boundary", _psaw_zero_based_layer),
 ]
 
 

@@ -570,3 +570,48 @@ def test_gate_mixed_decisions_follow_the_rule():
     assert np.array_equal(sets[(0, 2)], O.anchor_set(S2, n + 3, 2, 8))
     assert np.array_equal(sets[(1, 2)], O.reuse_set(S2, m, 1, n + 3, n + 3, 2, 8))
     assert np.array_equal(sets[(0, 3)], O.reuse_set(S2, m, 1, n + 3, n + 4, 2, 8))
+
+
+# ---------------------------------------------------------------- PSAW
+
+def test_psaw_boundary_closed_forms():
+    # Eq. psaw: nothing below l_s and at l_s itself (phi^0 = 1); at the top
+    # layer l = N the boundary is floor((1 - phi^alpha) t)
+    N, l_s, phi, alpha = 32, 24, 0.7, 1.0
+    assert all(O.psaw_boundary(l, N, 1000, l_s, phi, alpha) == 0 for l in range(1, l_s + 1))
+    assert O.psaw_boundary(N, N, 1000, l_s, phi, alpha) == 300
+    assert O.psaw_boundary(N, N, 10, l_s, 0.5, 2.0) == 7            # 1 - 0.25 = 0.75
+    b = [O.psaw_boundary(l, N, 4096, l_s, phi, alpha) for l in range(l_s, N + 1)]
+    assert b == sorted(b) and b[-1] < 4096 * 0.31                   # monotone in depth
+    assert O.psaw_boundary(N, N, 4096, l_s, phi, 0.0) == 0          # alpha = 0: no pruning
+
+
+def test_psaw_visible_set_by_definition():
+    # 1-based masked range (C_sink, P) against the 0-based restriction
+    N, l_s, phi, alpha, sink = 8, 6, 0.6, 1.0, 3
+    for layer0 in range(N):
+        for n in (1, 2, 3, 5, 40, 97):
+            P = O.psaw_boundary(layer0 + 1, N, n, l_s, phi, alpha)
+            visible1 = [p for p in range(1, n + 1) if p <= sink or p >= P]
+            start = O.psaw_visible_start(layer0, N, n, sink, l_s, phi, alpha)
+            S = np.arange(n)
+            assert list(O.psaw_restrict(S, start, sink, n) + 1) == visible1, (layer0, n)
+
+
+def test_psaw_schedule_is_the_cis_set_under_the_mask():
+    # CPE: the schedule with PSAW attends exactly the CIS set restricted to
+    # the visible positions; without pruning layers it is the CIS schedule
+    K, Qs, n = _gate_inputs(8, L=4, T=6)
+    kw = dict(sink=4, window=16, s=3, G=2, r=1, k=24)
+    for psaw in ((4, 2, 0.5, 1.0), (4, 5, 0.5, 1.0)):
+        plain = _run_schedule(O.DecodeOracle(**kw), Qs, K, n, 4, 6)
+        cpe = _run_schedule(O.DecodeOracle(psaw=psaw, **kw), Qs, K, n, 4, 6)
+        for (l, j), S in plain.items():
+            start = O.psaw_visible_start(l, 4, n + j + 1, 4, *psaw[1:])
+            assert np.array_equal(cpe[(l, j)], O.psaw_restrict(S, start, 4, n + j + 1))
+            if psaw[1] == 5:
+                assert np.array_equal(cpe[(l, j)], S)
+        top = cpe[(3, 5)]
+        if psaw[1] == 2:
+            start = O.psaw_visible_start(3, 4, n + 6, 4, 2, 0.5, 1.0)
+            assert start > 4 and not np.any((top >= 4) & (top < start))
