@@ -86,13 +86,27 @@ def record_step(run, j, gated):
     for l in range(run.L):
         if gated:
             pool, plen, urow, utail = run.set_for(l, j)
-            rows[l] = int((plen.reshape(-1)[urow.long()] + (seq - utail)).sum())
+            pool = pool.reshape(-1, pool.shape[-1])[urow.long()]
+            plen = plen.reshape(-1)[urow.long()]
         else:
-            s_idx, s_len, tail = run.set_for(l, j)
-            r = int(s_len.sum())
-            if tail is not None:   # rows [n0_b, n_b) of every kv head follow the set
-                r += int((run.seq_lens[j] - tail).sum()) * w.hkv
-            rows[l] = r
+            pool, plen, tail = run.set_for(l, j)
+            pool, plen = pool.reshape(-1, pool.shape[-1]), plen.reshape(-1)
+            utail = seq if tail is None else tail.repeat_interleave(w.hkv)
+        start = run.psaw_start.get((l, j))
+        if start is None:
+            rows[l] = int((plen + (seq - utail)).sum())
+        else:
+            # rows the PSAW mask leaves: set entries and tail positions outside
+            # [sink, start)
+            lo = w.sink
+            hi = start.repeat_interleave(w.hkv).view(-1, 1)
+            col = torch.arange(pool.shape[-1], device=pool.device).view(1, -1)
+            inset = (col < plen.view(-1, 1)) & (pool < utail.view(-1, 1))
+            vis = inset & ((pool < lo) | (pool >= hi))
+            t0 = utail.view(-1)
+            tail_vis = (seq - torch.maximum(t0, torch.maximum(hi.view(-1), torch.full_like(t0, lo)))
+                        ).clamp(min=0) + (torch.minimum(seq, torch.full_like(t0, lo)) - t0).clamp(min=0)
+            rows[l] = int(vis.sum() + tail_vis.sum())
         run.attend(l, j)
     return rows, sel
 
@@ -216,6 +230,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-step-sets", action="store_true",
                     help="rebuild the dilated shared set at every step instead of once per refresh")
+    ap.add_argument("--psaw", action="store_true",
+                    help="progressive sliding attention window on the top layers (Sec. 5.1 "
+                         "defaults: l_s = floor(3N/4), phi = 0.7, alpha = 1): CPE with --gate")
     ap.add_argument("--gate", type=float, default=None, metavar="TAU",
                     help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
                          "fixed refresh period (blocks of refresh_every steps)")
@@ -235,7 +252,7 @@ def main():
 
     from paper_2602_08329_amd import binding as B
     from paper_2602_08329_amd import synth
-    from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner
+    from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner, psaw_defaults
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -256,10 +273,11 @@ def main():
     if gated and args.per_step_sets:
         print("--gate and --per-step-sets exclude each other", file=sys.stderr)
         sys.exit(2)
+    psaw = psaw_defaults(len(inp.K)) if args.psaw else None
     if gated:
-        run = GatedDecodeRunner(inp, dev, tau=args.gate)
+        run = GatedDecodeRunner(inp, dev, tau=args.gate, psaw=psaw)
     else:
-        run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets)
+        run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets, psaw=psaw)
 
     # one untimed pass over all steps: set sizes and selection bytes
     set_lens = {}
@@ -354,6 +372,7 @@ def main():
             "paged": w.paged, "decode_steps_cycled": T,
             "shared_sets": ("similarity gate" if gated else
                             "per step" if args.per_step_sets else "per refresh + decoded tail"),
+            "psaw": ({"l_s": psaw[0], "phi": psaw[1], "alpha": psaw[2]} if psaw else None),
         },
         "effective_gbps": round(eff_gbps, 1),
         "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),

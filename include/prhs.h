@@ -302,17 +302,24 @@ prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_param
                               size_t ws_bytes, void* stream);
 
 /* Token-sparse decode attention where every (b, kv head g) attends its own
- * row of a set pool plus a decoded tail (Def. 3.1 and 3.2, Sec. 2.2): with
- * r = unit_row[u], n = seq_lens[b] and t0 = clamp(unit_tail[u], 0, n),
+ * row of a set pool plus a decoded tail (Def. 3.1 and 3.2, Sec. 2.2),
+ * optionally under the progressive sliding attention window (Sec. 4.2,
+ * Eq. psaw): with r = unit_row[u], n = seq_lens[b] and
+ * t0 = clamp(unit_tail[u], 0, n),
  *   S = {i in pool_idx[r][0 .. min(pool_len[r], set_cap)) : i < t0} U [t0, n),
- * and the outputs of prhs_sparse_decode_attn over S.  A row outside
- * [0, pool_rows) gives an empty set.  pool_idx: [pool_rows][set_cap] int32;
- * unit_row, unit_tail: [B*Hkv] int32 (prhs_gate's row_anchor or row_other,
- * and tail).  Precondition: pool_len[r] + n - t0 <= set_cap.
- * ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
+ * minus, when psaw_start is given, the positions in
+ * [psaw_sink, psaw_start[b]) (the layer's masked range; psaw_start[b] is the
+ * first visible non-sink position), and the outputs of
+ * prhs_sparse_decode_attn over S.  A row outside [0, pool_rows) gives an
+ * empty set.  pool_idx: [pool_rows][set_cap] int32; unit_row, unit_tail:
+ * [B*Hkv] int32 (prhs_gate's row_anchor or row_other, and tail; or the
+ * identity rows and per-unit anchor lengths of the fixed schedule's sets);
+ * psaw_start: [B] int32 or NULL.  Precondition: pool_len[r] + n - t0 <=
+ * set_cap.  ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
-                                  const int32_t* unit_row, const int32_t* unit_tail, float scale,
+                                  const int32_t* unit_row, const int32_t* unit_tail,
+                                  const int32_t* psaw_start, int32_t psaw_sink, float scale,
                                   float* out, float* lse, void* ws, size_t ws_bytes,
                                   void* stream);
 

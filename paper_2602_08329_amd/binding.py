@@ -117,8 +117,8 @@ def lib():
         L.prhs_select_gated.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, vp, i32, vp, vp, i32,
                                         vp, vp, vp, sz, vp]
         L.prhs_pool_decode_attn.restype = i32
-        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, ctypes.c_float,
-                                            vp, vp, vp, sz, vp]
+        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, vp, i32,
+                                            ctypes.c_float, vp, vp, vp, sz, vp]
         L.prhs_last_error.restype = ctypes.c_char_p
         L.prhs_last_error.argtypes = []
         _lib = L
@@ -344,10 +344,13 @@ def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, sh
 
 
 def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale, out, lse, ws,
-                          stream=None):
+                          stream=None, psaw_start=None, psaw_sink=0):
     """Attention where unit u attends pool row unit_row[u] plus the tail
-    [unit_tail[u], n_b).  pool_idx [..][set_cap] (any leading dims, flattened
-    to rows), pool_len with the same leading dims."""
+    [unit_tail[u], n_b), without the positions [psaw_sink, psaw_start[b])
+    when psaw_start [B] is given.  pool_idx [..][set_cap] (any leading dims,
+    flattened to rows), pool_len with the same leading dims."""
+    if psaw_start is not None:
+        _need(psaw_start, torch.int32, "psaw_start", 1)
     _q_dtype(kv, q)
     _need(pool_idx, torch.int32, "pool_idx")
     _need(pool_len, torch.int32, "pool_len")
@@ -362,8 +365,9 @@ def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale,
         _need(lse, torch.float32, "lse", 2)
     _need(ws, torch.uint8, "ws")
     check(lib().prhs_pool_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(pool_idx), _ptr(pool_len),
-                                      rows, cap, _ptr(unit_row), _ptr(unit_tail), float(scale),
-                                      _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+                                      rows, cap, _ptr(unit_row), _ptr(unit_tail),
+                                      _ptr(psaw_start), int(psaw_sink), float(scale), _ptr(out),
+                                      _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def prhs_dense_decode_attn(kv, q, scale, out, lse, ws, stream=None):

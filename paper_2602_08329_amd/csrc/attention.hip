@@ -55,6 +55,8 @@ struct AttnArgs {
   const int32_t* unit_row;    // [units] or null: pool row of set_idx each unit attends
   const int32_t* unit_tail;   // [units] with unit_row: first position of the unit's tail
   int pool_rows;
+  const int32_t* psaw_start;  // [B] or null: positions in [psaw_sink, psaw_start[b]) are skipped
+  int psaw_sink;
   int set_cap;
   float scale_log2;
   int chunk, nsplit;
@@ -73,6 +75,7 @@ struct AttnArgs {
 struct UnitSpan {
   int L, base, t0;
   const int32_t* idx;
+  int mask_lo, mask_hi;  // rows at positions in [mask_lo, mask_hi) are skipped (PSAW)
 };
 
 template <bool DENSE>
@@ -80,9 +83,14 @@ __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, i
   UnitSpan sp;
   sp.t0 = nb;
   sp.idx = nullptr;
+  sp.mask_lo = sp.mask_hi = 0;
   if (DENSE) {
     sp.L = sp.base = nb;
     return sp;
+  }
+  if (a.psaw_start) {
+    sp.mask_lo = a.psaw_sink;
+    sp.mask_hi = a.psaw_start[b];
   }
   int row = u, t0 = nb;
   bool tail = false;
@@ -145,11 +153,15 @@ __device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t* idx
     if (r < n) {
       if (DENSE) {
         pos[k] = t;
-      } else if (t < sp.base) {
-        const int p = idx[t];
-        pos[k] = p < sp.t0 ? p : -1;
       } else {
-        pos[k] = sp.t0 + (t - sp.base);
+        int p;
+        if (t < sp.base) {
+          p = idx[t];
+          p = p < sp.t0 ? p : -1;
+        } else {
+          p = sp.t0 + (t - sp.base);
+        }
+        pos[k] = (p >= sp.mask_lo && p < sp.mask_hi) ? -1 : p;
       }
     }
   }
@@ -718,6 +730,8 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.unit_row = dense ? nullptr : s.unit_row;
   a.unit_tail = dense ? nullptr : s.unit_tail;
   a.pool_rows = s.pool_rows;
+  a.psaw_start = dense ? nullptr : s.psaw_start;
+  a.psaw_sink = s.psaw_sink;
   a.set_cap = s.set_cap;
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   const int rows_cap = dense ? s.kv.max_seq_len : s.set_cap;

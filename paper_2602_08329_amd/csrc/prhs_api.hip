@@ -302,7 +302,8 @@ prhs_status prhs_dilate_reuse(const prhs_params* params, int32_t batch, int32_t 
 static prhs_status attention_common(const prhs_kv* kv, const void* q, const int32_t* set_idx,
                                     const int32_t* set_len, int32_t set_cap,
                                     const int32_t* tail_start, const int32_t* unit_row,
-                                    const int32_t* unit_tail, int32_t pool_rows, float scale,
+                                    const int32_t* unit_tail, int32_t pool_rows,
+                                    const int32_t* psaw_start, int32_t psaw_sink, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream, bool dense, const char* name) {
   prhs_status st = check_kv_shape(kv);
@@ -331,6 +332,8 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   a.unit_row = unit_row;
   a.unit_tail = unit_tail;
   a.pool_rows = pool_rows;
+  a.psaw_start = psaw_start;
+  a.psaw_sink = psaw_sink;
   a.set_cap = set_cap;
   a.scale = scale;
   a.out = out;
@@ -343,8 +346,9 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int3
                                     const int32_t* set_len, int32_t set_cap, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream) {
-  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, scale,
-                          out, lse, ws, ws_bytes, stream, false, "prhs_sparse_decode_attn launch");
+  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, nullptr,
+                          0, scale, out, lse, ws, ws_bytes, stream, false,
+                          "prhs_sparse_decode_attn launch");
 }
 
 prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32_t* set_idx,
@@ -354,21 +358,23 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32
   if (kv && kv->batch > 0 && !anchor_lens)
     return fail(PRHS_E_INVALID, "anchor_lens must be non-NULL");
   return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, nullptr, nullptr, 0,
-                          scale, out, lse, ws, ws_bytes, stream, false,
+                          nullptr, 0, scale, out, lse, ws, ws_bytes, stream, false,
                           "prhs_reuse_decode_attn launch");
 }
 
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
-                                  const int32_t* unit_row, const int32_t* unit_tail, float scale,
+                                  const int32_t* unit_row, const int32_t* unit_tail,
+                                  const int32_t* psaw_start, int32_t psaw_sink, float scale,
                                   float* out, float* lse, void* ws, size_t ws_bytes,
                                   void* stream) {
   if (pool_rows < 0) return fail(PRHS_E_INVALID, "pool_rows must be >= 0");
+  if (psaw_sink < 0) return fail(PRHS_E_INVALID, "psaw_sink must be >= 0");
   if (kv && kv->batch > 0 && (!unit_row || !unit_tail))
     return fail(PRHS_E_INVALID, "unit_row and unit_tail must be non-NULL");
   return attention_common(kv, q, pool_idx, pool_len, set_cap, nullptr, unit_row, unit_tail,
-                          pool_rows, scale, out, lse, ws, ws_bytes, stream, false,
-                          "prhs_pool_decode_attn launch");
+                          pool_rows, psaw_start, psaw_sink, scale, out, lse, ws, ws_bytes,
+                          stream, false, "prhs_pool_decode_attn launch");
 }
 
 prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
@@ -413,8 +419,9 @@ prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, 
 
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, scale, out,
-                          lse, ws, ws_bytes, stream, true, "prhs_dense_decode_attn launch");
+  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr, 0,
+                          scale, out, lse, ws, ws_bytes, stream, true,
+                          "prhs_dense_decode_attn launch");
 }
 
 }  // extern "C"

@@ -139,6 +139,8 @@ struct AttnLaunch {
   const int32_t* unit_row;    // [B*Hkv] or null: pool row each unit attends
   const int32_t* unit_tail;   // [B*Hkv] with unit_row: first position of the unit's tail
   int pool_rows;              // rows of set_idx when unit_row is given
+  const int32_t* psaw_start;  // [B] or null: positions in [psaw_sink, psaw_start[b]) are masked
+  int psaw_sink;
   int set_cap;
   float scale;
   float* out;

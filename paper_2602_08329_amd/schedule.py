@@ -25,11 +25,29 @@ import torch
 from . import binding as B
 
 
+def psaw_first_visible(layer, n_layers, n, sink, l_s, phi, alpha):
+    """First visible non-sink position of 0-based `layer` at length n under
+    the progressive sliding attention window (Sec. 4.2, Eq. psaw): the
+    1-based boundary P = floor((1 - phi^(alpha (l - l_s) / (N - l_s))) n) for
+    1-based layer l = layer + 1 >= l_s (else 0) masks the 1-based positions
+    strictly between the sink and P, i.e. 0-based [sink, P - 1)."""
+    lb = layer + 1
+    P = 0
+    if lb >= l_s:
+        P = int(math.floor((1.0 - phi ** (alpha * (lb - l_s) / (n_layers - l_s))) * n))
+    return max(min(sink, n), P - 1)
+
+
+def psaw_defaults(n_layers):
+    """Sec. 5.1: pruning from l_s = floor(3 N / 4), phi = 0.7, alpha = 1."""
+    return (3 * n_layers) // 4, 0.7, 1.0
+
+
 class DecodeRunner:
     """Runs the hot path of a synthetic workload (paper_2602_08329_amd.synth)
     whose inputs already live on the GPU."""
 
-    def __init__(self, inp, device="cuda", per_step_sets=False):
+    def __init__(self, inp, device="cuda", per_step_sets=False, psaw=None):
         w = inp.w
         self.per_step_sets = per_step_sets
         self.reuses = w.G > 1 or w.s > 1   # some layer-step attends a shared set
@@ -70,6 +88,21 @@ class DecodeRunner:
         self.ws_dense = B.workspace(B.prhs_workspace_size(B.PRHS_OP_DENSE_ATTN, kv0, self.params), dev)
         self.out = torch.zeros(Bsz, w.hq, w.d, dtype=torch.float32, device=dev)
         self.lse = torch.zeros(Bsz, w.hq, dtype=torch.float32, device=dev)
+        # PSAW (Sec. 4.2): psaw = (l_s, phi, alpha); first visible position per
+        # (layer, step) for the layers that prune, and identity pool rows and
+        # per-unit lengths to attend the schedule's sets through the pool form
+        self.psaw = psaw
+        self.psaw_start = {}
+        if psaw is not None:
+            l_s, phi, alpha = psaw
+            for l in range(self.L):
+                for j in range(T):
+                    st = [psaw_first_visible(l, self.L, n + j + 1, w.sink, l_s, phi, alpha)
+                          for n in w.n_ctx]
+                    if any(x > min(w.sink, n + j + 1) for x, n in zip(st, w.n_ctx)):
+                        self.psaw_start[(l, j)] = torch.tensor(st, dtype=i32, device=dev)
+            self.unit_ids = torch.arange(Bsz * w.hkv, dtype=i32, device=dev)
+            self.unit_lens = self.seq_lens.repeat_interleave(w.hkv, dim=1).contiguous()
 
     # -- pieces -------------------------------------------------------------
     def refresh(self, gi, j):
@@ -118,7 +151,17 @@ class DecodeRunner:
         s, n, tail = self.set_for(l, j)
         out = self.out if out is None else out
         lse = self.lse if lse is None else lse
-        if tail is None:
+        start = self.psaw_start.get((l, j))
+        if start is not None:
+            # the same set through the pool form, under the layer's PSAW mask
+            if tail is None:
+                utail = self.unit_lens[j]
+            else:
+                utail = tail.repeat_interleave(self.w.hkv).contiguous()
+            B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.unit_ids, utail,
+                                    self.scale, out, lse, self.ws_attn, psaw_start=start,
+                                    psaw_sink=self.w.sink)
+        elif tail is None:
             B.prhs_sparse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.scale, out, lse,
                                       self.ws_attn)
         else:
@@ -164,8 +207,8 @@ class GatedDecodeRunner(DecodeRunner):
     queries, retrieval flags and lengths per slot, and the set pool
     [2][s][B][Hkv][set_cap] (kind 0 critical sets, kind 1 shared sets)."""
 
-    def __init__(self, inp, device="cuda", tau=0.8):
-        super().__init__(inp, device)
+    def __init__(self, inp, device="cuda", tau=0.8, psaw=None):
+        super().__init__(inp, device, psaw=psaw)
         w = self.w
         self.tau = float(tau)
         dev, i32 = self.device, torch.int32
@@ -210,7 +253,8 @@ class GatedDecodeRunner(DecodeRunner):
         pool, plen, rows, tail = self.set_for(l, j)
         B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], pool, plen, rows, tail,
                                 self.scale, self.out if out is None else out,
-                                self.lse if lse is None else lse, self.ws_attn)
+                                self.lse if lse is None else lse, self.ws_attn,
+                                psaw_start=self.psaw_start.get((l, j)), psaw_sink=self.w.sink)
 
     def retrieving_units(self):
         """Units of every group that retrieved at the last gated step."""

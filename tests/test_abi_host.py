@@ -237,15 +237,13 @@ def test_select_gated_and_pool_attention_validation(L):
                              cap - 1, 0x6, 0x7, 0x8, n.value, None)
     assert st == B.PRHS_E_CAPACITY
     L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 300, ctypes.byref(n))
-    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, -1, 300, 0x4, 0x5, 0.1, 0x6, None,
-                                 0x7, n.value, None)
-    assert st == B.PRHS_E_INVALID
-    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 8, 300, None, 0x5, 0.1, 0x6, None,
-                                 0x7, n.value, None)
-    assert st == B.PRHS_E_INVALID
-    st = L.prhs_pool_decode_attn(ctypes.byref(kv), 0x1, 0x2, 0x3, 8, 300, 0x4, 0x5, 0.1, 0x6, None,
-                                 0x7, n.value - 1, None)
-    assert st == B.PRHS_E_WORKSPACE
+    pool = lambda rows, urow, sink, wsb: L.prhs_pool_decode_attn(  # noqa: E731
+        ctypes.byref(kv), 0x1, 0x2, 0x3, rows, 300, urow, 0x5, None, sink, 0.1, 0x6, None, 0x7, wsb,
+        None)
+    assert pool(-1, 0x4, 0, n.value) == B.PRHS_E_INVALID
+    assert pool(8, None, 0, n.value) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, -2, n.value) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, 0, n.value - 1) == B.PRHS_E_WORKSPACE
 
 
 def test_dilate_validation_and_empty_batch(L):

@@ -107,14 +107,15 @@ def test_gate_extreme_thresholds():
             assert got[t] == [expect[t - 1]] * U, (tau, t, got[t])
 
 
-def run_gated(w, tau, steps, units_out, layers=None, units_set=None):
+def run_gated(w, tau, steps, units_out, layers=None, units_set=None, psaw=None):
     inp = synth.generate(w, device=DEV, layers=layers)
     L = len(inp.K)
-    run = GatedDecodeRunner(inp, DEV, tau=tau)
+    run = GatedDecodeRunner(inp, DEV, tau=tau, psaw=psaw)
     units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
     units_set = units if units_set is None else units_set
     dec = {u: O.GatedDecodeOracle(w.sink, w.window, w.s, w.G, tau, r=w.r, k=w.k, k_num=w.k_num,
                                   k_den=w.k_den, dilate_m=w.dilate_m) for u in units_set}
+    # with PSAW the sets are compared before the mask and the outputs after it
     out = torch.empty(w.batch, w.hq, w.d, device=DEV)
     lse = torch.empty(w.batch, w.hq, device=DEV)
     cache = {}
@@ -144,6 +145,8 @@ def run_gated(w, tau, steps, units_out, layers=None, units_set=None):
                 base = pool_h[r, : plen_h[r]]
                 got = np.concatenate([base[base < t0], np.arange(t0, n)])
                 assert np.array_equal(got, S), f"l{l} j{j} b{b} g{g}: set differs"
+                if psaw is not None:
+                    S = O.psaw_restrict(S, O.psaw_visible_start(l, L, n, w.sink, *psaw), w.sink, n)
                 if (b, g) in units_out:
                     key = (l, b, g)
                     if key not in cache:
@@ -190,6 +193,13 @@ def test_gated_schedule_config2_full_size():
     w = synth.workload(2)
     run_gated(w, 0.8, range(8), {(0, 0), (3, 7)}, layers=4,
               units_set=[(b, g) for b in range(4) for g in (0, 3, 7)])
+
+
+def test_gated_schedule_config1_cut_cpe():
+    # CPE: the similarity gate with PSAW on the top layers
+    w = synth.workload(1).replace(layers=8, batch=2, n_ctx=(2048, 1500))
+    run_gated(w, 0.8, range(8), {(0, 0), (1, 17)}, psaw=(6, 0.3, 1.0),
+              units_set=[(b, g) for b in range(2) for g in (0, 17)])
 
 
 def test_pool_attention_row_outside_pool_is_empty():

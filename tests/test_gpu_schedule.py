@@ -47,15 +47,19 @@ class UnitCache:
         return self.c[key]
 
 
-def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets=False):
+def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets=False,
+                 psaw=None):
     """Runs the runner and the oracle side by side; compares the sets of
     units_set (default: all units) and the outputs of units_out at every
     (layer, step).  The oracle reads a unit's keys only where the schedule
     refreshes.  A reused set attended with a tail is compared as the stored
-    set followed by the tail positions."""
+    set followed by the tail positions.  With psaw = (l_s, phi, alpha) the
+    outputs are checked against attention over the set under the oracle's
+    PSAW mask, and the runner's first visible positions against the
+    oracle's."""
     inp = synth.generate(w, device=DEV, layers=layers)
     L = len(inp.K)
-    run = DecodeRunner(inp, DEV, per_step_sets=per_step_sets)
+    run = DecodeRunner(inp, DEV, per_step_sets=per_step_sets, psaw=psaw)
     cache = UnitCache(inp)
     all_units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
     units_set = all_units if units_set is None else units_set
@@ -86,6 +90,11 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets
                     got = np.concatenate([got, np.arange(tail[b], n)])
                 assert len(got) == len(S), f"l{l} j{j} b{b} g{g}: |set| {len(got)} != {len(S)}"
                 assert np.array_equal(got, S), f"l{l} j{j} b{b} g{g}: set differs"
+                if psaw is not None:
+                    start = O.psaw_visible_start(l, L, n, w.sink, *psaw)
+                    st = run.psaw_start.get((l, j))
+                    assert (st.cpu().numpy()[b] if st is not None else min(w.sink, n)) == start
+                    S = O.psaw_restrict(S, start, w.sink, n)
                 if (b, g) in units_out:
                     K, V = cache.get(l, b, g)
                     for i in range(w.g):
@@ -97,6 +106,19 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets
                         assert abs(ls[b, h] - lr) <= 1e-4 * max(1, abs(lr))
     print(f"{w.name}: worst relative error {worst:.3e}")
     return worst
+
+
+def test_config1_cut_schedule_psaw():
+    # CPE on the fixed schedule: 8 layers, pruning from l_s = 6 with a
+    # strong window so the masked range holds selected positions
+    w = synth.workload(1).replace(layers=8, batch=2, n_ctx=(2048, 1500))
+    units = {(b, g) for b in range(2) for g in (0, 17, 31)}
+    run_schedule(w, range(8), units, psaw=(6, 0.3, 1.0))
+
+
+def test_config3_cut_schedule_paged_psaw():
+    w = synth.workload(3).replace(layers=4, n_ctx=(20000,), heavy=100)
+    run_schedule(w, range(w.steps), {(0, 0), (0, 5)}, psaw=(3, 0.5, 2.0))
 
 
 def test_config0_full_schedule():
