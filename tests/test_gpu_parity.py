@@ -236,6 +236,10 @@ SELECT_CASES = [
      dict(k=100, sink=4, window=32)),
     ("fused-balanced-d64", "bf16", 64, False, 8, 8,
      tuple(40 + (i * 577) % 3000 for i in range(40)), dict(k=70, sink=2, window=16)),
+    # the largest query group (16 heads per kv head) on both paths
+    ("g16-radix", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
+    ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(128)),
+     dict(k=50, sink=4, window=16)),
 ]
 
 
@@ -535,3 +539,24 @@ def test_split_merge_workspace_reused_across_calls():
                 yr, lr = O.sparse_attention(Qg[i], K, V, sets[(b, g)])
                 assert_close(y[b, g * 4 + i], ls[b, g * 4 + i], yr, lr, TOL["bf16"],
                              f"call {call} b{b} g{g}")
+
+
+def test_empty_batch_is_a_no_op_on_every_entry_point():
+    # batch 0: every call returns OK without touching the device buffers
+    inp = synth.random_inputs(1, 8, 2, 128, (100,), seed=71, device=DEV)
+    kv0 = B.KV(inp.K[0][:0], inp.V[0][:0], torch.zeros(0, dtype=torch.int32, device=DEV),
+               inp.w.capacity, 8)
+    p = B.params(k=8, sink=4, window=8, refresh_every=2)
+    q0 = inp.q[0, 0][:0]
+    z3 = torch.zeros(0, 2, 64, dtype=torch.int32, device=DEV)
+    z2 = torch.zeros(0, 2, dtype=torch.int32, device=DEV)
+    out = torch.zeros(0, 8, 128, device=DEV)
+    lse = torch.zeros(0, 8, device=DEV)
+    ws = B.workspace(1, DEV)
+    B.prhs_select(kv0, q0, p, z3, z2, z3, z2, ws)
+    B.prhs_select_shared(kv0, q0, p, z3, z2, z3, z2, z3.clone(), z2.clone(), ws)
+    B.prhs_sparse_decode_attn(kv0, q0, z3, z2, 0.1, out, lse, ws)
+    B.prhs_reuse_decode_attn(kv0, q0, z3, z2, torch.zeros(0, dtype=torch.int32, device=DEV),
+                             0.1, out, lse, ws)
+    B.prhs_dense_decode_attn(kv0, q0, 0.1, out, lse, ws)
+    torch.cuda.synchronize()
