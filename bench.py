@@ -223,9 +223,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=32)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--config", type=int, default=1, help="workload index 0-4")
-    ap.add_argument("--batch", type=int, default=None, help="workload 4: batch (16 or 64)")
-    ap.add_argument("--nmax", type=int, default=None, help="workload 4: max context")
+    ap.add_argument("--config", type=int, default=1, help="workload index 0-5")
+    ap.add_argument("--batch", type=int, default=None, help="workloads 4, 5: batch")
+    ap.add_argument("--nmax", type=int, default=None, help="workloads 4, 5: max context")
+    ap.add_argument("--block", type=int, default=None, help="workload 5: CIS block size s")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-step-sets", action="store_true",
@@ -260,7 +261,7 @@ def main():
     B.lib()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = synth.workload(args.config, batch=args.batch, nmax=args.nmax)
+    w = synth.workload(args.config, batch=args.batch, nmax=args.nmax, block=args.block)
     T = w.steps
     K_steps, W_steps = args.steps, args.warmup
     log(f"workload {w.name}: generating inputs on the GPU")

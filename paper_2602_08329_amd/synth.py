@@ -83,12 +83,16 @@ def _seq_lengths(seed, batch, nmax):
     return tuple(int(x) for x in rng.integers(lo, nmax - 16 + 1, size=batch))
 
 
-def workload(index, batch=None, nmax=None):
-    """The five paper-shaped workloads.
+def workload(index, batch=None, nmax=None, block=None):
+    """The paper-shaped workloads.
 
     0 tiny fp32 MHA; 1 LLaMA-2-7B-shaped MHA at 4k; 2 Mistral-7B-shaped GQA at
     32k; 3 LLaMA-3-8B-shaped GQA at 128k on a paged cache; 4 GQA throughput
-    sweep with mixed sequence lengths (batch in {16, 64}, nmax in {8k, 16k}).
+    sweep with mixed sequence lengths (batch in {16, 64}, nmax in {8k, 16k});
+    5 the operator benchmark of the efficiency evaluation (Sec. 5.4):
+    LLaMA-2-7B-shaped MHA, batch in {8, 16}, context in {1k, 2k, 4k}, token
+    budget 1/8 of the context with C_sink 16 and C_local 64 (the budget split
+    of Sec. 5.3), CIS blocks of `block` in {8, 16} steps, no layer sharing.
     """
     if index == 0:
         return Workload("tiny-mha-f32-1k", "f32", 1, 1, 4, 4, 64, (1024,), 16,
@@ -112,6 +116,13 @@ def workload(index, batch=None, nmax=None):
                         _seq_lengths(1238 + batch + nmax, batch, nmax), 16,
                         k=0, k_num=1, k_den=20, window=128, sink=4, s=4, G=1, heavy=8,
                         seed=1238)
+    if index == 5:
+        batch = 16 if batch is None else batch
+        nmax = 2048 if nmax is None else nmax
+        block = 16 if block is None else block
+        return Workload(f"paper-op-b{batch}-n{nmax}-s{block}", "bf16", 32, batch, 32, 32, 128,
+                        (nmax,) * batch, 16, k=max(0, nmax // 8 - 80), window=64, sink=16,
+                        s=block, G=1, heavy=8, layer_corr=0.8, seed=1239 + batch + nmax + block)
     raise ValueError(f"no workload {index}")
 
 

@@ -121,6 +121,14 @@ def test_config3_cut_schedule_paged_psaw():
     run_schedule(w, range(w.steps), {(0, 0), (0, 5)}, psaw=(3, 0.5, 2.0))
 
 
+def test_paper_operator_shape_cut_schedule():
+    # the efficiency evaluation's shape (Sec. 5.4): MHA, budget 1/8, sink 16,
+    # window 64, blocks of 8 steps
+    w = synth.workload(5, batch=2, nmax=2048, block=8).replace(layers=2)
+    run_schedule(w, range(w.steps), {(0, 0), (1, 31)},
+                 units_set=[(b, g) for b in range(2) for g in (0, 9, 31)])
+
+
 def test_config0_full_schedule():
     w = synth.workload(0)
     units = {(0, g) for g in range(w.hkv)}
