@@ -27,9 +27,10 @@
 //   O^T (d x 16 heads)      += V_tile^T . P^T, P split into bf16 hi + lo parts so
 //                              the probabilities keep ~16 significant bits.
 // The key order inside a tile and the dimension order inside a row are
-// permuted identically on both operands of each product, so every lane loads
-// contiguous bytes: K rows as d/2-byte runs of one key, V rows as full
-// 256-byte rows across 16 lanes (coalesced), and no LDS transpose is needed.
+// permuted identically on both operands of each product, so loads need no LDS
+// transpose: the 4 lanes holding one key read one contiguous 64-byte piece of
+// its row per load (product kk takes dims 32kk + 8grp .. 32kk + 8grp + 7 in
+// lane group grp), and V rows are read whole across 16 lanes.
 // fp32 inputs take a vector-ALU path (16 lanes per row, one query head per
 // workgroup).
 #include <stdlib.h>
@@ -67,14 +68,13 @@ struct AttnArgs {
 };
 
 // The rows a unit attends, in order: the first `base` come from its index
-// set `idx` (entries at or beyond t0 are skipped), then the tail positions
+// set (entries at or beyond t0 are skipped), then the tail positions
 // [t0, t0 + L - base).  Dense: rows are the positions [0, n_b).  Without a
 // tail t0 = n_b.  L never exceeds set_cap, the bound the split geometry uses.
 // The set is row u of set_idx, or with a pool the row unit_row[u] (a row
 // outside the pool gives an empty set) and the tail from unit_tail[u].
 struct UnitSpan {
   int L, base, t0;
-  const int32_t* idx;
   int mask_lo, mask_hi;  // rows at positions in [mask_lo, mask_hi) are skipped (PSAW)
 };
 
@@ -82,7 +82,6 @@ template <bool DENSE>
 __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, int nb) {
   UnitSpan sp;
   sp.t0 = nb;
-  sp.idx = nullptr;
   sp.mask_lo = sp.mask_hi = 0;
   if (DENSE) {
     sp.L = sp.base = nb;
@@ -100,14 +99,12 @@ __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, i
     tail = true;
     if (row < 0 || row >= a.pool_rows) {
       sp.L = sp.base = 0;
-      sp.idx = a.set_idx;
       return sp;
     }
   } else if (a.tail_start) {
     t0 = a.tail_start[b];
     tail = true;
   }
-  sp.idx = a.set_idx + (size_t)row * a.set_cap;
   int L = a.set_len[row];
   L = L < 0 ? 0 : (L > a.set_cap ? a.set_cap : L);
   sp.base = L;
@@ -137,13 +134,38 @@ __device__ __forceinline__ int32_t phys_row(const KvView& kv, int b, int g, int 
   return (phys * kv.hkv + g) * kv.page_size + (pos - page * kv.page_size);
 }
 
-// Resolves list entries [start, start + n) of the unit to row ids in s_row.
-// All index loads of a thread are issued before any is used, then all table
-// loads: two memory latencies for the whole chunk.  n <= blockDim * 8.
+// Loads the set entries [start, start + chunk) of unit u before the unit's
+// length is known, so that these loads share one memory latency with the
+// length loads.  Entries at or past the length are loaded and never used; a
+// set row holds set_cap entries, so every load stays inside it.
+template <bool DENSE>
+__device__ __forceinline__ void prefetch_entries(const AttnArgs& a, int u, int start,
+                                                 int32_t (&raw)[kRowsPerThread]) {
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) raw[k] = -1;
+  if (DENSE) return;
+  int row = u;
+  bool ok = true;
+  if (a.unit_row) {
+    row = a.unit_row[u];
+    ok = row >= 0 && row < a.pool_rows;
+  }
+  const int32_t* idx = a.set_idx + (size_t)(ok ? row : 0) * a.set_cap;
+  const int lim = min(start + a.chunk, a.set_cap);
+#pragma unroll
+  for (int k = 0; k < kRowsPerThread; ++k) {
+    const int t = start + (int)threadIdx.x + k * (int)blockDim.x;
+    if (ok && t < lim) raw[k] = idx[t];
+  }
+}
+
+// Resolves list entries [start, start + n) of the unit to row ids in s_row,
+// from the entries prefetch_entries loaded; for a paged cache all block-table
+// loads of a thread are issued before any is used.  n <= blockDim * 8.
 template <bool DENSE, bool PAGED>
-__device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t* idx, int start, int n,
-                                           const UnitSpan& sp, int nb, int b, int g,
-                                           int32_t* s_row) {
+__device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t (&raw)[kRowsPerThread],
+                                           int start, int n, const UnitSpan& sp, int nb, int b,
+                                           int g, int32_t* s_row) {
   int pos[kRowsPerThread];
 #pragma unroll
   for (int k = 0; k < kRowsPerThread; ++k) {
@@ -156,7 +178,7 @@ __device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t* idx
       } else {
         int p;
         if (t < sp.base) {
-          p = idx[t];
+          p = raw[k];
           p = p < sp.t0 ? p : -1;
         } else {
           p = sp.t0 + (t - sp.base);
@@ -193,11 +215,11 @@ template <int DB>
 __device__ __forceinline__ VRow<DB> load_vrow(const __bf16* p) {
   VRow<DB> v;
   if constexpr (DB == 8) {
-    const uint4 x = *(const uint4*)p;
-    v.w[0] = x.x; v.w[1] = x.y; v.w[2] = x.z; v.w[3] = x.w;
+    const u32x4_t x = stream_load16(p);
+    v.w[0] = x[0]; v.w[1] = x[1]; v.w[2] = x[2]; v.w[3] = x[3];
   } else {
-    const uint2 x = *(const uint2*)p;
-    v.w[0] = x.x; v.w[1] = x.y;
+    const u32x2_t x = stream_load8(p);
+    v.w[0] = x[0]; v.w[1] = x[1];
   }
   return v;
 }
@@ -230,9 +252,9 @@ __device__ __forceinline__ void load_tile(Tile<D>& T, const int32_t* s_row, int 
   for (int s = 0; s < 2; ++s) {
     const int rk = r0 + 16 * s + col;
     const int row = rk < n ? s_row[rk] : -1;
-    const uint4* kp = (const uint4*)(kb + (int64_t)(row < 0 ? 0 : row) * D + grp * (D / 4));
+    const uint4* kp = (const uint4*)(kb + (int64_t)(row < 0 ? 0 : row) * D + grp * 8);
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) T.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[kk]);
+    for (int kk = 0; kk < KS; ++kk) T.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[4 * kk]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int rv = r0 + 16 * s + grp * 4 + j;
@@ -337,10 +359,25 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   const int split = blockIdx.x, u = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = u / hkv, g = u % hkv;
+  const int start = split * a.chunk;
+  const int nwaves = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  // set entries, query and lengths load together
+  int32_t raw[kRowsPerThread];
+  prefetch_entries<DENSE>(a, u, start, raw);
+  const __bf16* qb = (const __bf16*)a.q;
+  bf16x8_t qf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) {
+    const int qh = col < G ? col : 0;
+    const uint4* qp = (const uint4*)(qb + ((size_t)b * hq + g * G + qh) * D + grp * 8);
+    const uint4 v = qp[4 * kk];
+    qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
+  }
   const int nb = kv_seq_len(a.kv, b);
   const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
   const int L = sp.L;
-  const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
     for (int e = threadIdx.x; e < G * D; e += blockDim.x)
       write_final(a, (size_t)b * hq + g * G + e / D, D, e % D, -INFINITY, 0.f, 0.f);
@@ -348,20 +385,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   }
   if (start >= L) return;
   const int n = min(L, start + a.chunk) - start;
-  const int nwaves = blockDim.x >> 6;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int col = lane & 15, grp = lane >> 4;
-
-  const __bf16* qb = (const __bf16*)a.q;
-  bf16x8_t qf[KS];
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
-    const int qh = col < G ? col : 0;
-    const uint4* qp = (const uint4*)(qb + ((size_t)b * hq + g * G + qh) * D + grp * (D / 4));
-    const uint4 v = qp[kk];
-    qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
-  }
-  stage_rows<DENSE, PAGED>(a, sp.idx, start, n, sp, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, raw, start, n, sp, nb, b, g, s_row);
 
   const __bf16* kb = (const __bf16*)a.kv.k;
   const __bf16* vb = (const __bf16*)a.kv.v;
@@ -448,10 +472,12 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   const int split = blockIdx.x, bh = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, g = h / G, u = b * hkv + g;
+  const int start = split * a.chunk;
+  int32_t raw[kRowsPerThread];
+  prefetch_entries<DENSE>(a, u, start, raw);
   const int nb = kv_seq_len(a.kv, b);
   const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
   const int L = sp.L;
-  const int start = split * a.chunk;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
     for (int dim = threadIdx.x; dim < D; dim += blockDim.x)
       write_final(a, bh, D, dim, -INFINITY, 0.f, 0.f);
@@ -466,7 +492,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   float qv[DPL];
 #pragma unroll
   for (int i = 0; i < DPL; ++i) qv[i] = qp[i];
-  stage_rows<DENSE, PAGED>(a, sp.idx, start, n, sp, nb, b, g, s_row);
+  stage_rows<DENSE, PAGED>(a, raw, start, n, sp, nb, b, g, s_row);
   const float* kb = (const float*)a.kv.k;
   const float* vb = (const float*)a.kv.v;
   float m_run = -INFINITY, l_run = 0.f, o[DPL];

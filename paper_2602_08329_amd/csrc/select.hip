@@ -161,8 +161,10 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
 
 // bf16 scoring on MFMA: per 16 keys, S[key][head] = K_tile(16 x d) . Q^T(d x 16)
 // with the group's g <= 16 query heads in the columns (unused columns zero).
-// Lane l loads d/2 contiguous bytes of key l%16; the contraction runs over a
-// permutation of d shared by both operands.  Products of bf16 values are exact
+// Lane l holds d/4 dims of key l%16; each load instruction reads one
+// contiguous 64-byte piece of every key of the tile (product kk takes dims
+// 32kk + 8(l/16) .. +7), and the contraction runs over this permutation of d,
+// shared by both operands.  Products of bf16 values are exact
 // in fp32 and the accumulation is fp32.  Each wave handles 64 keys per step
 // and prefetches its next step's 16 loads while multiplying the current one.
 template <int D, int SUB = 4>
@@ -190,9 +192,9 @@ __device__ __forceinline__ void score_load(ScoreStep<D, SUB>& S, const SelArgs& 
 #pragma unroll
   for (int s = 0; s < SUB; ++s) {
     const int32_t row = score_row<D, PAGED>(a, rg, b, g, t + s * 16 + col, end, p0, s_page);
-    const uint4* kp = (const uint4*)(kbase + (int64_t)(row < 0 ? 0 : row) * D + grp * (D / 4));
+    const uint4* kp = (const uint4*)(kbase + (int64_t)(row < 0 ? 0 : row) * D + grp * 8);
 #pragma unroll
-    for (int kk = 0; kk < D / 32; ++kk) S.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[kk]);
+    for (int kk = 0; kk < D / 32; ++kk) S.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[4 * kk]);
   }
 }
 
@@ -263,8 +265,8 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) {
     const int qh = col < G ? col : 0;
-    const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * (D / 4));
-    const uint4 v = qp[kk];
+    const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * 8);
+    const uint4 v = qp[4 * kk];
     qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
   int gp = 1;
@@ -849,8 +851,8 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int qh = col < G ? col : 0;
-      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * (D / 4));
-      const uint4 v = qp[kk];
+      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * 8);
+      const uint4 v = qp[4 * kk];
       qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
     }
     int gp = 1;
