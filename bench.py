@@ -237,6 +237,8 @@ def main():
     ap.add_argument("--gate", type=float, default=None, metavar="TAU",
                     help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
                          "fixed refresh period (blocks of refresh_every steps)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches instead of replays of a captured HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -294,6 +296,11 @@ def main():
     torch.cuda.synchronize()
 
     def timed(fn, label, order=None):
+        """Warm-up steps, then the K timed steps: by default the launches of
+        the K steps are captured once into a HIP graph, replayed once
+        untimed and once timed, so the region holds the same kernels
+        back to back without host launch overhead; with --eager they are
+        launched one by one from Python."""
         order = order or (lambda i: i % T)
         for i in range(W_steps):
             fn(order(i))
@@ -301,16 +308,27 @@ def main():
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
         js = [order(W_steps + i) for i in range(K_steps)]
+        graph = None
+        if not args.eager:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for j in js:
+                    fn(j)
+            graph.replay()
         torch.cuda.synchronize()
         ev0.record()
         t = time.perf_counter()
-        for j in js:
-            fn(j)
+        if graph is not None:
+            graph.replay()
+        else:
+            for j in js:
+                fn(j)
         ev1.record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t
         ms = ev0.elapsed_time(ev1)
         log(f"{label}: {ms / K_steps:.3f} ms/step (wall {wall * 1e3 / K_steps:.3f} ms/step)")
+        del graph
         return ms, js
 
     log(f"timing {K_steps} sparse decode steps after {W_steps} warm-up steps")
@@ -374,6 +392,7 @@ def main():
             "shared_sets": ("similarity gate" if gated else
                             "per step" if args.per_step_sets else "per refresh + decoded tail"),
             "psaw": ({"l_s": psaw[0], "phi": psaw[1], "alpha": psaw[2]} if psaw else None),
+            "launch": "eager" if args.eager else "hip-graph replay",
         },
         "effective_gbps": round(eff_gbps, 1),
         "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),

@@ -15,9 +15,9 @@
 // L2 slice per workgroup.
 //
 // Latency: the workgroup first resolves every list entry of its chunk to a
-// physical row id (index load, and block-table load for paged caches, each
-// issued for the whole chunk at once) and stages the ids in LDS.  Waves then
-// walk 32-row tiles with two register buffers: the 16 K/V loads of the next
+// physical row id (the set entries load together with the unit's lengths,
+// then block-table loads for paged caches) and stages the ids in LDS.  Waves
+// then walk 32-row tiles with two register buffers: the K/V loads of the next
 // tile are in flight while the current tile is multiplied.  Loads are issued
 // unconditionally (a missing row reads row 0) and invalid rows are masked
 // afterwards, so no load waits on a branch.
@@ -26,11 +26,14 @@
 //   S^T (32 keys x 16 heads) = K_tile . Q^T  (v_mfma_f32_16x16x32_bf16, two 16-row halves)
 //   O^T (d x 16 heads)      += V_tile^T . P^T, P split into bf16 hi + lo parts so
 //                              the probabilities keep ~16 significant bits.
-// The key order inside a tile and the dimension order inside a row are
-// permuted identically on both operands of each product, so loads need no LDS
-// transpose: the 4 lanes holding one key read one contiguous 64-byte piece of
-// its row per load (product kk takes dims 32kk + 8grp .. 32kk + 8grp + 7 in
-// lane group grp), and V rows are read whole across 16 lanes.
+// Every K and V load reads whole rows (d/8 lanes of 16 bytes per row), the
+// pattern that sustains full bandwidth per CU; the MFMA operand order of K
+// (4 lanes per key) would read 64-byte pieces of 16 rows per load, which
+// this chip serves at well under half that rate.  K therefore goes through
+// a per-wave LDS tile (XOR-swizzled, conflict-free both ways) into operand
+// order; the dimension order inside a row is permuted identically on K and
+// Q.  V needs no transpose: a lane's 8 rows x 8 dims block feeds the second
+// product directly.  K and V bytes are read once, with the streaming policy.
 // fp32 inputs take a vector-ALU path (16 lanes per row, one query head per
 // workgroup).
 #include <stdlib.h>
@@ -230,37 +233,70 @@ __device__ __forceinline__ uint32_t vrow_elem(const VRow<DB>& v, int e) {
   return (e & 1) ? (w >> 16) : (w & 0xFFFFu);
 }
 
-// Registers of one wave's 32-row tile: K operand rows (16s + col), V rows
-// (16s + 4 grp + j) and the validity of the V rows, which are also the rows
-// of the lane's logits.
+// Registers of one wave's 32-row tile: K rows as loaded (whole rows, D/8
+// lanes of 16 bytes per row, so every load reads whole 128-byte lines), V
+// rows (16s + 4 grp + j) and the validity of the V rows, which are also the
+// rows of the lane's logits.
 template <int D>
 struct Tile {
-  static constexpr int KS = D / 32;
+  static constexpr int KS = D / 32;  // products per 16-row half = K loads per half
   static constexpr int DB = D / 16;
-  bf16x8_t kf[2][KS];
+  u32x4_t kraw[2][KS];
   VRow<DB> vf[2][4];
   uint32_t ok;
 };
 
+// K staging in LDS: a wave's 32 x D tile, row-major in 16-byte chunks, chunk
+// c of tile row r at slot c ^ (r mod D/8), so that both the row-wise writes
+// and the MFMA-order reads (16 rows, one chunk each) hit distinct banks.
+template <int D>
+__device__ __forceinline__ int kst_slot(int r, int c) {
+  constexpr int CH = D / 8;
+  return r * CH + (c ^ (r & (CH - 1)));
+}
+
+// LDS bytes per wave: its K staging tile, reused at the end for its G output
+// rows of D + 1 floats.
+__host__ __device__ constexpr int attn_wave_bytes(int D, int G) {
+  return ((32 * D * 2 > G * (D + 1) * 4 ? 32 * D * 2 : G * (D + 1) * 4) + 15) & ~15;
+}
+
 template <int D>
 __device__ __forceinline__ void load_tile(Tile<D>& T, const int32_t* s_row, int r0, int n,
-                                          const __bf16* kb, const __bf16* vb, int col, int grp) {
+                                          const __bf16* kb, const __bf16* vb, int lane) {
   constexpr int KS = D / 32;
   constexpr int DB = D / 16;
+  constexpr int CH = D / 8, RPI = 64 / CH;  // chunks per row, rows per K load
+  const int col = lane & 15, grp = lane >> 4;
+  const int kc = lane % CH, kr = lane / CH;
+  // all row ids of the tile first (unconditional LDS reads: s_row spans whole
+  // tiles), then every load, so that no load waits on a single LDS read
+  int rk[2][KS], rv[2][4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int r = r0 + 16 * s + j * RPI + kr;
+      const int x = s_row[r];
+      rk[s][j] = r < n ? x : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + 16 * s + grp * 4 + j;
+      const int x = s_row[r];
+      rv[s][j] = r < n ? x : -1;
+    }
+  }
   T.ok = 0u;
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
-    const int rk = r0 + 16 * s + col;
-    const int row = rk < n ? s_row[rk] : -1;
-    const uint4* kp = (const uint4*)(kb + (int64_t)(row < 0 ? 0 : row) * D + grp * 8);
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) T.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[4 * kk]);
+    for (int j = 0; j < KS; ++j)
+      T.kraw[s][j] = stream_load16(kb + (int64_t)(rk[s][j] < 0 ? 0 : rk[s][j]) * D + kc * 8);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int rv = r0 + 16 * s + grp * 4 + j;
-      const int vrow = rv < n ? s_row[rv] : -1;
-      T.vf[s][j] = load_vrow<DB>(vb + (int64_t)(vrow < 0 ? 0 : vrow) * D + col * DB);
-      if (vrow >= 0) T.ok |= 1u << (s * 4 + j);
+      T.vf[s][j] = load_vrow<DB>(vb + (int64_t)(rv[s][j] < 0 ? 0 : rv[s][j]) * D + col * DB);
+      if (rv[s][j] >= 0) T.ok |= 1u << (s * 4 + j);
     }
   }
 }
@@ -275,9 +311,27 @@ struct WaveState {
 
 template <int D>
 __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const bf16x8_t* qf,
-                                             float scale_log2) {
+                                             float scale_log2, u32x4_t* kst, int lane) {
   constexpr int KS = D / 32;
   constexpr int DB = D / 16;
+  constexpr int CH = D / 8, RPI = 64 / CH;
+  const int col = lane & 15, grp = lane >> 4;
+  // K rows to MFMA operand order through the wave's LDS tile: lane (col,
+  // grp) takes dims 32kk + 8grp .. +7 of tile row 16s + col for product kk.
+  // LDS operations of one wave complete in order; the wave barriers keep
+  // the compiler from moving them across each other.
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int j = 0; j < KS; ++j) kst[kst_slot<D>(16 * s + j * RPI + lane / CH, lane % CH)] = T.kraw[s][j];
+  __builtin_amdgcn_wave_barrier();
+  bf16x8_t kf[2][KS];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      kf[s][kk] = __builtin_bit_cast(bf16x8_t, kst[kst_slot<D>(16 * s + col, 4 * kk + grp)]);
+  __builtin_amdgcn_wave_barrier();
   float x[2][4];
   float mt = -INFINITY;
 #pragma unroll
@@ -285,7 +339,7 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(T.kf[s][kk], qf[kk], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s][kk], qf[kk], acc, 0, 0, 0);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool ok = (T.ok >> (s * 4 + e)) & 1u;
@@ -352,12 +406,15 @@ template <int D, bool DENSE, bool PAGED>
 __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   constexpr int KS = D / 32;
   constexpr int DB = D / 16;
-  extern __shared__ float dyn[];  // [nwaves][G][D + 1] wave outputs
+  // dynamic LDS: [nwaves][attn_wave_bytes] wave regions (K staging, then the
+  // wave's outputs), then the staged row ids [blockDim * kRowsPerThread]
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
   __shared__ float sm_m[8][16];
   __shared__ float sm_l[8][16];
-  __shared__ int32_t s_row[512 * kRowsPerThread];
   const int split = blockIdx.x, u = blockIdx.y;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
+  const int wbytes = attn_wave_bytes(D, G);
+  int32_t* s_row = (int32_t*)(dyn + (size_t)(blockDim.x >> 6) * wbytes);
   const int b = u / hkv, g = u % hkv;
   const int start = split * a.chunk;
   const int nwaves = blockDim.x >> 6;
@@ -402,23 +459,24 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
   const int iters = wave < ntiles ? (ntiles - wave + nwaves - 1) / nwaves : 0;
   if (iters > 0) {
     Tile<D> A, B;
+    u32x4_t* kst = (u32x4_t*)(dyn + (size_t)wave * wbytes);
     const int step = 32 * nwaves;
     int r0 = wave * 32;
-    load_tile<D>(A, s_row, r0, n, kb, vb, col, grp);
+    load_tile<D>(A, s_row, r0, n, kb, vb, lane);
     int i = 0;
     for (; i + 2 < iters; i += 2) {
-      load_tile<D>(B, s_row, r0 + step, n, kb, vb, col, grp);
-      consume_tile<D>(A, st, qf, a.scale_log2);
-      load_tile<D>(A, s_row, r0 + 2 * step, n, kb, vb, col, grp);
-      consume_tile<D>(B, st, qf, a.scale_log2);
+      load_tile<D>(B, s_row, r0 + step, n, kb, vb, lane);
+      consume_tile<D>(A, st, qf, a.scale_log2, kst, lane);
+      load_tile<D>(A, s_row, r0 + 2 * step, n, kb, vb, lane);
+      consume_tile<D>(B, st, qf, a.scale_log2, kst, lane);
       r0 += 2 * step;
     }
     if (i + 1 < iters) {
-      load_tile<D>(B, s_row, r0 + step, n, kb, vb, col, grp);
-      consume_tile<D>(A, st, qf, a.scale_log2);
-      consume_tile<D>(B, st, qf, a.scale_log2);
+      load_tile<D>(B, s_row, r0 + step, n, kb, vb, lane);
+      consume_tile<D>(A, st, qf, a.scale_log2, kst, lane);
+      consume_tile<D>(B, st, qf, a.scale_log2, kst, lane);
     } else {
-      consume_tile<D>(A, st, qf, a.scale_log2);
+      consume_tile<D>(A, st, qf, a.scale_log2, kst, lane);
     }
   }
 
@@ -429,7 +487,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     sm_l[wave][col] = st.l;
   }
   if (col < G) {
-    float* wo = dyn + ((size_t)wave * G + col) * (D + 1);
+    float* wo = (float*)(dyn + (size_t)wave * wbytes) + col * (D + 1);
 #pragma unroll
     for (int blk = 0; blk < DB; ++blk)
 #pragma unroll
@@ -445,7 +503,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     if (M != -INFINITY) {
       for (int w = 0; w < nwaves; ++w) {
         const float f = exp2f(sm_m[w][h] - M);
-        num += f * dyn[((size_t)w * G + h) * (D + 1) + dim];
+        num += f * ((const float*)(dyn + (size_t)w * wbytes))[h * (D + 1) + dim];
         den += f * sm_l[w][h];
       }
     }
@@ -672,7 +730,8 @@ template <int D, bool DENSE, bool PAGED>
 hipError_t launch_typed(const AttnArgs& a, int dtype, int units, int waves, hipStream_t stream) {
   if (dtype == 1) {
     const int G = a.kv.hq / a.kv.hkv;
-    const size_t dyn = (size_t)waves * G * (D + 1) * sizeof(float);
+    const size_t dyn = (size_t)waves * attn_wave_bytes(D, G) +
+                       (size_t)64 * waves * kRowsPerThread * sizeof(int32_t);
     if (dyn > 65536) {
       const hipError_t e = hipFuncSetAttribute((const void*)attn_split_bf16<D, DENSE, PAGED>,
                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);

@@ -161,17 +161,28 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
 
 // bf16 scoring on MFMA: per 16 keys, S[key][head] = K_tile(16 x d) . Q^T(d x 16)
 // with the group's g <= 16 query heads in the columns (unused columns zero).
-// Lane l holds d/4 dims of key l%16; each load instruction reads one
-// contiguous 64-byte piece of every key of the tile (product kk takes dims
-// 32kk + 8(l/16) .. +7), and the contraction runs over this permutation of d,
-// shared by both operands.  Products of bf16 values are exact
-// in fp32 and the accumulation is fp32.  Each wave handles 64 keys per step
-// and prefetches its next step's 16 loads while multiplying the current one.
+// Keys are loaded whole, d/8 lanes of 16 bytes per key (the operand order,
+// 4 lanes per key, would read 64-byte pieces of 16 keys per load, which this
+// chip serves at well under half the rate), with the streaming cache policy,
+// and reach operand order through a per-wave LDS tile of 16 keys: lane l
+// takes dims 32kk + 8(l/16) .. +7 of key l%16 for product kk, the same
+// permutation of d as the query operand.  Products of bf16 values are exact
+// in fp32 and the accumulation is fp32.  Each wave handles 16 SUB keys per
+// step and prefetches its next step's loads while multiplying the current
+// one.
 template <int D, int SUB = 4>
 struct ScoreStep {
   static constexpr int kSub = SUB;  // 16-key sub-tiles per step
-  bf16x8_t kf[SUB][D / 32];
+  u32x4_t kraw[SUB][D / 32];        // sub-tile s, load j: key 16s + j (64 / (d/8)) + l / (d/8)
 };
+
+// Slot of 16-byte chunk c of key r (< 16) in a wave's LDS tile, XOR-swizzled
+// so that the whole-key writes and the operand-order reads hit distinct banks.
+template <int D>
+__device__ __forceinline__ int score_slot(int r, int c) {
+  constexpr int CH = D / 8;
+  return r * CH + (c ^ (r & (CH - 1)));
+}
 
 template <int D, bool PAGED>
 __device__ __forceinline__ int32_t score_row(const SelArgs& a, const RowGeom& rg, int b, int g,
@@ -187,27 +198,43 @@ __device__ __forceinline__ int32_t score_row(const SelArgs& a, const RowGeom& rg
 template <int D, bool PAGED, int SUB>
 __device__ __forceinline__ void score_load(ScoreStep<D, SUB>& S, const SelArgs& a, const RowGeom& rg,
                                            int b, int g, int t, int end, int p0,
-                                           const int32_t* s_page, int col, int grp) {
+                                           const int32_t* s_page, int lane) {
+  constexpr int CH = D / 8, RPI = 64 / CH;  // chunks per key, keys per load
   const __bf16* kbase = (const __bf16*)a.kv.k;
+  const int kc = lane % CH, kr = lane / CH;
 #pragma unroll
-  for (int s = 0; s < SUB; ++s) {
-    const int32_t row = score_row<D, PAGED>(a, rg, b, g, t + s * 16 + col, end, p0, s_page);
-    const uint4* kp = (const uint4*)(kbase + (int64_t)(row < 0 ? 0 : row) * D + grp * 8);
+  for (int s = 0; s < SUB; ++s)
 #pragma unroll
-    for (int kk = 0; kk < D / 32; ++kk) S.kf[s][kk] = __builtin_bit_cast(bf16x8_t, kp[4 * kk]);
-  }
+    for (int j = 0; j < D / 32; ++j) {
+      const int32_t row =
+          score_row<D, PAGED>(a, rg, b, g, t + s * 16 + j * RPI + kr, end, p0, s_page);
+      S.kraw[s][j] = stream_load16(kbase + (int64_t)(row < 0 ? 0 : row) * D + kc * 8);
+    }
 }
 
+// kst: the wave's LDS tile of 16 x d bf16.  LDS operations of one wave
+// complete in order; the wave barriers keep the compiler from moving them
+// across each other.
 template <int D, int SUB>
 __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const bf16x8_t* qf, int G,
-                                              int gp, int t, int end, int col, int grp,
-                                              uint32_t* keys, uint32_t* hist) {
+                                              int gp, int t, int end, int lane, uint32_t* keys,
+                                              uint32_t* hist, u32x4_t* kst) {
+  constexpr int CH = D / 8, RPI = 64 / CH;
+  const int col = lane & 15, grp = lane >> 4;
 #pragma unroll
   for (int s = 0; s < SUB; ++s) {
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) kst[score_slot<D>(j * RPI + lane / CH, lane % CH)] = S.kraw[s][j];
+    __builtin_amdgcn_wave_barrier();
+    bf16x8_t kf[D / 32];
+#pragma unroll
+    for (int kk = 0; kk < D / 32; ++kk)
+      kf[kk] = __builtin_bit_cast(bf16x8_t, kst[score_slot<D>(col, 4 * kk + grp)]);
+    __builtin_amdgcn_wave_barrier();
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < D / 32; ++kk)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(S.kf[s][kk], qf[kk], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kk], qf[kk], acc, 0, 0, 0);
     float v[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = col < G ? acc[e] : -INFINITY;
@@ -234,6 +261,7 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
   constexpr int KS = D / 32;
   __shared__ uint32_t hist[kHistBins];
   __shared__ int32_t s_page[kScoreChunk + 1];
+  __shared__ u32x4_t s_kst[kScoreBlock / 64][16 * (D / 8)];
   const int row = blockIdx.y;
   if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
@@ -278,21 +306,21 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
   if (iters > 0) {
     ScoreStep<D> A, B;
     int t = t0;
-    score_load<D, PAGED>(A, a, rg, b, g, t, end, p0, s_page, col, grp);
+    score_load<D, PAGED>(A, a, rg, b, g, t, end, p0, s_page, lane);
     int i = 0;
     for (; i + 2 < iters; i += 2) {
-      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, col, grp);
-      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
-      score_load<D, PAGED>(A, a, rg, b, g, t + 512, end, p0, s_page, col, grp);
-      score_consume<D>(B, qf, G, gp, t + 256, end, col, grp, keys, hist);
+      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, lane);
+      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
+      score_load<D, PAGED>(A, a, rg, b, g, t + 512, end, p0, s_page, lane);
+      score_consume<D>(B, qf, G, gp, t + 256, end, lane, keys, hist, s_kst[wave]);
       t += 512;
     }
     if (i + 1 < iters) {
-      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, col, grp);
-      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
-      score_consume<D>(B, qf, G, gp, t + 256, end, col, grp, keys, hist);
+      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, lane);
+      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D>(B, qf, G, gp, t + 256, end, lane, keys, hist, s_kst[wave]);
     } else {
-      score_consume<D>(A, qf, G, gp, t, end, col, grp, keys, hist);
+      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
     }
   }
   __syncthreads();
@@ -834,6 +862,7 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   __shared__ uint32_t s_krem, s_cnt;
   __shared__ int s_len[kBalanceMaxBatch];
   __shared__ int s_row;
+  __shared__ u32x4_t s_kst[BLOCK / 64][16 * (D / 8)];
   const int row = fused_row(a, blockIdx.x, s_len, &s_row);
   if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
@@ -863,21 +892,21 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
     if (iters > 0) {
       ScoreStep<D, 2> A, B;
       int t = t0;
-      score_load<D, false>(A, a, rg, b, g, t, M, 0, nullptr, col, grp);
+      score_load<D, false>(A, a, rg, b, g, t, M, 0, nullptr, lane);
       int i = 0;
       for (; i + 2 < iters; i += 2) {
-        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, col, grp);
-        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
-        score_load<D, false>(A, a, rg, b, g, t + 2 * kStride, M, 0, nullptr, col, grp);
-        score_consume<D>(B, qf, G, gp, t + kStride, M, col, grp, s_keys, h);
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
+        score_load<D, false>(A, a, rg, b, g, t + 2 * kStride, M, 0, nullptr, lane);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
         t += 2 * kStride;
       }
       if (i + 1 < iters) {
-        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, col, grp);
-        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
-        score_consume<D>(B, qf, G, gp, t + kStride, M, col, grp, s_keys, h);
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
       } else {
-        score_consume<D>(A, qf, G, gp, t, M, col, grp, s_keys, h);
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
       }
     }
   }
@@ -985,6 +1014,7 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
+constexpr int kLdsBytes = 160 * 1024;  // LDS of one CU
 static_assert(kFusedMaxKeys <= 32 * kHistBins, "the shared-set bitmap reuses the histogram");
 constexpr int kFusedMinRows = 128;    // enough rows to occupy the chip one per CU
 
@@ -1089,10 +1119,19 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {
     const size_t dyn = (size_t)a.mcap * 4;
     a.balance_cus = balance_cus();
-    // one 1024-thread workgroup per CU while the rows fit the CUs; beyond,
-    // 512-thread workgroups so that two share a CU and one's selection
-    // overlaps the other's scoring
-    const bool wide = a.balance_cus <= 0 || rows <= a.balance_cus;
+    // one 1024-thread workgroup per CU while the rows fit the CUs and its
+    // LDS (static part plus the key array) fits the CU's 160 KB; otherwise
+    // 512-thread workgroups, two to a CU where they fit, so that one's
+    // selection overlaps the other's scoring
+    bool wide = a.balance_cus <= 0 || rows <= a.balance_cus;
+    if (wide) {
+      hipFuncAttributes fa;
+      const hipError_t ea =
+          s.kv.d == 128 ? hipFuncGetAttributes(&fa, (const void*)select_fused<128, 1024>)
+                        : hipFuncGetAttributes(&fa, (const void*)select_fused<64, 1024>);
+      if (ea != hipSuccess) return ea;
+      wide = fa.sharedSizeBytes + dyn <= (size_t)kLdsBytes;
+    }
     hipError_t e = hipSuccess;
 #define PRHS_FUSED_LAUNCH(DV, BL)                                                           \
   {                                                                                         \

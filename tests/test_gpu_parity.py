@@ -236,6 +236,12 @@ SELECT_CASES = [
      dict(k=100, sink=4, window=32)),
     ("fused-balanced-d64", "bf16", 64, False, 8, 8,
      tuple(40 + (i * 577) % 3000 for i in range(40)), dict(k=70, sink=2, window=16)),
+    # long middle ranges on 128 rows: up to ~21k keys the key array fits LDS
+    # beside the 1024-thread workgroup's staging; beyond, 512 threads
+    ("fused-wide-21k", "bf16", 128, False, 32, 8, (21000, 16000) * 8,
+     dict(k=1000, sink=4, window=128)),
+    ("fused-narrow-24k", "bf16", 128, False, 32, 8, (24000, 23000) * 8,
+     dict(k_num=1, k_den=20, sink=4, window=128)),
     # the largest query group (16 heads per kv head) on both paths
     ("g16-radix", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
     ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(128)),
