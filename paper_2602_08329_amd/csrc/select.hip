@@ -35,6 +35,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kScoreBlock = 256;
 constexpr int kScoreChunk = 1024;   // keys per score workgroup
+constexpr int kScoreSub = 2;        // 16-key sub-tiles per wave step of score_bf16
 constexpr int kFilterBlock = 256;
 constexpr int kFilterPerThread = 16;
 constexpr int kFilterChunk = kFilterBlock * kFilterPerThread;
@@ -257,7 +258,7 @@ __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const 
 }
 
 template <int D, bool PAGED>
-__global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
+__global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(4))) void score_bf16(SelArgs a) {
   constexpr int KS = D / 32;
   __shared__ uint32_t hist[kHistBins];
   __shared__ int32_t s_page[kScoreChunk + 1];
@@ -301,24 +302,26 @@ __global__ __launch_bounds__(kScoreBlock) void score_bf16(SelArgs a) {
   while (gp < G) gp <<= 1;
   uint32_t* keys = a.keys + (size_t)row * a.mcap;
 
-  const int t0 = base + wave * 64;
-  const int iters = t0 < end ? (end - t0 + 255) / 256 : 0;
+  // each wave takes 16 kScoreSub keys per step, the workgroup kStep
+  constexpr int kStep = 16 * kScoreSub * (kScoreBlock / 64);
+  const int t0 = base + wave * 16 * kScoreSub;
+  const int iters = t0 < end ? (end - t0 + kStep - 1) / kStep : 0;
   if (iters > 0) {
-    ScoreStep<D> A, B;
+    ScoreStep<D, kScoreSub> A, B;
     int t = t0;
     score_load<D, PAGED>(A, a, rg, b, g, t, end, p0, s_page, lane);
     int i = 0;
     for (; i + 2 < iters; i += 2) {
-      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, lane);
+      score_load<D, PAGED>(B, a, rg, b, g, t + kStep, end, p0, s_page, lane);
       score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
-      score_load<D, PAGED>(A, a, rg, b, g, t + 512, end, p0, s_page, lane);
-      score_consume<D>(B, qf, G, gp, t + 256, end, lane, keys, hist, s_kst[wave]);
-      t += 512;
+      score_load<D, PAGED>(A, a, rg, b, g, t + 2 * kStep, end, p0, s_page, lane);
+      score_consume<D>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
+      t += 2 * kStep;
     }
     if (i + 1 < iters) {
-      score_load<D, PAGED>(B, a, rg, b, g, t + 256, end, p0, s_page, lane);
+      score_load<D, PAGED>(B, a, rg, b, g, t + kStep, end, p0, s_page, lane);
       score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
-      score_consume<D>(B, qf, G, gp, t + 256, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
     } else {
       score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
     }
