@@ -42,7 +42,9 @@ constexpr int kFilterChunk = kFilterBlock * kFilterPerThread;
 constexpr int kFinishBlock = 1024;
 constexpr int kFinishPerThread = 8;  // candidates per thread per pass
 constexpr int kFinishTies = 4096;    // level-1 ties the finish kernel keeps in LDS
-constexpr int kFinishSegBits = 32768; // positions per bitmap segment of the finish kernel (3 x 4 KB)
+// positions per bitmap segment of the finish kernel (3 bitmaps of 8 KB): whole
+// words, and below 2^16 so that per-segment counts fit 16-bit fields
+constexpr int kFinishSegBits = 65504;
 
 struct SelArgs {
   KvView kv;
@@ -558,15 +560,17 @@ __device__ void radix_global(const SelArgs& a, uint32_t* cnt, uint2* sel, uint2*
 
 // Threshold T with exactly k of the n distinct composites get(0..n-1) at or
 // above it (1 <= k <= n): radix select over 11-bit digits of the 54-bit
-// values, stopping as soon as a whole bin is taken.  The values must be
+// values, stopping as soon as a whole bin is taken.  With lv0 > 0 the digits
+// of levels below lv0 are already known: `prefix` (under `pmask`) holds them,
+// and k counts within the composites that share them.  The values must be
 // readable from LDS.  Every thread must call it.
 template <typename Get>
 __device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, uint32_t* h, uint32_t* scan,
-                                    int* s_bin, uint32_t* s_krem, uint32_t* s_cnt) {
+                                    int* s_bin, uint32_t* s_krem, uint32_t* s_cnt, int lv0 = 0,
+                                    uint64_t prefix = 0, uint64_t pmask = 0) {
   const int tid = threadIdx.x;
-  uint64_t prefix = 0, pmask = 0;
   uint32_t krem = k;
-  for (int lv = 0; lv < 5; ++lv) {
+  for (int lv = lv0; lv < 5; ++lv) {
     const int sh = lv < 4 ? 43 - 11 * lv : 0;
     const uint64_t dmask = lv < 4 ? 0x7FFull : 0x3FFull;
     for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
@@ -609,18 +613,40 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   uint32_t* cnt = a.counters + row * 4;
   uint2* sel = a.sel + (size_t)row * a.selcap;
   uint32_t n_lds = 0;  // staged ties in dyn[0, n_lds)
+  // m from the budget before clamping to the middle range (floor(k / 3) by
+  // default), clamped to the winners
+  const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
+  const long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
+  const uint32_t kb_u = rg.kb > 0 ? (uint32_t)rg.kb : 0u;
+  const uint32_t m0 = (uint32_t)(mm > (long long)kb_u ? kb_u : mm);
+  // digits already known from the global histograms: the k-th largest lies
+  // in level-0 bin b0 and level-1 bin b1, krem1 deep among the staged ties;
+  // the m-th largest lies in level-0 bin bm0, kremm0 deep
+  int b0 = -1, b1 = -1, bm0 = -1;
+  uint32_t krem1 = 0, kremm0 = 0;
+  bool m_resolved0 = false;
 
   if (rg.kb > 0 && rg.kb < rg.m) {
     for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
     __syncthreads();
+    if (m0 > 0) {
+      find_threshold<kFinishBlock>(h, m0, scan, &s_bin, &s_krem, &s_cnt);
+      bm0 = s_bin;
+      kremm0 = s_krem;
+      m_resolved0 = s_cnt == s_krem;
+      __syncthreads();
+    }
     find_threshold<kFinishBlock>(h, (uint32_t)rg.kb, scan, &s_bin, &s_krem, &s_cnt);
+    b0 = s_bin;
     if (s_cnt != s_krem) {
       const uint32_t krem0 = s_krem;
       __syncthreads();
       for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist1[(size_t)row * kHistBins + i];
       __syncthreads();
       find_threshold<kFinishBlock>(h, krem0, scan, &s_bin, &s_krem, &s_cnt);
-      const uint32_t b1 = (uint32_t)s_bin, krem1 = s_krem, c1 = s_cnt;
+      b1 = s_bin;
+      krem1 = s_krem;
+      const uint32_t c1 = s_cnt;
       const bool resolved1 = c1 == krem1;
       const bool in_lds = !resolved1 && c1 + (uint32_t)rg.kb <= (uint32_t)a.sortcap;
       const uint32_t count0 = min(coherent_load(&cnt[1]), (uint32_t)a.mcap);
@@ -632,6 +658,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       if (in_lds) {
         n_lds = kept;
       } else if (!resolved1) {
+        b1 = -1;
         radix_global(a, cnt, sel, cand2, a.cand + (size_t)row * a.mcap,
                      min(kept, (uint32_t)a.mcap), krem1, 2, h, scan, &s_bin, &s_krem, &s_cnt,
                      &s_base);
@@ -645,17 +672,27 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   for (uint32_t i = n_lds + tid; i < total; i += kFinishBlock) dyn[i] = composite(sel[i - n_lds]);
   __syncthreads();
   // winners: the kout largest composites; top: the m largest of them
-  const uint32_t kout = min(total, (uint32_t)(rg.kb > 0 ? rg.kb : 0));
-  // m from the budget before clamping to the middle range, then clamped to
-  // the winners (floor(k_b / 3) by default)
-  const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
-  long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
+  const uint32_t kout = min(total, kb_u);
   const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
   auto get = [&](uint32_t i) { return dyn[i]; };
-  const uint64_t c_k = kout < total ? lds_kth_largest(get, total, kout, h, scan, &s_bin, &s_krem, &s_cnt)
-                                    : 0ull;
-  const uint64_t c_m = m > 0 ? lds_kth_largest(get, total, m, h, scan, &s_bin, &s_krem, &s_cnt)
-                             : ~0ull;
+  constexpr uint64_t kD0 = 0x7FFull << 43, kD1 = 0x7FFull << 32;
+  uint64_t c_k = 0ull;
+  if (kout < total) {
+    if (b1 >= 0 && n_lds > 0 && n_sel + krem1 == kout)  // among the ties, from level 2
+      c_k = lds_kth_largest(get, n_lds, krem1, h, scan, &s_bin, &s_krem, &s_cnt, 2,
+                            ((uint64_t)b0 << 43) | ((uint64_t)b1 << 32), kD0 | kD1);
+    else
+      c_k = lds_kth_largest(get, total, kout, h, scan, &s_bin, &s_krem, &s_cnt);
+  }
+  uint64_t c_m = ~0ull;
+  if (m > 0) {
+    if (bm0 >= 0 && m == m0)  // level-0 digit from the global histogram
+      c_m = m_resolved0 ? (uint64_t)bm0 << 43
+                        : lds_kth_largest(get, total, kremm0, h, scan, &s_bin, &s_krem, &s_cnt, 1,
+                                          (uint64_t)bm0 << 43, kD0);
+    else
+      c_m = lds_kth_largest(get, total, m, h, scan, &s_bin, &s_krem, &s_cnt);
+  }
   // One ordered pass over the middle range writes all outputs: per bitmap
   // segment the winners W (x >= c_k), the top m T (x >= c_m) and the +-r
   // neighbours D of T are marked together, and one scan of four packed counts
@@ -703,8 +740,8 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       }
     }
     __syncthreads();
-    // thread t owns words [t*wpt, (t+1)*wpt); a segment holds at most 2^15
-    // positions, so each packed 16-bit count fits
+    // thread t owns words [t*wpt, (t+1)*wpt); a segment holds fewer than
+    // 2^16 positions, so each packed 16-bit count fits
     const int wpt = (nwords + kFinishBlock - 1) / kFinishBlock;
     const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
     uint64_t cnt = 0;
