@@ -5,12 +5,18 @@
 // length (Eq. neighboring), and optionally only for the rows a similarity
 // gate sends to retrieval.
 //
-// Two paths, both on the caller's stream:
-//   select_fused   many short contiguous bf16 rows: one workgroup per row
-//                  scores into LDS, takes exact thresholds for k and m over
-//                  the 32-bit keys and compacts in position order (which
-//                  settles ties) -- one launch;
-//   radix path     otherwise, one launch each:
+// Three paths, all on the caller's stream (select_path picks one):
+//   select_fused   middle range within LDS, contiguous bf16, rows filling
+//                  more than half the CUs: one workgroup per row scores into
+//                  LDS, takes exact thresholds for k and m over the 32-bit
+//                  keys and compacts in position order (which settles ties)
+//                  -- one launch;
+//   keyed path     middle range within LDS, fewer rows (or a paged or fp32
+//                  cache): score_* without histograms spreads each row over
+//                  many workgroups and writes its keys, then select_keyed
+//                  runs select_fused's selection half, one workgroup per row
+//                  -- two launches;
+//   radix path     longer middle ranges, one launch each:
 //     select_clear   zero the per-row histograms and counters
 //     score_*        sigma_i = max_h q_h . k_i (raw, fp32) -> order-preserving
 //                    u32 key; fused histogram of the top 11 key bits
@@ -218,7 +224,7 @@ __device__ __forceinline__ void score_load(ScoreStep<D, SUB>& S, const SelArgs& 
 // kst: the wave's LDS tile of 16 x d bf16.  LDS operations of one wave
 // complete in order; the wave barriers keep the compiler from moving them
 // across each other.
-template <int D, int SUB>
+template <int D, int SUB, bool HIST = true>
 __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const bf16x8_t* qf, int G,
                                               int gp, int t, int end, int lane, uint32_t* keys,
                                               uint32_t* hist, u32x4_t* kst) {
@@ -252,14 +258,16 @@ __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const 
         if (i < end) {
           const uint32_t key = score_key(v[e]);
           keys[i] = key;
-          atomicAdd(&hist[key >> 21], 1u);
+          if (HIST) atomicAdd(&hist[key >> 21], 1u);
         }
       }
     }
   }
 }
 
-template <int D, bool PAGED>
+// HIST: also accumulate the rows' level-0 histograms into hist0 (the radix
+// path); without, the keys alone (the keyed path builds its histogram in LDS).
+template <int D, bool PAGED, bool HIST>
 __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(4))) void score_bf16(SelArgs a) {
   constexpr int KS = D / 32;
   __shared__ uint32_t hist[kHistBins];
@@ -315,26 +323,28 @@ __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(4))
     int i = 0;
     for (; i + 2 < iters; i += 2) {
       score_load<D, PAGED>(B, a, rg, b, g, t + kStep, end, p0, s_page, lane);
-      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D, kScoreSub, HIST>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
       score_load<D, PAGED>(A, a, rg, b, g, t + 2 * kStep, end, p0, s_page, lane);
-      score_consume<D>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D, kScoreSub, HIST>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
       t += 2 * kStep;
     }
     if (i + 1 < iters) {
       score_load<D, PAGED>(B, a, rg, b, g, t + kStep, end, p0, s_page, lane);
-      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
-      score_consume<D>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D, kScoreSub, HIST>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D, kScoreSub, HIST>(B, qf, G, gp, t + kStep, end, lane, keys, hist, s_kst[wave]);
     } else {
-      score_consume<D>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
+      score_consume<D, kScoreSub, HIST>(A, qf, G, gp, t, end, lane, keys, hist, s_kst[wave]);
     }
   }
-  __syncthreads();
-  flush_hist(hist, a.hist0 + (size_t)row * kHistBins);
+  if (HIST) {
+    __syncthreads();
+    flush_hist(hist, a.hist0 + (size_t)row * kHistBins);
+  }
 }
 
 // fp32 scoring on the vector ALU: one key per thread, the group's query heads
 // staged in LDS, sequential fp32 fused multiply-adds over d.
-template <int D>
+template <int D, bool HIST>
 __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
   __shared__ uint32_t hist[kHistBins];
   __shared__ float qs[16 * D];
@@ -373,10 +383,10 @@ __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
     }
     const uint32_t key = score_key(best);
     keys[i] = key;
-    atomicAdd(&hist[key >> 21], 1u);
+    if (HIST) atomicAdd(&hist[key >> 21], 1u);
   }
   __syncthreads();
-  flush_hist(hist, a.hist0 + (size_t)row * kHistBins);
+  if (HIST) flush_hist(hist, a.hist0 + (size_t)row * kHistBins);
 }
 
 // Level-0 split of a chunk of keys: keys above the threshold bin are
@@ -891,66 +901,18 @@ __device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
   return *s_row;
 }
 
-template <int D, int BLOCK>
-__global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
-  constexpr int KS = D / 32;
-  extern __shared__ uint32_t s_keys[];  // [middle length]
-  __shared__ uint32_t h[kHistBins];
-  __shared__ uint32_t scan[BLOCK / 64 + 1];
-  __shared__ uint64_t scan64[BLOCK / 64 + 1];
-  __shared__ int s_bin;
-  __shared__ uint32_t s_krem, s_cnt;
-  __shared__ int s_len[kBalanceMaxBatch];
-  __shared__ int s_row;
-  __shared__ u32x4_t s_kst[BLOCK / 64][16 * (D / 8)];
-  const int row = fused_row(a, blockIdx.x, s_len, &s_row);
-  if (row_skipped(a, row)) return;
-  const int b = row / a.kv.hkv, g = row % a.kv.hkv;
-  const RowGeom rg = row_geom(a, b);
+// Selection half of the fused refresh, after the row's middle-range keys
+// (order-preserving u32, position order) are in s_keys and their level-0
+// histogram (key >> 21) in h: exact thresholds for the k_b and m largest,
+// one ordered compaction in position order (which also settles ties) into
+// top m, other winners and the anchor set, and with a shared-set output the
+// dilated shared set.  Reached by every thread of the workgroup.
+template <int BLOCK>
+__device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, uint32_t* s_keys,
+                                  uint32_t* h, uint32_t* scan, uint64_t* scan64, int* s_bin,
+                                  uint32_t* s_krem, uint32_t* s_cnt) {
   const int tid = threadIdx.x;
   const int M = rg.m;
-  for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
-  __syncthreads();
-  if (rg.kb > 0) {
-    const int lane = tid & 63, wave = tid >> 6;
-    const int col = lane & 15, grp = lane >> 4;
-    const int G = a.kv.hq / a.kv.hkv;
-    const __bf16* q = (const __bf16*)a.q;
-    bf16x8_t qf[KS];
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const int qh = col < G ? col : 0;
-      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * 8);
-      const uint4 v = qp[4 * kk];
-      qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
-    }
-    int gp = 1;
-    while (gp < G) gp <<= 1;
-    constexpr int kStride = 32 * (BLOCK / 64);
-    const int t0 = wave * 32;
-    const int iters = t0 < M ? (M - t0 + kStride - 1) / kStride : 0;
-    if (iters > 0) {
-      ScoreStep<D, 2> A, B;
-      int t = t0;
-      score_load<D, false>(A, a, rg, b, g, t, M, 0, nullptr, lane);
-      int i = 0;
-      for (; i + 2 < iters; i += 2) {
-        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
-        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
-        score_load<D, false>(A, a, rg, b, g, t + 2 * kStride, M, 0, nullptr, lane);
-        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
-        t += 2 * kStride;
-      }
-      if (i + 1 < iters) {
-        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
-        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
-        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
-      } else {
-        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
-      }
-    }
-  }
-  __syncthreads();
   const int se = rg.sink_end;
   const uint32_t kout = (uint32_t)rg.kb;
   const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
@@ -964,12 +926,12 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
 #pragma unroll
   for (int j = 0; j < kBinsPerThread; ++j) h_keep[j] = h[tid + j * BLOCK];
   const KeyThreshold tm =
-      key_threshold<BLOCK>(s_keys, (uint32_t)M, m, h, h, scan, &s_bin, &s_krem, &s_cnt);
+      key_threshold<BLOCK>(s_keys, (uint32_t)M, m, h, h, scan, s_bin, s_krem, s_cnt);
 #pragma unroll
   for (int j = 0; j < kBinsPerThread; ++j) h[tid + j * BLOCK] = h_keep[j];
   __syncthreads();
   const KeyThreshold tk =
-      key_threshold<BLOCK>(s_keys, (uint32_t)M, kout, h, h, scan, &s_bin, &s_krem, &s_cnt);
+      key_threshold<BLOCK>(s_keys, (uint32_t)M, kout, h, h, scan, s_bin, s_krem, s_cnt);
   // h becomes the bitmap of the dilated shared set over the middle indices
   // (M <= 32 * kHistBins); the scan below orders the clearing before marking
   const bool shared = a.shared_idx != nullptr;
@@ -1051,37 +1013,121 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   }
 }
 
+template <int D, int BLOCK>
+__global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
+  constexpr int KS = D / 32;
+  extern __shared__ uint32_t s_keys[];  // [middle length]
+  __shared__ uint32_t h[kHistBins];
+  __shared__ uint32_t scan[BLOCK / 64 + 1];
+  __shared__ uint64_t scan64[BLOCK / 64 + 1];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_krem, s_cnt;
+  __shared__ int s_len[kBalanceMaxBatch];
+  __shared__ int s_row;
+  __shared__ u32x4_t s_kst[BLOCK / 64][16 * (D / 8)];
+  const int row = fused_row(a, blockIdx.x, s_len, &s_row);
+  if (row_skipped(a, row)) return;
+  const int b = row / a.kv.hkv, g = row % a.kv.hkv;
+  const RowGeom rg = row_geom(a, b);
+  const int tid = threadIdx.x;
+  const int M = rg.m;
+  for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
+  __syncthreads();
+  if (rg.kb > 0) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int G = a.kv.hq / a.kv.hkv;
+    const __bf16* q = (const __bf16*)a.q;
+    bf16x8_t qf[KS];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int qh = col < G ? col : 0;
+      const uint4* qp = (const uint4*)(q + ((size_t)b * a.kv.hq + g * G + qh) * D + grp * 8);
+      const uint4 v = qp[4 * kk];
+      qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
+    }
+    int gp = 1;
+    while (gp < G) gp <<= 1;
+    constexpr int kStride = 32 * (BLOCK / 64);
+    const int t0 = wave * 32;
+    const int iters = t0 < M ? (M - t0 + kStride - 1) / kStride : 0;
+    if (iters > 0) {
+      ScoreStep<D, 2> A, B;
+      int t = t0;
+      score_load<D, false>(A, a, rg, b, g, t, M, 0, nullptr, lane);
+      int i = 0;
+      for (; i + 2 < iters; i += 2) {
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
+        score_load<D, false>(A, a, rg, b, g, t + 2 * kStride, M, 0, nullptr, lane);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
+        t += 2 * kStride;
+      }
+      if (i + 1 < iters) {
+        score_load<D, false>(B, a, rg, b, g, t + kStride, M, 0, nullptr, lane);
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
+        score_consume<D>(B, qf, G, gp, t + kStride, M, lane, s_keys, h, s_kst[wave]);
+      } else {
+        score_consume<D>(A, qf, G, gp, t, M, lane, s_keys, h, s_kst[wave]);
+      }
+    }
+  }
+  __syncthreads();
+  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, scan, scan64, &s_bin, &s_krem, &s_cnt);
+}
+
+// Selection of one row whose middle-range keys a scoring kernel (without
+// histograms) wrote to the workspace: the keys go to LDS with their level-0
+// histogram, then the fused refresh's selection half.  Used when the rows
+// fill at most half the CUs, so that scoring first spreads each row over
+// many workgroups.  All of a thread's key loads are issued before any is
+// stored.
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void select_keyed(SelArgs a) {
+  constexpr int kPer = 16;  // keys per thread per batch
+  extern __shared__ uint32_t s_keys[];  // [middle length]
+  __shared__ uint32_t h[kHistBins];
+  __shared__ uint32_t scan[BLOCK / 64 + 1];
+  __shared__ uint64_t scan64[BLOCK / 64 + 1];
+  __shared__ int s_bin;
+  __shared__ uint32_t s_krem, s_cnt;
+  const int row = blockIdx.x;
+  if (row_skipped(a, row)) return;
+  const RowGeom rg = row_geom(a, row / a.kv.hkv);
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
+  __syncthreads();
+  if (rg.kb > 0) {
+    const uint32_t* keys = a.keys + (size_t)row * a.mcap;
+    for (int base = 0; base < rg.m; base += BLOCK * kPer) {
+      uint32_t v[kPer];
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int i = base + tid + k * BLOCK;
+        v[k] = i < rg.m ? keys[i] : 0u;
+      }
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int i = base + tid + k * BLOCK;
+        if (i < rg.m) {
+          s_keys[i] = v[k];
+          atomicAdd(&h[v[k] >> 21], 1u);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, scan, scan64, &s_bin, &s_krem, &s_cnt);
+}
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
 constexpr int kLdsBytes = 160 * 1024;  // LDS of one CU
 static_assert(kFusedMaxKeys <= 32 * kHistBins, "the shared-set bitmap reuses the histogram");
-constexpr int kFusedMinRows = 128;    // enough rows to occupy the chip one per CU
 
-// The fused path: bf16, contiguous, many rows, middle range within LDS.
-// PRHS_SELECT_PATH=fused|split overrides the choice (a tuning knob, read once
-// per process; the fused path still needs a contiguous bf16 cache that fits).
-bool use_fused_select(int dtype, bool paged, int rows, int mcap) {
-  static const int force = [] {
-    const char* e = getenv("PRHS_SELECT_PATH");
-    if (!e) return 0;
-    if (e[0] == 'f') return 1;
-    if (e[0] == 's') return -1;
-    return 0;
-  }();
-  if (dtype != 1 || paged || mcap > kFusedMaxKeys) return false;
-  if (force != 0) return force > 0;
-  return rows >= kFusedMinRows;
-}
-
-// CUs of the current device, for the fused refresh's row balancing (0 when
-// unknown or when PRHS_SELECT_BALANCE=0).
-int balance_cus() {
-  static const int enabled = [] {
-    const char* e = getenv("PRHS_SELECT_BALANCE");
-    return e ? atoi(e) : 1;
-  }();
-  if (!enabled) return 0;
+// CUs of the current device (0 when unknown).
+int device_cus() {
   static int cus[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
@@ -1092,6 +1138,44 @@ int balance_cus() {
     cus[dev] = n > 0 ? n : -1;
   }
   return cus[dev] > 0 ? cus[dev] : 0;
+}
+
+enum class SelPath { kFused, kKeyed, kRadix };
+
+// The refresh's launch sequence.  Middle ranges that fit LDS: one fused
+// launch when the rows (one workgroup each) fill more than half the CUs and
+// the cache is contiguous bf16, else scoring spread over many workgroups per
+// row followed by one selection workgroup per row (keyed).  Longer middle
+// ranges: the radix path (clear, score, filter, finish).
+// PRHS_SELECT_PATH=fused|keyed|split forces a path where it applies.
+SelPath select_path(int dtype, bool paged, int rows, int mcap) {
+  static const int force = [] {
+    const char* e = getenv("PRHS_SELECT_PATH");
+    if (!e) return 0;
+    if (e[0] == 'f') return 1;
+    if (e[0] == 'k') return 2;
+    if (e[0] == 's') return 3;
+    return 0;
+  }();
+  const bool fits = mcap <= kFusedMaxKeys;
+  const bool fused_ok = fits && dtype == 1 && !paged;
+  if (force == 1 && fused_ok) return SelPath::kFused;
+  if (force == 2 && fits) return SelPath::kKeyed;
+  if (force == 3) return SelPath::kRadix;
+  if (!fits) return SelPath::kRadix;
+  const int cus = device_cus();
+  if (fused_ok && (cus <= 0 || 2 * rows > cus)) return SelPath::kFused;
+  return SelPath::kKeyed;
+}
+
+// CUs of the current device, for the fused refresh's row balancing (0 when
+// unknown or when PRHS_SELECT_BALANCE=0).
+int balance_cus() {
+  static const int enabled = [] {
+    const char* e = getenv("PRHS_SELECT_BALANCE");
+    return e ? atoi(e) : 1;
+  }();
+  return enabled ? device_cus() : 0;
 }
 
 struct SelLayout {
@@ -1155,8 +1239,9 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.balance_cus = 0;
   a.row_choice = s.row_choice;
 
+  const SelPath path = select_path(s.dtype, s.kv.paged != 0, rows, a.mcap);
   // many short contiguous bf16 rows: the whole refresh in one launch
-  if (use_fused_select(s.dtype, s.kv.paged != 0, rows, a.mcap)) {
+  if (path == SelPath::kFused) {
     const size_t dyn = (size_t)a.mcap * 4;
     a.balance_cus = balance_cus();
     // one 1024-thread workgroup per CU while the rows fit the CUs and its
@@ -1191,20 +1276,39 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   }
   // the middle range is shorter than max_seq_len; size grids by max_seq_len
   const int mid_max = a.mcap;
-  hipLaunchKernelGGL(select_clear, dim3(rows), dim3(256), 0, stream, a);
+  const bool radix = path == SelPath::kRadix;
+  if (radix) hipLaunchKernelGGL(select_clear, dim3(rows), dim3(256), 0, stream, a);
   const dim3 sgrid((mid_max + kScoreChunk - 1) / kScoreChunk, rows);
-  if (s.dtype == 1) {
-    const bool paged = s.kv.paged != 0;
-    if (s.kv.d == 128) {
-      if (paged) hipLaunchKernelGGL((score_bf16<128, true>), sgrid, dim3(kScoreBlock), 0, stream, a);
-      else hipLaunchKernelGGL((score_bf16<128, false>), sgrid, dim3(kScoreBlock), 0, stream, a);
-    } else {
-      if (paged) hipLaunchKernelGGL((score_bf16<64, true>), sgrid, dim3(kScoreBlock), 0, stream, a);
-      else hipLaunchKernelGGL((score_bf16<64, false>), sgrid, dim3(kScoreBlock), 0, stream, a);
-    }
+#define PRHS_SCORE_LAUNCH(HIST)                                                               \
+  if (s.dtype == 1) {                                                                         \
+    const bool paged = s.kv.paged != 0;                                                       \
+    if (s.kv.d == 128) {                                                                      \
+      if (paged) hipLaunchKernelGGL((score_bf16<128, true, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);  \
+      else hipLaunchKernelGGL((score_bf16<128, false, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);       \
+    } else {                                                                                  \
+      if (paged) hipLaunchKernelGGL((score_bf16<64, true, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);   \
+      else hipLaunchKernelGGL((score_bf16<64, false, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);        \
+    }                                                                                         \
+  } else {                                                                                    \
+    if (s.kv.d == 128) hipLaunchKernelGGL((score_f32<128, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);   \
+    else hipLaunchKernelGGL((score_f32<64, HIST>), sgrid, dim3(kScoreBlock), 0, stream, a);                  \
+  }
+  if (radix) {
+    PRHS_SCORE_LAUNCH(true)
   } else {
-    if (s.kv.d == 128) hipLaunchKernelGGL(score_f32<128>, sgrid, dim3(kScoreBlock), 0, stream, a);
-    else hipLaunchKernelGGL(score_f32<64>, sgrid, dim3(kScoreBlock), 0, stream, a);
+    PRHS_SCORE_LAUNCH(false)
+  }
+#undef PRHS_SCORE_LAUNCH
+  if (!radix) {
+    // keyed: one 1024-thread selection workgroup per row over the keys in LDS
+    const size_t dyn = (size_t)a.mcap * 4;
+    if (dyn > 65536) {
+      const hipError_t e = hipFuncSetAttribute((const void*)select_keyed<1024>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(select_keyed<1024>, dim3(rows), dim3(1024), dyn, stream, a);
+    return hipGetLastError();
   }
   const dim3 fgrid((mid_max + kFilterChunk - 1) / kFilterChunk, rows);
   hipLaunchKernelGGL(select_filter, fgrid, dim3(kFilterBlock), 0, stream, a);

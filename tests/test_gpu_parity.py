@@ -209,6 +209,8 @@ def check_select(inp, lens, p, layer=0, step=0):
 
 SELECT_CASES = [
     # name, dtype, d, paged, hq, hkv, lens, params
+    # few rows, middle range within LDS: the keyed path (multi-workgroup
+    # scoring, then one selection workgroup per row)
     ("ragged-gqa", "bf16", 128, False, 8, 2, (5000, 2100, 70), dict(k=300, sink=4, window=64)),
     ("mha-d64-paged", "bf16", 64, True, 4, 4, (3000, 1500), dict(k=100, sink=4, window=32)),
     ("g8", "bf16", 128, False, 16, 2, (4500,), dict(k=64, sink=0, window=0)),
@@ -219,16 +221,27 @@ SELECT_CASES = [
     ("f32", "f32", 64, False, 4, 4, (1025, 300), dict(k=64, sink=4, window=32)),
     ("f32-paged-gqa", "f32", 128, True, 8, 2, (2000,), dict(k=50, sink=2, window=8)),
     ("big-k", "bf16", 128, False, 4, 1, (20000,), dict(k=9000, sink=4, window=64)),
-    # 16 sequences x 8 kv heads = 128 rows: the single-launch refresh path
-    ("fused-ragged", "bf16", 128, False, 32, 8,
-     (3000, 2100, 70, 1500, 999, 2048, 300, 2999, 1200, 640, 77, 2500, 1800, 33, 2222, 1024),
+    ("keyed-128-rows", "bf16", 128, False, 32, 8, tuple(300 + (i * 997) % 5000 for i in range(16)),
      dict(k=150, sink=4, window=32)),
-    ("fused-mha-d64", "bf16", 64, False, 8, 8, (900, 1300) * 8, dict(k=60, sink=2, window=16)),
-    ("fused-k-ge-middle", "bf16", 128, False, 16, 8, (400, 150) * 8, dict(k=5000, sink=4, window=16)),
-    ("fused-k-zero", "bf16", 128, False, 16, 8, (400, 900) * 8, dict(k=0, sink=4, window=16)),
-    ("fused-short", "bf16", 128, False, 8, 8, (3, 20, 21, 22, 40, 60, 5, 1) * 2,
+    # middle ranges beyond LDS: the radix path (clear, score, filter, finish),
+    # including a k whose level-1 ties overflow the LDS buffer
+    ("radix-ragged-gqa", "bf16", 128, False, 8, 2, (30000, 26000, 70), dict(k=300, sink=4, window=64)),
+    ("radix-paged-d64", "bf16", 64, True, 4, 4, (27000,), dict(k=100, sink=4, window=32)),
+    ("radix-big-k", "bf16", 128, False, 4, 1, (30000,), dict(k=12000, sink=4, window=64)),
+    ("radix-f32-paged", "f32", 128, True, 8, 2, (26000,), dict(k=50, sink=2, window=8)),
+    ("radix-ratio", "bf16", 128, True, 8, 2, (40000, 25000), dict(k_num=1, k_den=20, sink=4, window=128)),
+    ("radix-g16", "bf16", 128, True, 32, 2, (30000,), dict(k=200, sink=4, window=64)),
+    # 17 sequences x 8 kv heads = 136 rows, more than half the CUs: the
+    # single-launch refresh path
+    ("fused-ragged", "bf16", 128, False, 32, 8,
+     (3000, 2100, 70, 1500, 999, 2048, 300, 2999, 1200, 640, 77, 2500, 1800, 33, 2222, 1024, 1700),
+     dict(k=150, sink=4, window=32)),
+    ("fused-mha-d64", "bf16", 64, False, 8, 8, (900, 1300) * 8 + (1100,), dict(k=60, sink=2, window=16)),
+    ("fused-k-ge-middle", "bf16", 128, False, 16, 8, (400, 150) * 8 + (300,), dict(k=5000, sink=4, window=16)),
+    ("fused-k-zero", "bf16", 128, False, 16, 8, (400, 900) * 8 + (600,), dict(k=0, sink=4, window=16)),
+    ("fused-short", "bf16", 128, False, 8, 8, (3, 20, 21, 22, 40, 60, 5, 1) * 2 + (9,),
      dict(k=5, sink=4, window=16)),
-    ("fused-ratio", "bf16", 128, False, 32, 8, (9000, 4100) * 8,
+    ("fused-ratio", "bf16", 128, False, 32, 8, (9000, 4100) * 8 + (6000,),
      dict(k_num=1, k_den=20, sink=4, window=128)),
     # 40 x 8 = 320 rows, more than the CUs: workgroups take rows by length rank
     ("fused-balanced", "bf16", 128, False, 16, 8,
@@ -236,15 +249,15 @@ SELECT_CASES = [
      dict(k=100, sink=4, window=32)),
     ("fused-balanced-d64", "bf16", 64, False, 8, 8,
      tuple(40 + (i * 577) % 3000 for i in range(40)), dict(k=70, sink=2, window=16)),
-    # long middle ranges on 128 rows: up to ~21k keys the key array fits LDS
+    # long middle ranges on 136 rows: up to ~21k keys the key array fits LDS
     # beside the 1024-thread workgroup's staging; beyond, 512 threads
-    ("fused-wide-21k", "bf16", 128, False, 32, 8, (21000, 16000) * 8,
+    ("fused-wide-21k", "bf16", 128, False, 32, 8, (21000, 16000) * 8 + (12000,),
      dict(k=1000, sink=4, window=128)),
-    ("fused-narrow-24k", "bf16", 128, False, 32, 8, (24000, 23000) * 8,
+    ("fused-narrow-24k", "bf16", 128, False, 32, 8, (24000, 23000) * 8 + (20000,),
      dict(k_num=1, k_den=20, sink=4, window=128)),
-    # the largest query group (16 heads per kv head) on both paths
-    ("g16-radix", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
-    ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(128)),
+    # the largest query group (16 heads per kv head) on each path
+    ("g16-keyed", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
+    ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(136)),
      dict(k=50, sink=4, window=16)),
 ]
 
@@ -324,9 +337,10 @@ def test_select_all_ties_lowest_positions():
 
 
 def test_select_fused_all_ties():
-    # all scores equal on the single-launch path: ties go to the lower positions
-    lens = (2500, 1700) * 8
-    inp = synth.random_inputs(16, 8, 8, 128, lens, seed=14, grid=True, device=DEV)
+    # all scores equal on the single-launch path (136 rows): ties go to the
+    # lower positions
+    lens = (2500, 1700) * 8 + (2100,)
+    inp = synth.random_inputs(17, 8, 8, 128, lens, seed=14, grid=True, device=DEV)
     for K in inp.K:
         K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, 0.75)))
     topk, tlen = check_select(inp, lens, B.params(k=120, sink=4, window=32))
@@ -334,9 +348,10 @@ def test_select_fused_all_ties():
 
 
 def test_select_all_ties_beyond_lds_budget():
-    # every score equal on a row longer than the finish kernel's LDS tie buffer:
-    # the tie-break runs through the global radix levels over positions
-    lens = (14000,)
+    # every score equal on a row longer than LDS (radix path) and than the
+    # finish kernel's LDS tie buffer: the tie-break runs through the global
+    # radix levels over positions
+    lens = (30000,)
     inp = synth.random_inputs(1, 4, 1, 128, lens, seed=12, grid=True, device=DEV)
     for K in inp.K:
         K.copy_(torch.where(torch.isnan(K), K, torch.full_like(K, -0.5)))
@@ -344,9 +359,9 @@ def test_select_all_ties_beyond_lds_budget():
     assert list(topk[0, 0, :3]) == [4, 5, 6]
 
 
-def test_select_coarse_grid_many_ties():
+@pytest.mark.parametrize("lens", [(6000, 2500), (30000, 26000)], ids=["keyed", "radix"])
+def test_select_coarse_grid_many_ties(lens):
     # values in {-1/16, 0, 1/16}: very many exact ties at the threshold
-    lens = (6000, 2500)
     inp = synth.random_inputs(2, 8, 2, 128, lens, seed=4, grid=True, device=DEV)
     for t in inp.K + [inp.q]:
         t.copy_(torch.where(torch.isnan(t), t, torch.clamp(torch.round(t.float()), -1, 1).to(t.dtype) / 16))
