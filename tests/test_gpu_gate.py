@@ -173,6 +173,15 @@ def test_gated_schedule_config1_cut():
     assert 1 / w.s <= ratio <= 1
 
 
+def test_gated_schedule_fused_rows():
+    # 5 sequences x 32 kv heads = 160 rows, more than half the CUs: the gated
+    # refresh on the single-launch path, non-retrieving rows exiting at once
+    w = synth.workload(1).replace(layers=4, batch=5, n_ctx=(1500, 900, 1200, 700, 1100), steps=8)
+    ratio = run_gated(w, 0.8, range(w.steps), {(0, 0), (4, 31)},
+                      units_set=[(b, g) for b in range(5) for g in (0, 13, 31)])
+    assert 1 / w.s <= ratio <= 1
+
+
 def test_gated_schedule_config0_full():
     w = synth.workload(0)
     run_gated(w, 0.85, range(w.steps), {(0, g) for g in range(w.hkv)})
