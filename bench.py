@@ -255,7 +255,8 @@ def main():
 
     from paper_2602_08329_amd import binding as B
     from paper_2602_08329_amd import synth
-    from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner, psaw_defaults
+    from paper_2602_08329_amd.schedule import (DecodeRunner, GatedDecodeRunner, capture_steps,
+                                               psaw_defaults)
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -310,10 +311,7 @@ def main():
         js = [order(W_steps + i) for i in range(K_steps)]
         graph = None
         if not args.eager:
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph):
-                for j in js:
-                    fn(j)
+            graph = capture_steps(fn, js)
             graph.replay()
         torch.cuda.synchronize()
         ev0.record()

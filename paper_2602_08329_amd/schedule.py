@@ -43,6 +43,21 @@ def psaw_defaults(n_layers):
     return (3 * n_layers) // 4, 0.7, 1.0
 
 
+def capture_steps(fn, steps):
+    """Captures the launches of fn(j) for j in steps (for example a runner's
+    step, selection_step or dense_step) into a HIP graph and returns it
+    (torch.cuda.CUDAGraph); replay() reruns the same launches on the same
+    buffers, back to back on the current stream and without host launch
+    overhead.  Every launch of the path takes the current stream and none
+    records a memset, so a replay computes what the eager calls compute.  The
+    runner's host-side schedule checks run at capture time."""
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for j in steps:
+            fn(j)
+    return graph
+
+
 class DecodeRunner:
     """Runs the hot path of a synthetic workload (paper_2602_08329_amd.synth)
     whose inputs already live on the GPU."""

@@ -13,7 +13,7 @@ import torch
 
 from paper_2602_08329_amd import binding as B
 from paper_2602_08329_amd import synth
-from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner
+from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner, capture_steps
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -50,9 +50,7 @@ def _check_graph(w, runner, replays=3):
     ref = {k: (o.clone(), s.clone()) for k, (o, s) in bufs.items()}
     assert all(torch.isfinite(o).all() for o, _ in ref.values())
 
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        _cycle(run, steps, bufs)
+    g = capture_steps(lambda j: run.step(j, outs=[bufs[(l, j)] for l in range(run.L)]), steps)
     torch.cuda.synchronize()
     spare = (torch.empty(w.batch, w.hq, w.d, device=DEV), torch.empty(w.batch, w.hq, device=DEV))
     for rep in range(replays):
