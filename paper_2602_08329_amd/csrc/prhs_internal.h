@@ -17,12 +17,11 @@ constexpr int kHistBins = 2048;
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
-// Loads of V rows, which a launch reads whole and once, take the
-// non-temporal (streaming) cache policy: on this chip a streaming read
-// sustains about 7 TB/s with it and about 6 TB/s with the default policy.
-// K operand loads keep the default policy: a 128-byte line of a K row is
-// read by two load instructions, and a streaming line is evicted after its
-// first hit.
+// Loads of K and V rows, which a launch reads once, with the non-temporal
+// (streaming) cache policy: on this chip a streaming read sustains about
+// 7 TB/s with it and about 6 TB/s with the default policy.  Only for loads
+// that read whole 128-byte lines per instruction: a line shared by several
+// load instructions is evicted after its first hit and fetched again.
 __device__ __forceinline__ u32x4_t stream_load16(const void* p) {
   return __builtin_nontemporal_load((const u32x4_t*)p);
 }
