@@ -26,6 +26,10 @@ Readings of passages that the paper leaves open:
   neighbourhood of its top-m and every position from the anchor's window start
   up to the current length (Eq. neighboring, with the neighbourhood clipped to
   the valid positions as in the CIS parameterisation appendix).
+* PSAW at prefill: the query at position i has the i + 1 tokens [0, i] in
+  view, so Eq. psaw is taken at t = i + 1; it attends the causal range [0, i]
+  restricted to the sink and [max(C_sink, P - 1), i] (the same set a decode
+  step at length i + 1 attends).
 * Cross-layer sharing: groups of G consecutive layers; the first layer of a
   group is the anchor that scores; the others reuse its selection over their
   own K/V.  Refresh happens at decode steps j with j mod s == 0.
@@ -70,6 +74,9 @@ __all__ = [
     "psaw_boundary",
     "psaw_visible_start",
     "psaw_restrict",
+    "psaw_prefill_visible",
+    "prefill_visible_set",
+    "prefill_attention",
 ]
 
 
@@ -403,6 +410,44 @@ def psaw_restrict(S, start, sink, n):
     S = np.asarray(S, dtype=np.int64)
     sink_end = min(sink, n)
     return S[(S < sink_end) | ((S >= start) & (S < n))]
+
+
+# ---------------------------------------------------------------------------
+# PSAW at prefill (Sec. 4.2: the window narrows during prefill as well as
+# decoding; the prefill panel of the PSAW/ETF figure)
+# ---------------------------------------------------------------------------
+
+def psaw_prefill_visible(layer0, n_layers, T, sink, l_s, phi, alpha):
+    """First visible non-sink position of every query of a prefill of T
+    tokens at 0-based layer `layer0`.  The query at 0-based position i has
+    the i + 1 tokens [0, i] in view, so Eq. psaw is taken at t = i + 1: its
+    first visible position is psaw_visible_start(layer0, ..., n = i + 1).
+    Returns int64 [T]."""
+    return np.array([psaw_visible_start(layer0, n_layers, i + 1, sink, l_s, phi, alpha)
+                     for i in range(T)], dtype=np.int64)
+
+
+def prefill_visible_set(i, sink, vis=None):
+    """Keys the query at position i attends at prefill: the causal range
+    [0, i] (Eq. attn_eq over the tokens in view), restricted under PSAW to
+    [0, C_sink) U [vis, i]."""
+    S = np.arange(i + 1, dtype=np.int64)
+    return S if vis is None else psaw_restrict(S, vis, sink, i + 1)
+
+
+def prefill_attention(Q, K, V, n, sink=0, vis_start=None, scale=None):
+    """Prefill attention of one query head over a prompt of n tokens: row i
+    of Q (position i) attends prefill_visible_set(i, sink, vis_start[i]) of
+    its kv head's K, V; rows at positions >= n (past the prompt) give y = 0
+    and lse = -inf.  Returns (y [T][d], lse [T])."""
+    Q = _f64(Q)
+    T, d = Q.shape
+    y = np.zeros((T, d))
+    lse = np.full(T, -np.inf)
+    for i in range(min(T, n)):
+        S = prefill_visible_set(i, sink, None if vis_start is None else int(vis_start[i]))
+        y[i], lse[i] = sparse_attention(Q[i], K[: i + 1], V[: i + 1], S, scale)
+    return y, lse
 
 
 # ---------------------------------------------------------------------------

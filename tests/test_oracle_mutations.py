@@ -101,6 +101,16 @@ _orig = {name: getattr(M, name) for name in
 
 PINS = [getattr(P, n) for n in dir(P) if n.startswith("test_")]
 
+def _prefill_vis_at_i(layer0, n_layers, T, sink, l_s, phi, alpha):
+    return np.array([M.psaw_visible_start(layer0, n_layers, max(i, 1), sink, l_s, phi, alpha)
+                     for i in range(T)], dtype=np.int64)
+
+
+def _prefill_set_inclusive_mask(i, sink, vis=None):
+    S = np.arange(i + 1, dtype=np.int64)
+    return S if vis is None else S[(S < sink) | (S > vis)]
+
+
 MUTANTS = [
     ("dense_attention", _wrong_scale_dense),
     ("dense_attention", _lse_missing_max),
@@ -116,6 +126,8 @@ MUTANTS = [
     ("group_similar", _group_any_head),
     ("psaw_visible_start", _psaw_start_p_not_p_minus_1),
     ("psaw_boundary", _psaw_zero_based_layer),
+    ("psaw_prefill_visible", _prefill_vis_at_i),
+    ("prefill_visible_set", _prefill_set_inclusive_mask),
 ]
 
 

@@ -615,3 +615,74 @@ def test_psaw_schedule_is_the_cis_set_under_the_mask():
         if psaw[1] == 2:
             start = O.psaw_visible_start(3, 4, n + 6, 4, 2, 0.5, 1.0)
             assert start > 4 and not np.any((top >= 4) & (top < start))
+
+
+# ---------------------------------------------------------------- PSAW at prefill
+
+def _causal_matrix_form(Q, K, V, scale):
+    # the whole prompt at once: masked logit matrix, row softmax, one product
+    T = Q.shape[0]
+    Z = (Q @ K[:T].T) * scale
+    Z[np.triu_indices(T, 1)] = -np.inf
+    mx = Z.max(axis=1, keepdims=True)
+    E = np.exp(Z - mx)
+    den = E.sum(axis=1, keepdims=True)
+    return (E / den) @ V[:T], (mx + np.log(den)).ravel()
+
+
+def test_prefill_causal_matches_matrix_form():
+    rng = np.random.default_rng(71)
+    T, d = 37, 16
+    Q, K, V = (rng.standard_normal((T, d)) for _ in range(3))
+    y, lse = O.prefill_attention(Q, K, V, T)
+    y2, lse2 = _causal_matrix_form(Q, K, V, 1 / math.sqrt(d))
+    assert np.allclose(y, y2, atol=1e-12) and np.allclose(lse, lse2, atol=1e-12)
+    # below the pruning depth PSAW leaves the prompt causal
+    vis = O.psaw_prefill_visible(2, 8, T, 4, 6, 0.7, 1.0)
+    assert list(vis) == [min(4, i + 1) for i in range(T)]
+    y3, _ = O.prefill_attention(Q, K, V, T, sink=4, vis_start=vis)
+    assert np.allclose(y3, y2, atol=1e-12)
+
+
+def test_prefill_psaw_top_layer_and_monotone():
+    N, l_s, phi, alpha, sink = 32, 24, 0.7, 1.0, 4
+    vis = O.psaw_prefill_visible(N - 1, N, 500, sink, l_s, phi, alpha)
+    assert list(vis) == [max(min(sink, i + 1), math.floor(0.3 * (i + 1)) - 1) for i in range(500)]
+    for layer0 in range(l_s - 1, N):
+        v = O.psaw_prefill_visible(layer0, N, 300, sink, l_s, phi, alpha)
+        assert np.all(np.diff(v) >= 0)        # the window's start only moves forward
+
+
+def test_prefill_row_is_the_decode_set_at_its_length():
+    # query i of a prefill sees what a decode step at length i + 1 sees
+    N, l_s, phi, alpha, sink = 8, 5, 0.5, 1.5, 3
+    for layer0 in (4, 6, 7):
+        vis = O.psaw_prefill_visible(layer0, N, 60, sink, l_s, phi, alpha)
+        for i in range(60):
+            n = i + 1
+            start = O.psaw_visible_start(layer0, N, n, sink, l_s, phi, alpha)
+            assert np.array_equal(O.prefill_visible_set(i, sink, int(vis[i])),
+                                  O.psaw_restrict(np.arange(n), start, sink, n))
+            P = O.psaw_boundary(layer0 + 1, N, n, l_s, phi, alpha)
+            visible1 = [p for p in range(1, n + 1) if p <= sink or p >= P]
+            assert list(O.prefill_visible_set(i, sink, int(vis[i])) + 1) == visible1
+
+
+def test_prefill_psaw_rows_match_masked_matrix_form():
+    # the top layer of a small prompt: each row against the matrix form with
+    # the masked columns removed by hand
+    rng = np.random.default_rng(72)
+    T, d, sink = 50, 8, 2
+    Q, K, V = (rng.standard_normal((T, d)) for _ in range(3))
+    vis = O.psaw_prefill_visible(3, 4, T, sink, 2, 0.3, 1.0)
+    assert vis[-1] > sink
+    y, lse = O.prefill_attention(Q, K, V, T, sink=sink, vis_start=vis)
+    for i in range(T):
+        cols = [j for j in range(i + 1) if j < sink or j >= vis[i]]
+        z = (K[cols] @ Q[i]) / math.sqrt(d)
+        w = np.exp(z - z.max())
+        assert np.allclose(y[i], (w / w.sum()) @ V[cols], atol=1e-12)
+        assert abs(lse[i] - (z.max() + math.log(w.sum()))) < 1e-12
+    # rows past the prompt are empty
+    y4, lse4 = O.prefill_attention(Q, K, V, 20)
+    assert np.all(y4[20:] == 0) and np.all(np.isneginf(lse4[20:]))
