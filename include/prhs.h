@@ -242,6 +242,33 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
                                    float* out, float* lse, void* ws, size_t ws_bytes,
                                    void* stream);
 
+/* Causal prefill attention of the prompts under the progressive sliding
+ * attention window (Sec. 4.2, Eq. psaw: the window narrows during prefill as
+ * well as decoding).  For every (b, query head h) with g = h / (Hq/Hkv) and
+ * every query position i < min(seq_lens[b], q_len), the query at position i
+ * attends the keys
+ *   S_i = {p <= i : p < sink  or  p >= vis_start[i]}
+ * of kv head g (with vis_start NULL, S_i = [0, i]: plain causal attention);
+ * y_i = sum_{p in S_i} softmax(scale * q_i . k_p) v_p and lse_i as in
+ * prhs_sparse_decode_attn.  For a layer of a model with N layers, the
+ * window's first visible position at query i is Eq. psaw taken at
+ * t = i + 1 (the tokens in view), so vis_start[i] = max(min(sink, i + 1),
+ * P_l(i + 1) - 1) in 0-based positions.  Query rows at positions
+ * >= seq_lens[b] (and < q_len) give
+ * y = 0 and lse = -inf.
+ * kv:        contiguous bf16 cache holding the prompt of sequence b at
+ *            positions [0, seq_lens[b]) (paged caches and fp32 inputs give
+ *            PRHS_E_UNSUPPORTED).
+ * q:         [batch][num_q_heads][q_len][head_dim] bf16 device array; row i is
+ *            the query at position i.
+ * vis_start: [q_len] int32 device array or NULL.
+ * out:       [batch][num_q_heads][q_len][head_dim] fp32; lse:
+ *            [batch][num_q_heads][q_len] fp32 or NULL.
+ * No workspace.  Caller owns every buffer; batch * num_q_heads <= 65535. */
+prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
+                              const int32_t* vis_start, int32_t sink, float scale, float* out,
+                              float* lse, void* stream);
+
 /* Dense decode attention over every cached key [0, seq_lens[b]) (Eq. attn_eq):
  * the baseline the sparse path is measured against, and the k = n special
  * case.  Same outputs and conventions as prhs_sparse_decode_attn.

@@ -40,7 +40,7 @@ EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
     "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_select_gated",
-    "prhs_pool_decode_attn", "prhs_last_error",
+    "prhs_pool_decode_attn", "prhs_prefill_attn", "prhs_last_error",
 ]
 
 
@@ -119,6 +119,8 @@ def lib():
         L.prhs_pool_decode_attn.restype = i32
         L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, vp, i32,
                                             ctypes.c_float, vp, vp, vp, sz, vp]
+        L.prhs_prefill_attn.restype = i32
+        L.prhs_prefill_attn.argtypes = [P(PrhsKv), vp, i32, vp, i32, ctypes.c_float, vp, vp, vp]
         L.prhs_last_error.restype = ctypes.c_char_p
         L.prhs_last_error.argtypes = []
         _lib = L
@@ -368,6 +370,29 @@ def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale,
                                       rows, cap, _ptr(unit_row), _ptr(unit_tail),
                                       _ptr(psaw_start), int(psaw_sink), float(scale), _ptr(out),
                                       _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def prhs_prefill_attn(kv, q, scale, out, lse=None, vis_start=None, sink=0, stream=None):
+    """Causal prefill attention of the prompts (kv holds them; seq_lens are
+    their lengths) for the queries q [B][Hq][T][d] at positions 0 .. T - 1,
+    under the PSAW mask when vis_start [T] int32 is given."""
+    _need(q, kv.dtype, "q", 4)
+    B_, H_, T, d = q.shape
+    if (B_, H_, d) != (kv.c.batch, kv.c.num_q_heads, kv.c.head_dim):
+        raise ValueError(f"q must be [B][Hq][T][d], got {tuple(q.shape)}")
+    _need(out, torch.float32, "out", 4)
+    if tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    if lse is not None:
+        _need(lse, torch.float32, "lse", 3)
+        if tuple(lse.shape) != (B_, H_, T):
+            raise ValueError("lse must be [B][Hq][T]")
+    if vis_start is not None:
+        _need(vis_start, torch.int32, "vis_start", 1)
+        if vis_start.numel() != T:
+            raise ValueError("vis_start must have T entries")
+    check(lib().prhs_prefill_attn(ctypes.byref(kv.c), _ptr(q), int(T), _ptr(vis_start), int(sink),
+                                  float(scale), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def prhs_dense_decode_attn(kv, q, scale, out, lse, ws, stream=None):

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libprhs.so")
-SOURCES = ["prhs_api.hip", "select.hip", "dilate.hip", "attention.hip", "gate.hip"]
+SOURCES = ["prhs_api.hip", "select.hip", "dilate.hip", "attention.hip", "gate.hip", "prefill.hip"]
 
 ARCH = "gfx950"
 FLAGS = [

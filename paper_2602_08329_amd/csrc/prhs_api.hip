@@ -417,6 +417,35 @@ prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, 
   return device_status(prhs::launch_gate(a, (hipStream_t)stream), "prhs_gate launch");
 }
 
+prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
+                              const int32_t* vis_start, int32_t sink, float scale, float* out,
+                              float* lse, void* stream) {
+  prhs_status st = check_kv_shape(kv);
+  if (st != PRHS_OK) return st;
+  if ((st = check_kv_data(kv)) != PRHS_OK) return st;
+  if (kv->layout != PRHS_KV_CONTIGUOUS)
+    return fail(PRHS_E_UNSUPPORTED, "prefill attention needs a contiguous cache");
+  if (kv->dtype != PRHS_BF16)
+    return fail(PRHS_E_UNSUPPORTED, "prefill attention is built for bf16 inputs");
+  if (q_len < 0) return fail(PRHS_E_INVALID, "q_len must be >= 0 (got %d)", q_len);
+  if (sink < 0) return fail(PRHS_E_INVALID, "sink must be >= 0");
+  if (!(scale == scale)) return fail(PRHS_E_INVALID, "scale is NaN");
+  if ((long long)kv->batch * kv->num_q_heads > 65535)
+    return fail(PRHS_E_UNSUPPORTED, "batch * num_q_heads must be <= 65535");
+  if (kv->batch == 0 || q_len == 0) return PRHS_OK;
+  if (!q || !out) return fail(PRHS_E_INVALID, "q and out must be non-NULL");
+  prhs::PrefillLaunch a;
+  a.kv = view_of(kv);
+  a.q = q;
+  a.T = q_len;
+  a.vis_start = vis_start;
+  a.sink = sink;
+  a.scale = scale;
+  a.out = out;
+  a.lse = lse;
+  return device_status(prhs::launch_prefill(a, (hipStream_t)stream), "prhs_prefill_attn launch");
+}
+
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
   return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr, 0,

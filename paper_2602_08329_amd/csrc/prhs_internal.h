@@ -185,4 +185,16 @@ struct GateLaunch {
 };
 hipError_t launch_gate(const GateLaunch& a, hipStream_t stream);
 
+struct PrefillLaunch {
+  KvView kv;                  // contiguous bf16 cache holding the prompts
+  const void* q;              // [B][Hq][T][d]
+  int T;
+  const int32_t* vis_start;   // [T] or null
+  int sink;
+  float scale;
+  float* out;                 // [B][Hq][T][d]
+  float* lse;                 // [B][Hq][T] or null
+};
+hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
+
 }  // namespace prhs

@@ -38,6 +38,15 @@ def psaw_first_visible(layer, n_layers, n, sink, l_s, phi, alpha):
     return max(min(sink, n), P - 1)
 
 
+def psaw_prefill_visible(layer, n_layers, T, sink, l_s, phi, alpha, device="cuda"):
+    """First visible non-sink position of every query of a prefill of T
+    tokens at 0-based `layer` (int32 [T] on `device`, for prhs_prefill_attn):
+    the query at position i has the i + 1 tokens [0, i] in view, so Eq. psaw
+    is taken at n = i + 1."""
+    vis = [psaw_first_visible(layer, n_layers, i + 1, sink, l_s, phi, alpha) for i in range(T)]
+    return torch.tensor(vis, dtype=torch.int32, device=device)
+
+
 def psaw_defaults(n_layers):
     """Sec. 5.1: pruning from l_s = floor(3 N / 4), phi = 0.7, alpha = 1."""
     return (3 * n_layers) // 4, 0.7, 1.0
