@@ -218,6 +218,165 @@ def copy_calibration():
                       "gbps": round(2 * n / ms / 1e6, 1)}), flush=True)
 
 
+PREFILL_METRIC = ("prefill attention µs/layer + TFLOP/s (% of bf16 MFMA peak); "
+                  "PSAW speedup vs causal")
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_main(args):
+    """Prefill attention of every layer of a LLaMA-2-7B-shaped model (32
+    layers, 32 heads, d 128) over seeded synthetic prompts: the layers from
+    l_s on under the PSAW mask (Sec. 5.1 defaults, C_sink 16), the others
+    causal; timed against all layers causal.  A step is one pass over the 32
+    layers.  Flops counted are the useful ones: 4 d per (query, visible key)
+    pair per head (q.k and p.v)."""
+    import numpy as np
+    import torch
+
+    from paper_2602_08329_amd import binding as B
+    from paper_2602_08329_amd.schedule import capture_steps, psaw_defaults, psaw_prefill_visible
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    B.lib()
+    dev = torch.device("cuda:0")
+    L, H, d, sink = 32, 32, 128, 16
+    Bsz = args.batch or 1
+    T = args.nmax or 4096
+    K_steps, W_steps = args.steps, args.warmup
+    l_s, phi, alpha = psaw_defaults(L)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(4242 + T)
+    log(f"prefill: {L} layers, batch {Bsz}, {H} heads, d {d}, prompt {T}")
+    qs = [torch.randn(Bsz, H, T, d, generator=gen, device=dev).to(torch.bfloat16) for _ in range(L)]
+    Ks = [torch.randn(Bsz, H, T, d, generator=gen, device=dev).to(torch.bfloat16) for _ in range(L)]
+    Vs = [torch.randn(Bsz, H, T, d, generator=gen, device=dev).to(torch.bfloat16) for _ in range(L)]
+    seq = torch.full((Bsz,), T, dtype=torch.int32, device=dev)
+    kvs = [B.KV(Ks[l], Vs[l], seq, T, H) for l in range(L)]
+    vis = [psaw_prefill_visible(l, L, T, sink, l_s, phi, alpha, device=dev) if l + 1 >= l_s
+           else None for l in range(L)]
+    out = torch.empty(Bsz, H, T, d, device=dev)
+    lse = torch.empty(Bsz, H, T, device=dev)
+    scale = 1.0 / math.sqrt(d)
+
+    def step(psaw):
+        for l in range(L):
+            B.prhs_prefill_attn(kvs[l], qs[l], scale, out, lse,
+                                vis_start=vis[l] if psaw else None, sink=sink)
+
+    def timed(psaw, label):
+        for _ in range(W_steps):
+            step(psaw)
+        torch.cuda.synchronize()
+        graph = None if args.eager else capture_steps(lambda _j: step(psaw), range(K_steps))
+        if graph is not None:
+            graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        if graph is not None:
+            graph.replay()
+        else:
+            for _ in range(K_steps):
+                step(psaw)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        log(f"{label}: {ms / K_steps:.3f} ms/step")
+        del graph
+        return ms
+
+    ms_psaw = timed(True, "prefill, PSAW on layers >= l_s")
+    ms_causal = timed(False, "prefill, all layers causal")
+    # useful flops: visible (query, key) pairs x 4 d, per head and prompt
+    i = np.arange(T, dtype=np.int64)
+    pairs_causal = int((i + 1).sum())
+    pairs = 0
+    for l in range(L):
+        if vis[l] is None:
+            pairs += pairs_causal
+        else:
+            v = vis[l].cpu().numpy().astype(np.int64)
+            se = np.minimum(sink, i + 1)
+            pairs += int((se + (i + 1 - np.maximum(v, se))).sum())
+    flops = 4.0 * d * H * Bsz * pairs
+    flops_causal = 4.0 * d * H * Bsz * pairs_causal * L
+    us_layer = ms_psaw * 1e3 / (K_steps * L)
+    tflops = flops * K_steps / (ms_psaw * 1e-3) / 1e12
+    tflops_causal = flops_causal * K_steps / (ms_causal * 1e-3) / 1e12
+    result = {
+        "metric": PREFILL_METRIC,
+        "value": round(us_layer, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": K_steps,
+        "warmup": W_steps,
+        "ms_per_step": round(ms_psaw / K_steps, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"llama2-7b-prefill-b{Bsz}-{T}", "layers": L, "batch": Bsz,
+                   "heads": H, "head_dim": d, "prompt": T, "sink": sink,
+                   "psaw": {"l_s": l_s, "phi": phi, "alpha": alpha},
+                   "launch": "eager" if args.eager else "hip-graph replay"},
+        "causal_us_per_layer": round(ms_causal * 1e3 / (K_steps * L), 3),
+        "speedup_vs_causal": round(ms_causal / ms_psaw, 3),
+        "visible_pair_fraction": round(pairs / (pairs_causal * L), 4),
+        "roofline": {"kernel": "attn_prefill_bf16", "bound": "mfma", "achieved": round(tflops, 1),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "causal_achieved": round(tflops_causal, 1),
+                     "note": "useful flops (4 d per visible query-key pair and head) over the "
+                             "timed prefill; the kernel issues more (16-column tiles, the "
+                             "probabilities' low bf16 part)"},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = prefill_cpu_baseline(qs, Ks, Vs, vis, T, sink, scale, L, H, Bsz,
+                                                      args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def prefill_cpu_baseline(qs, Ks, Vs, vis, T, sink, scale, L, H, Bsz, budget_s):
+    """The oracle's prefill attention for one head of a causal layer and one
+    head of the top (pruning) layer, scaled to every head and layer (the
+    causal head stands for the layers below l_s, the top-layer head,
+    conservatively, for the pruning layers)."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+
+    rows = T
+    times = {}
+    with threadpool_limits(limits=1):
+        for name, l in (("causal", 0), ("psaw", L - 1)):
+            q = qs[l][0, 0].float().cpu().numpy()
+            K = Ks[l][0, 0].float().cpu().numpy()
+            V = Vs[l][0, 0].float().cpu().numpy()
+            v = None if vis[l] is None else vis[l].cpu().numpy()
+            # rows sampled evenly until the time budget is half spent
+            step = max(1, T // 256)
+            t0 = time.perf_counter()
+            done = 0
+            for i in range(T - 1, -1, -step):
+                S = O.prefill_visible_set(i, sink, None if v is None else int(v[i]))
+                O.sparse_attention(q[i], K[: i + 1], V[: i + 1], S, scale)
+                done += 1
+                if time.perf_counter() - t0 > budget_s / 2:
+                    break
+            dt = time.perf_counter() - t0
+            times[name] = dt / done * rows   # per head, all rows
+    n_psaw = sum(1 for x in vis if x is not None)
+    per_step = (times["causal"] * (L - n_psaw) + times["psaw"] * n_psaw) * H * Bsz
+    return {"value": round(per_step * 1e6 / L, 1), "unit": "us/layer", "cores": 1,
+            "kind": "oracle", "cpu": platform.machine(),
+            "sample": f"every {max(1, T // 256)}-th query row (from the last) of head 0 of layer 0 "
+                      f"(causal) and layer {L - 1} (PSAW), scaled to {H} heads x {L} layers"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -239,6 +398,9 @@ def main():
                          "fixed refresh period (blocks of refresh_every steps)")
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches instead of replays of a captured HIP graph")
+    ap.add_argument("--prefill", action="store_true",
+                    help="prefill attention under the PSAW mask instead of the decode step "
+                         "(LLaMA-2-7B shape; --nmax prompt length, --batch prompts)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -250,6 +412,9 @@ def main():
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the hot path has no multi-GPU mode)", file=sys.stderr)
         sys.exit(2)
+    if args.prefill:
+        prefill_main(args)
+        return
 
     import torch
 

@@ -8,11 +8,13 @@
 // head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the 16
 // columns of its MFMA tiles, so a wave owns its queries' whole softmax and
 // writes their outputs itself.  Key tiles of 32 rows are loaded once per
-// workgroup (whole rows, streaming cache policy) into LDS, double-buffered,
-// and every wave computes
+// workgroup (whole rows, streaming cache policy) into two LDS buffers -- K
+// row-major, V transposed so that each MFMA operand is one 16-byte read --
+// the loads of a tile issued two tiles ahead of its use, and every wave computes
 //   S^T (32 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, two 16-row halves)
 //   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts)
-// with an online softmax per query.  A block visits only the key tiles that
+// with an online softmax per query.  Tiles that every
+// query of a wave sees whole skip the per-element mask.  A block visits only the key tiles that
 // meet its queries' visible ranges -- the sink [0, C_sink) and the band from
 // the smallest vis_start of its queries to its last query -- so tiles that
 // PSAW masks for every query of the block are never loaded: that is the
@@ -40,11 +42,6 @@ struct PrefillArgs {
   float* out;             // [B][Hq][T][D]
   float* lse;             // [B][Hq][T] or null
 };
-
-__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
 
 // K tile in LDS: 16-byte chunk c of tile row r at slot c ^ (r mod D/8), so
 // the whole-row writes and the MFMA-order reads (16 rows, one chunk each)
@@ -78,15 +75,116 @@ __device__ __forceinline__ void tile_load(TileRegs<D>& R, const __bf16* kb, cons
   }
 }
 
+// V tile in LDS, transposed: row `dim` holds the tile's 32 values of that
+// dim in the key order of the probabilities (key 16s + 4g + e at position
+// 8g + 4s + e, so a lane's 8 keys are one 16-byte block), the block index
+// XOR-swizzled by (dim >> 2) & 3 so that the operand reads (16 dims, one
+// block each) hit distinct banks.  64 bytes per dim.
+__device__ __forceinline__ int vt_pos(int key) {
+  return 8 * ((key & 15) >> 2) + 4 * (key >> 4) + (key & 3);
+}
+__device__ __forceinline__ int vt_byte(int dim, int pos) {
+  return dim * 64 + 16 * ((pos >> 3) ^ ((dim >> 2) & 3)) + 2 * (pos & 7);
+}
+
 template <int D>
 __device__ __forceinline__ void tile_store(const TileRegs<D>& R, u32x4_t* sk, u32x4_t* sv) {
   constexpr int CH = D / 8;
+  unsigned char* vt = (unsigned char*)sv;
 #pragma unroll
   for (int j = 0; j < TileRegs<D>::RPL; ++j) {
     const int e = (int)threadIdx.x + j * 256;
     const int r = e / CH, c = e % CH;
     sk[k_slot<D>(r, c)] = R.k[j];
-    sv[e] = R.v[j];  // row-major: row r, chunk c
+    const int pos = vt_pos(r);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = R.v[j][w];  // dims 8c + 2w (low half) and 8c + 2w + 1
+      *(uint16_t*)(vt + vt_byte(8 * c + 2 * w, pos)) = (uint16_t)(x & 0xFFFFu);
+      *(uint16_t*)(vt + vt_byte(8 * c + 2 * w + 1, pos)) = (uint16_t)(x >> 16);
+    }
+  }
+}
+
+// One key tile against one wave's 16 queries: S^T, the per-(key, query)
+// mask, the online softmax and O^T += V^T P^T (as in the decode kernel, with
+// the query positions in the columns).
+template <int D>
+__device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* svx, int ks,
+                                             const bf16x8_t* qf, int qi, bool qvalid, int my_vis,
+                                             int sink, float scale_log2, bool full, float& m_run,
+                                             float& l_run, f32x4_t* o) {
+  constexpr int KS = D / 32;
+  constexpr int DB = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  // S^T for this wave's 16 queries: lane (col, grp) gets keys ks + 16s + 4grp + e
+  float x[2][4];
+  float mt = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, sk[k_slot<D>(16 * s + col, 4 * kk + grp)]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
+    }
+    // the MFMA output row is the key, the column the query: lane (col,
+    // grp) holds query col of its wave for keys 4 grp + e of half s
+    if (full) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[s][e] = acc[e] * scale_log2;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int p = ks + 16 * s + 4 * grp + e;
+        const bool vis = qvalid && p <= qi && (p < sink || p >= my_vis);
+        x[s][e] = vis ? acc[e] * scale_log2 : -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mt = fmaxf(mt, x[s][e]);
+  }
+  mt = fmaxf(mt, __shfl_xor(mt, 16));
+  mt = fmaxf(mt, __shfl_xor(mt, 32));
+  const float m_new = fmaxf(m_run, mt);
+  {
+    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
+  }
+  float psum = 0.f;
+  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+  if (m_run != -INFINITY) {
+    uint32_t hb[8], lb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float pr = __builtin_amdgcn_exp2f(x[j >> 2][j & 3] - m_run);
+      psum += pr;
+      const __bf16 h = (__bf16)pr;
+      hb[j] = __builtin_bit_cast(uint16_t, h);
+      lb[j] = __builtin_bit_cast(uint16_t, (__bf16)(pr - (float)h));
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
+      lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+    }
+  }
+  l_run += psum;
+  const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+  const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+  // V^T operand of product blk: lane (col, grp) takes dim 16 blk + col, its
+  // 8 keys (the keys of its probabilities) as one 16-byte block
+  const unsigned char* vt = (const unsigned char*)svx;
+#pragma unroll
+  for (int blk = 0; blk < DB; ++blk) {
+    const int dim = 16 * blk + col;
+    const bf16x8_t av = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vt + vt_byte(dim, 8 * grp)));
+    o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
+    o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
   }
 }
 
@@ -136,6 +234,14 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
   // this lane's query and its first visible non-sink position
   const bool qvalid = qi <= qlast;
   const int my_vis = (a.vis && qvalid) ? a.vis[qi] : 0;
+  // a tile needs no mask for this wave when all 16 of its queries lie in
+  // the prompt, the tile ends at or before the first of them, and it lies
+  // inside the sink or at or past the largest of their vis_start
+  const int qw0 = q0 + 16 * wave;
+  const bool wave_all = qw0 + 15 <= qlast;
+  int wvis = my_vis;
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) wvis = max(wvis, __shfl_xor(wvis, off));
   bf16x8_t qf[KS];
   {
     const __bf16* qp = a.q + (qrow + (qvalid ? qi : q0)) * D + grp * 8;
@@ -156,106 +262,40 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  TileRegs<D> R;
+  // two tiles in flight: tile t + 2 loads while tile t is multiplied
+  TileRegs<D> RA, RB;
   auto tile_start = [&](int t) { return (t < nsink ? t : tb0 + (t - nsink)) * kKTile; };
-  if (ntiles > 0) tile_load<D>(R, kb, vb, row0, tile_start(0), n);
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int ks = tile_start(t);
-    tile_store<D>(R, s_k[buf], s_v[buf]);
+  auto full_tile = [&](int ks) {
+    return wave_all && ks + kKTile - 1 <= qw0 && (ks + kKTile <= a.sink || ks >= wvis);
+  };
+  if (ntiles > 0) tile_load<D>(RA, kb, vb, row0, tile_start(0), n);
+  if (ntiles > 0) tile_load<D>(RB, kb, vb, row0, tile_start(min(1, ntiles - 1)), n);
+  for (int t = 0; t < ntiles; t += 2) {
+    tile_store<D>(RA, s_k[0], s_v[0]);
     __syncthreads();
-    if (t + 1 < ntiles) tile_load<D>(R, kb, vb, row0, tile_start(t + 1), n);
-    // S^T for this wave's 16 queries: lane (col, grp) gets keys ks + 16s + 4grp + e
-    float x[2][4];
-    float mt = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, s_k[buf][k_slot<D>(16 * s + col, 4 * kk + grp)]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int p = ks + 16 * s + 4 * grp + e;
-        // the MFMA output row is the key, the column the query: lane (col,
-        // grp) holds query col of its wave for keys 4 grp + e of half s
-        const bool vis = qvalid && p <= qi && (p < a.sink || p >= my_vis);
-        x[s][e] = vis ? acc[e] * a.scale_log2 : -INFINITY;
-        mt = fmaxf(mt, x[s][e]);
-      }
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    float alpha = 1.f, psum = 0.f;
-    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
-    if (m_new != -INFINITY) {
-      alpha = exp2f(m_run - m_new);
-      uint32_t hb[8], lb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float pr = exp2f(x[j >> 2][j & 3] - m_new);
-        psum += pr;
-        hb[j] = bf16_bits_rne(pr);
-        lb[j] = bf16_bits_rne(pr - __uint_as_float(hb[j] << 16));
-      }
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
-        lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
-      }
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-    const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-    // V operand: lane (col, grp) takes dims col DB .. col DB + DB - 1 of the
-    // 8 rows 16s + 4grp + j, the rows of its probabilities
-    const uint32_t* sv = (const uint32_t*)s_v[buf];
-    uint32_t vw[2][4][DB / 2];
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int w = 0; w < DB / 2; ++w)
-          vw[s][j][w] = sv[((16 * s + 4 * grp + j) * D + col * DB) / 2 + w];
-#pragma unroll
-    for (int blk = 0; blk < DB; ++blk) {
-      o[blk] *= alpha;
-      uint32_t aw[4];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const int j0 = 2 * w, j1 = 2 * w + 1;
-        const uint32_t e0 = vw[j0 >> 2][j0 & 3][blk >> 1], e1 = vw[j1 >> 2][j1 & 3][blk >> 1];
-        const uint32_t v0 = (blk & 1) ? (e0 >> 16) : (e0 & 0xFFFFu);
-        const uint32_t v1 = (blk & 1) ? (e1 >> 16) : (e1 & 0xFFFFu);
-        aw[w] = v0 | (v1 << 16);
-      }
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
-      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
-      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
-    }
+    // unconditional (past the last tile it reloads the last one), so that
+    // the wait before a store counts only the loads of the older tile
+    tile_load<D>(RA, kb, vb, row0, tile_start(min(t + 2, ntiles - 1)), n);
+    prefill_tile<D>(s_k[0], s_v[0], tile_start(t), qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
+                    full_tile(tile_start(t)), m_run, l_run, o);
+    if (t + 1 >= ntiles) break;
+    tile_store<D>(RB, s_k[1], s_v[1]);
+    __syncthreads();
+    tile_load<D>(RB, kb, vb, row0, tile_start(min(t + 3, ntiles - 1)), n);
+    prefill_tile<D>(s_k[1], s_v[1], tile_start(t + 1), qf, qi, qvalid, my_vis, a.sink,
+                    a.scale_log2, full_tile(tile_start(t + 1)), m_run, l_run, o);
   }
 
-  // lane (col, grp) holds dims (4 grp + i) DB + blk of query col
+  // lane (col, grp) holds dims 16 blk + 4 grp .. 16 blk + 4 grp + 3 of query col
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   if (qi < a.T) {
-    float* op = a.out + (qrow + qi) * D;
+    float* op = a.out + (qrow + qi) * D + 4 * grp;
     const float inv = (qvalid && l_run > 0.f) ? 1.f / l_run : 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float v[DB];
-#pragma unroll
-      for (int blk = 0; blk < DB; ++blk) v[blk] = o[blk][i] * inv;
-      float* dst = op + (grp * 4 + i) * DB;
-#pragma unroll
-      for (int blk = 0; blk < DB; blk += 4)
-        *(float4*)(dst + blk) = make_float4(v[blk], v[blk + 1], v[blk + 2], v[blk + 3]);
-    }
+    for (int blk = 0; blk < DB; ++blk)
+      *(float4*)(op + 16 * blk) =
+          make_float4(o[blk][0] * inv, o[blk][1] * inv, o[blk][2] * inv, o[blk][3] * inv);
     if (a.lse && grp == 0)
       a.lse[qrow + qi] = (qvalid && l_run > 0.f) ? (m_run + log2f(l_run)) * kLn2 : -INFINITY;
   }
