@@ -264,7 +264,8 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
  * vis_start: [q_len] int32 device array or NULL.
  * out:       [batch][num_q_heads][q_len][head_dim] fp32; lse:
  *            [batch][num_q_heads][q_len] fp32 or NULL.
- * No workspace.  Caller owns every buffer; batch * num_q_heads <= 65535. */
+ * No workspace.  Caller owns every buffer; ceil(q_len / 64) * batch * num_q_heads
+ * must be below 2^31 (PRHS_E_UNSUPPORTED otherwise). */
 prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
                               const int32_t* vis_start, int32_t sink, float scale, float* out,
                               float* lse, void* stream);

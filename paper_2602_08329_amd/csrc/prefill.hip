@@ -19,7 +19,8 @@
 // the smallest vis_start of its queries to its last query -- so tiles that
 // PSAW masks for every query of the block are never loaded: that is the
 // prefill work PSAW saves.  Inside a tile the mask is per (key, query).
-// Blocks are issued longest first (the last query blocks see the most keys).
+// Blocks are ordered per XCD: each XCD takes whole (batch, head) units, a
+// unit's query blocks longest first (the last blocks see the most keys).
 #include "prhs_internal.h"
 
 namespace prhs {
@@ -30,6 +31,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kQBlock = 64;   // query positions per workgroup (4 waves x 16)
 constexpr int kKTile = 32;    // key rows per tile
+constexpr int kXcds = 8;      // accelerator dies, each with its own L2
 constexpr float kLn2 = 0.69314718055994530942f;
 
 struct PrefillArgs {
@@ -196,8 +198,15 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
   __shared__ u32x4_t s_k[2][kKTile * CH];
   __shared__ u32x4_t s_v[2][kKTile * CH];
   __shared__ int s_vmin;
-  const int qb = (int)gridDim.x - 1 - (int)blockIdx.x;  // longest blocks first
-  const int bh = blockIdx.y;
+  // Workgroups go to the 8 XCDs round-robin by id; id L runs unit-major
+  // slot (L mod 8) * (N / 8) + L / 8, so that each XCD works through its
+  // own (batch, head) units one after another and a unit's K and V stay in
+  // that XCD's L2.  Within a unit the longest query blocks come first.
+  const int nqb = (a.T + kQBlock - 1) / kQBlock;
+  const int N = (int)gridDim.x, L = (int)blockIdx.x;
+  const int M = (N % kXcds == 0) ? (L % kXcds) * (N / kXcds) + L / kXcds : L;
+  const int bh = M / nqb;
+  const int qb = nqb - 1 - M % nqb;
   const int hq = a.kv.hq, G = hq / a.kv.hkv;
   const int b = bh / hq, h = bh % hq, g = h / G;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -314,7 +323,7 @@ hipError_t launch_prefill(const PrefillLaunch& s, hipStream_t stream) {
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   a.out = s.out;
   a.lse = s.lse;
-  const dim3 grid((s.T + kQBlock - 1) / kQBlock, s.kv.batch * s.kv.hq);
+  const dim3 grid(((s.T + kQBlock - 1) / kQBlock) * s.kv.batch * s.kv.hq);
   if (s.kv.d == 128)
     hipLaunchKernelGGL(attn_prefill_bf16<128>, grid, dim3(256), 0, stream, a);
   else
