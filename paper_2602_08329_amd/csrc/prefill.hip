@@ -4,21 +4,22 @@
 // attends the keys p <= i with p < C_sink or p >= vis_start[i]; without
 // vis_start every p <= i (plain causal attention, Eq. attn_eq per position).
 //
-// attn_prefill_bf16<D>: one workgroup per (64 query positions, batch, query
-// head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the 16
-// columns of its MFMA tiles, so a wave owns its queries' whole softmax and
-// writes their outputs itself.  Key tiles of 32 rows are loaded once per
-// workgroup (whole rows, streaming cache policy) into two LDS buffers -- K
-// row-major, V transposed so that each MFMA operand is one 16-byte read --
-// the loads of a tile issued two tiles ahead of its use, and every wave computes
-//   S^T (32 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, two 16-row halves)
-//   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts)
-// with an online softmax per query.  Tiles that every
-// query of a wave sees whole skip the per-element mask.  A block visits only the key tiles that
+// attn_prefill_bf16<D>: one workgroup per (192 query positions, batch,
+// query head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the
+// 16 columns of its MFMA tiles, so a wave owns its queries' whole softmax
+// and writes their outputs itself.  Key tiles of 64 rows are loaded once
+// per workgroup (whole rows, streaming cache policy, one tile ahead of its
+// use) into two LDS buffers -- K row-major, V transposed so that each MFMA
+// operand is one 16-byte read -- and every wave computes
+//   S^T (64 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, four 16-row blocks)
+//   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts, 32 keys per product)
+// with an online softmax per query.  A block visits only the key tiles that
 // meet its queries' visible ranges -- the sink [0, C_sink) and the band from
 // the smallest vis_start of its queries to its last query -- so tiles that
 // PSAW masks for every query of the block are never loaded: that is the
-// prefill work PSAW saves.  Inside a tile the mask is per (key, query).
+// prefill work PSAW saves.  Inside the block a wave skips the tiles masked
+// for all of its queries and takes the per-(key, query) mask only on tiles
+// that some of its queries see in part.
 // Blocks are ordered per XCD: each XCD takes whole (batch, head) units, a
 // unit's query blocks longest first (the last blocks see the most keys).
 #include "prhs_internal.h"
@@ -29,8 +30,10 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kQBlock = 64;   // query positions per workgroup (4 waves x 16)
-constexpr int kKTile = 32;    // key rows per tile
+constexpr int kQBlock = 192;  // query positions per workgroup (16 per wave, 12 waves)
+constexpr int kThreads = kQBlock / 16 * 64;
+constexpr int kKTile = 64;    // key rows per tile
+static_assert(kKTile % 32 == 0, "a tile is whole 32-key sub-tiles");
 constexpr int kXcds = 8;      // accelerator dies, each with its own L2
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -54,11 +57,12 @@ __device__ __forceinline__ int k_slot(int r, int c) {
   return r * CH + (c ^ (r & (CH - 1)));
 }
 
-// Whole-row loads of tile rows [ks, ks + 32): each thread takes RPL 16-byte
-// chunks of K and of V.  Rows at or past n (the prompt) read row n - 1.
+// Whole-row loads of tile rows [ks, ks + kKTile): each thread takes up to
+// RPL 16-byte chunks of K and of V (threads past the tile's chunks take none).
+// Rows at or past n (the prompt) read row n - 1.
 template <int D>
 struct TileRegs {
-  static constexpr int RPL = kKTile * (D / 8) / 256;  // chunks per thread
+  static constexpr int RPL = (kKTile * (D / 8) + kThreads - 1) / kThreads;  // chunks per thread
   u32x4_t k[RPL], v[RPL];
 };
 
@@ -68,7 +72,8 @@ __device__ __forceinline__ void tile_load(TileRegs<D>& R, const __bf16* kb, cons
   constexpr int CH = D / 8;
 #pragma unroll
   for (int j = 0; j < TileRegs<D>::RPL; ++j) {
-    const int e = (int)threadIdx.x + j * 256;
+    const int e = (int)threadIdx.x + j * kThreads;
+    if (e >= kKTile * CH) break;
     const int r = e / CH, c = e % CH;
     const int p = min(ks + r, n - 1);
     const int64_t off = (unit_row0 + p) * D + c * 8;
@@ -77,11 +82,12 @@ __device__ __forceinline__ void tile_load(TileRegs<D>& R, const __bf16* kb, cons
   }
 }
 
-// V tile in LDS, transposed: row `dim` holds the tile's 32 values of that
-// dim in the key order of the probabilities (key 16s + 4g + e at position
+// V tile in LDS, transposed, as kKTile / 32 sub-tiles of 32 keys (D x 64
+// bytes each): row `dim` of a sub-tile holds its 32 values of that dim in
+// the key order of the probabilities (key 16s + 4g + e at position
 // 8g + 4s + e, so a lane's 8 keys are one 16-byte block), the block index
 // XOR-swizzled by (dim >> 2) & 3 so that the operand reads (16 dims, one
-// block each) hit distinct banks.  64 bytes per dim.
+// block each) hit distinct banks.
 __device__ __forceinline__ int vt_pos(int key) {
   return 8 * ((key & 15) >> 2) + 4 * (key >> 4) + (key & 3);
 }
@@ -95,15 +101,17 @@ __device__ __forceinline__ void tile_store(const TileRegs<D>& R, u32x4_t* sk, u3
   unsigned char* vt = (unsigned char*)sv;
 #pragma unroll
   for (int j = 0; j < TileRegs<D>::RPL; ++j) {
-    const int e = (int)threadIdx.x + j * 256;
+    const int e = (int)threadIdx.x + j * kThreads;
+    if (e >= kKTile * CH) break;
     const int r = e / CH, c = e % CH;
     sk[k_slot<D>(r, c)] = R.k[j];
-    const int pos = vt_pos(r);
+    unsigned char* vts = vt + (r >> 5) * (D * 64);
+    const int pos = vt_pos(r & 31);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const uint32_t x = R.v[j][w];  // dims 8c + 2w (low half) and 8c + 2w + 1
-      *(uint16_t*)(vt + vt_byte(8 * c + 2 * w, pos)) = (uint16_t)(x & 0xFFFFu);
-      *(uint16_t*)(vt + vt_byte(8 * c + 2 * w + 1, pos)) = (uint16_t)(x >> 16);
+      *(uint16_t*)(vts + vt_byte(8 * c + 2 * w, pos)) = (uint16_t)(x & 0xFFFFu);
+      *(uint16_t*)(vts + vt_byte(8 * c + 2 * w + 1, pos)) = (uint16_t)(x >> 16);
     }
   }
 }
@@ -116,15 +124,16 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
                                              const bf16x8_t* qf, int qi, bool qvalid, int my_vis,
                                              int sink, float scale_log2, bool full, float& m_run,
                                              float& l_run, f32x4_t* o) {
-  constexpr int KS = D / 32;
-  constexpr int DB = D / 16;
+  constexpr int KS = D / 32;       // products per 16-key block of S
+  constexpr int DB = D / 16;       // 16-dim blocks of O^T
+  constexpr int NB = kKTile / 16;  // 16-key blocks of the tile
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   // S^T for this wave's 16 queries: lane (col, grp) gets keys ks + 16s + 4grp + e
-  float x[2][4];
+  float x[NB][4];
   float mt = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < NB; ++s) {
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
@@ -132,7 +141,7 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
     }
     // the MFMA output row is the key, the column the query: lane (col,
-    // grp) holds query col of its wave for keys 4 grp + e of half s
+    // grp) holds query col of its wave for keys 4 grp + e of block s
     if (full) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) x[s][e] = acc[e] * scale_log2;
@@ -150,49 +159,54 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   mt = fmaxf(mt, __shfl_xor(mt, 16));
   mt = fmaxf(mt, __shfl_xor(mt, 32));
   const float m_new = fmaxf(m_run, mt);
-  {
-    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+  const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+  m_run = m_new;
+  l_run *= alpha;
 #pragma unroll
-    for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
-  }
+  for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
+  // per 32-key sub-tile u: P^T as bf16 hi + lo parts (lane (col, grp)
+  // holds keys 32u + 16h + 4 grp + e, h = 0, 1), then the V^T products
+  const unsigned char* vt = (const unsigned char*)svx;
   float psum = 0.f;
-  uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
-  if (m_run != -INFINITY) {
-    uint32_t hb[8], lb[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float pr = __builtin_amdgcn_exp2f(x[j >> 2][j & 3] - m_run);
-      psum += pr;
-      const __bf16 h = (__bf16)pr;
-      hb[j] = __builtin_bit_cast(uint16_t, h);
-      lb[j] = __builtin_bit_cast(uint16_t, (__bf16)(pr - (float)h));
+  for (int u = 0; u < NB / 2; ++u) {
+    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
+    if (m_run != -INFINITY) {
+      uint32_t hb[8], lb[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float pr = __builtin_amdgcn_exp2f(x[2 * u + (j >> 2)][j & 3] - m_run);
+        psum += pr;
+        const __bf16 h = (__bf16)pr;
+        hb[j] = __builtin_bit_cast(uint16_t, h);
+        lb[j] = __builtin_bit_cast(uint16_t, (__bf16)(pr - (float)h));
+      }
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
+        lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+      }
     }
+    const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+    const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+    // V^T operand of product blk: lane (col, grp) takes dim 16 blk + col, its
+    // 8 keys (the keys of its probabilities) as one 16-byte block
+    const unsigned char* vts = vt + u * (D * 64);
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
-      lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+    for (int blk = 0; blk < DB; ++blk) {
+      const int dim = 16 * blk + col;
+      const bf16x8_t av =
+          __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vts + vt_byte(dim, 8 * grp)));
+      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
+      o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
     }
   }
   l_run += psum;
-  const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-  const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-  // V^T operand of product blk: lane (col, grp) takes dim 16 blk + col, its
-  // 8 keys (the keys of its probabilities) as one 16-byte block
-  const unsigned char* vt = (const unsigned char*)svx;
-#pragma unroll
-  for (int blk = 0; blk < DB; ++blk) {
-    const int dim = 16 * blk + col;
-    const bf16x8_t av = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vt + vt_byte(dim, 8 * grp)));
-    o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
-    o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
-  }
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
-  constexpr int KS = D / 32;   // products per 16-key half of S
+__global__ __launch_bounds__(kThreads) void attn_prefill_bf16(PrefillArgs a) {
+  constexpr int KS = D / 32;   // products per 16-key block of S
   constexpr int DB = D / 16;   // output blocks of 16 dims per lane group
   constexpr int CH = D / 8;    // 16-byte chunks per row
   __shared__ u32x4_t s_k[2][kKTile * CH];
@@ -218,12 +232,12 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
   const int qlast = min(q0 + kQBlock, n) - 1;      // last query of the block inside the prompt
 
   if (qlast < q0) {  // the whole block lies past the prompt: empty rows
-    for (int e = tid; e < kQBlock * D; e += 256) {
+    for (int e = tid; e < kQBlock * D; e += kThreads) {
       const int i = q0 + e / D;
       if (i < a.T) a.out[(qrow + i) * D + e % D] = 0.f;
     }
     if (a.lse)
-      for (int i = q0 + tid; i < min(q0 + kQBlock, a.T); i += 256) a.lse[qrow + i] = -INFINITY;
+      for (int i = q0 + tid; i < min(q0 + kQBlock, a.T); i += kThreads) a.lse[qrow + i] = -INFINITY;
     return;
   }
 
@@ -233,8 +247,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
   if (wave == 0) {
     int v = sink_end;
     if (a.vis) {
-      const int i = q0 + lane;
-      v = i <= qlast ? a.vis[i] : 0x7FFFFFFF;
+      v = 0x7FFFFFFF;
+      for (int i = q0 + lane; i <= qlast; i += 64) v = min(v, a.vis[i]);
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off));
     }
@@ -248,9 +262,16 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
   // inside the sink or at or past the largest of their vis_start
   const int qw0 = q0 + 16 * wave;
   const bool wave_all = qw0 + 15 <= qlast;
-  int wvis = my_vis;
+  int wvis = my_vis, wvmin = qvalid ? my_vis : 0x7FFFFFFF;
 #pragma unroll
-  for (int off = 1; off < 16; off <<= 1) wvis = max(wvis, __shfl_xor(wvis, off));
+  for (int off = 1; off < 16; off <<= 1) {
+    wvis = max(wvis, __shfl_xor(wvis, off));
+    wvmin = min(wvmin, __shfl_xor(wvmin, off));
+  }
+  // and it needs no work at all when it lies past the wave's last query or
+  // between the sink and the smallest of their vis_start (every product
+  // would be masked; skipping leaves O, m and l exactly as they are)
+  const int wlast = min(qw0 + 15, qlast);
   bf16x8_t qf[KS];
   {
     const __bf16* qp = a.q + (qrow + (qvalid ? qi : q0)) * D + grp * 8;
@@ -271,28 +292,23 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(PrefillArgs a) {
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // two tiles in flight: tile t + 2 loads while tile t is multiplied
-  TileRegs<D> RA, RB;
+  TileRegs<D> R;
   auto tile_start = [&](int t) { return (t < nsink ? t : tb0 + (t - nsink)) * kKTile; };
   auto full_tile = [&](int ks) {
     return wave_all && ks + kKTile - 1 <= qw0 && (ks + kKTile <= a.sink || ks >= wvis);
   };
-  if (ntiles > 0) tile_load<D>(RA, kb, vb, row0, tile_start(0), n);
-  if (ntiles > 0) tile_load<D>(RB, kb, vb, row0, tile_start(min(1, ntiles - 1)), n);
-  for (int t = 0; t < ntiles; t += 2) {
-    tile_store<D>(RA, s_k[0], s_v[0]);
+  auto masked_tile = [&](int ks) {
+    return ks > wlast || (ks >= a.sink && ks + kKTile - 1 < wvmin);
+  };
+  if (ntiles > 0) tile_load<D>(R, kb, vb, row0, tile_start(0), n);
+  for (int t = 0; t < ntiles; ++t) {
+    tile_store<D>(R, s_k[t & 1], s_v[t & 1]);
     __syncthreads();
-    // unconditional (past the last tile it reloads the last one), so that
-    // the wait before a store counts only the loads of the older tile
-    tile_load<D>(RA, kb, vb, row0, tile_start(min(t + 2, ntiles - 1)), n);
-    prefill_tile<D>(s_k[0], s_v[0], tile_start(t), qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
-                    full_tile(tile_start(t)), m_run, l_run, o);
-    if (t + 1 >= ntiles) break;
-    tile_store<D>(RB, s_k[1], s_v[1]);
-    __syncthreads();
-    tile_load<D>(RB, kb, vb, row0, tile_start(min(t + 3, ntiles - 1)), n);
-    prefill_tile<D>(s_k[1], s_v[1], tile_start(t + 1), qf, qi, qvalid, my_vis, a.sink,
-                    a.scale_log2, full_tile(tile_start(t + 1)), m_run, l_run, o);
+    tile_load<D>(R, kb, vb, row0, tile_start(min(t + 1, ntiles - 1)), n);
+    const int ks = tile_start(t);
+    if (!masked_tile(ks))
+      prefill_tile<D>(s_k[t & 1], s_v[t & 1], ks, qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
+                      full_tile(ks), m_run, l_run, o);
   }
 
   // lane (col, grp) holds dims 16 blk + 4 grp .. 16 blk + 4 grp + 3 of query col
@@ -325,9 +341,9 @@ hipError_t launch_prefill(const PrefillLaunch& s, hipStream_t stream) {
   a.lse = s.lse;
   const dim3 grid(((s.T + kQBlock - 1) / kQBlock) * s.kv.batch * s.kv.hq);
   if (s.kv.d == 128)
-    hipLaunchKernelGGL(attn_prefill_bf16<128>, grid, dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(attn_prefill_bf16<128>, grid, dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_prefill_bf16<64>, grid, dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(attn_prefill_bf16<64>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 

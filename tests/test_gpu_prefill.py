@@ -116,7 +116,7 @@ def test_prefill_query_span_shorter_than_prompt():
                 seed=9)
 
 
-@pytest.mark.parametrize("T,sink", [(1, 4), (64, 0), (65, 1), (33, 40)])
+@pytest.mark.parametrize("T,sink", [(1, 4), (64, 0), (65, 1), (33, 40), (192, 3), (193, 70)])
 def test_prefill_small_and_block_edges(T, sink):
     run_prefill(1, 2, 1, 128, (T,), T, psaw=(1, 0.2, 1.0), layer=1, n_layers=2, sink=sink,
                 seed=11 + T)
