@@ -174,14 +174,14 @@ def cpu_baseline(run, budget_s):
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
-def committed_traffic(workload):
-    """HBM bytes per sparse-attention launch measured with rocprofv3 counters
+def committed_traffic(profile, source):
+    """HBM bytes per launch of a kernel measured with rocprofv3 counters
     (FETCH_SIZE and WRITE_SIZE, scaled by a plain-copy calibration) and
-    recorded in profiles/; None when there is no record for this workload or
-    the attention kernel source changed since it was taken."""
+    recorded in profiles/<profile>; None when there is no record or the
+    kernel's source file (csrc/<source>) changed since it was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"attn_split_bf16_{workload}_pmc.md")
-    src = os.path.join(ROOT, "paper_2602_08329_amd", "csrc", "attention.hip")
+    path = os.path.join(ROOT, "profiles", profile)
+    src = os.path.join(ROOT, "paper_2602_08329_amd", "csrc", source)
     if not os.path.exists(path) or not os.path.exists(src):
         return None
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
@@ -190,7 +190,7 @@ def committed_traffic(workload):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    if fields.get("attention.hip sha256") != digest:
+    if fields.get(f"{source} sha256") != digest:
         return None
     try:
         return int(fields["traffic bytes per launch"])
@@ -327,7 +327,9 @@ def prefill_main(args):
         "visible_pair_fraction": round(pairs / (pairs_causal * L), 4),
         "roofline": {"kernel": "attn_prefill_bf16", "bound": "mfma", "achieved": round(tflops, 1),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": committed_traffic(f"attn_prefill_bf16_llama2-7b-prefill-b{Bsz}-{T}.md",
+                                                  "prefill.hip"),
                      "causal_achieved": round(tflops_causal, 1),
                      "note": "useful flops (4 d per visible query-key pair and head) over the "
                              "timed prefill; the kernel issues more (16-column tiles, the "
@@ -528,7 +530,7 @@ def main():
     avg_bytes = sum(launch_bytes) / len(launch_bytes)
     avg_dur = ms_attn * 1e-3 / (K_steps * run.L)
     achieved = avg_bytes / avg_dur / 1e9
-    traffic = committed_traffic(w.name)
+    traffic = committed_traffic(f"attn_split_bf16_{w.name}_pmc.md", "attention.hip")
     L = run.L
     total_bytes = sum(per[j]["attn"] + per[j]["sel"] for j in js)
     us_layer_step = ms_sparse * 1e3 / (K_steps * L)

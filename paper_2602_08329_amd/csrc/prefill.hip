@@ -8,8 +8,9 @@
 // query head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the
 // 16 columns of its MFMA tiles, so a wave owns its queries' whole softmax
 // and writes their outputs itself.  Key tiles of 64 rows are loaded once
-// per workgroup (whole rows, streaming cache policy, one tile ahead of its
-// use) into two LDS buffers -- K row-major, V transposed so that each MFMA
+// per workgroup (whole rows, one tile ahead of its use; the default cache
+// policy, since the unit's other query blocks read the same rows) into two
+// LDS buffers -- K row-major, V transposed so that each MFMA
 // operand is one 16-byte read -- and every wave computes
 //   S^T (64 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, four 16-row blocks)
 //   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts, 32 keys per product)
@@ -77,8 +78,8 @@ __device__ __forceinline__ void tile_load(TileRegs<D>& R, const __bf16* kb, cons
     const int r = e / CH, c = e % CH;
     const int p = min(ks + r, n - 1);
     const int64_t off = (unit_row0 + p) * D + c * 8;
-    R.k[j] = stream_load16(kb + off);
-    R.v[j] = stream_load16(vb + off);
+    R.k[j] = *(const u32x4_t*)(kb + off);
+    R.v[j] = *(const u32x4_t*)(vb + off);
   }
 }
 
