@@ -262,6 +262,7 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
  * q:         [batch][num_q_heads][q_len][head_dim] bf16 device array; row i is
  *            the query at position i.
  * vis_start: [q_len] int32 device array or NULL.
+ * scale:     softmax scale, positive and finite (PRHS_E_INVALID otherwise).
  * out:       [batch][num_q_heads][q_len][head_dim] fp32; lse:
  *            [batch][num_q_heads][q_len] fp32 or NULL.
  * No workspace.  Caller owns every buffer; ceil(q_len / 64) * batch * num_q_heads

@@ -4,8 +4,8 @@
 // attends the keys p <= i with p < C_sink or p >= vis_start[i]; without
 // vis_start every p <= i (plain causal attention, Eq. attn_eq per position).
 //
-// attn_prefill_bf16<D>: one workgroup per (192 query positions, batch,
-// query head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the
+// attn_prefill_bf16<D, QB>: one workgroup per (QB = 192 or 256 query
+// positions, batch, query head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the
 // 16 columns of its MFMA tiles, so a wave owns its queries' whole softmax
 // and writes their outputs itself.  Key tiles of 64 rows are loaded once
 // per workgroup (whole rows, one tile ahead of its use; the default cache
@@ -14,7 +14,7 @@
 // operand is one 16-byte read -- and every wave computes
 //   S^T (64 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, four 16-row blocks)
 //   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts, 32 keys per product)
-// with an online softmax per query.  A block visits only the key tiles that
+// with an online softmax per query (rescaled lazily).  A block visits only the key tiles that
 // meet its queries' visible ranges -- the sink [0, C_sink) and the band from
 // the smallest vis_start of its queries to its last query -- so tiles that
 // PSAW masks for every query of the block are never loaded: that is the
@@ -29,14 +29,22 @@ namespace prhs {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kQBlock = 192;  // query positions per workgroup (16 per wave, 12 waves)
-constexpr int kThreads = kQBlock / 16 * 64;
+// Query positions per workgroup, 16 per wave: 256 (16 waves) when the
+// launch has at least kWideMinGroupsPerCu workgroups per CU, 192 (12 waves)
+// otherwise, where the longer blocks would leave the last round of
+// workgroups short of CUs.
+constexpr int kQBlockWide = 256;
+constexpr int kQBlockNarrow = 192;
+constexpr int kWideMinGroupsPerCu = 4;
 constexpr int kKTile = 64;    // key rows per tile
 static_assert(kKTile % 32 == 0, "a tile is whole 32-key sub-tiles");
 constexpr int kXcds = 8;      // accelerator dies, each with its own L2
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kLazyLog2 = 8.f;  // log2 of the largest probability between rescales
 
 struct PrefillArgs {
   KvView kv;
@@ -61,19 +69,19 @@ __device__ __forceinline__ int k_slot(int r, int c) {
 // Whole-row loads of tile rows [ks, ks + kKTile): each thread takes up to
 // RPL 16-byte chunks of K and of V (threads past the tile's chunks take none).
 // Rows at or past n (the prompt) read row n - 1.
-template <int D>
+template <int D, int NT>
 struct TileRegs {
-  static constexpr int RPL = (kKTile * (D / 8) + kThreads - 1) / kThreads;  // chunks per thread
+  static constexpr int RPL = (kKTile * (D / 8) + NT - 1) / NT;  // chunks per thread
   u32x4_t k[RPL], v[RPL];
 };
 
-template <int D>
-__device__ __forceinline__ void tile_load(TileRegs<D>& R, const __bf16* kb, const __bf16* vb,
+template <int D, int NT>
+__device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const __bf16* kb, const __bf16* vb,
                                           int64_t unit_row0, int ks, int n) {
   constexpr int CH = D / 8;
 #pragma unroll
-  for (int j = 0; j < TileRegs<D>::RPL; ++j) {
-    const int e = (int)threadIdx.x + j * kThreads;
+  for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
+    const int e = (int)threadIdx.x + j * NT;
     if (e >= kKTile * CH) break;
     const int r = e / CH, c = e % CH;
     const int p = min(ks + r, n - 1);
@@ -96,13 +104,13 @@ __device__ __forceinline__ int vt_byte(int dim, int pos) {
   return dim * 64 + 16 * ((pos >> 3) ^ ((dim >> 2) & 3)) + 2 * (pos & 7);
 }
 
-template <int D>
-__device__ __forceinline__ void tile_store(const TileRegs<D>& R, u32x4_t* sk, u32x4_t* sv) {
+template <int D, int NT>
+__device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk, u32x4_t* sv) {
   constexpr int CH = D / 8;
   unsigned char* vt = (unsigned char*)sv;
 #pragma unroll
-  for (int j = 0; j < TileRegs<D>::RPL; ++j) {
-    const int e = (int)threadIdx.x + j * kThreads;
+  for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
+    const int e = (int)threadIdx.x + j * NT;
     if (e >= kKTile * CH) break;
     const int r = e / CH, c = e % CH;
     sk[k_slot<D>(r, c)] = R.k[j];
@@ -142,16 +150,17 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
     }
     // the MFMA output row is the key, the column the query: lane (col,
-    // grp) holds query col of its wave for keys 4 grp + e of block s
+    // grp) holds query col of its wave for keys 4 grp + e of block s.
+    // Raw products (scale_log2 > 0 is applied with the maximum's shift).
     if (full) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[s][e] = acc[e] * scale_log2;
+      for (int e = 0; e < 4; ++e) x[s][e] = acc[e];
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int p = ks + 16 * s + 4 * grp + e;
         const bool vis = qvalid && p <= qi && (p < sink || p >= my_vis);
-        x[s][e] = vis ? acc[e] * scale_log2 : -INFINITY;
+        x[s][e] = vis ? acc[e] : -INFINITY;
       }
     }
 #pragma unroll
@@ -159,12 +168,17 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   }
   mt = fmaxf(mt, __shfl_xor(mt, 16));
   mt = fmaxf(mt, __shfl_xor(mt, 32));
-  const float m_new = fmaxf(m_run, mt);
-  const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-  m_run = m_new;
-  l_run *= alpha;
+  // lazy rescaling: the reference m_run (and with it O and l) moves only
+  // when some query of the wave sees its maximum rise by more than 2^8, so
+  // the probabilities stay below 2^8; O / l does not depend on the reference
+  const float m_new = fmaxf(m_run, mt * scale_log2);
+  if (__builtin_amdgcn_ballot_w64(m_new > m_run + kLazyLog2)) {
+    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
 #pragma unroll
-  for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
+    for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
+  }
   // per 32-key sub-tile u: P^T as bf16 hi + lo parts (lane (col, grp)
   // holds keys 32u + 16h + 4 grp + e, h = 0, 1), then the V^T products
   const unsigned char* vt = (const unsigned char*)svx;
@@ -173,19 +187,19 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   for (int u = 0; u < NB / 2; ++u) {
     uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
     if (m_run != -INFINITY) {
-      uint32_t hb[8], lb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float pr = __builtin_amdgcn_exp2f(x[2 * u + (j >> 2)][j & 3] - m_run);
-        psum += pr;
-        const __bf16 h = (__bf16)pr;
-        hb[j] = __builtin_bit_cast(uint16_t, h);
-        lb[j] = __builtin_bit_cast(uint16_t, (__bf16)(pr - (float)h));
-      }
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
-        lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+        // probabilities of keys 2w and 2w + 1 of this lane's 8, converted
+        // as a pair (round to nearest even), then the pair of remainders
+        const int j0 = 2 * w, j1 = 2 * w + 1;
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(x[2 * u + (j0 >> 2)][j0 & 3], scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(x[2 * u + (j1 >> 2)][j1 & 3], scale_log2, -m_run));
+        psum += p0 + p1;
+        const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
+        const float r0 = p0 - __uint_as_float(h << 16);
+        const float r1 = p1 - __uint_as_float(h & 0xFFFF0000u);
+        hi[w] = h;
+        lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{r0, r1}, bf16x2_t));
       }
     }
     const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
@@ -205,8 +219,10 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   l_run += psum;
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_prefill_bf16(PrefillArgs a) {
+template <int D, int QB>
+__global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a) {
+  constexpr int kQBlock = QB;
+  constexpr int kThreads = QB / 16 * 64;
   constexpr int KS = D / 32;   // products per 16-key block of S
   constexpr int DB = D / 16;   // output blocks of 16 dims per lane group
   constexpr int CH = D / 8;    // 16-byte chunks per row
@@ -293,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void attn_prefill_bf16(PrefillArgs a) {
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  TileRegs<D> R;
+  TileRegs<D, kThreads> R;
   auto tile_start = [&](int t) { return (t < nsink ? t : tb0 + (t - nsink)) * kKTile; };
   auto full_tile = [&](int ks) {
     return wave_all && ks + kKTile - 1 <= qw0 && (ks + kKTile <= a.sink || ks >= wvis);
@@ -301,11 +317,11 @@ __global__ __launch_bounds__(kThreads) void attn_prefill_bf16(PrefillArgs a) {
   auto masked_tile = [&](int ks) {
     return ks > wlast || (ks >= a.sink && ks + kKTile - 1 < wvmin);
   };
-  if (ntiles > 0) tile_load<D>(R, kb, vb, row0, tile_start(0), n);
+  if (ntiles > 0) tile_load<D, kThreads>(R, kb, vb, row0, tile_start(0), n);
   for (int t = 0; t < ntiles; ++t) {
-    tile_store<D>(R, s_k[t & 1], s_v[t & 1]);
+    tile_store<D, kThreads>(R, s_k[t & 1], s_v[t & 1]);
     __syncthreads();
-    tile_load<D>(R, kb, vb, row0, tile_start(min(t + 1, ntiles - 1)), n);
+    tile_load<D, kThreads>(R, kb, vb, row0, tile_start(min(t + 1, ntiles - 1)), n);
     const int ks = tile_start(t);
     if (!masked_tile(ks))
       prefill_tile<D>(s_k[t & 1], s_v[t & 1], ks, qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
@@ -340,11 +356,20 @@ hipError_t launch_prefill(const PrefillLaunch& s, hipStream_t stream) {
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   a.out = s.out;
   a.lse = s.lse;
-  const dim3 grid(((s.T + kQBlock - 1) / kQBlock) * s.kv.batch * s.kv.hq);
-  if (s.kv.d == 128)
-    hipLaunchKernelGGL(attn_prefill_bf16<128>, grid, dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(attn_prefill_bf16<64>, grid, dim3(kThreads), 0, stream, a);
+  const long long units = (long long)s.kv.batch * s.kv.hq;
+  const int cus = device_cus();
+  const bool wide = cus > 0 && ((s.T + kQBlockWide - 1) / kQBlockWide) * units >=
+                                   (long long)kWideMinGroupsPerCu * cus;
+  const int qb = wide ? kQBlockWide : kQBlockNarrow;
+  const dim3 grid((unsigned)(((s.T + qb - 1) / qb) * units));
+  const dim3 block(qb / 16 * 64);
+  if (s.kv.d == 128) {
+    if (wide) hipLaunchKernelGGL((attn_prefill_bf16<128, kQBlockWide>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_prefill_bf16<128, kQBlockNarrow>), grid, block, 0, stream, a);
+  } else {
+    if (wide) hipLaunchKernelGGL((attn_prefill_bf16<64, kQBlockWide>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((attn_prefill_bf16<64, kQBlockNarrow>), grid, block, 0, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -429,7 +429,8 @@ prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
     return fail(PRHS_E_UNSUPPORTED, "prefill attention is built for bf16 inputs");
   if (q_len < 0) return fail(PRHS_E_INVALID, "q_len must be >= 0 (got %d)", q_len);
   if (sink < 0) return fail(PRHS_E_INVALID, "sink must be >= 0");
-  if (!(scale == scale)) return fail(PRHS_E_INVALID, "scale is NaN");
+  if (!(scale > 0.f && scale < INFINITY))
+    return fail(PRHS_E_INVALID, "scale must be positive and finite");
   if ((long long)((q_len + 63) / 64) * kv->batch * kv->num_q_heads > 0x7FFFFFFFLL)
     return fail(PRHS_E_UNSUPPORTED, "ceil(q_len / 64) * batch * num_q_heads must be < 2^31");
   if (kv->batch == 0 || q_len == 0) return PRHS_OK;

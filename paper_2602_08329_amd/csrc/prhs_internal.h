@@ -197,4 +197,7 @@ struct PrefillLaunch {
 };
 hipError_t launch_prefill(const PrefillLaunch& a, hipStream_t stream);
 
+// Compute units of the current device (cached per device; 0 if unknown).
+int device_cus();
+
 }  // namespace prhs

@@ -1126,7 +1126,9 @@ constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
 constexpr int kLdsBytes = 160 * 1024;  // LDS of one CU
 static_assert(kFusedMaxKeys <= 32 * kHistBins, "the shared-set bitmap reuses the histogram");
 
-// CUs of the current device (0 when unknown).
+}  // namespace
+
+// CUs of the current device (0 when unknown); also used by the prefill launch.
 int device_cus() {
   static int cus[64] = {0};
   int dev = 0;
@@ -1139,6 +1141,8 @@ int device_cus() {
   }
   return cus[dev] > 0 ? cus[dev] : 0;
 }
+
+namespace {
 
 enum class SelPath { kFused, kKeyed, kRadix };
 

@@ -257,6 +257,24 @@ def test_dilate_validation_and_empty_batch(L):
     assert _select(L, kv0, B.params(k=8, window=4), q=None) == B.PRHS_OK
 
 
+def test_prefill_validation(L):
+    kv = _kv()
+    pre = lambda kv=kv, q=0x4000, T=300, sink=4, scale=0.1, out=0x5000: L.prhs_prefill_attn(  # noqa: E731
+        ctypes.byref(kv), q, T, None, sink, scale, out, None, None)
+    for bad in (0.0, -0.1, float("nan"), float("inf")):
+        assert pre(scale=bad) == B.PRHS_E_INVALID
+    assert b"scale" in L.prhs_last_error()
+    assert pre(T=-1) == B.PRHS_E_INVALID
+    assert pre(sink=-1) == B.PRHS_E_INVALID
+    assert pre(q=None) == B.PRHS_E_INVALID
+    assert pre(out=None) == B.PRHS_E_INVALID
+    assert pre(kv=_kv(dtype=B.PRHS_F32)) == B.PRHS_E_UNSUPPORTED
+    assert pre(kv=_kv(layout=B.PRHS_KV_PAGED, block_table=0xA000)) == B.PRHS_E_UNSUPPORTED
+    assert pre(T=0, q=None, out=None) == B.PRHS_OK     # nothing to do, no device work
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert pre(kv=kv0, q=None, out=None) == B.PRHS_OK
+
+
 def test_workspace_size_errors(L):
     n = ctypes.c_size_t(7)
     assert L.prhs_workspace_size(99, None, None, 0, ctypes.byref(n)) == B.PRHS_E_INVALID

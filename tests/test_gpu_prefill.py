@@ -2,7 +2,8 @@
 against the oracle's prefill_attention: plain causal layers and pruning
 layers, GQA and MHA, d 64 and 128, ragged prompts (rows past a prompt are
 empty), query spans shorter than the prompt, and sampled rows of a full
-LLaMA-2-7B-shaped 4k prefill.  Outputs within 2e-3 of the fp64 oracle per
+LLaMA-2-7B-shaped 4k prefill and of launches large enough to take the
+256-query blocks.  Outputs within 2e-3 of the fp64 oracle per
 (batch, head, query) row in the max norm, lse within 1e-4."""
 
 import math
@@ -129,6 +130,18 @@ def test_prefill_full_size_llama2_4k_sampled():
     rows = [0, 1, 63, 64, 1000, 2047, 3000, 4031, 4095]
     run_prefill(1, 32, 32, 128, (T,), T, psaw=(24, 0.7, 1.0), layer=31, n_layers=32, sink=4,
                 seed=13, rows=rows, heads=[0, 17, 31])
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_wide_blocks_sampled(d):
+    # enough (batch, head) units that the launch takes 256-query blocks
+    # (at least 4 workgroups per CU); ragged prompts, GQA, a pruning layer
+    lens = (1024, 1000, 777, 1024, 600, 1024, 513, 1024)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    assert -(-1024 // 256) * len(lens) * 32 >= 4 * cus
+    rows = [0, 1, 255, 256, 511, 512, 776, 777, 999, 1023]
+    run_prefill(8, 32, 8, d, lens, 1024, psaw=(6, 0.5, 1.0), layer=7, n_layers=8, sink=16,
+                seed=17 + d, rows=rows, heads=[0, 13, 31])
 
 
 def test_prefill_rejects_paged_and_fp32():
