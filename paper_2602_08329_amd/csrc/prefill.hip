@@ -116,11 +116,19 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk
     sk[k_slot<D>(r, c)] = R.k[j];
     unsigned char* vts = vt + (r >> 5) * (D * 64);
     const int pos = vt_pos(r & 31);
+    // word w of the chunk holds dims 8c + 2w (low half) and 8c + 2w + 1;
+    // the store of step w writes word (w + rot) mod 4, rot = (c >> 1) mod 4,
+    // so that one store instruction spreads its lanes over all four bank
+    // quarters of the dim rows (2-way bank conflicts instead of 8-way)
+    const int rot = (c >> 1) & 3;
+    u32x4_t x = R.v[j];
+    if (rot & 1) x = u32x4_t{x[1], x[2], x[3], x[0]};
+    if (rot & 2) x = u32x4_t{x[2], x[3], x[0], x[1]};
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const uint32_t x = R.v[j][w];  // dims 8c + 2w (low half) and 8c + 2w + 1
-      *(uint16_t*)(vts + vt_byte(8 * c + 2 * w, pos)) = (uint16_t)(x & 0xFFFFu);
-      *(uint16_t*)(vts + vt_byte(8 * c + 2 * w + 1, pos)) = (uint16_t)(x >> 16);
+      const int dim = 8 * c + 2 * ((w + rot) & 3);
+      *(uint16_t*)(vts + vt_byte(dim, pos)) = (uint16_t)(x[w] & 0xFFFFu);
+      *(uint16_t*)(vts + vt_byte(dim + 1, pos)) = (uint16_t)(x[w] >> 16);
     }
   }
 }
@@ -135,72 +143,77 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
                                              float& l_run, f32x4_t* o) {
   constexpr int KS = D / 32;       // products per 16-key block of S
   constexpr int DB = D / 16;       // 16-dim blocks of O^T
-  constexpr int NB = kKTile / 16;  // 16-key blocks of the tile
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  // S^T for this wave's 16 queries: lane (col, grp) gets keys ks + 16s + 4grp + e
-  float x[NB][4];
-  float mt = -INFINITY;
-#pragma unroll
-  for (int s = 0; s < NB; ++s) {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, sk[k_slot<D>(16 * s + col, 4 * kk + grp)]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
-    }
-    // the MFMA output row is the key, the column the query: lane (col,
-    // grp) holds query col of its wave for keys 4 grp + e of block s.
-    // Raw products (scale_log2 > 0 is applied with the maximum's shift).
-    if (full) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[s][e] = acc[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int p = ks + 16 * s + 4 * grp + e;
-        const bool vis = qvalid && p <= qi && (p < sink || p >= my_vis);
-        x[s][e] = vis ? acc[e] : -INFINITY;
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) mt = fmaxf(mt, x[s][e]);
-  }
-  mt = fmaxf(mt, __shfl_xor(mt, 16));
-  mt = fmaxf(mt, __shfl_xor(mt, 32));
-  // lazy rescaling: the reference m_run (and with it O and l) moves only
-  // when some query of the wave sees its maximum rise by more than 2^8, so
-  // the probabilities stay below 2^8; O / l does not depend on the reference
-  const float m_new = fmaxf(m_run, mt * scale_log2);
-  if (__builtin_amdgcn_ballot_w64(m_new > m_run + kLazyLog2)) {
-    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
-#pragma unroll
-    for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
-  }
-  // per 32-key sub-tile u: P^T as bf16 hi + lo parts (lane (col, grp)
-  // holds keys 32u + 16h + 4 grp + e, h = 0, 1), then the V^T products
   const unsigned char* vt = (const unsigned char*)svx;
-  float psum = 0.f;
+  // the tile in 32-key sub-tiles u, each taken through the whole step
+  // (scores, mask, softmax update, products) so that only its 8 scores per
+  // lane are live at a time
 #pragma unroll
-  for (int u = 0; u < NB / 2; ++u) {
+  for (int u = 0; u < kKTile / 32; ++u) {
+    // S^T for this wave's 16 queries: lane (col, grp) gets keys
+    // ks + 32u + 16h + 4grp + e of 16-key block h
+    float x[2][4];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int s = 2 * u + h;
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, sk[k_slot<D>(16 * s + col, 4 * kk + grp)]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
+      }
+      // the MFMA output row is the key, the column the query: lane (col,
+      // grp) holds query col of its wave for keys 4 grp + e of block s.
+      // Raw products (scale_log2 > 0 is applied with the maximum's shift).
+      if (full) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[h][e] = acc[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int p = ks + 16 * s + 4 * grp + e;
+          const bool vis = qvalid && p <= qi && (p < sink || p >= my_vis);
+          x[h][e] = vis ? acc[e] : -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mt = fmaxf(mt, x[h][e]);
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    // lazy rescaling: the reference m_run (and with it O and l) moves only
+    // when some query of the wave sees its maximum rise by more than 2^8, so
+    // the probabilities stay below 2^8; O / l does not depend on the reference
+    const float m_new = fmaxf(m_run, mt * scale_log2);
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run + kLazyLog2)) {
+      const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int blk = 0; blk < DB; ++blk) o[blk] *= alpha;
+    }
+    // P^T as bf16 hi + lo parts: lane (col, grp) holds keys 32u + 16h +
+    // 4 grp + e, in the K-index order 8 grp + 4h + e of the products
     uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
     if (m_run != -INFINITY) {
+      float psum = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         // probabilities of keys 2w and 2w + 1 of this lane's 8, converted
         // as a pair (round to nearest even), then the pair of remainders
         const int j0 = 2 * w, j1 = 2 * w + 1;
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(x[2 * u + (j0 >> 2)][j0 & 3], scale_log2, -m_run));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(x[2 * u + (j1 >> 2)][j1 & 3], scale_log2, -m_run));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(x[j0 >> 2][j0 & 3], scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(x[j1 >> 2][j1 & 3], scale_log2, -m_run));
         psum += p0 + p1;
-        const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
-        const float r0 = p0 - __uint_as_float(h << 16);
-        const float r1 = p1 - __uint_as_float(h & 0xFFFF0000u);
-        hi[w] = h;
+        const uint32_t hp = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
+        const float r0 = p0 - __uint_as_float(hp << 16);
+        const float r1 = p1 - __uint_as_float(hp & 0xFFFF0000u);
+        hi[w] = hp;
         lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{r0, r1}, bf16x2_t));
       }
+      l_run += psum;
     }
     const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
     const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
@@ -216,7 +229,6 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
       o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
     }
   }
-  l_run += psum;
 }
 
 template <int D, int QB>
@@ -285,6 +297,9 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
     wvis = max(wvis, __shfl_xor(wvis, off));
     wvmin = min(wvmin, __shfl_xor(wvmin, off));
   }
+  // every 16-lane group holds the wave's 16 queries: the results are uniform
+  wvis = __builtin_amdgcn_readfirstlane(wvis);
+  wvmin = __builtin_amdgcn_readfirstlane(wvmin);
   // and it needs no work at all when it lies past the wave's last query or
   // between the sink and the smallest of their vis_start (every product
   // would be masked; skipping leaves O, m and l exactly as they are)
