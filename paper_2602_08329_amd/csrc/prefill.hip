@@ -31,6 +31,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Query positions per workgroup, 16 per wave: 256 (16 waves) when the
@@ -91,18 +92,12 @@ __device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const __bf16* kb, 
   }
 }
 
-// V tile in LDS, transposed, as kKTile / 32 sub-tiles of 32 keys (D x 64
-// bytes each): row `dim` of a sub-tile holds its 32 values of that dim in
-// the key order of the probabilities (key 16s + 4g + e at position
-// 8g + 4s + e, so a lane's 8 keys are one 16-byte block), the block index
-// XOR-swizzled by (dim >> 2) & 3 so that the operand reads (16 dims, one
-// block each) hit distinct banks.
-__device__ __forceinline__ int vt_pos(int key) {
-  return 8 * ((key & 15) >> 2) + 4 * (key >> 4) + (key & 3);
-}
-__device__ __forceinline__ int vt_byte(int dim, int pos) {
-  return dim * 64 + 16 * ((pos >> 3) ^ ((dim >> 2) & 3)) + 2 * (pos & 7);
-}
+// V tile in LDS: row-major, key rows of D * 2 bytes padded to
+// vrow_bytes<D> (32 bytes more), so that the transposing operand reads below
+// (4 key rows x 4 pieces of 8 bytes per 16 lanes) hit distinct banks and
+// every read of a row's pieces is the lane's base address plus a constant.
+template <int D>
+constexpr int vrow_bytes() { return D * 2 + 32; }
 
 template <int D, int NT>
 __device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk, u32x4_t* sv) {
@@ -114,22 +109,7 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk
     if (e >= kKTile * CH) break;
     const int r = e / CH, c = e % CH;
     sk[k_slot<D>(r, c)] = R.k[j];
-    unsigned char* vts = vt + (r >> 5) * (D * 64);
-    const int pos = vt_pos(r & 31);
-    // word w of the chunk holds dims 8c + 2w (low half) and 8c + 2w + 1;
-    // the store of step w writes word (w + rot) mod 4, rot = (c >> 1) mod 4,
-    // so that one store instruction spreads its lanes over all four bank
-    // quarters of the dim rows (2-way bank conflicts instead of 8-way)
-    const int rot = (c >> 1) & 3;
-    u32x4_t x = R.v[j];
-    if (rot & 1) x = u32x4_t{x[1], x[2], x[3], x[0]};
-    if (rot & 2) x = u32x4_t{x[2], x[3], x[0], x[1]};
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const int dim = 8 * c + 2 * ((w + rot) & 3);
-      *(uint16_t*)(vts + vt_byte(dim, pos)) = (uint16_t)(x[w] & 0xFFFFu);
-      *(uint16_t*)(vts + vt_byte(dim + 1, pos)) = (uint16_t)(x[w] >> 16);
-    }
+    *(u32x4_t*)((unsigned char*)sv + r * vrow_bytes<D>() + c * 16) = R.v[j];
   }
 }
 
@@ -145,7 +125,6 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   constexpr int DB = D / 16;       // 16-dim blocks of O^T
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const unsigned char* vt = (const unsigned char*)svx;
   // the tile in 32-key sub-tiles u, each taken through the whole step
   // (scores, mask, softmax update, products) so that only its 8 scores per
   // lane are live at a time
@@ -217,14 +196,21 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
     }
     const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
     const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
-    // V^T operand of product blk: lane (col, grp) takes dim 16 blk + col, its
-    // 8 keys (the keys of its probabilities) as one 16-byte block
-    const unsigned char* vts = vt + u * (D * 64);
+    // V^T operand of product blk (16 dims x 32 keys; lane (col, grp) needs
+    // dim 16 blk + col at its 8 keys, the keys of its probabilities) by two
+    // transposing LDS loads from the row-major tile: in each 16-lane group,
+    // lane 4e + q points at the 8-byte piece (dims 16 blk + 4q .. + 3) of
+    // key row 32u + 16h + 4 grp + e, and the load hands lane col the values
+    // of dim 16 blk + col at its group's 4 rows, e = 0 .. 3.
+    const unsigned char* vrow = (const unsigned char*)svx +
+                                (32 * u + 4 * grp + (col >> 2)) * vrow_bytes<D>() + 8 * (col & 3);
 #pragma unroll
     for (int blk = 0; blk < DB; ++blk) {
-      const int dim = 16 * blk + col;
-      const bf16x8_t av =
-          __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)(vts + vt_byte(dim, 8 * grp)));
+      const v4i16_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16_t*)(vrow + 32 * blk));
+      const v4i16_t a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16_t*)(vrow + 16 * vrow_bytes<D>() + 32 * blk));
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
       o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
       o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
     }
@@ -239,7 +225,7 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   constexpr int DB = D / 16;   // output blocks of 16 dims per lane group
   constexpr int CH = D / 8;    // 16-byte chunks per row
   __shared__ u32x4_t s_k[2][kKTile * CH];
-  __shared__ u32x4_t s_v[2][kKTile * CH];
+  __shared__ u32x4_t s_v[2][kKTile * vrow_bytes<D>() / 16];
   __shared__ int s_vmin;
   // Workgroups go to the 8 XCDs round-robin by id; id L runs unit-major
   // slot (L mod 8) * (N / 8) + L / 8, so that each XCD works through its
