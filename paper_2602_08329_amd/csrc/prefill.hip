@@ -113,6 +113,17 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk
   }
 }
 
+// Maximum over the lanes col, col + 16, col + 32 and col + 48 (one query's
+// four lane groups), by the cross-half and cross-row lane swaps: each swap
+// of a value with itself leaves a lane holding its own value and its
+// partner's, one in each result.
+__device__ __forceinline__ float max_over_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // One key tile against one wave's 16 queries: S^T, the per-(key, query)
 // mask, the online softmax and O^T += V^T P^T (as in the decode kernel, with
 // the query positions in the columns).
@@ -138,11 +149,15 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
     for (int h = 0; h < 2; ++h) {
       const int s = 2 * u + h;
       f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      // raised issue priority around the MFMA runs, so that a wave ready to
+      // issue products goes ahead of waves doing softmax work
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, sk[k_slot<D>(16 * s + col, 4 * kk + grp)]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[kk], acc, 0, 0, 0);
       }
+      __builtin_amdgcn_s_setprio(0);
       // the MFMA output row is the key, the column the query: lane (col,
       // grp) holds query col of its wave for keys 4 grp + e of block s.
       // Raw products (scale_log2 > 0 is applied with the maximum's shift).
@@ -160,8 +175,7 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
 #pragma unroll
       for (int e = 0; e < 4; ++e) mt = fmaxf(mt, x[h][e]);
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    mt = max_over_groups(mt);
     // lazy rescaling: the reference m_run (and with it O and l) moves only
     // when some query of the wave sees its maximum rise by more than 2^8, so
     // the probabilities stay below 2^8; O / l does not depend on the reference
@@ -204,6 +218,7 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
     // of dim 16 blk + col at its group's 4 rows, e = 0 .. 3.
     const unsigned char* vrow = (const unsigned char*)svx +
                                 (32 * u + 4 * grp + (col >> 2)) * vrow_bytes<D>() + 8 * (col & 3);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int blk = 0; blk < DB; ++blk) {
       const v4i16_t a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -214,6 +229,7 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
       o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, o[blk], 0, 0, 0);
       o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, plo, o[blk], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
   }
 }
 
