@@ -198,9 +198,18 @@ __device__ __forceinline__ void stage_rows(const AttnArgs& a, const int32_t (&ra
   __syncthreads();
 }
 
-__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Maximum over the lanes col, col + 16, col + 32 and col + 48 (the four
+// lane groups of one MFMA column), by the cross-half and cross-row lane
+// swaps: each swap of a value with itself leaves a lane holding its own
+// value and its partner's, one in each result.
+__device__ __forceinline__ float max_over_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 template <int DB>
@@ -227,11 +236,6 @@ __device__ __forceinline__ VRow<DB> load_vrow(const __bf16* p) {
   return v;
 }
 
-template <int DB>
-__device__ __forceinline__ uint32_t vrow_elem(const VRow<DB>& v, int e) {
-  const uint32_t w = v.w[e >> 1];
-  return (e & 1) ? (w >> 16) : (w & 0xFFFFu);
-}
 
 // Registers of one wave's 32-row tile: K rows as loaded (whole rows, D/8
 // lanes of 16 bytes per row, so every load reads whole 128-byte lines), V
@@ -351,8 +355,7 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
       }
     }
   }
-  mt = fmaxf(mt, __shfl_xor(mt, 16));
-  mt = fmaxf(mt, __shfl_xor(mt, 32));
+  mt = max_over_groups(mt);
   const float m_new = fmaxf(st.m, mt);
   float alpha = 1.f, psum = 0.f;
   uint32_t hi[4], lo[4];
@@ -360,19 +363,17 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
 #pragma unroll
     for (int w = 0; w < 4; ++w) hi[w] = lo[w] = 0u;
   } else {
-    alpha = exp2f(st.m - m_new);
-    uint32_t hb[8], lb[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float p = exp2f(x[j >> 2][j & 3] - m_new);
-      psum += p;
-      hb[j] = bf16_bits_rne(p);
-      lb[j] = bf16_bits_rne(p - __uint_as_float(hb[j] << 16));
-    }
+    alpha = __builtin_amdgcn_exp2f(st.m - m_new);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      hi[w] = hb[2 * w] | (hb[2 * w + 1] << 16);
-      lo[w] = lb[2 * w] | (lb[2 * w + 1] << 16);
+      const int j0 = 2 * w, j1 = 2 * w + 1;
+      const float p0 = __builtin_amdgcn_exp2f(x[j0 >> 2][j0 & 3] - m_new);
+      const float p1 = __builtin_amdgcn_exp2f(x[j1 >> 2][j1 & 3] - m_new);
+      psum += p0 + p1;
+      const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
+      hi[w] = h;
+      lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+          f32x2_t{p0 - __uint_as_float(h << 16), p1 - __uint_as_float(h & 0xFFFF0000u)}, bf16x2_t));
     }
   }
   st.l = st.l * alpha + psum;
@@ -386,8 +387,10 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const int j0 = 2 * w, j1 = 2 * w + 1;
-      aw[w] = vrow_elem<DB>(T.vf[j0 >> 2][j0 & 3], blk) |
-              (vrow_elem<DB>(T.vf[j1 >> 2][j1 & 3], blk) << 16);
+      // element blk of rows j0 (low half) and j1 (high half), one byte
+      // permute: selector bytes 0-3 index the second source, 4-7 the first
+      aw[w] = __builtin_amdgcn_perm(T.vf[j1 >> 2][j1 & 3].w[blk >> 1], T.vf[j0 >> 2][j0 & 3].w[blk >> 1],
+                                    (blk & 1) ? 0x07060302u : 0x05040100u);
     }
     const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
     st.o[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, phi, st.o[blk], 0, 0, 0);
