@@ -356,19 +356,28 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
     }
   }
   mt = max_over_groups(mt);
+  // lazy rescaling: the reference st.m (and with it o and l) moves only when
+  // some head of the wave sees its maximum rise by more than 2^8, so the
+  // probabilities stay below 2^8; o / l does not depend on the reference
   const float m_new = fmaxf(st.m, mt);
-  float alpha = 1.f, psum = 0.f;
+  if (__builtin_amdgcn_ballot_w64(m_new > st.m + 8.f)) {
+    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(st.m - m_new);
+    st.m = m_new;
+    st.l *= alpha;
+#pragma unroll
+    for (int blk = 0; blk < DB; ++blk) st.o[blk] *= alpha;
+  }
+  float psum = 0.f;
   uint32_t hi[4], lo[4];
-  if (m_new == -INFINITY) {
+  if (st.m == -INFINITY) {
 #pragma unroll
     for (int w = 0; w < 4; ++w) hi[w] = lo[w] = 0u;
   } else {
-    alpha = __builtin_amdgcn_exp2f(st.m - m_new);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const int j0 = 2 * w, j1 = 2 * w + 1;
-      const float p0 = __builtin_amdgcn_exp2f(x[j0 >> 2][j0 & 3] - m_new);
-      const float p1 = __builtin_amdgcn_exp2f(x[j1 >> 2][j1 & 3] - m_new);
+      const float p0 = __builtin_amdgcn_exp2f(x[j0 >> 2][j0 & 3] - st.m);
+      const float p1 = __builtin_amdgcn_exp2f(x[j1 >> 2][j1 & 3] - st.m);
       psum += p0 + p1;
       const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
       hi[w] = h;
@@ -376,13 +385,11 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
           f32x2_t{p0 - __uint_as_float(h << 16), p1 - __uint_as_float(h & 0xFFFF0000u)}, bf16x2_t));
     }
   }
-  st.l = st.l * alpha + psum;
-  st.m = m_new;
+  st.l += psum;
   const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
   const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
   for (int blk = 0; blk < DB; ++blk) {
-    st.o[blk] *= alpha;
     uint32_t aw[4];
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
