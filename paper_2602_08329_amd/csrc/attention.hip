@@ -349,11 +349,20 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
       const bool ok = (T.ok >> (s * 4 + e)) & 1u;
       x[s][e] = ok ? acc[e] * scale_log2 : -INFINITY;
       mt = fmaxf(mt, x[s][e]);
-      if (!ok) {
-#pragma unroll
-        for (int w = 0; w < DB / 2; ++w) T.vf[s][e].w[w] = 0u;
-      }
     }
+  }
+  // rows past the set read a stand-in row: zero their V values (a zero
+  // probability times a non-finite value would still be NaN), only in the
+  // waves that have such rows
+  if (__builtin_amdgcn_ballot_w64(T.ok != 0xFFu)) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (!((T.ok >> (s * 4 + e)) & 1u)) {
+#pragma unroll
+          for (int w = 0; w < DB / 2; ++w) T.vf[s][e].w[w] = 0u;
+        }
   }
   mt = max_over_groups(mt);
   // lazy rescaling: the reference st.m (and with it o and l) moves only when
@@ -367,23 +376,21 @@ __device__ __forceinline__ void consume_tile(Tile<D>& T, WaveState<D>& st, const
 #pragma unroll
     for (int blk = 0; blk < DB; ++blk) st.o[blk] *= alpha;
   }
+  // while st.m is -inf every score is -inf too: a finite reference makes
+  // every probability 0 without a branch
+  const float mref = st.m == -INFINITY ? 0.f : st.m;
   float psum = 0.f;
   uint32_t hi[4], lo[4];
-  if (st.m == -INFINITY) {
 #pragma unroll
-    for (int w = 0; w < 4; ++w) hi[w] = lo[w] = 0u;
-  } else {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const int j0 = 2 * w, j1 = 2 * w + 1;
-      const float p0 = __builtin_amdgcn_exp2f(x[j0 >> 2][j0 & 3] - st.m);
-      const float p1 = __builtin_amdgcn_exp2f(x[j1 >> 2][j1 & 3] - st.m);
-      psum += p0 + p1;
-      const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
-      hi[w] = h;
-      lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
-          f32x2_t{p0 - __uint_as_float(h << 16), p1 - __uint_as_float(h & 0xFFFF0000u)}, bf16x2_t));
-    }
+  for (int w = 0; w < 4; ++w) {
+    const int j0 = 2 * w, j1 = 2 * w + 1;
+    const float p0 = __builtin_amdgcn_exp2f(x[j0 >> 2][j0 & 3] - mref);
+    const float p1 = __builtin_amdgcn_exp2f(x[j1 >> 2][j1 & 3] - mref);
+    psum += p0 + p1;
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
+    hi[w] = h;
+    lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+        f32x2_t{p0 - __uint_as_float(h << 16), p1 - __uint_as_float(h & 0xFFFF0000u)}, bf16x2_t));
   }
   st.l += psum;
   const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));

@@ -189,25 +189,26 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
     }
     // P^T as bf16 hi + lo parts: lane (col, grp) holds keys 32u + 16h +
     // 4 grp + e, in the K-index order 8 grp + 4h + e of the products
-    uint32_t hi[4] = {0u, 0u, 0u, 0u}, lo[4] = {0u, 0u, 0u, 0u};
-    if (m_run != -INFINITY) {
-      float psum = 0.f;
+    // while m_run is -inf every score is -inf too: a finite reference makes
+    // every probability 0 without a branch
+    const float mref = m_run == -INFINITY ? 0.f : m_run;
+    uint32_t hi[4], lo[4];
+    float psum = 0.f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // probabilities of keys 2w and 2w + 1 of this lane's 8, converted
-        // as a pair (round to nearest even), then the pair of remainders
-        const int j0 = 2 * w, j1 = 2 * w + 1;
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(x[j0 >> 2][j0 & 3], scale_log2, -m_run));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(x[j1 >> 2][j1 & 3], scale_log2, -m_run));
-        psum += p0 + p1;
-        const uint32_t hp = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
-        const float r0 = p0 - __uint_as_float(hp << 16);
-        const float r1 = p1 - __uint_as_float(hp & 0xFFFF0000u);
-        hi[w] = hp;
-        lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{r0, r1}, bf16x2_t));
-      }
-      l_run += psum;
+    for (int w = 0; w < 4; ++w) {
+      // probabilities of keys 2w and 2w + 1 of this lane's 8, converted
+      // as a pair (round to nearest even), then the pair of remainders
+      const int j0 = 2 * w, j1 = 2 * w + 1;
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(x[j0 >> 2][j0 & 3], scale_log2, -mref));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(x[j1 >> 2][j1 & 3], scale_log2, -mref));
+      psum += p0 + p1;
+      const uint32_t hp = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{p0, p1}, bf16x2_t));
+      const float r0 = p0 - __uint_as_float(hp << 16);
+      const float r1 = p1 - __uint_as_float(hp & 0xFFFF0000u);
+      hi[w] = hp;
+      lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{r0, r1}, bf16x2_t));
     }
+    l_run += psum;
     const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
     const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
     // V^T operand of product blk (16 dims x 32 keys; lane (col, grp) needs
