@@ -253,7 +253,26 @@ def prefill_main(args):
     Ks = [torch.randn(Bsz, H, T, d, generator=gen, device=dev).to(torch.bfloat16) for _ in range(L)]
     Vs = [torch.randn(Bsz, H, T, d, generator=gen, device=dev).to(torch.bfloat16) for _ in range(L)]
     seq = torch.full((Bsz,), T, dtype=torch.int32, device=dev)
-    kvs = [B.KV(Ks[l], Vs[l], seq, T, H) for l in range(L)]
+    if args.paged:
+        # 16-token pages of every prompt in one pool, in a seeded random order
+        ps = 16
+        npg = (T + ps - 1) // ps
+        pgen = torch.Generator(device="cpu")
+        pgen.manual_seed(4243 + T)
+        perm = torch.randperm(Bsz * npg, generator=pgen).to(dev)
+        table = perm.view(Bsz, npg).to(torch.int32)
+
+        def paged(X):
+            Xp = torch.zeros(Bsz, H, npg * ps, d, dtype=X.dtype, device=dev)
+            Xp[:, :, :T] = X
+            pages = Xp.view(Bsz, H, npg, ps, d).permute(0, 2, 1, 3, 4).reshape(Bsz * npg, H, ps, d)
+            pool = torch.empty(pages.shape, dtype=X.dtype, device=dev)
+            pool[perm.long()] = pages
+            return pool
+
+        kvs = [B.KV(paged(Ks[l]), paged(Vs[l]), seq, T, H, table) for l in range(L)]
+    else:
+        kvs = [B.KV(Ks[l], Vs[l], seq, T, H) for l in range(L)]
     vis = [psaw_prefill_visible(l, L, T, sink, l_s, phi, alpha, device=dev) if l + 1 >= l_s
            else None for l in range(L)]
     out = torch.empty(Bsz, H, T, d, device=dev)
@@ -287,6 +306,7 @@ def prefill_main(args):
         del graph
         return ms
 
+    workload = f"llama2-7b-prefill-b{Bsz}-{T}" + ("-paged" if args.paged else "")
     ms_psaw = timed(True, "prefill, PSAW on layers >= l_s")
     ms_causal = timed(False, "prefill, all layers causal")
     # useful flops: visible (query, key) pairs x 4 d, per head and prompt
@@ -318,7 +338,7 @@ def prefill_main(args):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"llama2-7b-prefill-b{Bsz}-{T}", "layers": L, "batch": Bsz,
+        "config": {"workload": workload, "layers": L, "batch": Bsz,
                    "heads": H, "head_dim": d, "prompt": T, "sink": sink,
                    "psaw": {"l_s": l_s, "phi": phi, "alpha": alpha},
                    "launch": "eager" if args.eager else "hip-graph replay"},
@@ -328,8 +348,7 @@ def prefill_main(args):
         "roofline": {"kernel": "attn_prefill_bf16", "bound": "mfma", "achieved": round(tflops, 1),
                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": committed_traffic(f"attn_prefill_bf16_llama2-7b-prefill-b{Bsz}-{T}.md",
-                                                  "prefill.hip"),
+                     "traffic": committed_traffic(f"attn_prefill_bf16_{workload}.md", "prefill.hip"),
                      "causal_achieved": round(tflops_causal, 1),
                      "note": "useful flops (4 d per visible query-key pair and head) over the "
                              "timed prefill; the kernel issues more (16-column tiles, the "
@@ -400,6 +419,9 @@ def main():
                          "fixed refresh period (blocks of refresh_every steps)")
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches instead of replays of a captured HIP graph")
+    ap.add_argument("--paged", action="store_true",
+                    help="with --prefill: the prompts' K/V in a paged cache (16-token pages, "
+                         "seeded random page order)")
     ap.add_argument("--prefill", action="store_true",
                     help="prefill attention under the PSAW mask instead of the decode step "
                          "(LLaMA-2-7B shape; --nmax prompt length, --batch prompts)")

@@ -256,8 +256,8 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
  * P_l(i + 1) - 1) in 0-based positions.  Query rows at positions
  * >= seq_lens[b] (and < q_len) give
  * y = 0 and lse = -inf.
- * kv:        contiguous bf16 cache holding the prompt of sequence b at
- *            positions [0, seq_lens[b]) (paged caches and fp32 inputs give
+ * kv:        bf16 cache (contiguous or paged) holding the prompt of
+ *            sequence b at positions [0, seq_lens[b]) (fp32 inputs give
  *            PRHS_E_UNSUPPORTED).
  * q:         [batch][num_q_heads][q_len][head_dim] bf16 device array; row i is
  *            the query at position i.

@@ -69,26 +69,55 @@ __device__ __forceinline__ int k_slot(int r, int c) {
 
 // Whole-row loads of tile rows [ks, ks + kKTile): each thread takes up to
 // RPL 16-byte chunks of K and of V (threads past the tile's chunks take none).
-// Rows at or past n (the prompt) read row n - 1.
+// Rows at or past n (the prompt) read row n - 1.  A paged cache resolves
+// every row through the block table (a row outside the table's valid pages
+// reads element 0 of the cache instead: no access outside it).
 template <int D, int NT>
 struct TileRegs {
   static constexpr int RPL = (kKTile * (D / 8) + NT - 1) / NT;  // chunks per thread
   u32x4_t k[RPL], v[RPL];
 };
 
+// One thread's chunks of a tile: element offsets (contiguous cache), or
+// positions, resolved through the block table when the loads are issued
+// (paged cache; looking the pages up a tile earlier was slower).
 template <int D, int NT>
-__device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const __bf16* kb, const __bf16* vb,
-                                          int64_t unit_row0, int ks, int n) {
+struct TileOffs {
+  int64_t e[TileRegs<D, NT>::RPL];
+};
+
+// This thread's chunks of the tile at rows [ks, ks + kKTile).
+template <int D, int NT, bool PAGED>
+__device__ __forceinline__ void tile_offsets(TileOffs<D, NT>& off, const KvView& kv, int b, int g,
+                                             int64_t unit_row0, int ks, int n) {
+  constexpr int CH = D / 8;
+#pragma unroll
+  for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
+    const int e = (int)threadIdx.x + j * NT;
+    const int r = (e / CH) % kKTile, c = e % CH;
+    const int p = min(ks + r, n - 1);
+    if constexpr (PAGED) off.e[j] = p;
+    else off.e[j] = (unit_row0 + p) * D + c * 8;
+  }
+}
+
+template <int D, int NT, bool PAGED>
+__device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const KvView& kv, int b, int g,
+                                          const TileOffs<D, NT>& off) {
+  const __bf16* kb = (const __bf16*)kv.k;
+  const __bf16* vb = (const __bf16*)kv.v;
   constexpr int CH = D / 8;
 #pragma unroll
   for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
     const int e = (int)threadIdx.x + j * NT;
     if (e >= kKTile * CH) break;
-    const int r = e / CH, c = e % CH;
-    const int p = min(ks + r, n - 1);
-    const int64_t off = (unit_row0 + p) * D + c * 8;
-    R.k[j] = *(const u32x4_t*)(kb + off);
-    R.v[j] = *(const u32x4_t*)(vb + off);
+    int64_t o = off.e[j];
+    if constexpr (PAGED) {
+      const int64_t row = kv_row_offset(kv, b, g, (int)o);
+      o = (row < 0 ? 0 : row) + (e % CH) * 8;
+    }
+    R.k[j] = *(const u32x4_t*)(kb + o);
+    R.v[j] = *(const u32x4_t*)(vb + o);
   }
 }
 
@@ -234,7 +263,7 @@ __device__ __forceinline__ void prefill_tile(const u32x4_t* sk, const u32x4_t* s
   }
 }
 
-template <int D, int QB>
+template <int D, int QB, bool PAGED>
 __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a) {
   constexpr int kQBlock = QB;
   constexpr int kThreads = QB / 16 * 64;
@@ -319,8 +348,6 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   const int tb0 = max(nsink, band_lo / kKTile), tb1 = qlast / kKTile;
   const int ntiles = nsink + (tb1 >= tb0 ? tb1 - tb0 + 1 : 0);
 
-  const __bf16* kb = (const __bf16*)a.kv.k;
-  const __bf16* vb = (const __bf16*)a.kv.v;
   const int64_t row0 = ((int64_t)b * a.kv.hkv + g) * a.kv.capacity;
   float m_run = -INFINITY, l_run = 0.f;
   f32x4_t o[DB];
@@ -335,11 +362,18 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   auto masked_tile = [&](int ks) {
     return ks > wlast || (ks >= a.sink && ks + kKTile - 1 < wvmin);
   };
-  if (ntiles > 0) tile_load<D, kThreads>(R, kb, vb, row0, tile_start(0), n);
+  // chunk offsets (positions for a paged cache) one tile ahead of the loads
+  TileOffs<D, kThreads> offs;
+  if (ntiles > 0) {
+    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(0), n);
+    tile_load<D, kThreads, PAGED>(R, a.kv, b, g, offs);
+    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(min(1, ntiles - 1)), n);
+  }
   for (int t = 0; t < ntiles; ++t) {
     tile_store<D, kThreads>(R, s_k[t & 1], s_v[t & 1]);
     __syncthreads();
-    tile_load<D, kThreads>(R, kb, vb, row0, tile_start(min(t + 1, ntiles - 1)), n);
+    tile_load<D, kThreads, PAGED>(R, a.kv, b, g, offs);  // tile t + 1 (the last one again at the end)
+    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(min(t + 2, ntiles - 1)), n);
     const int ks = tile_start(t);
     if (!masked_tile(ks))
       prefill_tile<D>(s_k[t & 1], s_v[t & 1], ks, qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
@@ -381,13 +415,21 @@ hipError_t launch_prefill(const PrefillLaunch& s, hipStream_t stream) {
   const int qb = wide ? kQBlockWide : kQBlockNarrow;
   const dim3 grid((unsigned)(((s.T + qb - 1) / qb) * units));
   const dim3 block(qb / 16 * 64);
+#define PRHS_PREFILL_LAUNCH(DV, PG)                                                           \
+  do {                                                                                       \
+    if (wide)                                                                                \
+      hipLaunchKernelGGL((attn_prefill_bf16<DV, kQBlockWide, PG>), grid, block, 0, stream, a); \
+    else                                                                                     \
+      hipLaunchKernelGGL((attn_prefill_bf16<DV, kQBlockNarrow, PG>), grid, block, 0, stream, a); \
+  } while (0)
   if (s.kv.d == 128) {
-    if (wide) hipLaunchKernelGGL((attn_prefill_bf16<128, kQBlockWide>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_prefill_bf16<128, kQBlockNarrow>), grid, block, 0, stream, a);
+    if (s.kv.paged) PRHS_PREFILL_LAUNCH(128, true);
+    else PRHS_PREFILL_LAUNCH(128, false);
   } else {
-    if (wide) hipLaunchKernelGGL((attn_prefill_bf16<64, kQBlockWide>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((attn_prefill_bf16<64, kQBlockNarrow>), grid, block, 0, stream, a);
+    if (s.kv.paged) PRHS_PREFILL_LAUNCH(64, true);
+    else PRHS_PREFILL_LAUNCH(64, false);
   }
+#undef PRHS_PREFILL_LAUNCH
   return hipGetLastError();
 }
 

@@ -423,8 +423,6 @@ prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_kv_data(kv)) != PRHS_OK) return st;
-  if (kv->layout != PRHS_KV_CONTIGUOUS)
-    return fail(PRHS_E_UNSUPPORTED, "prefill attention needs a contiguous cache");
   if (kv->dtype != PRHS_BF16)
     return fail(PRHS_E_UNSUPPORTED, "prefill attention is built for bf16 inputs");
   if (q_len < 0) return fail(PRHS_E_INVALID, "q_len must be >= 0 (got %d)", q_len);

@@ -186,7 +186,7 @@ struct GateLaunch {
 hipError_t launch_gate(const GateLaunch& a, hipStream_t stream);
 
 struct PrefillLaunch {
-  KvView kv;                  // contiguous bf16 cache holding the prompts
+  KvView kv;                  // bf16 cache (contiguous or paged) holding the prompts
   const void* q;              // [B][Hq][T][d]
   int T;
   const int32_t* vis_start;   // [T] or null

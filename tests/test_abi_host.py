@@ -269,7 +269,7 @@ def test_prefill_validation(L):
     assert pre(q=None) == B.PRHS_E_INVALID
     assert pre(out=None) == B.PRHS_E_INVALID
     assert pre(kv=_kv(dtype=B.PRHS_F32)) == B.PRHS_E_UNSUPPORTED
-    assert pre(kv=_kv(layout=B.PRHS_KV_PAGED, block_table=0xA000)) == B.PRHS_E_UNSUPPORTED
+    assert pre(kv=_kv(layout=B.PRHS_KV_PAGED, block_table=None)) == B.PRHS_E_INVALID
     assert pre(T=0, q=None, out=None) == B.PRHS_OK     # nothing to do, no device work
     kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
     assert pre(kv=kv0, q=None, out=None) == B.PRHS_OK

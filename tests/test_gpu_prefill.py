@@ -1,7 +1,8 @@
 """GPU parity of prefill attention under the PSAW mask (prhs_prefill_attn)
 against the oracle's prefill_attention: plain causal layers and pruning
 layers, GQA and MHA, d 64 and 128, ragged prompts (rows past a prompt are
-empty), query spans shorter than the prompt, and sampled rows of a full
+empty), query spans shorter than the prompt, contiguous and paged caches,
+and sampled rows of a full
 LLaMA-2-7B-shaped 4k prefill and of launches large enough to take the
 256-query blocks.  Outputs within 2e-3 of the fp64 oracle per
 (batch, head, query) row in the max norm, lse within 1e-4."""
@@ -36,13 +37,13 @@ def _queries(batch, hq, T, d, seed):
 
 
 def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None, sink=4,
-                seed=0, rows=None, heads=None):
+                seed=0, rows=None, heads=None, paged=False, page_size=16):
     """psaw = (l_s, phi, alpha) with layer / n_layers: vis_start from Eq. psaw."""
-    inp = synth.random_inputs(batch, hq, hkv, d, lens, seed=seed, device=DEV)
-    K, V = inp.K[0], inp.V[0]
-    cap = K.shape[2]
+    inp = synth.random_inputs(batch, hq, hkv, d, lens, seed=seed, device=DEV, paged=paged,
+                              page_size=page_size)
+    cap = inp.w.capacity
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
-    kv = B.KV(K, V, seq, cap, hq)
+    kv = B.KV(inp.K[0], inp.V[0], seq, cap, hq, inp.block_table)
     q = _queries(batch, hq, T, d, seed + 1).to(DEV)
     vis = None
     if psaw is not None:
@@ -54,7 +55,6 @@ def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None
     torch.cuda.synchronize()
     y, ls = out.cpu().numpy(), lse.cpu().numpy()
     qh = q.float().cpu().numpy()
-    Kh, Vh = K.float().cpu().numpy(), V.float().cpu().numpy()
     vis_h = None if vis is None else vis.cpu().numpy()
     if vis_h is not None:
         ref_vis = O.psaw_prefill_visible(layer, n_layers, T, sink, *psaw)
@@ -63,10 +63,12 @@ def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None
     worst = 0.0
     for b in range(batch):
         n = min(lens[b], T)
+        units = {g: synth.gather_unit(inp, 0, b, g, max(n, 1)) for g in range(hkv)}
         for h in (range(hq) if heads is None else heads):
             g = h // G
+            Kg, Vg = units[g]
             if rows is None:
-                yr, lr = O.prefill_attention(qh[b, h], Kh[b, g], Vh[b, g], n, sink=sink,
+                yr, lr = O.prefill_attention(qh[b, h], Kg, Vg, n, sink=sink,
                                              vis_start=vis_h, scale=scale)
                 check_rows = range(T)
             else:
@@ -76,8 +78,8 @@ def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None
                 for i in check_rows:
                     if i < n:
                         S = O.prefill_visible_set(i, sink, None if vis_h is None else int(vis_h[i]))
-                        yr[i], lr[i] = O.sparse_attention(qh[b, h, i], Kh[b, g, : i + 1],
-                                                          Vh[b, g, : i + 1], S, scale)
+                        yr[i], lr[i] = O.sparse_attention(qh[b, h, i], Kg[: i + 1],
+                                                          Vg[: i + 1], S, scale)
             for i in check_rows:
                 if i >= n:
                     assert np.all(y[b, h, i] == 0) and ls[b, h, i] == -np.inf, (b, h, i)
@@ -144,7 +146,24 @@ def test_prefill_wide_blocks_sampled(d):
                 seed=17 + d, rows=rows, heads=[0, 13, 31])
 
 
-def test_prefill_rejects_paged_and_fp32():
+def test_prefill_paged_psaw_gqa():
+    # a paged cache (16-token pages in a seeded random order), ragged prompts
+    run_prefill(2, 8, 2, 128, (777, 300), 777, psaw=(6, 0.3, 1.0), layer=7, n_layers=8, sink=4,
+                seed=21, paged=True)
+
+
+def test_prefill_paged_causal_d64_small_pages():
+    run_prefill(3, 4, 4, 64, (129, 64, 250), 250, sink=2, seed=23, paged=True, page_size=8)
+
+
+def test_prefill_paged_wide_blocks_sampled():
+    lens = (1024, 1000, 777, 1024, 600, 1024, 513, 1024)
+    rows = [0, 255, 256, 599, 776, 1023]
+    run_prefill(8, 32, 8, 128, lens, 1024, psaw=(6, 0.5, 1.0), layer=7, n_layers=8, sink=16,
+                seed=25, rows=rows, heads=[0, 31], paged=True)
+
+
+def test_prefill_rejects_fp32():
     inp = synth.random_inputs(1, 2, 2, 64, (40,), dtype="f32", seed=1, device=DEV)
     seq = torch.tensor((40,), dtype=torch.int32, device=DEV)
     kv = B.KV(inp.K[0], inp.V[0], seq, inp.K[0].shape[2], 2)
