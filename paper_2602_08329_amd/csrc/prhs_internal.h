@@ -73,37 +73,52 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP lane moves:
+// shifts by 1, 2, 4, 8 inside each row of 16 lanes (a lane without a source
+// adds 0), then lane 15 of each row into the next row (rows 1, 3) and lane
+// 31 into rows 2 and 3.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
+// 64-bit values here are always packed narrow counters whose sums stay
+// inside their fields, so the two 32-bit halves scan independently.
+__device__ __forceinline__ uint64_t wave_inclusive_scan(uint64_t x) {
+  const uint32_t lo = wave_inclusive_scan((uint32_t)x);
+  const uint32_t hi = wave_inclusive_scan((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // Exclusive prefix sum over a workgroup of BLOCK threads; `scratch` holds
 // BLOCK/64 + 1 elements of LDS.  Returns this thread's exclusive prefix and
 // the block total in *total.  Must be reached by every thread.  With T =
 // uint64_t, several narrow counters packed into one word scan together as
-// long as no field overflows.
+// long as no field overflows (and none straddles bit 32).
 template <int BLOCK, typename T = uint32_t>
 __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
+  constexpr int W = BLOCK / 64;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  T x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    T y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+  const T x = wave_inclusive_scan(v);
   if (lane == 63) scratch[wave] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    T run = 0;
-    for (int w = 0; w < BLOCK / 64; ++w) {
-      T t = scratch[w];
-      scratch[w] = run;
-      run += t;
-    }
-    scratch[BLOCK / 64] = run;
+  // every thread adds up the wave totals itself (broadcast LDS reads)
+  T before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    const T s = scratch[w];
+    before += w < wave ? s : (T)0;
+    tot += s;
   }
-  __syncthreads();
-  const T res = scratch[wave] + x - v;
-  *total = scratch[BLOCK / 64];
-  __syncthreads();
-  return res;
+  *total = tot;
+  __syncthreads();  // scratch may be written again after return
+  return before + x - v;
 }
 
 // ---------------------------------------------------------------------------
