@@ -4,23 +4,24 @@
 // attends the keys p <= i with p < C_sink or p >= vis_start[i]; without
 // vis_start every p <= i (plain causal attention, Eq. attn_eq per position).
 //
-// attn_prefill_bf16<D, QB>: one workgroup per (QB = 192 or 256 query
-// positions, batch, query head); wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the
-// 16 columns of its MFMA tiles, so a wave owns its queries' whole softmax
-// and writes their outputs itself.  Key tiles of 64 rows are loaded once
-// per workgroup (whole rows, one tile ahead of its use; the default cache
-// policy, since the unit's other query blocks read the same rows) into two
-// LDS buffers -- K row-major, V transposed so that each MFMA
-// operand is one 16-byte read -- and every wave computes
+// attn_prefill_bf16<D, QB, PAGED>: one workgroup per (QB = 192 or 256
+// query positions, batch, query head), over a contiguous or paged cache;
+// wave w takes the 16 queries q0 + 16w .. q0 + 16w + 15 as the 16 columns
+// of its MFMA tiles, so a wave owns its queries' whole softmax and writes
+// their outputs itself.  Key tiles of 64 rows are loaded once per workgroup
+// (whole rows, one tile ahead of their use; the default cache policy, since
+// the unit's other query blocks read the same rows) into two LDS buffers,
+// K and V both row-major, and every wave computes
 //   S^T (64 keys x 16 queries) = K_tile . Q^T   (v_mfma_f32_16x16x32_bf16, four 16-row blocks)
-//   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts, 32 keys per product)
-// with an online softmax per query (rescaled lazily).  A block visits only the key tiles that
-// meet its queries' visible ranges -- the sink [0, C_sink) and the band from
-// the smallest vis_start of its queries to its last query -- so tiles that
-// PSAW masks for every query of the block are never loaded: that is the
-// prefill work PSAW saves.  Inside the block a wave skips the tiles masked
-// for all of its queries and takes the per-(key, query) mask only on tiles
-// that some of its queries see in part.
+//   O^T (d x 16 queries)      += V_tile^T . P^T (P as bf16 hi + lo parts, 32 keys per product;
+//                                                the V^T operand by transposing LDS reads)
+// with an online softmax per query (rescaled lazily).  A block visits only
+// the key tiles that meet its queries' visible ranges -- the sink
+// [0, C_sink) and the band from the smallest vis_start of its queries to
+// its last query -- so tiles that PSAW masks for every query of the block
+// are never loaded: that is the prefill work PSAW saves.  Inside the block a
+// wave skips the tiles masked for all of its queries and takes the
+// per-(key, query) mask only on tiles that some of its queries see in part.
 // Blocks are ordered per XCD: each XCD takes whole (batch, head) units, a
 // unit's query blocks longest first (the last blocks see the most keys).
 #include "prhs_internal.h"
