@@ -212,6 +212,14 @@ __device__ __forceinline__ float max_over_groups(float v) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Sum over the same four lanes.
+__device__ __forceinline__ float sum_over_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 template <int DB>
 struct VRow;
 template <>
@@ -497,8 +505,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     }
   }
 
-  st.l += __shfl_xor(st.l, 16);
-  st.l += __shfl_xor(st.l, 32);
+  st.l = sum_over_groups(st.l);
   if (grp == 0) {
     sm_m[wave][col] = st.m;
     sm_l[wave][col] = st.l;
@@ -519,7 +526,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     float num = 0.f, den = 0.f;
     if (M != -INFINITY) {
       for (int w = 0; w < nwaves; ++w) {
-        const float f = exp2f(sm_m[w][h] - M);
+        const float f = __builtin_amdgcn_exp2f(sm_m[w][h] - M);
         num += f * ((const float*)(dyn + (size_t)w * wbytes))[h * (D + 1) + dim];
         den += f * sm_l[w][h];
       }
@@ -595,8 +602,8 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
     const float m_new = fmaxf(m_run, mt);
     float alpha = 1.f, p = 0.f;
     if (m_new != -INFINITY) {
-      alpha = exp2f(m_run - m_new);
-      p = row >= 0 ? exp2f(x - m_new) : 0.f;
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      p = row >= 0 ? __builtin_amdgcn_exp2f(x - m_new) : 0.f;
     }
     l_run = l_run * alpha + p;
 #pragma unroll
@@ -626,7 +633,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
     float num = 0.f, den = 0.f;
     if (M != -INFINITY) {
       for (int w = 0; w < nwaves; ++w) {
-        const float f = exp2f(sm_m[w] - M);
+        const float f = __builtin_amdgcn_exp2f(sm_m[w] - M);
         num += f * sm_o[w][dim];
         den += f * sm_l[w];
       }
@@ -683,12 +690,12 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
 #pragma unroll
     for (int k = 0; k < kMergePerThread; ++k) bm = fmaxf(bm, m[k]);
     if (bm != -INFINITY) {
-      const float r = exp2f(mx - bm);
+      const float r = __builtin_amdgcn_exp2f(mx - bm);
       num *= r;
       den *= r;
 #pragma unroll
       for (int k = 0; k < kMergePerThread; ++k) {
-        const float f = exp2f(m[k] - bm);
+        const float f = __builtin_amdgcn_exp2f(m[k] - bm);
         num += f * o[k];
         den += f * l[k];
       }
@@ -702,7 +709,7 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   if (lane == 0) s_max[wave] = wm;
   __syncthreads();
   const float M = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));
-  const float f = (mx == -INFINITY || M == -INFINITY) ? 0.f : exp2f(mx - M);
+  const float f = (mx == -INFINITY || M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mx - M);
   s_red[sg][dim] = num * f;
   if (dim == 0) s_den[sg] = den * f;
   __syncthreads();
