@@ -212,6 +212,20 @@ __device__ __forceinline__ float max_over_groups(float v) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Maximum over all 64 lanes, in every lane: rotations by 8, 4, 2 and 1
+// inside each row of 16 lanes (DPP row_ror), then across the four rows.
+__device__ __forceinline__ float wave_max(float v) {
+#define PRHS_ROR_MAX(CTRL)                                                                    \
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), \
+                                                          CTRL, 0xF, 0xF, false)))
+  PRHS_ROR_MAX(0x128);  // row_ror:8
+  PRHS_ROR_MAX(0x124);  // row_ror:4
+  PRHS_ROR_MAX(0x122);  // row_ror:2
+  PRHS_ROR_MAX(0x121);  // row_ror:1
+#undef PRHS_ROR_MAX
+  return max_over_groups(v);
+}
+
 // Sum over the same four lanes.
 __device__ __forceinline__ float sum_over_groups(float v) {
   const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -703,9 +717,7 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
     }
   }
   // block-wide maximum
-  float wm = mx;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) wm = fmaxf(wm, __shfl_xor(wm, off));
+  const float wm = wave_max(mx);
   if (lane == 0) s_max[wave] = wm;
   __syncthreads();
   const float M = fmaxf(fmaxf(s_max[0], s_max[1]), fmaxf(s_max[2], s_max[3]));

@@ -168,6 +168,14 @@ __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
   }
 }
 
+// A DPP lane move of a float inside each row of 16 lanes (every lane has a
+// source for the moves used here).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF,
+                                                    0xF, false));
+}
+
 // bf16 scoring on MFMA: per 16 keys, S[key][head] = K_tile(16 x d) . Q^T(d x 16)
 // with the group's g <= 16 query heads in the columns (unused columns zero).
 // Keys are loaded whole, d/8 lanes of 16 bytes per key (the operand order,
@@ -247,9 +255,15 @@ __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const 
     float v[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) v[e] = col < G ? acc[e] : -INFINITY;
-    for (int off = 1; off < gp; off <<= 1) {
+    // maximum over the group's gp columns (aligned lane groups inside a row
+    // of 16) by DPP lane moves: swaps of neighbours and of pairs in each
+    // quad, then the mirrors of each half row and of the row
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], __shfl_xor(v[e], off, 16));
+    for (int e = 0; e < 4; ++e) {
+      if (gp > 1) v[e] = fmaxf(v[e], dpp_f32<0xB1>(v[e]));   // quad_perm [1,0,3,2]
+      if (gp > 2) v[e] = fmaxf(v[e], dpp_f32<0x4E>(v[e]));   // quad_perm [2,3,0,1]
+      if (gp > 4) v[e] = fmaxf(v[e], dpp_f32<0x141>(v[e]));  // row_half_mirror
+      if (gp > 8) v[e] = fmaxf(v[e], dpp_f32<0x140>(v[e]));  // row_mirror
     }
     if (col == 0) {
 #pragma unroll
