@@ -37,16 +37,18 @@ def _queries(batch, hq, T, d, seed):
 
 
 def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None, sink=4,
-                seed=0, rows=None, heads=None, paged=False, page_size=16):
-    """psaw = (l_s, phi, alpha) with layer / n_layers: vis_start from Eq. psaw."""
+                seed=0, rows=None, heads=None, paged=False, page_size=16, vis=None):
+    """psaw = (l_s, phi, alpha) with layer / n_layers: vis_start from Eq. psaw;
+    or vis: any first visible positions ([T] int32 on the host)."""
     inp = synth.random_inputs(batch, hq, hkv, d, lens, seed=seed, device=DEV, paged=paged,
                               page_size=page_size)
     cap = inp.w.capacity
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
     kv = B.KV(inp.K[0], inp.V[0], seq, cap, hq, inp.block_table)
     q = _queries(batch, hq, T, d, seed + 1).to(DEV)
-    vis = None
-    if psaw is not None:
+    if vis is not None:
+        vis = torch.as_tensor(vis, dtype=torch.int32).to(DEV)
+    elif psaw is not None:
         vis = psaw_prefill_visible(layer, n_layers, T, sink, *psaw, device=DEV)
     out = torch.full((batch, hq, T, d), float("nan"), device=DEV)
     lse = torch.full((batch, hq, T), float("nan"), device=DEV)
@@ -56,7 +58,7 @@ def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None
     y, ls = out.cpu().numpy(), lse.cpu().numpy()
     qh = q.float().cpu().numpy()
     vis_h = None if vis is None else vis.cpu().numpy()
-    if vis_h is not None:
+    if psaw is not None:
         ref_vis = O.psaw_prefill_visible(layer, n_layers, T, sink, *psaw)
         assert np.array_equal(vis_h, ref_vis), "first visible positions differ from Eq. psaw"
     G = hq // hkv
@@ -88,7 +90,8 @@ def run_prefill(batch, hq, hkv, d, lens, T, psaw=None, layer=None, n_layers=None
                 e = np.abs(y[b, h, i] - yr[i]).max() / den
                 worst = max(worst, e)
                 assert e <= TOL, f"b{b} h{h} row {i}: rel err {e:.3e}"
-                assert abs(ls[b, h, i] - lr[i]) <= 1e-4 * max(1.0, abs(lr[i])), (b, h, i)
+                assert ls[b, h, i] == lr[i] or abs(ls[b, h, i] - lr[i]) <= 1e-4 * max(1.0, abs(lr[i])), \
+                    (b, h, i)
     print(f"prefill worst relative error {worst:.2e}")
     return worst
 
@@ -161,6 +164,19 @@ def test_prefill_paged_wide_blocks_sampled():
     rows = [0, 255, 256, 599, 776, 1023]
     run_prefill(8, 32, 8, 128, lens, 1024, psaw=(6, 0.5, 1.0), layer=7, n_layers=8, sink=16,
                 seed=25, rows=rows, heads=[0, 31], paged=True)
+
+
+@pytest.mark.parametrize("sink", [0, 5])
+def test_prefill_arbitrary_vis_start(sink):
+    # first visible positions that no schedule would give: below the sink,
+    # inside the causal range, past the query itself (with sink 0 some rows
+    # then attend nothing: y = 0, lse = -inf), in blocks that vary row to row
+    T = 450
+    rng = np.random.default_rng(31 + sink)
+    vis = rng.integers(0, T + 20, size=T)
+    vis[::7] = 0
+    vis[3::11] = np.arange(3, T, 11) + 1     # just past the query
+    run_prefill(2, 4, 2, 128, (450, 333), T, sink=sink, seed=33, vis=vis)
 
 
 def test_prefill_rejects_fp32():
