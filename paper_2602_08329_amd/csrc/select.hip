@@ -499,7 +499,7 @@ __device__ __forceinline__ void block_publish() {
 // list sel; digit equal to bl is kept, either as a 64-bit composite in the LDS
 // buffer `keep_lds` or in the global list `keep_glb`.  Returns the number
 // kept.  Every thread of the workgroup must call it.
-__device__ uint32_t split_candidates(const SelArgs& a, uint32_t* cnt, uint2* sel, const uint2* src,
+__device__ uint32_t split_candidates(const SelArgs& a, uint32_t* nsel, uint2* sel, const uint2* src,
                                      uint32_t count, int level, uint32_t bl, bool resolved,
                                      uint64_t* keep_lds, uint2* keep_glb, uint32_t* scan,
                                      uint32_t* s_base) {
@@ -523,7 +523,10 @@ __device__ uint32_t split_candidates(const SelArgs& a, uint32_t* cnt, uint2* sel
     const uint32_t packed = ((uint32_t)__popc(tmask) << 16) | (uint32_t)__popc(kmask);
     uint32_t total;
     const uint32_t pre = block_exclusive_scan<kFinishBlock>(packed, scan, &total);
-    if (tid == 0) *s_base = (total >> 16) ? atomicAdd(&cnt[0], total >> 16) : 0u;
+    if (tid == 0) {
+      *s_base = *nsel;
+      *nsel += total >> 16;
+    }
     __syncthreads();
     uint32_t ot = *s_base + (pre >> 16), ok = kept + (pre & 0xFFFFu);
 #pragma unroll
@@ -546,7 +549,7 @@ __device__ uint32_t split_candidates(const SelArgs& a, uint32_t* cnt, uint2* sel
 
 // Radix select to the end inside the global candidate lists (levels from
 // `level` to 4), for the rare rows whose ties do not fit LDS.
-__device__ void radix_global(const SelArgs& a, uint32_t* cnt, uint2* sel, uint2* src, uint2* dst,
+__device__ void radix_global(const SelArgs& a, uint32_t* nsel, uint2* sel, uint2* src, uint2* dst,
                              uint32_t count, uint32_t krem, int level, uint32_t* h, uint32_t* scan,
                              int* s_bin, uint32_t* s_krem, uint32_t* s_cnt, uint32_t* s_base) {
   const int tid = threadIdx.x;
@@ -570,7 +573,7 @@ __device__ void radix_global(const SelArgs& a, uint32_t* cnt, uint2* sel, uint2*
     const uint32_t bl = (uint32_t)*s_bin;
     const bool resolved = *s_cnt == *s_krem;
     const uint32_t krem_next = *s_krem;
-    const uint32_t kept = split_candidates(a, cnt, sel, src, count, level, bl, resolved, nullptr,
+    const uint32_t kept = split_candidates(a, nsel, sel, src, count, level, bl, resolved, nullptr,
                                            dst, scan, s_base);
     block_publish();
     if (resolved) break;
@@ -629,6 +632,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   __shared__ uint64_t scan64[kFinishBlock / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt, s_base;
+  __shared__ uint32_t s_nsel;  // entries in the row's output list sel (only this workgroup appends)
   const int row = blockIdx.x;
   if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv;
@@ -636,6 +640,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   const int tid = threadIdx.x;
   uint32_t* cnt = a.counters + row * 4;
   uint2* sel = a.sel + (size_t)row * a.selcap;
+  const uint32_t nsel0 = coherent_load(&cnt[0]);  // the filter's winners
   uint32_t n_lds = 0;  // staged ties in dyn[0, n_lds)
   // m from the budget before clamping to the middle range (floor(k / 3) by
   // default), clamped to the winners
@@ -651,7 +656,18 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   bool m_resolved0 = false;
 
   if (rg.kb > 0 && rg.kb < rg.m) {
-    for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
+    // both histograms and the candidate count in one memory latency
+    constexpr int HPT = kHistBins / kFinishBlock;
+    uint32_t h0[HPT], h1[HPT];
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) {
+      h0[j] = a.hist0[(size_t)row * kHistBins + tid + j * kFinishBlock];
+      h1[j] = a.hist1[(size_t)row * kHistBins + tid + j * kFinishBlock];
+    }
+    const uint32_t count0_all = coherent_load(&cnt[1]);
+    if (tid == 0) s_nsel = nsel0;
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) h[tid + j * kFinishBlock] = h0[j];
     __syncthreads();
     if (m0 > 0) {
       find_threshold<kFinishBlock>(h, m0, scan, &s_bin, &s_krem, &s_cnt);
@@ -665,7 +681,8 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     if (s_cnt != s_krem) {
       const uint32_t krem0 = s_krem;
       __syncthreads();
-      for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = a.hist1[(size_t)row * kHistBins + i];
+#pragma unroll
+      for (int j = 0; j < HPT; ++j) h[tid + j * kFinishBlock] = h1[j];
       __syncthreads();
       find_threshold<kFinishBlock>(h, krem0, scan, &s_bin, &s_krem, &s_cnt);
       b1 = s_bin;
@@ -673,9 +690,9 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       const uint32_t c1 = s_cnt;
       const bool resolved1 = c1 == krem1;
       const bool in_lds = !resolved1 && c1 + (uint32_t)rg.kb <= (uint32_t)a.sortcap;
-      const uint32_t count0 = min(coherent_load(&cnt[1]), (uint32_t)a.mcap);
+      const uint32_t count0 = min(count0_all, (uint32_t)a.mcap);
       uint2* cand2 = a.cand2 + (size_t)row * a.mcap;
-      const uint32_t kept = split_candidates(a, cnt, sel, a.cand + (size_t)row * a.mcap, count0, 1,
+      const uint32_t kept = split_candidates(a, &s_nsel, sel, a.cand + (size_t)row * a.mcap, count0, 1,
                                              b1, resolved1, in_lds ? dyn : nullptr, cand2, scan,
                                              &s_base);
       block_publish();
@@ -683,15 +700,17 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
         n_lds = kept;
       } else if (!resolved1) {
         b1 = -1;
-        radix_global(a, cnt, sel, cand2, a.cand + (size_t)row * a.mcap,
+        radix_global(a, &s_nsel, sel, cand2, a.cand + (size_t)row * a.mcap,
                      min(kept, (uint32_t)a.mcap), krem1, 2, h, scan, &s_bin, &s_krem, &s_cnt,
                      &s_base);
       }
     }
+  } else if (tid == 0) {
+    s_nsel = nsel0;
   }
   block_publish();
 
-  const uint32_t n_sel = rg.kb > 0 ? min(coherent_load(&cnt[0]), (uint32_t)a.selcap) : 0u;
+  const uint32_t n_sel = rg.kb > 0 ? min(s_nsel, (uint32_t)a.selcap) : 0u;
   const uint32_t total = n_sel + n_lds;
   for (uint32_t i = n_lds + tid; i < total; i += kFinishBlock) dyn[i] = composite(sel[i - n_lds]);
   __syncthreads();
