@@ -39,6 +39,34 @@ def attention_bytes(w, rows):
     return rows * (2 * w.d * e + 4) + w.batch * w.hq * w.d * e + w.batch * w.hq * (w.d + 1) * 4
 
 
+def dense_bytes(w, lens):
+    """Algorithmic bytes of one dense attention launch over sequences of the
+    given lengths: every cached K and V row once, the queries, y and lse."""
+    e = 4 if w.dtype == "f32" else 2
+    return (2 * w.hkv * w.d * e * int(sum(lens)) + w.batch * w.hq * w.d * e
+            + w.batch * w.hq * (w.d + 1) * 4)
+
+
+def torch_sum_gbps():
+    """A library read stream for reference: torch's sum over a 4 GiB fp32
+    tensor, 5 timed passes after one warm-up.  (The dense attention kernel,
+    which reads every cached K and V row once, is the faster stream; its rate
+    is reported as dense_gbps.)"""
+    import torch
+    x = torch.ones(1 << 30, dtype=torch.float32, device="cuda")
+    x.sum()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        x.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = 5 * x.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x
+    return round(gbps, 1)
+
+
 def middle_len(w, n0):
     se = min(w.sink, n0)
     return max(se, n0 - w.window) - se
@@ -542,7 +570,9 @@ def main():
         for l in range(run.L):
             run.attend(l, j)
     ms_attn, js_attn = timed(attn_only, "attention only", order=order)
-    ms_dense, _ = timed(run.dense_step, "dense attention")
+    ms_dense, js_dense = timed(run.dense_step, "dense attention")
+    dense_total = sum(run.L * dense_bytes(w, run.seq_lens[j].tolist()) for j in js_dense)
+    stream_gbps = torch_sum_gbps()
 
     # dominant kernel: the sparse attention launch.  Its average duration is
     # the back-to-back attention-only loop above (HIP events on the launch
@@ -585,6 +615,8 @@ def main():
         "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),
         "speedup_vs_dense": round(ms_dense / ms_sparse, 3),
         "dense_us_per_layer_step": round(ms_dense * 1e3 / (K_steps * L), 3),
+        "dense_gbps": round(dense_total / (ms_dense * 1e-3) / 1e9, 1),
+        "torch_sum_gbps": stream_gbps,
         "selection_us_per_layer_step": round(ms_sel * 1e3 / (K_steps * L), 3),
         "attention_us_per_layer_step": round(ms_attn * 1e3 / (K_steps * L), 3),
         "roofline": {
