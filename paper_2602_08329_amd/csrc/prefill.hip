@@ -44,6 +44,7 @@ constexpr int kQBlockNarrow = 192;
 constexpr int kWideMinGroupsPerCu = 4;
 constexpr int kKTile = 64;    // key rows per tile
 static_assert(kKTile % 32 == 0, "a tile is whole 32-key sub-tiles");
+static_assert(kKTile <= 64, "wave 0 looks up one tile row per lane (paged caches)");
 constexpr int kXcds = 8;      // accelerator dies, each with its own L2
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kLazyLog2 = 8.f;  // log2 of the largest probability between rescales
@@ -79,31 +80,48 @@ struct TileRegs {
   u32x4_t k[RPL], v[RPL];
 };
 
-// One thread's chunks of a tile: element offsets (contiguous cache), or
-// positions, resolved through the block table when the loads are issued
-// (paged cache; looking the pages up a tile earlier was slower).
+// One thread's chunks of a tile: element offsets.  For a paged cache the
+// row offsets of each tile come from LDS, where wave 0 stores them (one
+// block-table read per row) two tiles ahead of the loads.
 template <int D, int NT>
 struct TileOffs {
   int64_t e[TileRegs<D, NT>::RPL];
 };
 
-// This thread's chunks of the tile at rows [ks, ks + kKTile).
-template <int D, int NT, bool PAGED>
-__device__ __forceinline__ void tile_offsets(TileOffs<D, NT>& off, const KvView& kv, int b, int g,
-                                             int64_t unit_row0, int ks, int n) {
+// This thread's chunks of the tile at rows [ks, ks + kKTile) of a
+// contiguous cache.
+template <int D, int NT>
+__device__ __forceinline__ void tile_offsets(TileOffs<D, NT>& off, int64_t unit_row0, int ks, int n) {
   constexpr int CH = D / 8;
 #pragma unroll
   for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
     const int e = (int)threadIdx.x + j * NT;
     const int r = (e / CH) % kKTile, c = e % CH;
-    const int p = min(ks + r, n - 1);
-    if constexpr (PAGED) off.e[j] = p;
-    else off.e[j] = (unit_row0 + p) * D + c * 8;
+    off.e[j] = (unit_row0 + min(ks + r, n - 1)) * D + c * 8;
   }
 }
 
-template <int D, int NT, bool PAGED>
-__device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const KvView& kv, int b, int g,
+// The same from the tile's row offsets in LDS (paged cache).
+template <int D, int NT>
+__device__ __forceinline__ void tile_offsets_lds(TileOffs<D, NT>& off, const int64_t* rows) {
+  constexpr int CH = D / 8;
+#pragma unroll
+  for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
+    const int e = (int)threadIdx.x + j * NT;
+    off.e[j] = rows[(e / CH) % kKTile] + (e % CH) * 8;
+  }
+}
+
+// Element offset of the row of position min(pos, n - 1) of (b, kv head g) in
+// a paged cache (element 0 for a position outside the table's valid pages:
+// no access outside the cache).
+__device__ __forceinline__ int64_t paged_row(const KvView& kv, int b, int g, int pos, int n) {
+  const int64_t row = kv_row_offset(kv, b, g, min(pos, n - 1));
+  return row < 0 ? 0 : row;
+}
+
+template <int D, int NT>
+__device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const KvView& kv,
                                           const TileOffs<D, NT>& off) {
   const __bf16* kb = (const __bf16*)kv.k;
   const __bf16* vb = (const __bf16*)kv.v;
@@ -112,13 +130,8 @@ __device__ __forceinline__ void tile_load(TileRegs<D, NT>& R, const KvView& kv, 
   for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
     const int e = (int)threadIdx.x + j * NT;
     if (e >= kKTile * CH) break;
-    int64_t o = off.e[j];
-    if constexpr (PAGED) {
-      const int64_t row = kv_row_offset(kv, b, g, (int)o);
-      o = (row < 0 ? 0 : row) + (e % CH) * 8;
-    }
-    R.k[j] = *(const u32x4_t*)(kb + o);
-    R.v[j] = *(const u32x4_t*)(vb + o);
+    R.k[j] = *(const u32x4_t*)(kb + off.e[j]);
+    R.v[j] = *(const u32x4_t*)(vb + off.e[j]);
   }
 }
 
@@ -274,6 +287,7 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   __shared__ u32x4_t s_k[2][kKTile * CH];
   __shared__ u32x4_t s_v[2][kKTile * vrow_bytes<D>() / 16];
   __shared__ int s_vmin;
+  __shared__ int64_t s_rows[2][PAGED ? kKTile : 1];  // paged: row offsets of upcoming tiles
   // Workgroups go to the 8 XCDs round-robin by id; id L runs unit-major
   // slot (L mod 8) * (N / 8) + L / 8, so that each XCD works through its
   // own (batch, head) units one after another and a unit's K and V stay in
@@ -363,22 +377,44 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   auto masked_tile = [&](int ks) {
     return ks > wlast || (ks >= a.sink && ks + kKTile - 1 < wvmin);
   };
-  // chunk offsets (positions for a paged cache) one tile ahead of the loads
+  // chunk offsets one tile ahead of the loads (contiguous cache); for a
+  // paged cache wave 0 reads the block table for tile t + 2 while tile t is
+  // multiplied and stores the row offsets in LDS
   TileOffs<D, kThreads> offs;
-  if (ntiles > 0) {
-    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(0), n);
-    tile_load<D, kThreads, PAGED>(R, a.kv, b, g, offs);
-    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(min(1, ntiles - 1)), n);
+  if constexpr (PAGED) {
+    if (ntiles > 0 && wave == 0) {
+      s_rows[0][lane] = paged_row(a.kv, b, g, tile_start(0) + lane, n);
+      s_rows[1][lane] = paged_row(a.kv, b, g, tile_start(min(1, ntiles - 1)) + lane, n);
+    }
+    __syncthreads();
+    if (ntiles > 0) {
+      tile_offsets_lds<D, kThreads>(offs, s_rows[0]);
+      tile_load<D, kThreads>(R, a.kv, offs);
+    }
+  } else if (ntiles > 0) {
+    tile_offsets<D, kThreads>(offs, row0, tile_start(0), n);
+    tile_load<D, kThreads>(R, a.kv, offs);
+    tile_offsets<D, kThreads>(offs, row0, tile_start(min(1, ntiles - 1)), n);
   }
   for (int t = 0; t < ntiles; ++t) {
     tile_store<D, kThreads>(R, s_k[t & 1], s_v[t & 1]);
     __syncthreads();
-    tile_load<D, kThreads, PAGED>(R, a.kv, b, g, offs);  // tile t + 1 (the last one again at the end)
-    tile_offsets<D, kThreads, PAGED>(offs, a.kv, b, g, row0, tile_start(min(t + 2, ntiles - 1)), n);
+    int64_t prow = 0;
+    if constexpr (PAGED) {
+      // the table read is issued before the tile loads, so waiting for it
+      // later does not wait for them
+      if (wave == 0) prow = paged_row(a.kv, b, g, tile_start(min(t + 2, ntiles - 1)) + lane, n);
+      tile_offsets_lds<D, kThreads>(offs, s_rows[(t + 1) & 1]);
+    }
+    tile_load<D, kThreads>(R, a.kv, offs);  // tile t + 1 (the last one again at the end)
+    if constexpr (!PAGED)
+      tile_offsets<D, kThreads>(offs, row0, tile_start(min(t + 2, ntiles - 1)), n);
     const int ks = tile_start(t);
     if (!masked_tile(ks))
       prefill_tile<D>(s_k[t & 1], s_v[t & 1], ks, qf, qi, qvalid, my_vis, a.sink, a.scale_log2,
                       full_tile(ks), m_run, l_run, o);
+    if constexpr (PAGED)
+      if (wave == 0) s_rows[t & 1][lane] = prow;  // tile t + 2, read after the next barrier
   }
 
   // lane (col, grp) holds dims 16 blk + 4 grp .. 16 blk + 4 grp + 3 of query col
