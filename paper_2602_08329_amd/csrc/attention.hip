@@ -49,6 +49,9 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kRowsPerThread = 8;   // staged list entries per thread
 constexpr int kMaxSplits = 4096;
+// Sparse sets of at most this many rows per unit are not split: a launch of
+// one workgroup per unit beats a split launch plus its merge launch.
+constexpr int kNoSplitRows = 512;
 
 struct AttnArgs {
   KvView kv;
@@ -823,6 +826,7 @@ void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int 
   if (c < cmin) c = cmin;
   const long long threads = dtype == 1 ? 64LL * wave_limit() : 256;
   const long long cmax = threads * kRowsPerThread;
+  if (!dense && rows <= kNoSplitRows && rows <= cmax) c = rows;
   if (c > cmax) c = cmax;
   if (c < gran) c = gran;
   const long long ns = (rows + c - 1) / c;
