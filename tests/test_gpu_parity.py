@@ -151,6 +151,33 @@ def test_sparse_attention_oracle_sets(dtype, d, paged, hq, hkv, lens):
                          f"b{b} g{g} |S|={len(S)}")
 
 
+@pytest.mark.parametrize("dtype,set_cap", [("bf16", 512), ("bf16", 513), ("f32", 512), ("f32", 513)])
+def test_sparse_attention_unsplit_boundary(dtype, set_cap):
+    """Sets of at most 512 rows per unit run in one launch without a merge,
+    longer ones split across workgroups: both sides of that boundary, with
+    sets filling the capacity and shorter ones."""
+    lens = (700, 512, 90)
+    d, hq, hkv = (128, 8, 2) if dtype == "bf16" else (64, 4, 4)
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=False,
+                              seed=41, grid=False, key_scale=1.5, device=DEV)
+    rng = np.random.default_rng(11)
+    sets = {}
+    for b, n in enumerate(lens):
+        for g in range(hkv):
+            top = min(n, set_cap)
+            size = top if g == 0 else int(rng.integers(1, top + 1))
+            sets[(b, g)] = sorted(rng.choice(n, size=size, replace=False).tolist())
+    y, lse = run_sparse(inp, lens, sets, set_cap)
+    gq = hq // hkv
+    for (b, g), S in sets.items():
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, 0, b, g)
+        for j in range(gq):
+            yr, lr = O.sparse_attention(Qg[j], K, V, S)
+            assert_close(y[b, g * gq + j], lse[b, g * gq + j], yr, lr, TOL[dtype],
+                         f"b{b} g{g} |S|={len(S)}")
+
+
 def test_sparse_full_set_matches_dense_kernel():
     lens = (1500, 333)
     inp = synth.random_inputs(2, 8, 2, 128, lens, seed=31, grid=False, device=DEV)
