@@ -52,7 +52,6 @@ __all__ = [
     "budget_k",
     "dilation_m",
     "topk_middle",
-    "topk_layout",
     "anchor_set",
     "reuse_set",
     "is_refresh",
@@ -198,14 +197,6 @@ def topk_middle(sigma, n0, k, sink, window):
     sc = _f64(sigma)[pos]
     order = np.lexsort((pos, -sc))  # primary: -score, secondary: position
     return pos[order][: min(k, pos.size)]
-
-
-def topk_layout(s_star, m):
-    """S* as the library lays it out: its m highest-ranked members, then the
-    rest, each part in ascending position order.  s_star is in rank order
-    (score descending, position ascending)."""
-    s_star = np.asarray(s_star, dtype=np.int64)
-    return np.concatenate([np.sort(s_star[:m]), np.sort(s_star[m:])])
 
 
 def anchor_set(s_star, n0, sink, window):

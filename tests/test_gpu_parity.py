@@ -13,6 +13,7 @@ import pytest
 import torch
 
 import oracle as O
+from tests.compare import topk_layout
 from paper_2602_08329_amd import binding as B
 from paper_2602_08329_amd import synth
 
@@ -227,7 +228,7 @@ def check_select(inp, lens, p, layer=0, step=0):
     for (b, g), (S, C) in ref.items():
         assert tlen[b, g] == len(S), f"b{b} g{g}: topk_len {tlen[b, g]} != {len(S)}"
         kb = O.budget_k(lens[b], p.k, p.k_num, p.k_den)
-        expect = O.topk_layout(S, O.dilation_m(kb, len(S), p.dilate_m))
+        expect = topk_layout(S, O.dilation_m(kb, len(S), p.dilate_m))
         assert np.array_equal(topk[b, g, : len(S)], expect), f"b{b} g{g}: top-k differs"
         assert slen[b, g] == len(C), f"b{b} g{g}: set_len {slen[b, g]} != {len(C)}"
         assert np.array_equal(sidx[b, g, : len(C)], C), f"b{b} g{g}: anchor set differs"
@@ -320,7 +321,7 @@ def check_select_shared(inp, lens, p):
     for (b, g), (S, C) in oracle_select(inp, lens, p).items():
         kb = O.budget_k(lens[b], p.k, p.k_num, p.k_den)
         m = O.dilation_m(kb, len(S), p.dilate_m)
-        assert tlen[b, g] == len(S) and np.array_equal(topk[b, g, : len(S)], O.topk_layout(S, m))
+        assert tlen[b, g] == len(S) and np.array_equal(topk[b, g, : len(S)], topk_layout(S, m))
         assert slen[b, g] == len(C) and np.array_equal(sidx[b, g, : len(C)], C)
         R = O.reuse_set(S, m, p.dilate_r, lens[b], lens[b], p.sink, p.window)
         assert hlen[b, g] == len(R), f"b{b} g{g}: shared_len {hlen[b, g]} != {len(R)}"

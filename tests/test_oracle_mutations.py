@@ -95,6 +95,26 @@ def _psaw_zero_based_layer(layer, n_layers, t, l_s, phi, alpha):
     return int(math.floor((1.0 - phi ** e) * t))
 
 
+def _mi_without_factor_2(delta, L):
+    return M.binary_entropy(delta) + delta * math.log(L)
+
+
+def _mi_in_bits(delta, L):
+    h = 0.0 if delta <= 0.0 or delta >= 1.0 else (
+        -delta * math.log2(delta) - (1 - delta) * math.log2(1 - delta))
+    return 2.0 * (h + delta * math.log2(L))
+
+
+def _binary_entropy_one_term(x):
+    return 0.0 if x <= 0.0 or x >= 1.0 else -x * math.log(x)
+
+
+def _budget_ceil(n0, k=None, k_num=0, k_den=0):
+    if k_den and k_den > 0:
+        return (k_num * n0 + k_den - 1) // k_den
+    return int(k)
+
+
 _orig = {name: getattr(M, name) for name in
          ["dense_attention", "topk_middle", "reuse_set", "ranking_scores",
           "region_bounds", "dilation_m", "is_refresh"]}
@@ -128,6 +148,10 @@ MUTANTS = [
     ("psaw_boundary", _psaw_zero_based_layer),
     ("psaw_prefill_visible", _prefill_vis_at_i),
     ("prefill_visible_set", _prefill_set_inclusive_mask),
+    ("mi_loss_bound", _mi_without_factor_2),
+    ("mi_loss_bound", _mi_in_bits),
+    ("binary_entropy", _binary_entropy_one_term),
+    ("budget_k", _budget_ceil),
 ]
 
 

@@ -15,6 +15,7 @@ import pytest
 import torch
 
 import oracle as O
+from tests.compare import topk_layout
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_budgets.json")
 
@@ -418,6 +419,64 @@ def test_mi_bound_monotone_on_restricted_domain():
     assert O.mi_loss_bound(0.0, 100) == 0.0
 
 
+def test_binary_entropy_closed_forms_and_library():
+    # h_b in nats: h_b(1/2) = ln 2, h_b(1/4) = 2 ln 2 - (3/4) ln 3, symmetric
+    # about 1/2, and equal to scipy's Shannon entropy of the pmf (x, 1 - x)
+    from scipy.stats import entropy
+    assert O.binary_entropy(0.5) == pytest.approx(math.log(2), abs=1e-15)
+    assert O.binary_entropy(0.25) == pytest.approx(2 * math.log(2) - 0.75 * math.log(3), abs=1e-15)
+    for x in (1e-6, 0.01, 0.3, 0.77, 0.999):
+        assert O.binary_entropy(x) == pytest.approx(O.binary_entropy(1 - x), abs=1e-15)
+        assert O.binary_entropy(x) == pytest.approx(float(entropy([x, 1 - x])), rel=1e-13)
+    assert O.binary_entropy(0.0) == 0.0 and O.binary_entropy(1.0) == 0.0
+
+
+def test_mi_bound_closed_forms():
+    # Eq. mi_bound, g(d) = 2 [h_b(d) + d ln L], with entropy and log in the
+    # same base (nats).  Hand values: d = 1/2, L = 2 gives 2 (ln 2 + ln 2 / 2)
+    # = 3 ln 2; d = 1/4, L = 8 gives 2 (2 ln 2 - 3/4 ln 3 + 3/4 ln 2).
+    assert O.mi_loss_bound(0.5, 2) == pytest.approx(3 * math.log(2), abs=1e-14)
+    assert O.mi_loss_bound(0.25, 8) == pytest.approx(
+        2 * (2.75 * math.log(2) - 0.75 * math.log(3)), abs=1e-14)
+    # h_b(d) + d ln L is maximised where its derivative ln((1 - d) / d) + ln L
+    # vanishes, at d = L / (1 + L) (the end of the footnote's domain), and the
+    # maximum is ln(1 + L): so g peaks at 2 ln(1 + L) there and nowhere higher
+    for L in (2, 7, 100, 4096, 131072):
+        d_star = L / (1 + L)
+        assert O.mi_loss_bound(d_star, L) == pytest.approx(2 * math.log1p(L), rel=1e-13)
+        xs = np.linspace(1e-6, 1 - 1e-6, 997)
+        assert max(O.mi_loss_bound(x, L) for x in xs) <= 2 * math.log1p(L) + 1e-12
+
+
+def test_mi_bound_dominates_entropy_continuity():
+    # the bound's building block (entropy continuity, MI-bound appendix,
+    # Step 2): |H(P) - H(Q)| <= h_b(eps) + eps ln m for pmfs on m <= L
+    # symbols with TV distance eps; so g(eps) / 2 bounds it for random pairs
+    from scipy.stats import entropy
+    rng = np.random.default_rng(40)
+    for _ in range(300):
+        m = int(rng.integers(2, 40))
+        P = rng.dirichlet(np.ones(m))
+        Q = rng.dirichlet(np.ones(m) * rng.uniform(0.2, 5))
+        eps = O.tv_distance(P, Q)
+        if eps >= m / (1 + m):
+            continue
+        gap = abs(float(entropy(P)) - float(entropy(Q)))
+        assert gap <= O.mi_loss_bound(eps, m) / 2 + 1e-12
+
+
+def test_proportional_budget_closed_forms():
+    # reading of the throughput sweep's "top-k 5% of each sequence's length":
+    # k_b = floor(n0 / 20), integer arithmetic, recomputed per refresh
+    cases = {1000: 50, 1019: 50, 1020: 51, 8192: 409, 16368: 818, 19: 0, 20: 1, 0: 0}
+    for n0, kb in cases.items():
+        assert O.budget_k(n0, k_num=1, k_den=20) == kb
+    # 3/64 of n0 and a fixed budget
+    assert O.budget_k(4096, k_num=3, k_den=64) == 192
+    assert O.budget_k(4095, k_num=3, k_den=64) == 191
+    assert O.budget_k(4096, k=256) == 256 and O.budget_k(10, k=256) == 256
+
+
 # ---------------------------------------------------------------- schedule
 
 def test_retrieval_ratio_closed_form():
@@ -455,7 +514,7 @@ def test_topk_layout_partitions_by_rank_then_position():
     sigma = rng.integers(-5, 6, size=300).astype(float)
     S = O.topk_middle(sigma, 300, 40, 4, 16)
     for m in (0, 1, 13, 40):
-        lay = O.topk_layout(S, m)
+        lay = topk_layout(S, m)
         assert sorted(lay.tolist()) == sorted(S.tolist())
         assert set(lay[:m].tolist()) == set(S[:m].tolist())
         assert list(lay[:m]) == sorted(lay[:m]) and list(lay[m:]) == sorted(lay[m:])
