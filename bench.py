@@ -120,7 +120,9 @@ def record_step(run, j, gated):
             pool, plen, tail = run.set_for(l, j)
             pool, plen = pool.reshape(-1, pool.shape[-1]), plen.reshape(-1)
             utail = seq if tail is None else tail.repeat_interleave(w.hkv)
-        start = run.psaw_start.get((l, j))
+        start = run.psaw_start(l, j)
+        if start is not None:
+            start = torch.tensor(start, dtype=torch.int32, device=pool.device)
         if start is None:
             rows[l] = int((plen + (seq - utail)).sum())
         else:
@@ -262,7 +264,7 @@ def prefill_main(args):
     import torch
 
     from paper_2602_08329_amd import binding as B
-    from paper_2602_08329_amd.schedule import capture_steps, psaw_defaults, psaw_prefill_visible
+    from paper_2602_08329_amd.schedule import capture_steps, psaw_defaults, psaw_layers
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -301,16 +303,18 @@ def prefill_main(args):
         kvs = [B.KV(paged(Ks[l]), paged(Vs[l]), seq, T, H, table) for l in range(L)]
     else:
         kvs = [B.KV(Ks[l], Vs[l], seq, T, H) for l in range(L)]
-    vis = [psaw_prefill_visible(l, L, T, sink, l_s, phi, alpha, device=dev) if l + 1 >= l_s
-           else None for l in range(L)]
+    ps = psaw_layers(L, sink, (l_s, phi, alpha))
+    # first visible position of every query row of the masking layers, from
+    # the library's Eq. psaw (for the useful-flop count and the CPU leg)
+    vis = [np.array([B.prhs_psaw_first_visible(ps[l], i + 1) for i in range(T)], dtype=np.int64)
+           if l in ps else None for l in range(L)]
     out = torch.empty(Bsz, H, T, d, device=dev)
     lse = torch.empty(Bsz, H, T, device=dev)
     scale = 1.0 / math.sqrt(d)
 
     def step(psaw):
         for l in range(L):
-            B.prhs_prefill_attn(kvs[l], qs[l], scale, out, lse,
-                                vis_start=vis[l] if psaw else None, sink=sink)
+            B.prhs_prefill_attn(kvs[l], qs[l], scale, out, lse, psaw=ps.get(l) if psaw else None)
 
     def timed(psaw, label):
         for _ in range(W_steps):
@@ -335,7 +339,7 @@ def prefill_main(args):
         return ms
 
     workload = f"llama2-7b-prefill-b{Bsz}-{T}" + ("-paged" if args.paged else "")
-    ms_psaw = timed(True, "prefill, PSAW on layers >= l_s")
+    ms_psaw = timed(True, "prefill, PSAW on layers > l_s")
     ms_causal = timed(False, "prefill, all layers causal")
     # useful flops: visible (query, key) pairs x 4 d, per head and prompt
     i = np.arange(T, dtype=np.int64)
@@ -345,7 +349,7 @@ def prefill_main(args):
         if vis[l] is None:
             pairs += pairs_causal
         else:
-            v = vis[l].cpu().numpy().astype(np.int64)
+            v = vis[l]
             se = np.minimum(sink, i + 1)
             pairs += int((se + (i + 1 - np.maximum(v, se))).sum())
     flops = 4.0 * d * H * Bsz * pairs
@@ -405,7 +409,7 @@ def prefill_cpu_baseline(qs, Ks, Vs, vis, T, sink, scale, L, H, Bsz, budget_s):
             q = qs[l][0, 0].float().cpu().numpy()
             K = Ks[l][0, 0].float().cpu().numpy()
             V = Vs[l][0, 0].float().cpu().numpy()
-            v = None if vis[l] is None else vis[l].cpu().numpy()
+            v = vis[l]
             # rows sampled evenly until the time budget is half spent
             step = max(1, T // 256)
             t0 = time.perf_counter()

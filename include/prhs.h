@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define PRHS_ABI_VERSION 1
+#define PRHS_ABI_VERSION 2
 
 typedef enum prhs_status {
   PRHS_OK = 0,
@@ -97,6 +97,29 @@ typedef struct prhs_params {
   int32_t layer_group;    /* G >= 1: layers l with l % G == 0 anchor their group */
 } prhs_params;
 
+/* Progressive sliding attention window of one layer (Sec. 4.2, Eq. psaw).
+ * For the layer with 0-based index `layer` of a model with `num_layers`
+ * layers, Eq. psaw's 1-based layer is l = layer + 1 and, at t tokens in view,
+ *   P_l(t) = floor((1 - phi^(alpha (l - l_s) / (N - l_s))) t)  for l >= l_s,
+ *   P_l(t) = 0                                                  otherwise.
+ * The window masks the 1-based positions strictly between C_sink and P, i.e.
+ * the 0-based range [sink, P - 1): the visible keys are
+ *   [0, min(sink, t)) U [first_visible, t),
+ *   first_visible = max(min(sink, t), P_l(t) - 1).
+ * The library evaluates the factor 1 - phi^e once per call on the host in
+ * binary64 (C pow) and P = floor(factor * t) in binary64 wherever it needs
+ * it, host or device, so every position agrees with the same formula
+ * evaluated in binary64.  Sec. 5.1's defaults: l_s = floor(3N/4), phi = 0.7,
+ * alpha = 1. */
+typedef struct prhs_psaw {
+  int32_t layer;       /* 0 <= layer < num_layers (0-based) */
+  int32_t num_layers;  /* N >= 1 */
+  int32_t l_s;         /* pruning depth, 1-based: 0 <= l_s < N */
+  int32_t sink;        /* C_sink >= 0 */
+  double phi;          /* 0 < phi <= 1 */
+  double alpha;        /* alpha >= 0, finite */
+} prhs_psaw;
+
 enum {
   PRHS_OP_SELECT = 0,
   PRHS_OP_DILATE_REUSE = 1,
@@ -106,9 +129,12 @@ enum {
 
 enum { PRHS_REUSE = 0, PRHS_REFRESH = 1 };
 
-/* Largest sort buffer of the top-k stage: k_b is clamped to the middle range
- * length, and the clamped value must not exceed this. */
-#define PRHS_MAX_TOPK 16384
+/* Largest top-k budget the selection supports: k_b, after clamping to the
+ * middle range length, must not exceed this (PRHS_E_UNSUPPORTED otherwise).
+ * For middle ranges beyond one CU's LDS the selection keeps the k_b winners
+ * as 8-byte (score, position) pairs in LDS next to its bitmap segment, which
+ * bounds k_b. */
+#define PRHS_MAX_TOPK 16000
 
 /* ABI version of the loaded library (PRHS_ABI_VERSION). */
 int32_t prhs_abi_version(void);
@@ -135,6 +161,13 @@ prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params
  * opens a block of refresh_every steps and `layer` opens a group of
  * layer_group layers, else PRHS_REUSE.  -1 on bad arguments. */
 int32_t prhs_schedule(int32_t step, int32_t layer, const prhs_params* params);
+
+/* Eq. psaw (Sec. 4.2): the first visible non-sink 0-based position of the
+ * layer described by `psaw` when n tokens are in view (a decode step at
+ * length n, or the prefill query at position n - 1), as defined at
+ * prhs_psaw.  Host function.  -1 when psaw is NULL or invalid or n < 0
+ * (prhs_last_error() then says why). */
+int32_t prhs_psaw_first_visible(const prhs_psaw* psaw, int32_t n);
 
 /* Refresh: score, top-k and anchor set for one layer (Sec. 4.1 Selection
  * Criteria; top-k oracle of Sec. 2.3).
@@ -246,30 +279,28 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q,
  * attention window (Sec. 4.2, Eq. psaw: the window narrows during prefill as
  * well as decoding).  For every (b, query head h) with g = h / (Hq/Hkv) and
  * every query position i < min(seq_lens[b], q_len), the query at position i
- * attends the keys
- *   S_i = {p <= i : p < sink  or  p >= vis_start[i]}
- * of kv head g (with vis_start NULL, S_i = [0, i]: plain causal attention);
- * y_i = sum_{p in S_i} softmax(scale * q_i . k_p) v_p and lse_i as in
- * prhs_sparse_decode_attn.  For a layer of a model with N layers, the
- * window's first visible position at query i is Eq. psaw taken at
- * t = i + 1 (the tokens in view), so vis_start[i] = max(min(sink, i + 1),
- * P_l(i + 1) - 1) in 0-based positions.  Query rows at positions
- * >= seq_lens[b] (and < q_len) give
- * y = 0 and lse = -inf.
+ * attends the keys of kv head g
+ *   S_i = {p <= i : p < sink  or  p >= first_visible(i + 1)}
+ * where the query at position i has the t = i + 1 tokens [0, i] in view and
+ * first_visible(t) is that of prhs_psaw (the same set a decode step at
+ * length i + 1 attends).  With psaw NULL, S_i = [0, i]: plain causal
+ * attention (Eq. attn_eq per position).  y_i = sum_{p in S_i} softmax(scale *
+ * q_i . k_p) v_p and lse_i as in prhs_sparse_decode_attn.  Query rows at
+ * positions >= seq_lens[b] (and < q_len) give y = 0 and lse = -inf.
  * kv:        bf16 cache (contiguous or paged) holding the prompt of
  *            sequence b at positions [0, seq_lens[b]) (fp32 inputs give
  *            PRHS_E_UNSUPPORTED).
  * q:         [batch][num_q_heads][q_len][head_dim] bf16 device array; row i is
  *            the query at position i.
- * vis_start: [q_len] int32 device array or NULL.
+ * psaw:      host descriptor of the layer's window, or NULL (causal).
  * scale:     softmax scale, positive and finite (PRHS_E_INVALID otherwise).
  * out:       [batch][num_q_heads][q_len][head_dim] fp32; lse:
  *            [batch][num_q_heads][q_len] fp32 or NULL.
  * No workspace.  Caller owns every buffer; ceil(q_len / 64) * batch * num_q_heads
  * must be below 2^31 (PRHS_E_UNSUPPORTED otherwise). */
 prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
-                              const int32_t* vis_start, int32_t sink, float scale, float* out,
-                              float* lse, void* stream);
+                              const prhs_psaw* psaw, float scale, float* out, float* lse,
+                              void* stream);
 
 /* Dense decode attention over every cached key [0, seq_lens[b]) (Eq. attn_eq):
  * the baseline the sparse path is measured against, and the k = n special
@@ -333,24 +364,22 @@ prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_param
 /* Token-sparse decode attention where every (b, kv head g) attends its own
  * row of a set pool plus a decoded tail (Def. 3.1 and 3.2, Sec. 2.2),
  * optionally under the progressive sliding attention window (Sec. 4.2,
- * Eq. psaw): with r = unit_row[u], n = seq_lens[b] and
- * t0 = clamp(unit_tail[u], 0, n),
+ * Eq. psaw; CIS + PSAW is the paper's CPE): with r = unit_row[u],
+ * n = seq_lens[b] and t0 = clamp(unit_tail[u], 0, n),
  *   S = {i in pool_idx[r][0 .. min(pool_len[r], set_cap)) : i < t0} U [t0, n),
- * minus, when psaw_start is given, the positions in
- * [psaw_sink, psaw_start[b]) (the layer's masked range; psaw_start[b] is the
- * first visible non-sink position), and the outputs of
+ * minus, when psaw is given, the positions in [psaw->sink, first_visible(n))
+ * (the layer's masked range at length n, prhs_psaw), and the outputs of
  * prhs_sparse_decode_attn over S.  A row outside [0, pool_rows) gives an
  * empty set.  pool_idx: [pool_rows][set_cap] int32; unit_row, unit_tail:
  * [B*Hkv] int32 (prhs_gate's row_anchor or row_other, and tail; or the
  * identity rows and per-unit anchor lengths of the fixed schedule's sets);
- * psaw_start: [B] int32 or NULL.  Precondition: pool_len[r] + n - t0 <=
+ * psaw: host descriptor or NULL.  Precondition: pool_len[r] + n - t0 <=
  * set_cap.  ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
                                   const int32_t* unit_row, const int32_t* unit_tail,
-                                  const int32_t* psaw_start, int32_t psaw_sink, float scale,
-                                  float* out, float* lse, void* ws, size_t ws_bytes,
-                                  void* stream);
+                                  const prhs_psaw* psaw, float scale, float* out, float* lse,
+                                  void* ws, size_t ws_bytes, void* stream);
 
 /* Message for the last non-OK status returned on the calling thread. */
 const char* prhs_last_error(void);

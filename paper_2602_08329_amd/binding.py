@@ -1,8 +1,10 @@
 """ctypes binding of libprhs (include/prhs.h).
 
-Argument marshalling only: tensors are checked for device, dtype, shape and
-contiguity, then their data pointers and the current HIP stream are handed to
-the C ABI.  Every step of the hot path runs in the library's HIP kernels; there
+Argument marshalling only: every tensor is checked for dtype, contiguity and
+its exact shape against the cache descriptor, and for living on the cache's
+GPU, before its data pointer and the current HIP stream are handed to the C
+ABI (so a wrongly shaped or host tensor raises ValueError instead of reaching
+a kernel).  Every step of the hot path runs in the library's HIP kernels; there
 is no fallback.  ``lib()`` raises when the library has not been built.
 """
 
@@ -34,13 +36,13 @@ PRHS_OP_DENSE_ATTN = 3
 
 PRHS_REUSE = 0
 PRHS_REFRESH = 1
-PRHS_MAX_TOPK = 16384
+PRHS_MAX_TOPK = 16000
 
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
     "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_select_gated",
-    "prhs_pool_decode_attn", "prhs_prefill_attn", "prhs_last_error",
+    "prhs_pool_decode_attn", "prhs_prefill_attn", "prhs_psaw_first_visible", "prhs_last_error",
 ]
 
 
@@ -63,6 +65,13 @@ class PrhsParams(ctypes.Structure):
         ("sink", ctypes.c_int32), ("window", ctypes.c_int32),
         ("dilate_m", ctypes.c_int32), ("dilate_r", ctypes.c_int32),
         ("refresh_every", ctypes.c_int32), ("layer_group", ctypes.c_int32),
+    ]
+
+
+class PrhsPsaw(ctypes.Structure):
+    _fields_ = [
+        ("layer", ctypes.c_int32), ("num_layers", ctypes.c_int32), ("l_s", ctypes.c_int32),
+        ("sink", ctypes.c_int32), ("phi", ctypes.c_double), ("alpha", ctypes.c_double),
     ]
 
 
@@ -117,10 +126,12 @@ def lib():
         L.prhs_select_gated.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, vp, i32, vp, vp, i32,
                                         vp, vp, vp, sz, vp]
         L.prhs_pool_decode_attn.restype = i32
-        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, vp, i32,
+        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, P(PrhsPsaw),
                                             ctypes.c_float, vp, vp, vp, sz, vp]
         L.prhs_prefill_attn.restype = i32
-        L.prhs_prefill_attn.argtypes = [P(PrhsKv), vp, i32, vp, i32, ctypes.c_float, vp, vp, vp]
+        L.prhs_prefill_attn.argtypes = [P(PrhsKv), vp, i32, P(PrhsPsaw), ctypes.c_float, vp, vp, vp]
+        L.prhs_psaw_first_visible.restype = i32
+        L.prhs_psaw_first_visible.argtypes = [P(PrhsPsaw), i32]
         L.prhs_last_error.restype = ctypes.c_char_p
         L.prhs_last_error.argtypes = []
         _lib = L
@@ -137,8 +148,25 @@ def params(k=0, sink=4, window=0, dilate_m=-1, dilate_r=1, refresh_every=1, laye
     return PrhsParams(k, k_num, k_den, sink, window, dilate_m, dilate_r, refresh_every, layer_group)
 
 
+def psaw(layer, num_layers, l_s, phi, alpha, sink):
+    """Descriptor of one layer's progressive sliding attention window (Eq. psaw)."""
+    return PrhsPsaw(int(layer), int(num_layers), int(l_s), int(sink), float(phi), float(alpha))
+
+
+def prhs_psaw_first_visible(ps, n):
+    """First visible non-sink position of the window `ps` with n tokens in view."""
+    v = lib().prhs_psaw_first_visible(ctypes.byref(ps), int(n))
+    if v < 0:
+        raise PrhsError(PRHS_E_INVALID, lib().prhs_last_error().decode())
+    return v
+
+
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _ref(x):
+    return None if x is None else ctypes.byref(x)
 
 
 def _stream(stream):
@@ -147,7 +175,8 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _need(t, dtype, name, dims=None):
+def _need(t, dtype, name, shape=None, dims=None):
+    """Type, dtype, contiguity and shape (exact `shape`, or `dims` dimensions)."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a tensor")
     if t.dtype != dtype:
@@ -156,6 +185,18 @@ def _need(t, dtype, name, dims=None):
         raise ValueError(f"{name} must be contiguous")
     if dims is not None and t.dim() != dims:
         raise ValueError(f"{name} must have {dims} dims, got {t.dim()}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _on_device(device, **tensors):
+    """Every given tensor lives on `device`, a GPU (checked after the shapes,
+    just before the launch)."""
+    if device.type != "cuda":
+        raise ValueError(f"the cache lives on {device}; the library runs on the GPU")
+    for name, t in tensors.items():
+        if t is not None and t.device != device:
+            raise ValueError(f"{name} is on {t.device}, the cache on {device}")
 
 
 class KV:
@@ -166,11 +207,9 @@ class KV:
     def __init__(self, K, V, seq_lens, max_seq_len, num_q_heads, block_table=None):
         if K.dtype not in (torch.float32, torch.bfloat16) or V.dtype != K.dtype:
             raise ValueError("K and V must both be float32 or bfloat16")
-        _need(K, K.dtype, "K", 4)
-        _need(V, K.dtype, "V", 4)
-        if V.shape != K.shape:
-            raise ValueError("K and V shapes differ")
-        _need(seq_lens, torch.int32, "seq_lens", 1)
+        _need(K, K.dtype, "K", dims=4)
+        _need(V, K.dtype, "V", shape=K.shape)
+        _need(seq_lens, torch.int32, "seq_lens", dims=1)
         self._keep = (K, V, seq_lens, block_table)
         d = K.shape[3]
         dt = PRHS_F32 if K.dtype == torch.float32 else PRHS_BF16
@@ -179,7 +218,7 @@ class KV:
             self.c = PrhsKv(B, num_q_heads, Hkv, d, dt, PRHS_KV_CONTIGUOUS, cap, 0, 0, 0,
                             K.data_ptr(), V.data_ptr(), None, seq_lens.data_ptr(), max_seq_len)
         else:
-            _need(block_table, torch.int32, "block_table", 2)
+            _need(block_table, torch.int32, "block_table", dims=2)
             P, Hkv, ps, _ = K.shape
             B, max_pages = block_table.shape
             self.c = PrhsKv(B, num_q_heads, Hkv, d, dt, PRHS_KV_PAGED, 0, ps, max_pages, P,
@@ -188,6 +227,23 @@ class KV:
         if seq_lens.numel() != self.c.batch:
             raise ValueError("seq_lens must have one entry per sequence")
         self.dtype = K.dtype
+        self.device = K.device
+
+    # shapes the entry points expect, from the descriptor
+    @property
+    def units(self):
+        return self.c.batch * self.c.num_kv_heads
+
+    def q_shape(self):
+        return (self.c.batch, self.c.num_q_heads, self.c.head_dim)
+
+    def per_unit(self, last=None):
+        base = (self.c.batch, self.c.num_kv_heads)
+        return base if last is None else base + (last,)
+
+    def check_device(self, **tensors):
+        K, V, seq_lens, table = self._keep
+        _on_device(self.device, K=K, V=V, seq_lens=seq_lens, block_table=table, **tensors)
 
     def with_seq_lens(self, seq_lens, max_seq_len=None):
         """Same cache, other lengths (a new descriptor)."""
@@ -222,18 +278,39 @@ def workspace(nbytes, device):
     return torch.zeros(max(1, nbytes), dtype=torch.uint8, device=device)
 
 
-def _q_dtype(kv, q):
-    _need(q, kv.dtype, "q", 3)
-    if q.shape != (kv.c.batch, kv.c.num_q_heads, kv.c.head_dim):
-        raise ValueError(f"q must be [B][Hq][d], got {tuple(q.shape)}")
+def _q(kv, q):
+    _need(q, kv.dtype, "q", shape=kv.q_shape())
+
+
+def _outputs(kv, out, lse):
+    _need(out, torch.float32, "out", shape=kv.q_shape())
+    if lse is not None:
+        _need(lse, torch.float32, "lse", shape=kv.q_shape()[:2])
+
+
+def _ws(ws):
+    _need(ws, torch.uint8, "ws", dims=1)
+
+
+def _selection_outputs(kv, topk_idx, topk_len, set_idx, set_len, shared_idx=None,
+                       shared_len=None):
+    _need(topk_idx, torch.int32, "topk_idx", dims=3)
+    _need(topk_idx, torch.int32, "topk_idx", shape=kv.per_unit(topk_idx.shape[-1]))
+    _need(topk_len, torch.int32, "topk_len", shape=kv.per_unit())
+    _need(set_idx, torch.int32, "set_idx", dims=3)
+    _need(set_idx, torch.int32, "set_idx", shape=kv.per_unit(set_idx.shape[-1]))
+    _need(set_len, torch.int32, "set_len", shape=kv.per_unit())
+    if shared_idx is not None or shared_len is not None:
+        _need(shared_idx, torch.int32, "shared_idx", shape=set_idx.shape)
+        _need(shared_len, torch.int32, "shared_len", shape=kv.per_unit())
 
 
 def prhs_select(kv, q, p, topk_idx, topk_len, set_idx, set_len, ws, stream=None):
-    _q_dtype(kv, q)
-    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
-                       (set_idx, "set_idx", 3), (set_len, "set_len", 2)):
-        _need(t, torch.int32, n, dims)
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _selection_outputs(kv, topk_idx, topk_len, set_idx, set_len)
+    _ws(ws)
+    kv.check_device(q=q, topk_idx=topk_idx, topk_len=topk_len, set_idx=set_idx, set_len=set_len,
+                    ws=ws)
     check(lib().prhs_select(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(topk_idx),
                             _ptr(topk_len), topk_idx.shape[-1], _ptr(set_idx), _ptr(set_len),
                             set_idx.shape[-1], _ptr(ws), ws.numel(), _stream(stream)))
@@ -243,14 +320,11 @@ def prhs_select_shared(kv, q, p, topk_idx, topk_len, set_idx, set_len, shared_id
                        stream=None):
     """prhs_select that also writes the dilated shared set at the anchor
     length (shared_idx has the same capacity as set_idx)."""
-    _q_dtype(kv, q)
-    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
-                       (set_idx, "set_idx", 3), (set_len, "set_len", 2),
-                       (shared_idx, "shared_idx", 3), (shared_len, "shared_len", 2)):
-        _need(t, torch.int32, n, dims)
-    if shared_idx.shape != set_idx.shape:
-        raise ValueError("shared_idx must have the shape of set_idx")
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _selection_outputs(kv, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len)
+    _ws(ws)
+    kv.check_device(q=q, topk_idx=topk_idx, topk_len=topk_len, set_idx=set_idx, set_len=set_len,
+                    shared_idx=shared_idx, shared_len=shared_len, ws=ws)
     check(lib().prhs_select_shared(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(topk_idx),
                                    _ptr(topk_len), topk_idx.shape[-1], _ptr(set_idx),
                                    _ptr(set_len), set_idx.shape[-1], _ptr(shared_idx),
@@ -258,24 +332,33 @@ def prhs_select_shared(kv, q, p, topk_idx, topk_len, set_idx, set_len, shared_id
 
 
 def prhs_dilate_reuse(p, topk_idx, topk_len, anchor_lens, seq_lens, set_idx, set_len, stream=None):
-    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
-                       (anchor_lens, "anchor_lens", 1), (seq_lens, "seq_lens", 1),
-                       (set_idx, "set_idx", 3), (set_len, "set_len", 2)):
-        _need(t, torch.int32, n, dims)
+    _need(topk_idx, torch.int32, "topk_idx", dims=3)
     B, Hkv, k_cap = topk_idx.shape
+    _need(topk_len, torch.int32, "topk_len", shape=(B, Hkv))
+    _need(anchor_lens, torch.int32, "anchor_lens", shape=(B,))
+    _need(seq_lens, torch.int32, "seq_lens", shape=(B,))
+    _need(set_idx, torch.int32, "set_idx", dims=3)
+    _need(set_idx, torch.int32, "set_idx", shape=(B, Hkv, set_idx.shape[-1]))
+    _need(set_len, torch.int32, "set_len", shape=(B, Hkv))
+    _on_device(topk_idx.device, topk_len=topk_len, anchor_lens=anchor_lens, seq_lens=seq_lens,
+               set_idx=set_idx, set_len=set_len)
     check(lib().prhs_dilate_reuse(ctypes.byref(p), B, Hkv, _ptr(topk_idx), _ptr(topk_len), k_cap,
                                   _ptr(anchor_lens), _ptr(seq_lens), _ptr(set_idx), _ptr(set_len),
                                   set_idx.shape[-1], _stream(stream)))
 
 
+def _sets(kv, set_idx, set_len):
+    _need(set_idx, torch.int32, "set_idx", dims=3)
+    _need(set_idx, torch.int32, "set_idx", shape=kv.per_unit(set_idx.shape[-1]))
+    _need(set_len, torch.int32, "set_len", shape=kv.per_unit())
+
+
 def prhs_sparse_decode_attn(kv, q, set_idx, set_len, scale, out, lse, ws, stream=None):
-    _q_dtype(kv, q)
-    _need(set_idx, torch.int32, "set_idx", 3)
-    _need(set_len, torch.int32, "set_len", 2)
-    _need(out, torch.float32, "out", 3)
-    if lse is not None:
-        _need(lse, torch.float32, "lse", 2)
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _sets(kv, set_idx, set_len)
+    _outputs(kv, out, lse)
+    _ws(ws)
+    kv.check_device(q=q, set_idx=set_idx, set_len=set_len, out=out, lse=lse, ws=ws)
     check(lib().prhs_sparse_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx), _ptr(set_len),
                                         set_idx.shape[-1], float(scale), _ptr(out), _ptr(lse),
                                         _ptr(ws), ws.numel(), _stream(stream)))
@@ -285,14 +368,13 @@ def prhs_reuse_decode_attn(kv, q, set_idx, set_len, anchor_lens, scale, out, lse
                            stream=None):
     """Attention over set U [anchor_lens[b], n_b): the reused set of a later
     step, with the set built once at the anchor length."""
-    _q_dtype(kv, q)
-    _need(set_idx, torch.int32, "set_idx", 3)
-    _need(set_len, torch.int32, "set_len", 2)
-    _need(anchor_lens, torch.int32, "anchor_lens", 1)
-    _need(out, torch.float32, "out", 3)
-    if lse is not None:
-        _need(lse, torch.float32, "lse", 2)
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _sets(kv, set_idx, set_len)
+    _need(anchor_lens, torch.int32, "anchor_lens", shape=(kv.c.batch,))
+    _outputs(kv, out, lse)
+    _ws(ws)
+    kv.check_device(q=q, set_idx=set_idx, set_len=set_len, anchor_lens=anchor_lens, out=out,
+                    lse=lse, ws=ws)
     check(lib().prhs_reuse_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx), _ptr(set_len),
                                        set_idx.shape[-1], _ptr(anchor_lens), float(scale),
                                        _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
@@ -304,22 +386,22 @@ def prhs_gate(q, seq_lens, tau, slot, ref_q, ref_valid, slot_lens, choice, row_a
     """Similarity gate for block step `slot`: q [B][Hq][d]; ref_q
     [S][B][Hq][d] (dtype of q); ref_valid [S][B*Hkv]; slot_lens [S][B];
     choice, row_anchor, row_other, tail [B*Hkv] int32 outputs."""
-    if q.dtype not in (torch.bfloat16, torch.float32):
-        raise ValueError("q must be bf16 or fp32")
-    _need(q, q.dtype, "q", 3)
-    _need(ref_q, q.dtype, "ref_q", 4)
+    if not isinstance(q, torch.Tensor) or q.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("q must be a bf16 or fp32 tensor")
+    _need(q, q.dtype, "q", dims=3)
     B, Hq, d = q.shape
+    _need(ref_q, q.dtype, "ref_q", dims=4)
     S = ref_q.shape[0]
-    if tuple(ref_q.shape[1:]) != (B, Hq, d):
-        raise ValueError("ref_q must be [S][B][Hq][d]")
-    for t, n, shape in ((seq_lens, "seq_lens", (B,)), (ref_valid, "ref_valid", (S, B * num_kv_heads)),
-                        (slot_lens, "slot_lens", (S, B)), (choice, "choice", (B * num_kv_heads,)),
-                        (row_anchor, "row_anchor", (B * num_kv_heads,)),
-                        (row_other, "row_other", (B * num_kv_heads,)),
-                        (tail, "tail", (B * num_kv_heads,))):
-        _need(t, torch.int32, n)
-        if tuple(t.shape) != shape:
-            raise ValueError(f"{n} must have shape {shape}, got {tuple(t.shape)}")
+    _need(ref_q, q.dtype, "ref_q", shape=(S, B, Hq, d))
+    U = B * num_kv_heads
+    for t, n, shape in ((seq_lens, "seq_lens", (B,)), (ref_valid, "ref_valid", (S, U)),
+                        (slot_lens, "slot_lens", (S, B)), (choice, "choice", (U,)),
+                        (row_anchor, "row_anchor", (U,)), (row_other, "row_other", (U,)),
+                        (tail, "tail", (U,))):
+        _need(t, torch.int32, n, shape=shape)
+    _on_device(q.device, seq_lens=seq_lens, ref_q=ref_q, ref_valid=ref_valid,
+               slot_lens=slot_lens, choice=choice, row_anchor=row_anchor, row_other=row_other,
+               tail=tail)
     dt = PRHS_BF16 if q.dtype == torch.bfloat16 else PRHS_F32
     check(lib().prhs_gate(B, Hq, num_kv_heads, d, dt, _ptr(q), _ptr(seq_lens), float(tau), S,
                           int(slot), _ptr(ref_q), _ptr(ref_valid), _ptr(slot_lens), _ptr(choice),
@@ -329,15 +411,12 @@ def prhs_gate(q, seq_lens, tau, slot, ref_q, ref_valid, slot_lens, choice, row_a
 def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len,
                       ws, stream=None):
     """prhs_select_shared for the units with choice < 0 only."""
-    _q_dtype(kv, q)
-    _need(choice, torch.int32, "choice")
-    for t, n, dims in ((topk_idx, "topk_idx", 3), (topk_len, "topk_len", 2),
-                       (set_idx, "set_idx", 3), (set_len, "set_len", 2),
-                       (shared_idx, "shared_idx", 3), (shared_len, "shared_len", 2)):
-        _need(t, torch.int32, n, dims)
-    if shared_idx.shape != set_idx.shape:
-        raise ValueError("shared_idx must have the shape of set_idx")
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _need(choice, torch.int32, "choice", shape=(kv.units,))
+    _selection_outputs(kv, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len)
+    _ws(ws)
+    kv.check_device(q=q, choice=choice, topk_idx=topk_idx, topk_len=topk_len, set_idx=set_idx,
+                    set_len=set_len, shared_idx=shared_idx, shared_len=shared_len, ws=ws)
     check(lib().prhs_select_gated(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), _ptr(choice),
                                   _ptr(topk_idx), _ptr(topk_len), topk_idx.shape[-1],
                                   _ptr(set_idx), _ptr(set_len), set_idx.shape[-1],
@@ -346,60 +425,53 @@ def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, sh
 
 
 def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale, out, lse, ws,
-                          stream=None, psaw_start=None, psaw_sink=0):
+                          stream=None, psaw=None):
     """Attention where unit u attends pool row unit_row[u] plus the tail
-    [unit_tail[u], n_b), without the positions [psaw_sink, psaw_start[b])
-    when psaw_start [B] is given.  pool_idx [..][set_cap] (any leading dims,
-    flattened to rows), pool_len with the same leading dims."""
-    if psaw_start is not None:
-        _need(psaw_start, torch.int32, "psaw_start", 1)
-    _q_dtype(kv, q)
+    [unit_tail[u], n_b), under the layer's PSAW mask (Eq. psaw) when psaw (a
+    PrhsPsaw) is given.  pool_idx [..][set_cap] (any leading dims, flattened
+    to rows), pool_len with the same leading dims."""
+    _q(kv, q)
     _need(pool_idx, torch.int32, "pool_idx")
-    _need(pool_len, torch.int32, "pool_len")
+    if pool_idx.dim() < 1:
+        raise ValueError("pool_idx must have at least one dimension")
     cap = pool_idx.shape[-1]
     rows = pool_idx.numel() // max(cap, 1)
-    if pool_len.numel() != rows:
-        raise ValueError("pool_len must have one entry per pool row")
-    _need(unit_row, torch.int32, "unit_row")
-    _need(unit_tail, torch.int32, "unit_tail")
-    _need(out, torch.float32, "out", 3)
-    if lse is not None:
-        _need(lse, torch.float32, "lse", 2)
-    _need(ws, torch.uint8, "ws")
+    _need(pool_len, torch.int32, "pool_len", shape=pool_idx.shape[:-1])
+    _need(unit_row, torch.int32, "unit_row", shape=(kv.units,))
+    _need(unit_tail, torch.int32, "unit_tail", shape=(kv.units,))
+    _outputs(kv, out, lse)
+    _ws(ws)
+    if psaw is not None and not isinstance(psaw, PrhsPsaw):
+        raise TypeError("psaw must be a PrhsPsaw (binding.psaw(...))")
+    kv.check_device(q=q, pool_idx=pool_idx, pool_len=pool_len, unit_row=unit_row,
+                    unit_tail=unit_tail, out=out, lse=lse, ws=ws)
     check(lib().prhs_pool_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(pool_idx), _ptr(pool_len),
-                                      rows, cap, _ptr(unit_row), _ptr(unit_tail),
-                                      _ptr(psaw_start), int(psaw_sink), float(scale), _ptr(out),
-                                      _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+                                      rows, cap, _ptr(unit_row), _ptr(unit_tail), _ref(psaw),
+                                      float(scale), _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
 
 
-def prhs_prefill_attn(kv, q, scale, out, lse=None, vis_start=None, sink=0, stream=None):
+def prhs_prefill_attn(kv, q, scale, out, lse=None, psaw=None, stream=None):
     """Causal prefill attention of the prompts (kv holds them; seq_lens are
     their lengths) for the queries q [B][Hq][T][d] at positions 0 .. T - 1,
-    under the PSAW mask when vis_start [T] int32 is given."""
-    _need(q, kv.dtype, "q", 4)
+    under the layer's PSAW mask (Eq. psaw) when psaw (a PrhsPsaw) is given."""
+    _need(q, kv.dtype, "q", dims=4)
     B_, H_, T, d = q.shape
-    if (B_, H_, d) != (kv.c.batch, kv.c.num_q_heads, kv.c.head_dim):
-        raise ValueError(f"q must be [B][Hq][T][d], got {tuple(q.shape)}")
-    _need(out, torch.float32, "out", 4)
-    if tuple(out.shape) != tuple(q.shape):
-        raise ValueError("out must have q's shape")
+    _need(q, kv.dtype, "q", shape=(kv.c.batch, kv.c.num_q_heads, T, kv.c.head_dim))
+    _need(out, torch.float32, "out", shape=q.shape)
     if lse is not None:
-        _need(lse, torch.float32, "lse", 3)
-        if tuple(lse.shape) != (B_, H_, T):
-            raise ValueError("lse must be [B][Hq][T]")
-    if vis_start is not None:
-        _need(vis_start, torch.int32, "vis_start", 1)
-        if vis_start.numel() != T:
-            raise ValueError("vis_start must have T entries")
-    check(lib().prhs_prefill_attn(ctypes.byref(kv.c), _ptr(q), int(T), _ptr(vis_start), int(sink),
-                                  float(scale), _ptr(out), _ptr(lse), _stream(stream)))
+        _need(lse, torch.float32, "lse", shape=(B_, H_, T))
+    if psaw is not None and not isinstance(psaw, PrhsPsaw):
+        raise TypeError("psaw must be a PrhsPsaw (binding.psaw(...))")
+    kv.check_device(q=q, out=out, lse=lse)
+    check(lib().prhs_prefill_attn(ctypes.byref(kv.c), _ptr(q), int(T), _ref(psaw), float(scale),
+                                  _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def prhs_dense_decode_attn(kv, q, scale, out, lse, ws, stream=None):
-    _q_dtype(kv, q)
-    _need(out, torch.float32, "out", 3)
-    if lse is not None:
-        _need(lse, torch.float32, "lse", 2)
-    _need(ws, torch.uint8, "ws")
+    _q(kv, q)
+    _outputs(kv, out, lse)
+    _ws(ws)
+    kv.check_device(q=q, out=out, lse=lse, ws=ws)
     check(lib().prhs_dense_decode_attn(ctypes.byref(kv.c), _ptr(q), float(scale), _ptr(out),
                                        _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))

@@ -62,8 +62,9 @@ struct AttnArgs {
   const int32_t* unit_row;    // [units] or null: pool row of set_idx each unit attends
   const int32_t* unit_tail;   // [units] with unit_row: first position of the unit's tail
   int pool_rows;
-  const int32_t* psaw_start;  // [B] or null: positions in [psaw_sink, psaw_start[b]) are skipped
-  int psaw_sink;
+  int psaw;                   // nonzero: positions in [psaw_sink, first visible) are skipped
+  double psaw_f;              // Eq. psaw factor of the layer (first visible at length n:
+  int psaw_sink;              // psaw_first_visible(psaw_f, psaw_sink, n))
   int set_cap;
   float scale_log2;
   int chunk, nsplit;
@@ -93,9 +94,9 @@ __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, i
     sp.L = sp.base = nb;
     return sp;
   }
-  if (a.psaw_start) {
+  if (a.psaw) {
     sp.mask_lo = a.psaw_sink;
-    sp.mask_hi = a.psaw_start[b];
+    sp.mask_hi = psaw_first_visible(a.psaw_f, a.psaw_sink, nb);
   }
   int row = u, t0 = nb;
   bool tail = false;
@@ -855,7 +856,8 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.unit_row = dense ? nullptr : s.unit_row;
   a.unit_tail = dense ? nullptr : s.unit_tail;
   a.pool_rows = s.pool_rows;
-  a.psaw_start = dense ? nullptr : s.psaw_start;
+  a.psaw = dense ? 0 : s.psaw;
+  a.psaw_f = s.psaw_f;
   a.psaw_sink = s.psaw_sink;
   a.set_cap = s.set_cap;
   a.scale_log2 = s.scale * 1.44269504088896340736f;

@@ -1,8 +1,10 @@
 // Causal prefill attention of a prompt under the progressive sliding
 // attention window (Sec. 4.2, Eq. psaw: the window narrows during prefill
 // as well as decoding).  The query at position i of sequence b (i < n_b)
-// attends the keys p <= i with p < C_sink or p >= vis_start[i]; without
-// vis_start every p <= i (plain causal attention, Eq. attn_eq per position).
+// attends the keys p <= i with p < C_sink or p >= vis_start(i), the first
+// visible position of Eq. psaw with the i + 1 tokens [0, i] in view (computed
+// per query from the layer's factor); without PSAW every p <= i (plain
+// causal attention, Eq. attn_eq per position).
 //
 // attn_prefill_bf16<D, QB, PAGED>: one workgroup per (QB = 192 or 256
 // query positions, batch, query head), over a contiguous or paged cache;
@@ -53,7 +55,8 @@ struct PrefillArgs {
   KvView kv;
   const __bf16* q;        // [B][Hq][T][D]
   int T;
-  const int32_t* vis;     // [T] or null
+  int psaw;               // nonzero: row i attends [0, sink) U [first visible at i + 1, i]
+  double psaw_f;          // Eq. psaw factor of the layer
   int sink;
   float scale_log2;
   float* out;             // [B][Hq][T][D]
@@ -322,9 +325,9 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   const int sink_end = min(a.sink, qlast + 1);
   if (wave == 0) {
     int v = sink_end;
-    if (a.vis) {
+    if (a.psaw) {
       v = 0x7FFFFFFF;
-      for (int i = q0 + lane; i <= qlast; i += 64) v = min(v, a.vis[i]);
+      for (int i = q0 + lane; i <= qlast; i += 64) v = min(v, psaw_first_visible(a.psaw_f, a.sink, i + 1));
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) v = min(v, __shfl_xor(v, off));
     }
@@ -332,7 +335,7 @@ __global__ __launch_bounds__(QB / 16 * 64) void attn_prefill_bf16(PrefillArgs a)
   }
   // this lane's query and its first visible non-sink position
   const bool qvalid = qi <= qlast;
-  const int my_vis = (a.vis && qvalid) ? a.vis[qi] : 0;
+  const int my_vis = (a.psaw && qvalid) ? psaw_first_visible(a.psaw_f, a.sink, qi + 1) : 0;
   // a tile needs no mask for this wave when all 16 of its queries lie in
   // the prompt, the tile ends at or before the first of them, and it lies
   // inside the sink or at or past the largest of their vis_start
@@ -440,7 +443,8 @@ hipError_t launch_prefill(const PrefillLaunch& s, hipStream_t stream) {
   a.kv = s.kv;
   a.q = (const __bf16*)s.q;
   a.T = s.T;
-  a.vis = s.vis_start;
+  a.psaw = s.psaw;
+  a.psaw_f = s.psaw_f;
   a.sink = s.sink;
   a.scale_log2 = s.scale * 1.44269504088896340736f;
   a.out = s.out;

@@ -1,6 +1,7 @@
 // C-ABI entry points of libprhs: host-side validation, workspace sizing and
 // dispatch to the kernel files.  Validation never touches the device, so every
 // error path can be exercised without a GPU.
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -114,6 +115,32 @@ long long middle_at(const prhs_params* p, long long n0) {
   return win_start - sink_end;
 }
 
+// Eq. psaw's factor 1 - phi^e of the layer, with e = alpha (l - l_s) /
+// (N - l_s) for the 1-based layer l = layer + 1 >= l_s, else 0 (no mask).
+// The order of operations is that of the formula, in binary64.
+prhs_status psaw_factor(const prhs_psaw* p, double* f) {
+  if (!p) return fail(PRHS_E_INVALID, "psaw is NULL");
+  if (p->num_layers < 1) return fail(PRHS_E_INVALID, "psaw: num_layers must be >= 1");
+  if (p->layer < 0 || p->layer >= p->num_layers)
+    return fail(PRHS_E_INVALID, "psaw: layer (%d) must lie in [0, num_layers = %d)", p->layer,
+                p->num_layers);
+  if (p->l_s < 0 || p->l_s >= p->num_layers)
+    return fail(PRHS_E_INVALID, "psaw: l_s (%d) must lie in [0, num_layers = %d)", p->l_s,
+                p->num_layers);
+  if (p->sink < 0) return fail(PRHS_E_INVALID, "psaw: sink must be >= 0");
+  if (!(p->phi > 0.0 && p->phi <= 1.0)) return fail(PRHS_E_INVALID, "psaw: phi must lie in (0, 1]");
+  if (!(p->alpha >= 0.0 && p->alpha <= 1e300))
+    return fail(PRHS_E_INVALID, "psaw: alpha must be finite and >= 0");
+  const int lb = p->layer + 1;
+  if (lb < p->l_s) {
+    *f = 0.0;
+    return PRHS_OK;
+  }
+  const double e = p->alpha * (double)(lb - p->l_s) / (double)(p->num_layers - p->l_s);
+  *f = 1.0 - pow(p->phi, e);
+  return PRHS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -146,6 +173,16 @@ int32_t prhs_set_capacity(const prhs_params* p, int32_t max_seq_len) {
 int32_t prhs_schedule(int32_t step, int32_t layer, const prhs_params* p) {
   if (check_params(p) != PRHS_OK || step < 0 || layer < 0) return -1;
   return (step % p->refresh_every == 0 && layer % p->layer_group == 0) ? PRHS_REFRESH : PRHS_REUSE;
+}
+
+int32_t prhs_psaw_first_visible(const prhs_psaw* psaw, int32_t n) {
+  double f = 0.0;
+  if (psaw_factor(psaw, &f) != PRHS_OK) return -1;
+  if (n < 0) {
+    fail(PRHS_E_INVALID, "n must be >= 0");
+    return -1;
+  }
+  return prhs::psaw_first_visible(f, psaw->sink, n);
 }
 
 prhs_status prhs_workspace_size(int32_t op, const prhs_kv* kv, const prhs_params* params,
@@ -303,7 +340,7 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
                                     const int32_t* set_len, int32_t set_cap,
                                     const int32_t* tail_start, const int32_t* unit_row,
                                     const int32_t* unit_tail, int32_t pool_rows,
-                                    const int32_t* psaw_start, int32_t psaw_sink, float scale,
+                                    const prhs_psaw* psaw, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream, bool dense, const char* name) {
   prhs_status st = check_kv_shape(kv);
@@ -316,6 +353,8 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
       return fail(PRHS_E_INVALID, "set_idx and set_len must be non-NULL");
   }
   if (!(scale == scale)) return fail(PRHS_E_INVALID, "scale is NaN");
+  double psaw_f = 0.0;
+  if (psaw && (st = psaw_factor(psaw, &psaw_f)) != PRHS_OK) return st;
   const int rows_cap = dense ? kv->max_seq_len : set_cap;
   const size_t wsz = prhs::attn_workspace_bytes(kv->dtype, dense, kv->batch, kv->num_q_heads,
                                                 kv->num_kv_heads, kv->head_dim, rows_cap);
@@ -332,8 +371,9 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   a.unit_row = unit_row;
   a.unit_tail = unit_tail;
   a.pool_rows = pool_rows;
-  a.psaw_start = psaw_start;
-  a.psaw_sink = psaw_sink;
+  a.psaw = psaw != nullptr;
+  a.psaw_f = psaw_f;
+  a.psaw_sink = psaw ? psaw->sink : 0;
   a.set_cap = set_cap;
   a.scale = scale;
   a.out = out;
@@ -347,7 +387,7 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int3
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream) {
   return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, nullptr,
-                          0, scale, out, lse, ws, ws_bytes, stream, false,
+                          scale, out, lse, ws, ws_bytes, stream, false,
                           "prhs_sparse_decode_attn launch");
 }
 
@@ -358,23 +398,21 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32
   if (kv && kv->batch > 0 && !anchor_lens)
     return fail(PRHS_E_INVALID, "anchor_lens must be non-NULL");
   return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, nullptr, nullptr, 0,
-                          nullptr, 0, scale, out, lse, ws, ws_bytes, stream, false,
+                          nullptr, scale, out, lse, ws, ws_bytes, stream, false,
                           "prhs_reuse_decode_attn launch");
 }
 
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
                                   const int32_t* unit_row, const int32_t* unit_tail,
-                                  const int32_t* psaw_start, int32_t psaw_sink, float scale,
-                                  float* out, float* lse, void* ws, size_t ws_bytes,
-                                  void* stream) {
+                                  const prhs_psaw* psaw, float scale, float* out, float* lse,
+                                  void* ws, size_t ws_bytes, void* stream) {
   if (pool_rows < 0) return fail(PRHS_E_INVALID, "pool_rows must be >= 0");
-  if (psaw_sink < 0) return fail(PRHS_E_INVALID, "psaw_sink must be >= 0");
   if (kv && kv->batch > 0 && (!unit_row || !unit_tail))
     return fail(PRHS_E_INVALID, "unit_row and unit_tail must be non-NULL");
   return attention_common(kv, q, pool_idx, pool_len, set_cap, nullptr, unit_row, unit_tail,
-                          pool_rows, psaw_start, psaw_sink, scale, out, lse, ws, ws_bytes,
-                          stream, false, "prhs_pool_decode_attn launch");
+                          pool_rows, psaw, scale, out, lse, ws, ws_bytes, stream, false,
+                          "prhs_pool_decode_attn launch");
 }
 
 prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
@@ -418,15 +456,16 @@ prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, 
 }
 
 prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
-                              const int32_t* vis_start, int32_t sink, float scale, float* out,
-                              float* lse, void* stream) {
+                              const prhs_psaw* psaw, float scale, float* out, float* lse,
+                              void* stream) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_kv_data(kv)) != PRHS_OK) return st;
   if (kv->dtype != PRHS_BF16)
     return fail(PRHS_E_UNSUPPORTED, "prefill attention is built for bf16 inputs");
   if (q_len < 0) return fail(PRHS_E_INVALID, "q_len must be >= 0 (got %d)", q_len);
-  if (sink < 0) return fail(PRHS_E_INVALID, "sink must be >= 0");
+  double psaw_f = 0.0;
+  if (psaw && (st = psaw_factor(psaw, &psaw_f)) != PRHS_OK) return st;
   if (!(scale > 0.f && scale < INFINITY))
     return fail(PRHS_E_INVALID, "scale must be positive and finite");
   if ((long long)((q_len + 63) / 64) * kv->batch * kv->num_q_heads > 0x7FFFFFFFLL)
@@ -437,8 +476,9 @@ prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
   a.kv = view_of(kv);
   a.q = q;
   a.T = q_len;
-  a.vis_start = vis_start;
-  a.sink = sink;
+  a.psaw = psaw != nullptr;
+  a.psaw_f = psaw_f;
+  a.sink = psaw ? psaw->sink : 0;
   a.scale = scale;
   a.out = out;
   a.lse = lse;
@@ -447,7 +487,7 @@ prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
 
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr, 0,
+  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr,
                           scale, out, lse, ws, ws_bytes, stream, true,
                           "prhs_dense_decode_attn launch");
 }

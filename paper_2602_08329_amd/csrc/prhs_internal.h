@@ -65,6 +65,17 @@ __device__ __forceinline__ int kv_seq_len(const KvView& kv, int b) {
   return n > kv.max_seq_len ? kv.max_seq_len : n;
 }
 
+// First visible non-sink position when n tokens are in view under the
+// progressive sliding attention window (Eq. psaw): P = floor(f n) with the
+// layer's factor f = 1 - phi^e (computed once on the host, binary64), and
+// the visible keys are [0, min(sink, n)) U [max(min(sink, n), P - 1), n).
+// f lies in [0, 1) and n < 2^22, so P fits an int.
+__host__ __device__ __forceinline__ int psaw_first_visible(double f, int sink, int n) {
+  const int P = (int)floor(f * (double)n);
+  const int se = sink < n ? sink : n;
+  return se > P - 1 ? se : P - 1;
+}
+
 // Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
 // -0.0 is mapped like +0.0.
 __device__ __forceinline__ uint32_t score_key(float f) {
@@ -169,7 +180,8 @@ struct AttnLaunch {
   const int32_t* unit_row;    // [B*Hkv] or null: pool row each unit attends
   const int32_t* unit_tail;   // [B*Hkv] with unit_row: first position of the unit's tail
   int pool_rows;              // rows of set_idx when unit_row is given
-  const int32_t* psaw_start;  // [B] or null: positions in [psaw_sink, psaw_start[b]) are masked
+  int psaw;                   // nonzero: positions in [psaw_sink, first visible) are masked
+  double psaw_f;              // the layer's factor 1 - phi^e of Eq. psaw
   int psaw_sink;
   int set_cap;
   float scale;
@@ -204,7 +216,8 @@ struct PrefillLaunch {
   KvView kv;                  // bf16 cache (contiguous or paged) holding the prompts
   const void* q;              // [B][Hq][T][d]
   int T;
-  const int32_t* vis_start;   // [T] or null
+  int psaw;                   // nonzero: the query at position i attends [0, sink) and
+  double psaw_f;              // [first visible at i + 1, i] (Eq. psaw factor psaw_f)
   int sink;
   float scale;
   float* out;                 // [B][Hq][T][d]

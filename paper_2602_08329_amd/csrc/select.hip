@@ -57,7 +57,7 @@ struct SelArgs {
   const void* q;
   int k, k_num, k_den, sink, window, dilate_m;
   int mcap, selcap;
-  int sortcap;         // LDS sort buffer entries of select_finish (power of two)
+  int sortcap;         // LDS sort buffer entries of select_finish (>= selcap)
   uint32_t* keys;      // [rows][mcap]
   uint32_t* hist0;     // [rows][2048]
   uint32_t* hist1;     // [rows][2048]
@@ -1349,11 +1349,19 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   }
   const dim3 fgrid((mid_max + kFilterChunk - 1) / kFilterChunk, rows);
   hipLaunchKernelGGL(select_filter, fgrid, dim3(kFilterBlock), 0, stream, a);
-  // LDS buffer: the k winners plus up to kFinishTies level-1 ties, then the
-  // bitmap segment
+  // LDS buffer: the k winners plus up to kFinishTies level-1 ties, as far as
+  // the CU's LDS holds them beside the kernel's static LDS and the bitmap
+  // segment; the host bound PRHS_MAX_TOPK keeps the winners alone inside it
+  static const long long finish_static = [] {
+    hipFuncAttributes fa;
+    return hipFuncGetAttributes(&fa, (const void*)select_finish) == hipSuccess
+               ? (long long)fa.sharedSizeBytes : -1LL;
+  }();
+  if (finish_static < 0) return hipErrorInvalidDeviceFunction;
+  const long long lds_cap = ((long long)kLdsBytes - finish_static - 3LL * kFinishSegBits / 8) / 8;
   long long cap = (long long)a.selcap + kFinishTies;
-  if (cap > PRHS_MAX_TOPK) cap = PRHS_MAX_TOPK;
-  if (cap < a.selcap) cap = a.selcap;
+  if (cap > lds_cap) cap = lds_cap;
+  if (cap < a.selcap) return hipErrorInvalidValue;  // unreachable for k_b <= PRHS_MAX_TOPK
   a.sortcap = (int)cap;
   const size_t dyn = (size_t)a.sortcap * 8 + 3 * kFinishSegBits / 8;
   if (dyn > 65536) {

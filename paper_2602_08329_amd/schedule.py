@@ -25,31 +25,20 @@ import torch
 from . import binding as B
 
 
-def psaw_first_visible(layer, n_layers, n, sink, l_s, phi, alpha):
-    """First visible non-sink position of 0-based `layer` at length n under
-    the progressive sliding attention window (Sec. 4.2, Eq. psaw): the
-    1-based boundary P = floor((1 - phi^(alpha (l - l_s) / (N - l_s))) n) for
-    1-based layer l = layer + 1 >= l_s (else 0) masks the 1-based positions
-    strictly between the sink and P, i.e. 0-based [sink, P - 1)."""
-    lb = layer + 1
-    P = 0
-    if lb >= l_s:
-        P = int(math.floor((1.0 - phi ** (alpha * (lb - l_s) / (n_layers - l_s))) * n))
-    return max(min(sink, n), P - 1)
-
-
-def psaw_prefill_visible(layer, n_layers, T, sink, l_s, phi, alpha, device="cuda"):
-    """First visible non-sink position of every query of a prefill of T
-    tokens at 0-based `layer` (int32 [T] on `device`, for prhs_prefill_attn):
-    the query at position i has the i + 1 tokens [0, i] in view, so Eq. psaw
-    is taken at n = i + 1."""
-    vis = [psaw_first_visible(layer, n_layers, i + 1, sink, l_s, phi, alpha) for i in range(T)]
-    return torch.tensor(vis, dtype=torch.int32, device=device)
-
-
 def psaw_defaults(n_layers):
     """Sec. 5.1: pruning from l_s = floor(3 N / 4), phi = 0.7, alpha = 1."""
     return (3 * n_layers) // 4, 0.7, 1.0
+
+
+def psaw_layers(n_layers, sink, psaw):
+    """Window descriptors (binding.psaw) of the layers that can mask keys
+    under psaw = (l_s, phi, alpha): the 1-based layer l = layer + 1 masks
+    only when l > l_s (at l = l_s the factor is 1 - phi^0 = 0).  Returns
+    {layer: descriptor}; the library evaluates Eq. psaw from them."""
+    if psaw is None:
+        return {}
+    l_s, phi, alpha = psaw
+    return {l: B.psaw(l, n_layers, l_s, phi, alpha, sink) for l in range(n_layers) if l + 1 > l_s}
 
 
 def capture_steps(fn, steps):
@@ -112,21 +101,23 @@ class DecodeRunner:
         self.ws_dense = B.workspace(B.prhs_workspace_size(B.PRHS_OP_DENSE_ATTN, kv0, self.params), dev)
         self.out = torch.zeros(Bsz, w.hq, w.d, dtype=torch.float32, device=dev)
         self.lse = torch.zeros(Bsz, w.hq, dtype=torch.float32, device=dev)
-        # PSAW (Sec. 4.2): psaw = (l_s, phi, alpha); first visible position per
-        # (layer, step) for the layers that prune, and identity pool rows and
-        # per-unit lengths to attend the schedule's sets through the pool form
+        # PSAW (Sec. 4.2): psaw = (l_s, phi, alpha); the layers that can mask
+        # attend the schedule's sets through the pool form (identity rows and
+        # per-unit anchor lengths) with their window descriptor
         self.psaw = psaw
-        self.psaw_start = {}
-        if psaw is not None:
-            l_s, phi, alpha = psaw
-            for l in range(self.L):
-                for j in range(T):
-                    st = [psaw_first_visible(l, self.L, n + j + 1, w.sink, l_s, phi, alpha)
-                          for n in w.n_ctx]
-                    if any(x > min(w.sink, n + j + 1) for x, n in zip(st, w.n_ctx)):
-                        self.psaw_start[(l, j)] = torch.tensor(st, dtype=i32, device=dev)
+        self.psaw_desc = psaw_layers(self.L, w.sink, psaw)
+        if self.psaw_desc:
             self.unit_ids = torch.arange(Bsz * w.hkv, dtype=i32, device=dev)
             self.unit_lens = self.seq_lens.repeat_interleave(w.hkv, dim=1).contiguous()
+
+    def psaw_start(self, l, j):
+        """First visible non-sink position of every sequence at layer l, step
+        j (host list, from the library's Eq. psaw), or None when the layer
+        does not mask."""
+        ps = self.psaw_desc.get(l)
+        if ps is None:
+            return None
+        return [B.prhs_psaw_first_visible(ps, n + j + 1) for n in self.w.n_ctx]
 
     # -- pieces -------------------------------------------------------------
     def refresh(self, gi, j):
@@ -175,16 +166,15 @@ class DecodeRunner:
         s, n, tail = self.set_for(l, j)
         out = self.out if out is None else out
         lse = self.lse if lse is None else lse
-        start = self.psaw_start.get((l, j))
-        if start is not None:
+        ps = self.psaw_desc.get(l)
+        if ps is not None:
             # the same set through the pool form, under the layer's PSAW mask
             if tail is None:
                 utail = self.unit_lens[j]
             else:
                 utail = tail.repeat_interleave(self.w.hkv).contiguous()
             B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.unit_ids, utail,
-                                    self.scale, out, lse, self.ws_attn, psaw_start=start,
-                                    psaw_sink=self.w.sink)
+                                    self.scale, out, lse, self.ws_attn, psaw=ps)
         elif tail is None:
             B.prhs_sparse_decode_attn(self.kv[l][j], self.inp.q[l, j], s, n, self.scale, out, lse,
                                       self.ws_attn)
@@ -203,7 +193,7 @@ class DecodeRunner:
         w = self.w
         shares = set(self.shares_at(j))
         for gi in range(self.groups):
-            if j % w.s == 0:
+            if B.prhs_schedule(j, gi * w.G, self.params) == B.PRHS_REFRESH:
                 self.refresh(gi, j)
             if gi in shares:
                 self.share(gi, j)
@@ -278,7 +268,7 @@ class GatedDecodeRunner(DecodeRunner):
         B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], pool, plen, rows, tail,
                                 self.scale, self.out if out is None else out,
                                 self.lse if lse is None else lse, self.ws_attn,
-                                psaw_start=self.psaw_start.get((l, j)), psaw_sink=self.w.sink)
+                                psaw=self.psaw_desc.get(l))
 
     def retrieving_units(self):
         """Units of every group that retrieved at the last gated step."""

@@ -40,7 +40,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version(L):
-    assert L.prhs_abi_version() == 1
+    assert L.prhs_abi_version() == 2
 
 
 def test_schedule_matches_oracle(L):
@@ -153,6 +153,14 @@ def test_select_capacity_and_workspace_errors(L):
     big = B.params(k=20000, sink=0, window=0)
     kv = _kv(capacity=30000, max_seq_len=30000)
     assert _select(L, kv, big, k_cap=20000, set_cap=30000) == B.PRHS_E_UNSUPPORTED
+    # the largest budget the selection supports, and one past it, on a middle
+    # range beyond LDS (the radix path, whose winners stay in LDS)
+    kv = _kv(capacity=40000, max_seq_len=40000)
+    at = B.params(k=B.PRHS_MAX_TOPK, sink=4, window=64)
+    past = B.params(k=B.PRHS_MAX_TOPK + 1, sink=4, window=64)
+    assert _select(L, kv, past, k_cap=B.PRHS_MAX_TOPK + 1, set_cap=40000) == B.PRHS_E_UNSUPPORTED
+    assert "sort limit" in L.prhs_last_error().decode()
+    assert _select(L, kv, at, k_cap=B.PRHS_MAX_TOPK, set_cap=40000, ws_bytes=0) == B.PRHS_E_WORKSPACE
 
 
 def test_attention_validation(L):
@@ -237,13 +245,15 @@ def test_select_gated_and_pool_attention_validation(L):
                              cap - 1, 0x6, 0x7, 0x8, n.value, None)
     assert st == B.PRHS_E_CAPACITY
     L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 300, ctypes.byref(n))
-    pool = lambda rows, urow, sink, wsb: L.prhs_pool_decode_attn(  # noqa: E731
-        ctypes.byref(kv), 0x1, 0x2, 0x3, rows, 300, urow, 0x5, None, sink, 0.1, 0x6, None, 0x7, wsb,
-        None)
-    assert pool(-1, 0x4, 0, n.value) == B.PRHS_E_INVALID
-    assert pool(8, None, 0, n.value) == B.PRHS_E_INVALID
-    assert pool(8, 0x4, -2, n.value) == B.PRHS_E_INVALID
-    assert pool(8, 0x4, 0, n.value - 1) == B.PRHS_E_WORKSPACE
+    good = B.psaw(7, 8, 6, 0.7, 1.0, 4)
+    pool = lambda rows, urow, ps, wsb: L.prhs_pool_decode_attn(  # noqa: E731
+        ctypes.byref(kv), 0x1, 0x2, 0x3, rows, 300, urow, 0x5, None if ps is None else ctypes.byref(ps),
+        0.1, 0x6, None, 0x7, wsb, None)
+    assert pool(-1, 0x4, None, n.value) == B.PRHS_E_INVALID
+    assert pool(8, None, None, n.value) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, B.psaw(7, 8, 6, 0.7, 1.0, -2), n.value) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, B.psaw(8, 8, 6, 0.7, 1.0, 4), n.value) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, good, n.value - 1) == B.PRHS_E_WORKSPACE
 
 
 def test_dilate_validation_and_empty_batch(L):
@@ -260,7 +270,8 @@ def test_dilate_validation_and_empty_batch(L):
 def test_prefill_validation(L):
     kv = _kv()
     pre = lambda kv=kv, q=0x4000, T=300, sink=4, scale=0.1, out=0x5000: L.prhs_prefill_attn(  # noqa: E731
-        ctypes.byref(kv), q, T, None, sink, scale, out, None, None)
+        ctypes.byref(kv), q, T, ctypes.byref(B.psaw(7, 8, 6, 0.7, 1.0, sink)), scale, out, None,
+        None)
     for bad in (0.0, -0.1, float("nan"), float("inf")):
         assert pre(scale=bad) == B.PRHS_E_INVALID
     assert b"scale" in L.prhs_last_error()
@@ -296,3 +307,107 @@ def test_binding_marshalling_checks():
                                   torch.zeros(1, 2, 8, dtype=torch.int32),
                                   torch.zeros(1, 2, dtype=torch.int32), 0.1,
                                   torch.zeros(1, 2, 64), None, torch.zeros(8, dtype=torch.uint8))
+
+
+@pytest.mark.parametrize("N,l_s,phi,alpha,sink", [(32, 24, 0.7, 1.0, 4), (8, 6, 0.3, 1.0, 16),
+                                                  (8, 4, 0.5, 1.5, 2), (4, 2, 0.01, 3.0, 0),
+                                                  (1, 0, 0.7, 1.0, 4), (12, 1, 0.95, 0.2, 70)])
+def test_psaw_first_visible_matches_oracle(L, N, l_s, phi, alpha, sink):
+    # Eq. psaw lives in the library: its first visible position equals the
+    # oracle's at every layer and at lengths across the whole range (decode
+    # lengths and every prefill row of a short prompt)
+    lens = list(range(0, 301)) + [1023, 4096, 4097, 32769, 131073, 131088, (1 << 22) - 1]
+    for layer in range(N):
+        ps = B.psaw(layer, N, l_s, phi, alpha, sink)
+        got = [B.prhs_psaw_first_visible(ps, n) for n in lens]
+        ref = [O.psaw_visible_start(layer, N, n, sink, l_s, phi, alpha) for n in lens]
+        assert got == ref, (layer, [(n, a, b) for n, a, b in zip(lens, got, ref) if a != b][:5])
+        pre = O.psaw_prefill_visible(layer, N, 300, sink, l_s, phi, alpha)
+        assert got[1:301] == pre.tolist()
+
+
+def test_psaw_descriptor_validation(L):
+    bad = [B.psaw(-1, 8, 6, 0.7, 1.0, 4), B.psaw(8, 8, 6, 0.7, 1.0, 4), B.psaw(0, 0, 0, 0.7, 1.0, 4),
+           B.psaw(7, 8, 8, 0.7, 1.0, 4), B.psaw(7, 8, -1, 0.7, 1.0, 4), B.psaw(7, 8, 6, 0.0, 1.0, 4),
+           B.psaw(7, 8, 6, 1.5, 1.0, 4), B.psaw(7, 8, 6, 0.7, -1.0, 4),
+           B.psaw(7, 8, 6, 0.7, float("inf"), 4), B.psaw(7, 8, 6, float("nan"), 1.0, 4),
+           B.psaw(7, 8, 6, 0.7, 1.0, -1)]
+    for ps in bad:
+        assert L.prhs_psaw_first_visible(ctypes.byref(ps), 100) == -1
+        assert L.prhs_last_error()
+        with pytest.raises(B.PrhsError):
+            B.prhs_psaw_first_visible(ps, 100)
+    assert L.prhs_psaw_first_visible(None, 100) == -1
+    assert L.prhs_psaw_first_visible(ctypes.byref(B.psaw(7, 8, 6, 0.7, 1.0, 4)), -1) == -1
+    # phi = 1 masks nothing at any depth
+    assert B.prhs_psaw_first_visible(B.psaw(7, 8, 6, 1.0, 1.0, 4), 1000) == 4
+
+
+def _host_kv(B_=2, hq=8, hkv=2, cap=64, d=64):
+    K = torch.zeros(B_, hkv, cap, d, dtype=torch.bfloat16)
+    return B.KV(K, K.clone(), torch.full((B_,), cap, dtype=torch.int32), cap, hq)
+
+
+def _i32(*shape):
+    return torch.zeros(*shape, dtype=torch.int32)
+
+
+def test_binding_rejects_wrong_shapes_before_any_launch():
+    # every tensor's shape is checked against the cache descriptor: a wrong
+    # one raises ValueError in the binding, before the library is called
+    kv = _host_kv()
+    q, ws = torch.zeros(2, 8, 64, dtype=torch.bfloat16), torch.zeros(16, dtype=torch.uint8)
+    out, lse = torch.zeros(2, 8, 64), torch.zeros(2, 8)
+    sets, lens = _i32(2, 2, 40), _i32(2, 2)
+    cases = [
+        lambda: B.prhs_sparse_decode_attn(kv, q, sets, lens, 0.1, torch.zeros(2, 2, 64), lse, ws),
+        lambda: B.prhs_sparse_decode_attn(kv, q, sets, lens, 0.1, out, torch.zeros(2, 2), ws),
+        lambda: B.prhs_sparse_decode_attn(kv, q, _i32(2, 8, 40), _i32(2, 8), 0.1, out, lse, ws),
+        lambda: B.prhs_sparse_decode_attn(kv, q, sets, _i32(2, 3), 0.1, out, lse, ws),
+        lambda: B.prhs_sparse_decode_attn(kv, q[:1], sets, lens, 0.1, out, lse, ws),
+        lambda: B.prhs_reuse_decode_attn(kv, q, sets, lens, _i32(3), 0.1, out, lse, ws),
+        lambda: B.prhs_dense_decode_attn(kv, q, 0.1, torch.zeros(2, 8, 32), lse, ws),
+        lambda: B.prhs_select(kv, q, B.params(k=4), _i32(2, 8, 4), _i32(2, 2), sets, lens, ws),
+        lambda: B.prhs_select(kv, q, B.params(k=4), _i32(2, 2, 4), _i32(2), sets, lens, ws),
+        lambda: B.prhs_select_shared(kv, q, B.params(k=4), _i32(2, 2, 4), _i32(2, 2), sets, lens,
+                                     _i32(2, 2, 39), lens, ws),
+        lambda: B.prhs_select_gated(kv, q, B.params(k=4), _i32(2), _i32(2, 2, 4), _i32(2, 2), sets,
+                                    lens, sets.clone(), lens.clone(), ws),
+        lambda: B.prhs_pool_decode_attn(kv, q, _i32(6, 40), _i32(5), _i32(4), _i32(4), 0.1, out,
+                                        lse, ws),
+        lambda: B.prhs_pool_decode_attn(kv, q, _i32(6, 40), _i32(6), _i32(3), _i32(4), 0.1, out,
+                                        lse, ws),
+        lambda: B.prhs_pool_decode_attn(kv, q, _i32(6, 40), _i32(6), _i32(4), _i32(5), 0.1, out,
+                                        lse, ws),
+        lambda: B.prhs_dilate_reuse(B.params(k=4), _i32(2, 2, 4), _i32(2, 2), _i32(3), _i32(2),
+                                    sets, lens),
+        lambda: B.prhs_dilate_reuse(B.params(k=4), _i32(2, 2, 4), _i32(2, 2), _i32(2), _i32(2),
+                                    _i32(2, 3, 40), lens),
+        lambda: B.prhs_gate(q, _i32(2), 0.8, 0, torch.zeros(4, 2, 8, 64, dtype=torch.bfloat16),
+                            _i32(4, 4), _i32(4, 2), _i32(3), _i32(4), _i32(4), _i32(4), 2),
+        lambda: B.prhs_prefill_attn(kv, torch.zeros(2, 8, 10, 64, dtype=torch.bfloat16), 0.1,
+                                    torch.zeros(2, 8, 9, 64)),
+        lambda: B.prhs_prefill_attn(kv, torch.zeros(2, 8, 10, 64, dtype=torch.bfloat16), 0.1,
+                                    torch.zeros(2, 8, 10, 64), torch.zeros(2, 8, 11)),
+    ]
+    for i, call in enumerate(cases):
+        with pytest.raises(ValueError):
+            call()
+            pytest.fail(f"case {i} was not rejected")
+
+
+def test_binding_rejects_host_tensors():
+    # correctly shaped tensors that are not on the GPU never reach the library
+    kv = _host_kv()
+    q, ws = torch.zeros(2, 8, 64, dtype=torch.bfloat16), torch.zeros(16, dtype=torch.uint8)
+    out, lse = torch.zeros(2, 8, 64), torch.zeros(2, 8)
+    with pytest.raises(ValueError, match="GPU"):
+        B.prhs_sparse_decode_attn(kv, q, _i32(2, 2, 40), _i32(2, 2), 0.1, out, lse, ws)
+    with pytest.raises(ValueError, match="GPU"):
+        B.prhs_dense_decode_attn(kv, q, 0.1, out, None, ws)
+    with pytest.raises(ValueError, match="GPU"):
+        B.prhs_dilate_reuse(B.params(k=4), _i32(2, 2, 4), _i32(2, 2), _i32(2), _i32(2),
+                            _i32(2, 2, 40), _i32(2, 2))
+    with pytest.raises(ValueError, match="GPU"):
+        B.prhs_gate(q, _i32(2), 0.8, 0, torch.zeros(4, 2, 8, 64, dtype=torch.bfloat16),
+                    _i32(4, 4), _i32(4, 2), _i32(4), _i32(4), _i32(4), _i32(4), 2)

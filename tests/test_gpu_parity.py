@@ -387,6 +387,14 @@ def test_select_all_ties_beyond_lds_budget():
     assert list(topk[0, 0, :3]) == [4, 5, 6]
 
 
+def test_select_largest_supported_topk():
+    # k = PRHS_MAX_TOPK on middle ranges beyond LDS (the radix path, whose
+    # finish kernel keeps every winner in LDS), one row clamped to its middle
+    lens = (40000, 16050)
+    inp = synth.random_inputs(2, 4, 1, 128, lens, seed=14, grid=True, device=DEV)
+    check_select(inp, lens, B.params(k=B.PRHS_MAX_TOPK, sink=4, window=64))
+
+
 @pytest.mark.parametrize("lens", [(6000, 2500), (30000, 26000)], ids=["keyed", "radix"])
 def test_select_coarse_grid_many_ties(lens):
     # values in {-1/16, 0, 1/16}: very many exact ties at the threshold

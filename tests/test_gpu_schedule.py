@@ -92,8 +92,8 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets
                 assert np.array_equal(got, S), f"l{l} j{j} b{b} g{g}: set differs"
                 if psaw is not None:
                     start = O.psaw_visible_start(l, L, n, w.sink, *psaw)
-                    st = run.psaw_start.get((l, j))
-                    assert (st.cpu().numpy()[b] if st is not None else min(w.sink, n)) == start
+                    st = run.psaw_start(l, j)
+                    assert (st[b] if st is not None else min(w.sink, n)) == start
                     S = O.psaw_restrict(S, start, w.sink, n)
                 if (b, g) in units_out:
                     K, V = cache.get(l, b, g)
