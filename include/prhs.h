@@ -252,6 +252,22 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q,
                                     int32_t set_cap, float scale, float* out, float* lse,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* prhs_sparse_decode_attn without a workspace argument, for callers that
+ * cannot allocate device memory (code under stream capture, tight serving
+ * loops, hosts that forbid allocation).  Same arguments, semantics and
+ * outputs as prhs_sparse_decode_attn, computed by the same kernels; the
+ * split-K partials live in a static array of 16 MiB that every device the
+ * library runs on holds until the process ends.  No call allocates or frees
+ * memory.  Calls whose partials would exceed the array
+ * (prhs_workspace_size(PRHS_OP_SPARSE_ATTN) > 16 MiB) return
+ * PRHS_E_UNSUPPORTED.  Every call on one device uses that device's single
+ * array: calls that overlap on one device (other streams, other host
+ * threads) race and must be ordered by the caller. */
+prhs_status prhs_sparse_decode_attn_static(const prhs_kv* kv, const void* q,
+                                           const int32_t* set_idx, const int32_t* set_len,
+                                           int32_t set_cap, float scale, float* out, float* lse,
+                                           void* stream);
+
 /* Token-sparse decode attention over a reused set (Def. 3.2 key-value sharing,
  * Sec. 2.2; Eq. neighboring): the shared set of a later decode step without
  * rebuilding it.

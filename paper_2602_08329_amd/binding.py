@@ -41,6 +41,7 @@ PRHS_MAX_TOPK = 16000
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
+    "prhs_sparse_decode_attn_static",
     "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_select_gated",
     "prhs_pool_decode_attn", "prhs_prefill_attn", "prhs_psaw_first_visible", "prhs_last_error",
 ]
@@ -114,6 +115,9 @@ def lib():
         L.prhs_sparse_decode_attn.restype = i32
         L.prhs_sparse_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, ctypes.c_float, vp, vp,
                                               vp, sz, vp]
+        L.prhs_sparse_decode_attn_static.restype = i32
+        L.prhs_sparse_decode_attn_static.argtypes = [P(PrhsKv), vp, vp, vp, i32, ctypes.c_float, vp,
+                                                     vp, vp]
         L.prhs_reuse_decode_attn.restype = i32
         L.prhs_reuse_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, vp, ctypes.c_float, vp,
                                              vp, vp, sz, vp]
@@ -362,6 +366,19 @@ def prhs_sparse_decode_attn(kv, q, set_idx, set_len, scale, out, lse, ws, stream
     check(lib().prhs_sparse_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx), _ptr(set_len),
                                         set_idx.shape[-1], float(scale), _ptr(out), _ptr(lse),
                                         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def prhs_sparse_decode_attn_static(kv, q, set_idx, set_len, scale, out, lse, stream=None):
+    """prhs_sparse_decode_attn with its split-K partials in the library's
+    static device array instead of a workspace: no allocation anywhere.
+    Calls that overlap on one GPU race."""
+    _q(kv, q)
+    _sets(kv, set_idx, set_len)
+    _outputs(kv, out, lse)
+    kv.check_device(q=q, set_idx=set_idx, set_len=set_len, out=out, lse=lse)
+    check(lib().prhs_sparse_decode_attn_static(ctypes.byref(kv.c), _ptr(q), _ptr(set_idx),
+                                               _ptr(set_len), set_idx.shape[-1], float(scale),
+                                               _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def prhs_reuse_decode_attn(kv, q, set_idx, set_len, anchor_lens, scale, out, lse, ws,

@@ -38,6 +38,8 @@
 // workgroup).
 #include <stdlib.h>
 
+#include <mutex>
+
 #include "prhs_internal.h"
 
 namespace prhs {
@@ -836,6 +838,30 @@ void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int 
   if (c > cmax) c = cmax;
   *chunk = (int)c;
   *nsplit = (int)((rows + c - 1) / c);
+}
+
+// Scratch for the split-K partials of prhs_sparse_decode_attn_static, the
+// entry point for callers that cannot allocate.  Every device that runs it
+// holds its own copy until the process ends; calls on one device share it.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+hipError_t attn_static_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 size_t attn_workspace_bytes(int dtype, bool dense, int batch, int hq, int hkv, int d,

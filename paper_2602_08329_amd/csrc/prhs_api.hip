@@ -391,6 +391,30 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int3
                           "prhs_sparse_decode_attn launch");
 }
 
+prhs_status prhs_sparse_decode_attn_static(const prhs_kv* kv, const void* q,
+                                           const int32_t* set_idx, const int32_t* set_len,
+                                           int32_t set_cap, float scale, float* out, float* lse,
+                                           void* stream) {
+  prhs_status st = check_kv_shape(kv);
+  if (st != PRHS_OK) return st;
+  if (set_cap < 0) return fail(PRHS_E_INVALID, "set_cap must be >= 0");
+  const size_t need = prhs::attn_workspace_bytes(kv->dtype, false, kv->batch, kv->num_q_heads,
+                                                 kv->num_kv_heads, kv->head_dim, set_cap);
+  if (need > prhs::kStaticScratchBytes)
+    return fail(PRHS_E_UNSUPPORTED,
+                "split-K partials of %zu bytes exceed the static scratch of %zu bytes", need,
+                prhs::kStaticScratchBytes);
+  if (kv->batch == 0) return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr,
+                                              nullptr, 0, nullptr, scale, out, lse, nullptr, 0,
+                                              stream, false, "prhs_sparse_decode_attn_static");
+  void* ws = nullptr;
+  if ((st = device_status(prhs::attn_static_scratch(&ws), "static scratch lookup")) != PRHS_OK)
+    return st;
+  return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, nullptr,
+                          scale, out, lse, ws, prhs::kStaticScratchBytes, stream, false,
+                          "prhs_sparse_decode_attn_static launch");
+}
+
 prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32_t* set_idx,
                                    const int32_t* set_len, int32_t set_cap,
                                    const int32_t* anchor_lens, float scale, float* out, float* lse,

@@ -195,6 +195,12 @@ void attn_split_geometry(int dtype, bool dense, int batch, int hq, int hkv, int 
 size_t attn_workspace_bytes(int dtype, bool dense, int batch, int hq, int hkv, int d,
                             int rows_cap);
 hipError_t launch_attention(const AttnLaunch& a, bool dense, hipStream_t stream);
+// Device address and size of this device's static scratch array for the
+// split-K partials of the no-allocation attention entry point (looked up
+// once per device with hipGetSymbolAddress; the array is never named on the
+// host otherwise).
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+hipError_t attn_static_scratch(void** ptr);
 
 struct GateLaunch {
   int batch, hq, hkv, d, dtype;

@@ -411,3 +411,19 @@ def test_binding_rejects_host_tensors():
     with pytest.raises(ValueError, match="GPU"):
         B.prhs_gate(q, _i32(2), 0.8, 0, torch.zeros(4, 2, 8, 64, dtype=torch.bfloat16),
                     _i32(4, 4), _i32(4, 2), _i32(4), _i32(4), _i32(4), _i32(4), 2)
+
+
+def test_static_attention_rejects_partials_beyond_its_scratch(L):
+    # partials of 64 x 64 heads x many splits exceed the 16 MiB static array:
+    # rejected on the host, before any device work
+    kv = _kv(batch=64, num_q_heads=64, num_kv_heads=8, capacity=100000, max_seq_len=100000)
+    st = L.prhs_sparse_decode_attn_static(ctypes.byref(kv), 0x1, 0x2, 0x3, 100000, 0.1, 0x4, None,
+                                          None)
+    assert st == B.PRHS_E_UNSUPPORTED and b"static scratch" in L.prhs_last_error()
+    n = ctypes.c_size_t(0)
+    L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 100000, ctypes.byref(n))
+    assert n.value > 16 << 20
+    # an empty batch is a no-op
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert L.prhs_sparse_decode_attn_static(ctypes.byref(kv0), None, None, None, 64, 0.1, None,
+                                            None, None) == B.PRHS_OK
