@@ -141,64 +141,166 @@ def record_step(run, j, gated):
     return rows, sel
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def allowed_cores():
+    """Cores this process may use: its affinity set, capped by
+    OMP_NUM_THREADS when that is set (the host's CPU share)."""
+    n = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return max(1, n)
+
+
+def _oracle_units(spec, units):
+    """Runs the oracle's decode schedule for the given units over one layer
+    group: units is [(K, V, qs)] with K[l], V[l] float64 caches per layer of
+    the group and qs[(l, j)] the unit's query group; returns nothing (the
+    results are discarded, only the time counts)."""
+    import oracle as O
+    layers, steps, n_ctx_of, gated = spec["layers"], spec["steps"], spec["n_ctx"], spec["tau"]
+    for b, K, V, qs in units:
+        if gated is not None:
+            dec = O.GatedDecodeOracle(spec["sink"], spec["window"], spec["s"], spec["G"], gated,
+                                      r=spec["r"], k=spec["k"], k_num=spec["k_num"],
+                                      k_den=spec["k_den"], dilate_m=spec["dilate_m"])
+        else:
+            dec = O.DecodeOracle(spec["sink"], spec["window"], spec["s"], spec["G"], r=spec["r"],
+                                 k=spec["k"], k_num=spec["k_num"], k_den=spec["k_den"],
+                                 dilate_m=spec["dilate_m"])
+        for j in range(steps):
+            n = n_ctx_of[b] + j + 1
+            for l in layers:
+                Qg = qs[(l, j)]
+                S = dec.step_set(l, j, Qg, K[l], n)
+                dec.attend(Qg, K[l][:n], V[l][:n], S)
+
+
+def _cpu_worker(conn):
+    """All-cores leg: receives its units' caches (float32, converted to
+    float64 before the clock starts), waits for the start signal, runs the
+    oracle on one core and reports its time; repeated per layer group."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):
+        while True:
+            msg = conn.recv()
+            if msg is None:
+                break
+            spec, raw = msg
+            units = [(b, {l: np.asarray(k, dtype=np.float64) for l, k in K.items()},
+                      {l: np.asarray(v, dtype=np.float64) for l, v in V.items()},
+                      {key: np.asarray(q, dtype=np.float64) for key, q in qs.items()})
+                     for b, K, V, qs in raw]
+            del raw
+            conn.send("ready")
+            conn.recv()
+            t0 = time.perf_counter()
+            _oracle_units(spec, units)
+            conn.send(time.perf_counter() - t0)
+
+
 def cpu_baseline(run, budget_s):
-    """Times the CPU oracle on a bounded sample of the same workload: whole
-    layer groups (every (batch, kv-head) unit, every decode step of the
-    cycle, in schedule order), group after group until the time budget is
-    spent; scaled to all layers.  Only the oracle calls are timed; copying the
-    caches to the host is not."""
+    """Times the CPU oracle on a bounded sample of the same workload, read
+    back from the device: whole layer groups (every (batch, kv-head) unit,
+    every decode step of the cycle, in schedule order), group after group
+    until about budget_s of one core's time is spent.  Two legs over the same
+    sample: one core, and every allowed core (one spawned worker process per
+    core, the units dealt round-robin; the clock runs from the start signal
+    to the last worker's result, after every worker holds its caches).  Only
+    oracle work is timed; scaled per layer-step."""
+    import multiprocessing as mp
+
     import numpy as np
     from threadpoolctl import threadpool_limits
 
-    import oracle as O
     from paper_2602_08329_amd import synth
 
     w = run.w
     inp = run.inp
     units = [(b, g) for b in range(w.batch) for g in range(w.hkv)]
-    spent = 0.0
+    cores = allowed_cores()
+    ctx = mp.get_context("spawn")
+    pipes, procs = [], []
+    for _ in range(cores if cores > 1 else 0):
+        parent, child = ctx.Pipe()
+        p = ctx.Process(target=_cpu_worker, args=(child,), daemon=True)
+        p.start()
+        pipes.append(parent)
+        procs.append(p)
+    spent1 = spent_all = 0.0
     layer_steps = 0
-    with threadpool_limits(limits=1):
+    try:
         for g0 in range(0, run.L, w.G):
             layers = list(range(g0, min(g0 + w.G, run.L)))
-            caches = {}
-            for l in layers:
-                for (b, g) in units:
-                    caches[(l, b, g)] = synth.gather_unit(inp, l, b, g, w.n_ctx[b] + w.steps)
-            qs = {}
-            for l in layers:
-                qh = inp.q[l].float().cpu().numpy().astype(np.float64)
-                for j in range(w.steps):
-                    for (b, g) in units:
-                        qs[(l, j, b, g)] = qh[j, b, g * w.g:(g + 1) * w.g]
-            if hasattr(run, "tau"):
-                decs = {u: O.GatedDecodeOracle(w.sink, w.window, w.s, w.G, run.tau, r=w.r, k=w.k,
-                                               k_num=w.k_num, k_den=w.k_den,
-                                               dilate_m=w.dilate_m) for u in units}
-            else:
-                decs = {u: O.DecodeOracle(w.sink, w.window, w.s, w.G, r=w.r, k=w.k,
-                                          k_num=w.k_num, k_den=w.k_den, dilate_m=w.dilate_m)
-                        for u in units}
-            t0 = time.perf_counter()
-            for j in range(w.steps):
+            spec = dict(layers=layers, steps=w.steps, n_ctx=list(w.n_ctx), sink=w.sink,
+                        window=w.window, s=w.s, G=w.G, r=w.r, k=w.k, k_num=w.k_num, k_den=w.k_den,
+                        dilate_m=w.dilate_m, tau=getattr(run, "tau", None))
+            qh = {l: inp.q[l].float().cpu().numpy().astype(np.float64) for l in layers}
+            data = []
+            for (b, g) in units:
+                K, V = {}, {}
                 for l in layers:
-                    for (b, g) in units:
-                        n = w.n_ctx[b] + j + 1
-                        K, V = caches[(l, b, g)]
-                        Qg = qs[(l, j, b, g)]
-                        S = decs[(b, g)].step_set(l, j, Qg, K, n)
-                        decs[(b, g)].attend(Qg, K[:n], V[:n], S)
-            spent += time.perf_counter() - t0
+                    K[l], V[l] = synth.gather_unit(inp, l, b, g, w.n_ctx[b] + w.steps)
+                qs = {(l, j): qh[l][j, b, g * w.g:(g + 1) * w.g] for l in layers
+                      for j in range(w.steps)}
+                data.append((b, K, V, qs))
+            with threadpool_limits(limits=1):
+                t0 = time.perf_counter()
+                _oracle_units(spec, data)
+                spent1 += time.perf_counter() - t0
+            if pipes:
+                for i, conn in enumerate(pipes):
+                    mine = [(b, {l: x.astype(np.float32) for l, x in K.items()},
+                             {l: x.astype(np.float32) for l, x in V.items()},
+                             {key: q.astype(np.float32) for key, q in qs.items()})
+                            for (b, K, V, qs) in data[i::len(pipes)]]
+                    conn.send((spec, mine))
+                    del mine
+                for conn in pipes:
+                    assert conn.recv() == "ready"
+                t0 = time.perf_counter()
+                for conn in pipes:
+                    conn.send("go")
+                for conn in pipes:
+                    conn.recv()
+                spent_all += time.perf_counter() - t0
             layer_steps += len(layers) * w.steps
-            del caches
-            if spent >= budget_s:
+            del data
+            if spent1 >= budget_s:
                 break
-    us = spent / layer_steps * 1e6
-    return {"value": round(us, 1), "unit": "us/layer-step", "cores": 1, "kind": "oracle",
-            "sample": (f"{layer_steps // w.steps} of {run.L} layers x {w.steps} decode steps x all "
-                       f"{len(units)} (batch, kv-head) units; {spent:.1f} s of oracle time; "
-                       "per layer-step"),
-            "cpu": platform.processor() or platform.machine()}
+    finally:
+        for conn in pipes:
+            try:
+                conn.send(None)
+            except (BrokenPipeError, OSError):
+                pass
+        for p in procs:
+            p.join(timeout=30)
+    us1 = spent1 / layer_steps * 1e6
+    sample = (f"{layer_steps // w.steps} of {run.L} layers x {w.steps} decode steps x all "
+              f"{len(units)} (batch, kv-head) units, per layer-step; {spent1:.1f} s on one core")
+    legs = [{"cores": 1, "value": round(us1, 1)}]
+    best = {"value": round(us1, 1), "cores": 1}
+    if pipes:
+        usn = spent_all / layer_steps * 1e6
+        legs.append({"cores": cores, "value": round(usn, 1)})
+        best = {"value": round(usn, 1), "cores": cores}
+        sample += f", {spent_all:.1f} s on {cores} cores"
+    return {"value": best["value"], "unit": "us/layer-step", "cores": best["cores"],
+            "kind": "oracle", "sample": sample, "legs": legs, "cpu": cpu_model(),
+            "allowed_cores": len(os.sched_getaffinity(0))}
 
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -425,82 +527,42 @@ def prefill_cpu_baseline(qs, Ks, Vs, vis, T, sink, scale, L, H, Bsz, budget_s):
     n_psaw = sum(1 for x in vis if x is not None)
     per_step = (times["causal"] * (L - n_psaw) + times["psaw"] * n_psaw) * H * Bsz
     return {"value": round(per_step * 1e6 / L, 1), "unit": "us/layer", "cores": 1,
-            "kind": "oracle", "cpu": platform.machine(),
+            "kind": "oracle", "cpu": cpu_model(),
             "sample": f"every {max(1, T // 256)}-th query row (from the last) of head 0 of layer 0 "
                       f"(causal) and layer {L - 1} (PSAW), scaled to {H} heads x {L} layers"}
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=32)
-    ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--config", type=int, default=1, help="workload index 0-5")
-    ap.add_argument("--batch", type=int, default=None, help="workloads 4, 5: batch")
-    ap.add_argument("--nmax", type=int, default=None, help="workloads 4, 5: max context")
-    ap.add_argument("--block", type=int, default=None, help="workload 5: CIS block size s")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--per-step-sets", action="store_true",
-                    help="rebuild the dilated shared set at every step instead of once per refresh")
-    ap.add_argument("--psaw", action="store_true",
-                    help="progressive sliding attention window on the top layers (Sec. 5.1 "
-                         "defaults: l_s = floor(3N/4), phi = 0.7, alpha = 1): CPE with --gate")
-    ap.add_argument("--gate", type=float, default=None, metavar="TAU",
-                    help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
-                         "fixed refresh period (blocks of refresh_every steps)")
-    ap.add_argument("--eager", action="store_true",
-                    help="time eager launches instead of replays of a captured HIP graph")
-    ap.add_argument("--paged", action="store_true",
-                    help="with --prefill: the prompts' K/V in a paged cache (16-token pages, "
-                         "seeded random page order)")
-    ap.add_argument("--prefill", action="store_true",
-                    help="prefill attention under the PSAW mask instead of the decode step "
-                         "(LLaMA-2-7B shape; --nmax prompt length, --batch prompts)")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device copy (HBM counter calibration)")
-    args = ap.parse_args()
-    if args.copy_calibration:
-        copy_calibration()
-        return
+def selection_kernels(w, cus):
+    """The refresh launches the library picks for this workload (the rule of
+    its select_path): one fused kernel when the middle range fits LDS, the
+    cache is contiguous bf16 and the rows fill more than half the CUs."""
+    rows = w.batch * w.hkv
+    fits = w.capacity <= 24576
+    if fits and w.dtype == "bf16" and not w.paged and 2 * rows > cus:
+        return "select_fused", 1
+    if fits:
+        return "score + select_keyed", 2
+    return "select_clear + score + select_filter + select_finish", 4
 
-    if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the hot path has no multi-GPU mode)", file=sys.stderr)
-        sys.exit(2)
-    if args.prefill:
-        prefill_main(args)
-        return
 
+def measure(w, args, dev, K_steps, W_steps, psaw=None, gated=False, tau=None):
+    """Times one workload's decode loop (sparse step, selection alone,
+    attention alone, one refresh of every group alone, dense) as HIP-graph
+    replays and returns (numbers, runner)."""
     import torch
 
-    from paper_2602_08329_amd import binding as B
     from paper_2602_08329_amd import synth
-    from paper_2602_08329_amd.schedule import (DecodeRunner, GatedDecodeRunner, capture_steps,
-                                               psaw_defaults)
+    from paper_2602_08329_amd.schedule import DecodeRunner, GatedDecodeRunner, capture_steps
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(2)
-    B.lib()
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    w = synth.workload(args.config, batch=args.batch, nmax=args.nmax, block=args.block)
     T = w.steps
-    K_steps, W_steps = args.steps, args.warmup
     log(f"workload {w.name}: generating inputs on the GPU")
     t0 = time.time()
     inp = synth.generate(w, device=dev)
     torch.cuda.synchronize()
     log(f"inputs ready in {time.time() - t0:.1f} s; "
         f"{sum(x.numel() * x.element_size() for x in inp.K + inp.V) / 2**30:.1f} GiB of KV")
-    gated = args.gate is not None
-    if gated and args.per_step_sets:
-        print("--gate and --per-step-sets exclude each other", file=sys.stderr)
-        sys.exit(2)
-    psaw = psaw_defaults(len(inp.K)) if args.psaw else None
     if gated:
-        run = GatedDecodeRunner(inp, dev, tau=args.gate, psaw=psaw)
+        run = GatedDecodeRunner(inp, dev, tau=tau, psaw=psaw)
     else:
         run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets, psaw=psaw)
 
@@ -522,7 +584,7 @@ def main():
         the K steps are captured once into a HIP graph, replayed once
         untimed and once timed, so the region holds the same kernels
         back to back without host launch overhead; with --eager they are
-        launched one by one from Python."""
+        launched one by one from Python.  HIP events on the launch stream."""
         order = order or (lambda i: i % T)
         for i in range(W_steps):
             fn(order(i))
@@ -574,31 +636,175 @@ def main():
         for l in range(run.L):
             run.attend(l, j)
     ms_attn, js_attn = timed(attn_only, "attention only", order=order)
+
+    # one refresh of every layer group at the refresh step j_blk, repeated:
+    # the selection launches alone, back to back
+    refresh = None
+    if not gated:
+        def refresh_only(_j):
+            for gi in range(run.groups):
+                run.refresh(gi, j_blk)
+        ms_ref, _ = timed(refresh_only, "refresh launches only", order=lambda i: j_blk)
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        name, nk = selection_kernels(w, cus)
+        refresh = dict(kernel=name, launches_per_refresh=nk, groups=run.groups,
+                       avg_us=ms_ref * 1e3 / (K_steps * run.groups),
+                       avg_bytes=per[j_blk]["sel"] / run.groups)
+        if args.per_step_sets:
+            refresh = None
+        else:
+            run.selection_step(j_blk)   # restore the block's sets
+
     ms_dense, js_dense = timed(run.dense_step, "dense attention")
     dense_total = sum(run.L * dense_bytes(w, run.seq_lens[j].tolist()) for j in js_dense)
-    stream_gbps = torch_sum_gbps()
 
-    # dominant kernel: the sparse attention launch.  Its average duration is
-    # the back-to-back attention-only loop above (HIP events on the launch
-    # stream, over the timed region); its bytes are the per-launch algorithmic
-    # bytes averaged over the same launches.
     launch_bytes = [attention_bytes(w, set_lens[(l, j)]) for j in js_attn for l in range(run.L)]
     avg_bytes = sum(launch_bytes) / len(launch_bytes)
     avg_dur = ms_attn * 1e-3 / (K_steps * run.L)
-    achieved = avg_bytes / avg_dur / 1e9
-    traffic = committed_traffic(f"attn_split_bf16_{w.name}_pmc.md", "attention.hip")
     L = run.L
     total_bytes = sum(per[j]["attn"] + per[j]["sel"] for j in js)
-    us_layer_step = ms_sparse * 1e3 / (K_steps * L)
     eff_gbps = total_bytes / (ms_sparse * 1e-3) / 1e9
+    num = dict(
+        workload=w.name, ms_sparse=ms_sparse, us_layer_step=ms_sparse * 1e3 / (K_steps * L),
+        eff_gbps=eff_gbps, speedup=ms_dense / ms_sparse,
+        dense_us=ms_dense * 1e3 / (K_steps * L),
+        dense_gbps=dense_total / (ms_dense * 1e-3) / 1e9,
+        sel_us=ms_sel * 1e3 / (K_steps * L), attn_us=ms_attn * 1e3 / (K_steps * L),
+        attn_launch=dict(avg_us=avg_dur * 1e6, avg_bytes=avg_bytes, launches=len(launch_bytes)),
+        refresh=refresh, retrieving=retrieving, groups=run.groups)
+    return num, run
+
+
+def roofline_of(w, num, copy_traffic=True):
+    """Roofline of the dominant kernel: the refresh launch when the
+    selection takes more of the step than attention and the refresh is one
+    kernel, else the sparse attention launch.  achieved = its algorithmic
+    bytes per launch / its average launch duration (HIP events over a loop
+    of only those launches)."""
+    ref = num["refresh"]
+    if ref is not None and num["sel_us"] > num["attn_us"] and ref["launches_per_refresh"] == 1:
+        achieved = ref["avg_bytes"] / (ref["avg_us"] * 1e-6) / 1e9
+        traffic = committed_traffic(f"{ref['kernel']}_{w.name}_pmc.md", "select.hip")
+        return {"kernel": ref["kernel"], "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": traffic if copy_traffic else None,
+                "avg_launch_us": round(ref["avg_us"], 3), "avg_launch_bytes": int(ref["avg_bytes"]),
+                "launches": ref["groups"]}
+    a = num["attn_launch"]
+    achieved = a["avg_bytes"] / (a["avg_us"] * 1e-6) / 1e9
+    kern = "attn_split_bf16" if w.dtype != "f32" else "attn_split_f32"
+    traffic = committed_traffic(f"{kern}_{w.name}_pmc.md", "attention.hip")
+    return {"kernel": kern + " (sparse)", "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic if copy_traffic else None, "avg_launch_us": round(a["avg_us"], 3),
+            "avg_launch_bytes": int(a["avg_bytes"]), "launches": a["launches"]}
+
+
+def summary_of(w, num):
+    """The numbers of one workload as the JSON line reports them."""
+    out = {
+        "workload": w.name,
+        "us_per_layer_step": round(num["us_layer_step"], 3),
+        "effective_gbps": round(num["eff_gbps"], 1),
+        "pct_hbm_peak": round(100 * num["eff_gbps"] / HBM_PEAK_GBPS, 2),
+        "speedup_vs_dense": round(num["speedup"], 3),
+        "dense_us_per_layer_step": round(num["dense_us"], 3),
+        "dense_gbps": round(num["dense_gbps"], 1),
+        "selection_us_per_layer_step": round(num["sel_us"], 3),
+        "attention_us_per_layer_step": round(num["attn_us"], 3),
+        "attention_launch": {"avg_us": round(num["attn_launch"]["avg_us"], 3),
+                             "frac": round(num["attn_launch"]["avg_bytes"]
+                                           / (num["attn_launch"]["avg_us"] * 1e-6) / 1e9
+                                           / HBM_PEAK_GBPS, 4)},
+    }
+    if num["refresh"] is not None:
+        r = num["refresh"]
+        out["refresh_launch"] = {"kernels": r["kernel"], "avg_us": round(r["avg_us"], 3),
+                                 "frac": round(r["avg_bytes"] / (r["avg_us"] * 1e-6) / 1e9
+                                               / HBM_PEAK_GBPS, 4)}
+    return out
+
+
+HEADLINE = (4, 64, 16384)      # the largest single-GPU workload: GQA sweep, B 64 x nmax 16k
+LONG_CONTEXT = (2, 3)          # 32k and 128k (paged) context, the speedup target's range
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", type=int, default=HEADLINE[0], help="workload index 0-5")
+    ap.add_argument("--batch", type=int, default=None, help="workloads 4, 5: batch")
+    ap.add_argument("--nmax", type=int, default=None, help="workloads 4, 5: max context")
+    ap.add_argument("--block", type=int, default=None, help="workload 5: CIS block size s")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-long-context", action="store_true",
+                    help="skip the 32k and 128k workloads measured after the headline")
+    ap.add_argument("--per-step-sets", action="store_true",
+                    help="rebuild the dilated shared set at every step instead of once per refresh")
+    ap.add_argument("--psaw", action="store_true",
+                    help="progressive sliding attention window on the top layers (Sec. 5.1 "
+                         "defaults: l_s = floor(3N/4), phi = 0.7, alpha = 1): CPE with --gate")
+    ap.add_argument("--gate", type=float, default=None, metavar="TAU",
+                    help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
+                         "fixed refresh period (blocks of refresh_every steps)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches instead of replays of a captured HIP graph")
+    ap.add_argument("--paged", action="store_true",
+                    help="with --prefill: the prompts' K/V in a paged cache (16-token pages, "
+                         "seeded random page order)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="prefill attention under the PSAW mask instead of the decode step "
+                         "(LLaMA-2-7B shape; --nmax prompt length, --batch prompts)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path has no multi-GPU mode)", file=sys.stderr)
+        sys.exit(2)
+    if args.prefill:
+        prefill_main(args)
+        return
+
+    import torch
+
+    from paper_2602_08329_amd import binding as B
+    from paper_2602_08329_amd import synth
+    from paper_2602_08329_amd.schedule import psaw_defaults
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    B.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    headline = (args.config == HEADLINE[0] and args.batch is None and args.nmax is None)
+    batch = HEADLINE[1] if headline else args.batch
+    nmax = HEADLINE[2] if headline else args.nmax
+    w = synth.workload(args.config, batch=batch, nmax=nmax, block=args.block)
+    K_steps, W_steps = args.steps, args.warmup
+    gated = args.gate is not None
+    if gated and args.per_step_sets:
+        print("--gate and --per-step-sets exclude each other", file=sys.stderr)
+        sys.exit(2)
+    psaw = psaw_defaults(w.layers) if args.psaw else None
+    num, run = measure(w, args, dev, K_steps, W_steps, psaw=psaw, gated=gated, tau=args.gate)
+    L = run.L
     result = {
         "metric": METRIC,
-        "value": round(us_layer_step, 3),
+        "value": round(num["us_layer_step"], 3),
         "unit": "us/layer-step",
         "n_gpus": 1,
         "steps": K_steps,
         "warmup": W_steps,
-        "ms_per_step": round(ms_sparse / K_steps, 4),
+        "ms_per_step": round(num["ms_sparse"] / K_steps, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -607,38 +813,49 @@ def main():
         "config": {
             "workload": w.name, "layers": w.layers, "batch": w.batch, "q_heads": w.hq,
             "kv_heads": w.hkv, "head_dim": w.d, "context": max(w.n_ctx),
+            "context_per_sequence": "uniform in [nmax/2, nmax - 16]" if w.k_den else "fixed",
             "k": w.k if not w.k_den else f"{w.k_num}/{w.k_den} n", "window": w.window,
             "sink": w.sink, "refresh_every": w.s, "layer_group": w.G, "dilate_r": w.r,
-            "paged": w.paged, "decode_steps_cycled": T,
+            "paged": w.paged, "decode_steps_cycled": w.steps,
             "shared_sets": ("similarity gate" if gated else
                             "per step" if args.per_step_sets else "per refresh + decoded tail"),
             "psaw": ({"l_s": psaw[0], "phi": psaw[1], "alpha": psaw[2]} if psaw else None),
             "launch": "eager" if args.eager else "hip-graph replay",
         },
-        "effective_gbps": round(eff_gbps, 1),
-        "pct_hbm_peak": round(100 * eff_gbps / HBM_PEAK_GBPS, 2),
-        "speedup_vs_dense": round(ms_dense / ms_sparse, 3),
-        "dense_us_per_layer_step": round(ms_dense * 1e3 / (K_steps * L), 3),
-        "dense_gbps": round(dense_total / (ms_dense * 1e-3) / 1e9, 1),
-        "torch_sum_gbps": stream_gbps,
-        "selection_us_per_layer_step": round(ms_sel * 1e3 / (K_steps * L), 3),
-        "attention_us_per_layer_step": round(ms_attn * 1e3 / (K_steps * L), 3),
-        "roofline": {
-            "kernel": "attn_split_bf16 (sparse)" if w.dtype != "f32" else "attn_split_f32 (sparse)",
-            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic, "avg_launch_us": round(avg_dur * 1e6, 3),
-            "avg_launch_bytes": int(avg_bytes), "launches": len(launch_bytes),
-        },
+        "effective_gbps": round(num["eff_gbps"], 1),
+        "pct_hbm_peak": round(100 * num["eff_gbps"] / HBM_PEAK_GBPS, 2),
+        "speedup_vs_dense": round(num["speedup"], 3),
+        "dense_us_per_layer_step": round(num["dense_us"], 3),
+        "dense_gbps": round(num["dense_gbps"], 1),
+        "selection_us_per_layer_step": round(num["sel_us"], 3),
+        "attention_us_per_layer_step": round(num["attn_us"], 3),
+        "roofline": roofline_of(w, num),
     }
+    s_ = summary_of(w, num)
+    for key in ("attention_launch", "refresh_launch"):
+        if key in s_:
+            result[key] = s_[key]
     if gated:
         result["gate"] = {"tau": args.gate,
-                          "retrieval_ratio": round(retrieving / (run.groups * w.batch * w.hkv * T), 4),
+                          "retrieval_ratio": round(num["retrieving"]
+                                                   / (num["groups"] * w.batch * w.hkv * w.steps), 4),
                           "note": "retrieving (anchor layer, kv head) units over all of them, "
                                   "measured over the decode-step cycle"}
     if not args.no_cpu_baseline:
-        log(f"timing the CPU oracle for about {args.cpu_seconds:.0f} s")
+        log(f"timing the CPU oracle for about {args.cpu_seconds:.0f} s on one core, then on "
+            f"{allowed_cores()} cores")
         result["cpu_baseline"] = cpu_baseline(run, args.cpu_seconds)
+    del run
+    torch.cuda.empty_cache()
+    if headline and not args.no_long_context and not gated and not args.per_step_sets:
+        result["long_context"] = []
+        for c in LONG_CONTEXT:
+            wl = synth.workload(c)
+            nl, rl = measure(wl, args, dev, K_steps, W_steps, psaw=psaw)
+            result["long_context"].append(summary_of(wl, nl))
+            del rl
+            torch.cuda.empty_cache()
+    result["stream_reference"] = {"torch_sum_gbps": torch_sum_gbps()}
     print(json.dumps(result), flush=True)
 
 
