@@ -1,9 +1,14 @@
 """Builds libprhs.so (HIP for gfx950) in-tree with hipcc.
 
     python -m paper_2602_08329_amd.build [-v]
+    python -m paper_2602_08329_amd.build --host-sanitize OUT.so
 
 Every source is recompiled on each call; objects go to ``_build/`` next to
 this file and the shared library to ``paper_2602_08329_amd/libprhs.so``.
+With --host-sanitize the host code (argument validation, workspace sizing,
+dispatch) is built with AddressSanitizer and UndefinedBehaviorSanitizer into
+OUT.so (objects beside it) for CPU-side checks; device code is built as usual
+and is not instrumented.
 """
 
 from __future__ import annotations
@@ -43,15 +48,27 @@ def hipcc():
     return path
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+# Host-side sanitizers (each flag applies to the host compilation only).
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+
+def build(verbose: bool = False, host_sanitize: str = None) -> str:
+    out_lib = LIB if host_sanitize is None else os.path.abspath(host_sanitize)
+    objdir = BUILD if host_sanitize is None else out_lib + ".objs"
+    os.makedirs(objdir, exist_ok=True)
     cc = hipcc()
+    flags = list(FLAGS)
+    link_extra = []
+    if host_sanitize is not None:
+        flags = [f if f != "-O3" else "-O1" for f in flags] + SANITIZE
+        link_extra = SANITIZE[:4]
     procs = []
     objs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(objdir, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmd = [cc, *FLAGS, *EXTRA_FLAGS.get(src, []), "-I", INCLUDE, "-I", CSRC, "-c",
+        cmd = [cc, *flags, *EXTRA_FLAGS.get(src, []), "-I", INCLUDE, "-I", CSRC, "-c",
                os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
@@ -67,16 +84,19 @@ def build(verbose: bool = False) -> str:
             print("\n".join(lines))
     if errors:
         raise RuntimeError("hipcc failed:\n" + "\n".join(errors))
-    tmp = LIB + ".tmp"
-    cmd = [cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
+    tmp = out_lib + ".tmp"
+    cmd = [cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *link_extra, *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out_lib)
+    return out_lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    san = None
+    if "--host-sanitize" in sys.argv:
+        san = sys.argv[sys.argv.index("--host-sanitize") + 1]
+    print(build(verbose="-v" in sys.argv, host_sanitize=san))

@@ -241,3 +241,52 @@ def test_pool_attention_row_outside_pool_is_empty():
     for i in range(2):
         yr, _ = O.sparse_attention(Qg[i], K, V, S, 0.1)
         assert np.abs(y[1, 2 + i] - yr).max() <= 2e-3 * np.abs(yr).max()
+
+
+@pytest.mark.parametrize("dtype,hq,hkv,tau", [("bf16", 8, 2, 0.8), ("f32", 4, 4, 0.7),
+                                               ("bf16", 32, 8, 0.9)])
+def test_gate_decisions_off_grid(dtype, hq, hkv, tau):
+    # queries off the grid: the gate's fp32 sums are no longer exact, so a
+    # decision may differ from the exact one only where some query head's
+    # exact cosine lies within 1e-4 of tau (fp32 rounding of d = 128 sums
+    # moves a cosine by about 3 gamma_d = 2.3e-5 at most).  The reference
+    # follows the gate's own retrievals, so later steps compare like for like.
+    S, Bsz, d = 6, 3, 128
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    g_ = torch.Generator().manual_seed(5 + hq)
+    base = torch.randn(Bsz, hq, d, generator=g_)
+    qs = [(base + 0.3 * t * torch.randn(Bsz, hq, d, generator=g_)).to(tdt) for t in range(S)]
+    U, G = Bsz * hkv, hq // hkv
+    ref_q = torch.zeros(S, Bsz, hq, d, dtype=tdt, device=DEV)
+    ref_valid = torch.zeros(S, U, dtype=torch.int32, device=DEV)
+    slot_lens = torch.zeros(S, Bsz, dtype=torch.int32, device=DEV)
+    outs = [torch.zeros(U, dtype=torch.int32, device=DEV) for _ in range(4)]
+    lens = torch.tensor([700, 800, 900], dtype=torch.int32, device=DEV)
+    anchors = {u: [] for u in range(U)}
+
+    def cosines(a, b):
+        a, b = np.atleast_2d(a), np.atleast_2d(b)
+        return (a * b).sum(1) / np.sqrt((a * a).sum(1) * (b * b).sum(1))
+
+    for t in range(S):
+        B.prhs_gate(qs[t].to(DEV), lens, tau, t, ref_q, ref_valid, slot_lens, *outs, hkv)
+        torch.cuda.synchronize()
+        choice = outs[0].cpu().numpy()
+        for u in range(U):
+            b, g = divmod(u, hkv)
+            Qg = qs[t][b, g * G:(g + 1) * G].double().numpy()
+            c = int(choice[u])
+            if t == 0:
+                assert c == -1
+            assert c == -1 or any(st == c for st, _ in anchors[u]), f"slot {t} unit {u}: {c}"
+            # the gate's choice c implies: slot c similar (c >= 0) and every
+            # later anchor not similar (every anchor when c = -1); where the
+            # exact decision differs, some head's cosine must sit at tau
+            for st, Qr in anchors[u]:
+                if c >= 0 and st < c:
+                    continue
+                if O.group_similar(Qg, Qr, tau) != (st == c):
+                    margin = np.abs(cosines(Qg, Qr) - tau).min()
+                    assert margin <= 1e-4, f"slot {t} unit {u} anchor {st}: margin {margin:.2e}"
+            if c == -1:
+                anchors[u].append((t, Qg))

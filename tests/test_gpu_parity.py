@@ -617,3 +617,81 @@ def test_empty_batch_is_a_no_op_on_every_entry_point():
                              0.1, out, lse, ws)
     B.prhs_dense_decode_attn(kv0, q0, 0.1, out, lse, ws)
     torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- off-grid inputs
+
+OFFGRID = ["g8", "ratio", "f32", "f32-paged-gqa", "keyed-128-rows", "radix-ragged-gqa",
+           "radix-paged-d64", "radix-f32-paged", "radix-ratio", "fused-ragged",
+           "fused-mha-d64", "fused-narrow-24k", "g16-keyed", "g16-fused"]
+
+
+def _near_threshold(sym, sigma, tau, tol, what):
+    for x in sym:
+        assert abs(sigma[x] - tau) <= tol, \
+            f"{what}: position {x} differs with score {sigma[x]!r} vs threshold {tau!r} (tol {tol:.2e})"
+
+
+@pytest.mark.parametrize("name", OFFGRID)
+def test_select_off_grid_within_rounding_of_threshold(name):
+    # N(0, 1) inputs that are not on the grid: the library's fp32 scores may
+    # differ from the exact ones by the dot-product rounding bound
+    # gamma_d * sum_d |q_d k_d| (gamma_d = d u / (1 - d u), u = 2^-24), so a
+    # position may swap in or out of the top k (or the top m) only when its
+    # exact score lies within twice the row's largest bound of the k-th
+    # (m-th) largest exact score; everything else must agree, and the anchor
+    # and shared sets must be exactly those the library's own top-k defines.
+    case = next(c for c in SELECT_CASES if c[0] == name)
+    _, dtype, d, paged, hq, hkv, lens, pk = case
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=97 + len(name), grid=False, device=DEV)
+    p = B.params(refresh_every=4, dilate_r=1, **pk)
+    w = inp.w
+    kv, _ = kv_for(inp, lens)
+    k_cap = max(1, B.prhs_max_topk(p, w.capacity))
+    set_cap = max(1, B.prhs_set_capacity(p, w.capacity))
+    shape = (w.batch, w.hkv)
+    topk = torch.full(shape + (k_cap,), -7, dtype=torch.int32, device=DEV)
+    tlen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    sidx = torch.full(shape + (set_cap,), -7, dtype=torch.int32, device=DEV)
+    slen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    hidx = torch.full(shape + (set_cap,), -7, dtype=torch.int32, device=DEV)
+    hlen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv, p), DEV)
+    B.prhs_select_shared(kv, inp.q[0, 0], p, topk, tlen, sidx, slen, hidx, hlen, ws)
+    torch.cuda.synchronize()
+    topk, tlen, sidx, slen = (t.cpu().numpy() for t in (topk, tlen, sidx, slen))
+    hidx, hlen = hidx.cpu().numpy(), hlen.cpu().numpy()
+    swaps = 0
+    for b, n0 in enumerate(lens):
+        for g in range(w.hkv):
+            K = synth.gather_unit(inp, 0, b, g, n0)[0]
+            Qg = synth.query_group(inp, 0, 0, b, g)
+            sigma = O.ranking_scores(Qg, K)
+            gam = d * 2.0 ** -24 / (1 - d * 2.0 ** -24)
+            bound = gam * (np.abs(K) @ np.abs(Qg).T).max(axis=1)
+            kb = O.budget_k(n0, p.k, p.k_num, p.k_den)
+            S = O.topk_middle(sigma, n0, kb, p.sink, p.window)
+            m = O.dilation_m(kb, len(S), p.dilate_m)
+            got = topk[b, g, : tlen[b, g]]
+            assert tlen[b, g] == len(S), f"b{b} g{g}: topk_len"
+            top, rest = got[:m], got[m:]
+            assert list(top) == sorted(top) and list(rest) == sorted(rest)
+            assert len(set(got.tolist())) == len(got)
+            se, wst = O.region_bounds(n0, p.sink, p.window)
+            assert np.all((got >= se) & (got < wst))
+            if len(S):
+                tol = 2 * bound[se:wst].max()
+                sym = set(got.tolist()) ^ set(S.tolist())
+                _near_threshold(sym, sigma, sigma[S[-1]], tol, f"{name} b{b} g{g} top-k")
+                if m:
+                    symm = set(top.tolist()) ^ set(S[:m].tolist())
+                    _near_threshold(symm, sigma, sigma[S[m - 1]], tol, f"{name} b{b} g{g} top-m")
+                    swaps += len(symm)
+                swaps += len(sym)
+            own = np.concatenate([top, rest])
+            C = O.anchor_set(own, n0, p.sink, p.window)
+            assert slen[b, g] == len(C) and np.array_equal(sidx[b, g, : len(C)], C)
+            R = O.reuse_set(own, m, p.dilate_r, n0, n0, p.sink, p.window)
+            assert hlen[b, g] == len(R) and np.array_equal(hidx[b, g, : len(R)], R)
+    print(f"{name}: {swaps} positions swapped at a threshold")

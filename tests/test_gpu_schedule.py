@@ -182,7 +182,7 @@ def test_config3_full_size_paged():
     run_schedule(w, (0, 1, 7), units, layers=1)
 
 
-@pytest.mark.parametrize("batch,nmax", [(16, 16384), (64, 8192)])
+@pytest.mark.parametrize("batch,nmax", [(16, 16384), (64, 8192), (64, 16384), (16, 8192)])
 def test_config4_full_size(batch, nmax):
     w = synth.workload(4, batch=batch, nmax=nmax)
     units = {(0, 0), (batch - 1, 7)}
