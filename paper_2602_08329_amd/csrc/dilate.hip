@@ -5,7 +5,7 @@
 // build_index_set and depends only on the anchor's top-k and the lengths.
 #include "prhs.h"
 #include "prhs_internal.h"
-#include "setops.cuh"
+#include "setops.h"
 
 namespace prhs {
 namespace {

@@ -31,7 +31,7 @@
 
 #include "prhs.h"
 #include "prhs_internal.h"
-#include "setops.cuh"
+#include "setops.h"
 
 namespace prhs {
 namespace {
