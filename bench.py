@@ -562,7 +562,7 @@ def measure(w, args, dev, K_steps, W_steps, psaw=None, gated=False, tau=None):
     log(f"inputs ready in {time.time() - t0:.1f} s; "
         f"{sum(x.numel() * x.element_size() for x in inp.K + inp.V) / 2**30:.1f} GiB of KV")
     if gated:
-        run = GatedDecodeRunner(inp, dev, tau=tau, psaw=psaw)
+        run = GatedDecodeRunner(inp, dev, tau=tau, psaw=psaw, concurrent=args.concurrent)
     else:
         run = DecodeRunner(inp, dev, per_step_sets=args.per_step_sets, psaw=psaw)
 
@@ -750,6 +750,9 @@ def main():
     ap.add_argument("--gate", type=float, default=None, metavar="TAU",
                     help="similarity-gated sharing with threshold TAU in [0, 1] instead of the "
                          "fixed refresh period (blocks of refresh_every steps)")
+    ap.add_argument("--concurrent", action="store_true",
+                    help="with --gate: the sharing units' attention on a second stream beside "
+                         "the refresh and the retrieving units' attention")
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches instead of replays of a captured HIP graph")
     ap.add_argument("--paged", action="store_true",
@@ -817,7 +820,8 @@ def main():
             "k": w.k if not w.k_den else f"{w.k_num}/{w.k_den} n", "window": w.window,
             "sink": w.sink, "refresh_every": w.s, "layer_group": w.G, "dilate_r": w.r,
             "paged": w.paged, "decode_steps_cycled": w.steps,
-            "shared_sets": ("similarity gate" if gated else
+            "shared_sets": (("similarity gate, concurrent branches" if args.concurrent else
+                             "similarity gate") if gated else
                             "per step" if args.per_step_sets else "per refresh + decoded tail"),
             "psaw": ({"l_s": psaw[0], "phi": psaw[1], "alpha": psaw[2]} if psaw else None),
             "launch": "eager" if args.eager else "hip-graph replay",

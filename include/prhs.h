@@ -129,6 +129,9 @@ enum {
 
 enum { PRHS_REUSE = 0, PRHS_REFRESH = 1 };
 
+/* Which units a pool attention launch attends (prhs_pool_decode_attn). */
+enum { PRHS_UNITS_ALL = 0, PRHS_UNITS_RETRIEVING = 1, PRHS_UNITS_SHARING = 2 };
+
 /* Largest top-k budget the selection supports: k_b, after clamping to the
  * middle range length, must not exceed this (PRHS_E_UNSUPPORTED otherwise).
  * For middle ranges beyond one CU's LDS the selection keeps the k_b winners
@@ -351,8 +354,11 @@ prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale
  * in binary64 from fp32 sums, which is exact when the inputs are on a grid
  * coarse enough for the fp32 sums to be exact.  0 <= tau <= 1.
  * Writes: choice[u] = j, or -1 when the unit retrieves now;
- *   ref_q[slot] = q; ref_valid[slot][u] = (choice[u] < 0);
- *   slot_lens[slot][b] = seq_lens[b];
+ *   with record != 0 also the step's record: ref_q[slot] = q;
+ *   ref_valid[slot][u] = (choice[u] < 0); slot_lens[slot][b] = seq_lens[b]
+ *   (record = 0 takes the same decisions and writes only the four outputs
+ *   below, e.g. into separate arrays for a branch that runs beside the
+ *   recording one);
  *   row_anchor[u] = pool row the group's anchor layer attends: the current
  *     slot's critical set when retrieving, else slot j's shared set;
  *   row_other[u] = pool row the group's other layers attend: the shared set
@@ -364,7 +370,28 @@ prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, 
                       int32_t dtype, const void* q, const int32_t* seq_lens, double tau,
                       int32_t num_slots, int32_t slot, void* ref_q, int32_t* ref_valid,
                       int32_t* slot_lens, int32_t* choice, int32_t* row_anchor,
-                      int32_t* row_other, int32_t* tail, void* stream);
+                      int32_t* row_other, int32_t* tail, int32_t record, void* stream);
+
+/* The gate and the refresh of the retrieving units in one call (Sec. 4.1,
+ * Similarity Criteria; Sec. 4.4: only retrieval heads score): exactly
+ * prhs_gate with record = 1 followed by prhs_select_gated on its choice, the
+ * gate's arrays as in prhs_gate and the selection's as in
+ * prhs_select_gated (set_idx / shared_idx: the current slot's pool rows of
+ * kind 0 and 1).  q and seq_lens come from kv and the query argument.  When
+ * the refresh runs as one fused launch (contiguous bf16 cache, middle range
+ * within one CU's LDS, rows filling more than half the CUs) the gate is
+ * taken inside that launch, one wave per row before it scores; otherwise
+ * the gate kernel runs first.  The decided units' outputs of this step
+ * (choice, row_anchor, row_other, tail) are written before any of them is
+ * needed by a later launch on the stream. */
+prhs_status prhs_gate_select(const prhs_kv* kv, const void* q, const prhs_params* params,
+                             double tau, int32_t num_slots, int32_t slot, void* ref_q,
+                             int32_t* ref_valid, int32_t* slot_lens, int32_t* choice,
+                             int32_t* row_anchor, int32_t* row_other, int32_t* tail,
+                             int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                             int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                             int32_t* shared_idx, int32_t* shared_len, void* ws, size_t ws_bytes,
+                             void* stream);
 
 /* prhs_select_shared for the units the gate sends to retrieval only:
  * (b, g) with choice[b][g] >= 0 are left untouched, the others get their
@@ -390,10 +417,18 @@ prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_param
  * [B*Hkv] int32 (prhs_gate's row_anchor or row_other, and tail; or the
  * identity rows and per-unit anchor lengths of the fixed schedule's sets);
  * psaw: host descriptor or NULL.  Precondition: pool_len[r] + n - t0 <=
- * set_cap.  ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes. */
+ * set_cap.  ws: >= prhs_workspace_size(PRHS_OP_SPARSE_ATTN, set_cap) bytes.
+ * units_side selects the units by the gate's decision: PRHS_UNITS_ALL every
+ * unit (unit_gate may be NULL); PRHS_UNITS_RETRIEVING only units with
+ * unit_gate[u] < 0; PRHS_UNITS_SHARING only units with unit_gate[u] >= 0
+ * (unit_gate: prhs_gate's choice, [B*Hkv]).  The other units' outputs are
+ * left untouched, so the retrieving and the sharing units of a layer can be
+ * attended by two launches that run concurrently (Sec. 4.4: shared heads do
+ * not wait for retrieval) with separate workspaces. */
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
                                   const int32_t* unit_row, const int32_t* unit_tail,
+                                  const int32_t* unit_gate, int32_t units_side,
                                   const prhs_psaw* psaw, float scale, float* out, float* lse,
                                   void* ws, size_t ws_bytes, void* stream);
 

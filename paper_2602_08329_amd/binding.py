@@ -36,13 +36,17 @@ PRHS_OP_DENSE_ATTN = 3
 
 PRHS_REUSE = 0
 PRHS_REFRESH = 1
+PRHS_UNITS_ALL = 0
+PRHS_UNITS_RETRIEVING = 1
+PRHS_UNITS_SHARING = 2
 PRHS_MAX_TOPK = 16000
 
 EXPORTS = [
     "prhs_abi_version", "prhs_max_topk", "prhs_set_capacity", "prhs_workspace_size",
     "prhs_schedule", "prhs_select", "prhs_select_shared", "prhs_dilate_reuse", "prhs_sparse_decode_attn",
     "prhs_sparse_decode_attn_static",
-    "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_select_gated",
+    "prhs_reuse_decode_attn", "prhs_dense_decode_attn", "prhs_gate", "prhs_gate_select",
+    "prhs_select_gated",
     "prhs_pool_decode_attn", "prhs_prefill_attn", "prhs_psaw_first_visible", "prhs_last_error",
 ]
 
@@ -125,13 +129,17 @@ def lib():
         L.prhs_dense_decode_attn.argtypes = [P(PrhsKv), vp, ctypes.c_float, vp, vp, vp, sz, vp]
         L.prhs_gate.restype = i32
         L.prhs_gate.argtypes = [i32, i32, i32, i32, i32, vp, vp, ctypes.c_double, i32, i32, vp, vp,
-                                vp, vp, vp, vp, vp, vp]
+                                vp, vp, vp, vp, vp, i32, vp]
+        L.prhs_gate_select.restype = i32
+        L.prhs_gate_select.argtypes = [P(PrhsKv), vp, P(PrhsParams), ctypes.c_double, i32, i32, vp,
+                                       vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, i32, vp, vp,
+                                       vp, sz, vp]
         L.prhs_select_gated.restype = i32
         L.prhs_select_gated.argtypes = [P(PrhsKv), vp, P(PrhsParams), vp, vp, vp, i32, vp, vp, i32,
                                         vp, vp, vp, sz, vp]
         L.prhs_pool_decode_attn.restype = i32
-        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, P(PrhsPsaw),
-                                            ctypes.c_float, vp, vp, vp, sz, vp]
+        L.prhs_pool_decode_attn.argtypes = [P(PrhsKv), vp, vp, vp, i32, i32, vp, vp, vp, i32,
+                                            P(PrhsPsaw), ctypes.c_float, vp, vp, vp, sz, vp]
         L.prhs_prefill_attn.restype = i32
         L.prhs_prefill_attn.argtypes = [P(PrhsKv), vp, i32, P(PrhsPsaw), ctypes.c_float, vp, vp, vp]
         L.prhs_psaw_first_visible.restype = i32
@@ -398,31 +406,66 @@ def prhs_reuse_decode_attn(kv, q, set_idx, set_len, anchor_lens, scale, out, lse
                                        _stream(stream)))
 
 
-def prhs_gate(q, seq_lens, tau, slot, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other,
-              tail, num_kv_heads, stream=None):
-    """Similarity gate for block step `slot`: q [B][Hq][d]; ref_q
-    [S][B][Hq][d] (dtype of q); ref_valid [S][B*Hkv]; slot_lens [S][B];
-    choice, row_anchor, row_other, tail [B*Hkv] int32 outputs."""
+def _gate_arrays(q, seq_lens, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other, tail,
+                 num_kv_heads):
     if not isinstance(q, torch.Tensor) or q.dtype not in (torch.bfloat16, torch.float32):
         raise ValueError("q must be a bf16 or fp32 tensor")
     _need(q, q.dtype, "q", dims=3)
-    B, Hq, d = q.shape
+    B_, Hq, d = q.shape
     _need(ref_q, q.dtype, "ref_q", dims=4)
     S = ref_q.shape[0]
-    _need(ref_q, q.dtype, "ref_q", shape=(S, B, Hq, d))
-    U = B * num_kv_heads
-    for t, n, shape in ((seq_lens, "seq_lens", (B,)), (ref_valid, "ref_valid", (S, U)),
-                        (slot_lens, "slot_lens", (S, B)), (choice, "choice", (U,)),
+    _need(ref_q, q.dtype, "ref_q", shape=(S, B_, Hq, d))
+    U = B_ * num_kv_heads
+    for t, n, shape in ((seq_lens, "seq_lens", (B_,)), (ref_valid, "ref_valid", (S, U)),
+                        (slot_lens, "slot_lens", (S, B_)), (choice, "choice", (U,)),
                         (row_anchor, "row_anchor", (U,)), (row_other, "row_other", (U,)),
                         (tail, "tail", (U,))):
         _need(t, torch.int32, n, shape=shape)
+    return S
+
+
+def prhs_gate(q, seq_lens, tau, slot, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other,
+              tail, num_kv_heads, stream=None, record=True):
+    """Similarity gate for block step `slot`: q [B][Hq][d]; ref_q
+    [S][B][Hq][d] (dtype of q); ref_valid [S][B*Hkv]; slot_lens [S][B];
+    choice, row_anchor, row_other, tail [B*Hkv] int32 outputs.  With
+    record=False the step is decided but not recorded (ref_q, ref_valid and
+    slot_lens are only read)."""
+    S = _gate_arrays(q, seq_lens, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other, tail,
+                     num_kv_heads)
     _on_device(q.device, seq_lens=seq_lens, ref_q=ref_q, ref_valid=ref_valid,
                slot_lens=slot_lens, choice=choice, row_anchor=row_anchor, row_other=row_other,
                tail=tail)
+    B_, Hq, d = q.shape
     dt = PRHS_BF16 if q.dtype == torch.bfloat16 else PRHS_F32
-    check(lib().prhs_gate(B, Hq, num_kv_heads, d, dt, _ptr(q), _ptr(seq_lens), float(tau), S,
+    check(lib().prhs_gate(B_, Hq, num_kv_heads, d, dt, _ptr(q), _ptr(seq_lens), float(tau), S,
                           int(slot), _ptr(ref_q), _ptr(ref_valid), _ptr(slot_lens), _ptr(choice),
-                          _ptr(row_anchor), _ptr(row_other), _ptr(tail), _stream(stream)))
+                          _ptr(row_anchor), _ptr(row_other), _ptr(tail), 1 if record else 0,
+                          _stream(stream)))
+
+
+def prhs_gate_select(kv, q, p, tau, slot, ref_q, ref_valid, slot_lens, choice, row_anchor,
+                     row_other, tail, topk_idx, topk_len, set_idx, set_len, shared_idx,
+                     shared_len, ws, stream=None):
+    """prhs_gate (recording the step) and the refresh of the retrieving units
+    in one call; the gate runs inside the refresh launch where that is one
+    fused kernel."""
+    _q(kv, q)
+    seq_lens = kv._keep[2]
+    S = _gate_arrays(q, seq_lens, ref_q, ref_valid, slot_lens, choice, row_anchor, row_other, tail,
+                     kv.c.num_kv_heads)
+    _selection_outputs(kv, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len)
+    _ws(ws)
+    kv.check_device(q=q, ref_q=ref_q, ref_valid=ref_valid, slot_lens=slot_lens, choice=choice,
+                    row_anchor=row_anchor, row_other=row_other, tail=tail, topk_idx=topk_idx,
+                    topk_len=topk_len, set_idx=set_idx, set_len=set_len, shared_idx=shared_idx,
+                    shared_len=shared_len, ws=ws)
+    check(lib().prhs_gate_select(ctypes.byref(kv.c), _ptr(q), ctypes.byref(p), float(tau), S,
+                                 int(slot), _ptr(ref_q), _ptr(ref_valid), _ptr(slot_lens),
+                                 _ptr(choice), _ptr(row_anchor), _ptr(row_other), _ptr(tail),
+                                 _ptr(topk_idx), _ptr(topk_len), topk_idx.shape[-1], _ptr(set_idx),
+                                 _ptr(set_len), set_idx.shape[-1], _ptr(shared_idx),
+                                 _ptr(shared_len), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, shared_idx, shared_len,
@@ -442,11 +485,15 @@ def prhs_select_gated(kv, q, p, choice, topk_idx, topk_len, set_idx, set_len, sh
 
 
 def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale, out, lse, ws,
-                          stream=None, psaw=None):
+                          stream=None, psaw=None, unit_gate=None, units_side=PRHS_UNITS_ALL):
     """Attention where unit u attends pool row unit_row[u] plus the tail
     [unit_tail[u], n_b), under the layer's PSAW mask (Eq. psaw) when psaw (a
     PrhsPsaw) is given.  pool_idx [..][set_cap] (any leading dims, flattened
-    to rows), pool_len with the same leading dims."""
+    to rows), pool_len with the same leading dims.  units_side (with the
+    gate's choice as unit_gate) restricts the launch to the retrieving or
+    the sharing units; the others' outputs are left as they are."""
+    if units_side != PRHS_UNITS_ALL:
+        _need(unit_gate, torch.int32, "unit_gate", shape=(kv.units,))
     _q(kv, q)
     _need(pool_idx, torch.int32, "pool_idx")
     if pool_idx.dim() < 1:
@@ -461,11 +508,12 @@ def prhs_pool_decode_attn(kv, q, pool_idx, pool_len, unit_row, unit_tail, scale,
     if psaw is not None and not isinstance(psaw, PrhsPsaw):
         raise TypeError("psaw must be a PrhsPsaw (binding.psaw(...))")
     kv.check_device(q=q, pool_idx=pool_idx, pool_len=pool_len, unit_row=unit_row,
-                    unit_tail=unit_tail, out=out, lse=lse, ws=ws)
+                    unit_tail=unit_tail, unit_gate=unit_gate, out=out, lse=lse, ws=ws)
     check(lib().prhs_pool_decode_attn(ctypes.byref(kv.c), _ptr(q), _ptr(pool_idx), _ptr(pool_len),
-                                      rows, cap, _ptr(unit_row), _ptr(unit_tail), _ref(psaw),
-                                      float(scale), _ptr(out), _ptr(lse), _ptr(ws), ws.numel(),
-                                      _stream(stream)))
+                                      rows, cap, _ptr(unit_row), _ptr(unit_tail),
+                                      _ptr(unit_gate) if units_side != PRHS_UNITS_ALL else None,
+                                      int(units_side), _ref(psaw), float(scale), _ptr(out),
+                                      _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def prhs_prefill_attn(kv, q, scale, out, lse=None, psaw=None, stream=None):

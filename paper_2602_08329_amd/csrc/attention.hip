@@ -64,6 +64,8 @@ struct AttnArgs {
   const int32_t* unit_row;    // [units] or null: pool row of set_idx each unit attends
   const int32_t* unit_tail;   // [units] with unit_row: first position of the unit's tail
   int pool_rows;
+  const int32_t* unit_gate;   // [units] or null: the gate's choice per unit
+  int units_side;             // 1: only units with unit_gate < 0; 2: only >= 0; else all
   int psaw;                   // nonzero: positions in [psaw_sink, first visible) are skipped
   double psaw_f;              // Eq. psaw factor of the layer (first visible at length n:
   int psaw_sink;              // psaw_first_visible(psaw_f, psaw_sink, n))
@@ -125,6 +127,14 @@ __device__ __forceinline__ UnitSpan unit_span(const AttnArgs& a, int u, int b, i
   }
   sp.L = L;
   return sp;
+}
+
+// Units a launch leaves alone (their outputs untouched): with a side filter,
+// the ones on the other side of the gate's decision.
+__device__ __forceinline__ bool unit_excluded(const AttnArgs& a, int u) {
+  if (!a.unit_gate || (a.units_side != 1 && a.units_side != 2)) return false;
+  const bool retrieving = a.unit_gate[u] < 0;
+  return a.units_side == 1 ? !retrieving : retrieving;
 }
 
 // Row id (element offset / d) of position pos of (b, kv head g), or -1 when
@@ -478,6 +488,7 @@ __global__ __launch_bounds__(512) void attn_split_bf16(AttnArgs a) {
     qf[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : make_uint4(0, 0, 0, 0));
   }
   const int nb = kv_seq_len(a.kv, b);
+  if (!DENSE && unit_excluded(a, u)) return;
   const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
   const int L = sp.L;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
@@ -578,6 +589,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
   int32_t raw[kRowsPerThread];
   prefetch_entries<DENSE>(a, u, start, raw);
   const int nb = kv_seq_len(a.kv, b);
+  if (!DENSE && unit_excluded(a, u)) return;
   const UnitSpan sp = unit_span<DENSE>(a, u, b, nb);
   const int L = sp.L;
   if (L == 0 && split == 0) {  // empty set: y = 0, lse = -inf
@@ -687,6 +699,7 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   const int bh = blockIdx.x;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, u = b * hkv + h / G;
+  if (!DENSE && unit_excluded(a, u)) return;
   const int L = unit_span<DENSE>(a, u, b, kv_seq_len(a.kv, b)).L;
   const int nsp = (L + a.chunk - 1) / a.chunk;
   if (nsp <= 1) return;
@@ -882,6 +895,8 @@ hipError_t launch_attention(const AttnLaunch& s, bool dense, hipStream_t stream)
   a.unit_row = dense ? nullptr : s.unit_row;
   a.unit_tail = dense ? nullptr : s.unit_tail;
   a.pool_rows = s.pool_rows;
+  a.unit_gate = dense ? nullptr : s.unit_gate;
+  a.units_side = s.units_side;
   a.psaw = dense ? 0 : s.psaw;
   a.psaw_f = s.psaw_f;
   a.psaw_sink = s.psaw_sink;

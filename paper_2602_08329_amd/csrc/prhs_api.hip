@@ -224,8 +224,8 @@ static prhs_status select_common(const prhs_kv* kv, const void* q, const prhs_pa
                                  int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
                                  int32_t* set_idx, int32_t* set_len, int32_t set_cap,
                                  int32_t* shared_idx, int32_t* shared_len, bool shared,
-                                 const int32_t* row_choice, void* ws, size_t ws_bytes,
-                                 void* stream, const char* name) {
+                                 const int32_t* row_choice, const prhs::GateLaunch* gate,
+                                 void* ws, size_t ws_bytes, void* stream, const char* name) {
   prhs_status st = check_kv_shape(kv);
   if (st != PRHS_OK) return st;
   if ((st = check_params(params)) != PRHS_OK) return st;
@@ -269,6 +269,7 @@ static prhs_status select_common(const prhs_kv* kv, const void* q, const prhs_pa
   a.shared_idx = shared ? shared_idx : nullptr;
   a.shared_len = shared ? shared_len : nullptr;
   a.row_choice = row_choice;
+  a.gate = gate;
   a.ws = ws;
   a.max_topk = kmax;
   return device_status(prhs::launch_select(a, (hipStream_t)stream), name);
@@ -279,7 +280,7 @@ prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* par
                         int32_t* set_len, int32_t set_cap, void* ws, size_t ws_bytes,
                         void* stream) {
   return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
-                       nullptr, nullptr, false, nullptr, ws, ws_bytes, stream,
+                       nullptr, nullptr, false, nullptr, nullptr, ws, ws_bytes, stream,
                        "prhs_select launch");
 }
 
@@ -289,7 +290,7 @@ prhs_status prhs_select_shared(const prhs_kv* kv, const void* q, const prhs_para
                                int32_t* shared_idx, int32_t* shared_len, void* ws,
                                size_t ws_bytes, void* stream) {
   return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
-                       shared_idx, shared_len, true, nullptr, ws, ws_bytes, stream,
+                       shared_idx, shared_len, true, nullptr, nullptr, ws, ws_bytes, stream,
                        "prhs_select_shared launch");
 }
 
@@ -300,7 +301,7 @@ prhs_status prhs_select_gated(const prhs_kv* kv, const void* q, const prhs_param
                               size_t ws_bytes, void* stream) {
   if (kv && kv->batch > 0 && !choice) return fail(PRHS_E_INVALID, "choice must be non-NULL");
   return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
-                       shared_idx, shared_len, true, choice, ws, ws_bytes, stream,
+                       shared_idx, shared_len, true, choice, nullptr, ws, ws_bytes, stream,
                        "prhs_select_gated launch");
 }
 
@@ -340,6 +341,7 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
                                     const int32_t* set_len, int32_t set_cap,
                                     const int32_t* tail_start, const int32_t* unit_row,
                                     const int32_t* unit_tail, int32_t pool_rows,
+                                    const int32_t* unit_gate, int32_t units_side,
                                     const prhs_psaw* psaw, float scale,
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream, bool dense, const char* name) {
@@ -371,6 +373,8 @@ static prhs_status attention_common(const prhs_kv* kv, const void* q, const int3
   a.unit_row = unit_row;
   a.unit_tail = unit_tail;
   a.pool_rows = pool_rows;
+  a.unit_gate = unit_gate;
+  a.units_side = units_side;
   a.psaw = psaw != nullptr;
   a.psaw_f = psaw_f;
   a.psaw_sink = psaw ? psaw->sink : 0;
@@ -387,7 +391,7 @@ prhs_status prhs_sparse_decode_attn(const prhs_kv* kv, const void* q, const int3
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     void* stream) {
   return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, nullptr,
-                          scale, out, lse, ws, ws_bytes, stream, false,
+                          0, nullptr, scale, out, lse, ws, ws_bytes, stream, false,
                           "prhs_sparse_decode_attn launch");
 }
 
@@ -405,13 +409,14 @@ prhs_status prhs_sparse_decode_attn_static(const prhs_kv* kv, const void* q,
                 "split-K partials of %zu bytes exceed the static scratch of %zu bytes", need,
                 prhs::kStaticScratchBytes);
   if (kv->batch == 0) return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr,
-                                              nullptr, 0, nullptr, scale, out, lse, nullptr, 0,
-                                              stream, false, "prhs_sparse_decode_attn_static");
+                                              nullptr, 0, nullptr, 0, nullptr, scale, out, lse,
+                                              nullptr, 0, stream, false,
+                                              "prhs_sparse_decode_attn_static");
   void* ws = nullptr;
   if ((st = device_status(prhs::attn_static_scratch(&ws), "static scratch lookup")) != PRHS_OK)
     return st;
   return attention_common(kv, q, set_idx, set_len, set_cap, nullptr, nullptr, nullptr, 0, nullptr,
-                          scale, out, lse, ws, prhs::kStaticScratchBytes, stream, false,
+                          0, nullptr, scale, out, lse, ws, prhs::kStaticScratchBytes, stream, false,
                           "prhs_sparse_decode_attn_static launch");
 }
 
@@ -422,28 +427,35 @@ prhs_status prhs_reuse_decode_attn(const prhs_kv* kv, const void* q, const int32
   if (kv && kv->batch > 0 && !anchor_lens)
     return fail(PRHS_E_INVALID, "anchor_lens must be non-NULL");
   return attention_common(kv, q, set_idx, set_len, set_cap, anchor_lens, nullptr, nullptr, 0,
-                          nullptr, scale, out, lse, ws, ws_bytes, stream, false,
+                          nullptr, 0, nullptr, scale, out, lse, ws, ws_bytes, stream, false,
                           "prhs_reuse_decode_attn launch");
 }
 
 prhs_status prhs_pool_decode_attn(const prhs_kv* kv, const void* q, const int32_t* pool_idx,
                                   const int32_t* pool_len, int32_t pool_rows, int32_t set_cap,
                                   const int32_t* unit_row, const int32_t* unit_tail,
+                                  const int32_t* unit_gate, int32_t units_side,
                                   const prhs_psaw* psaw, float scale, float* out, float* lse,
                                   void* ws, size_t ws_bytes, void* stream) {
   if (pool_rows < 0) return fail(PRHS_E_INVALID, "pool_rows must be >= 0");
   if (kv && kv->batch > 0 && (!unit_row || !unit_tail))
     return fail(PRHS_E_INVALID, "unit_row and unit_tail must be non-NULL");
+  if (units_side != PRHS_UNITS_ALL && units_side != PRHS_UNITS_RETRIEVING &&
+      units_side != PRHS_UNITS_SHARING)
+    return fail(PRHS_E_INVALID, "units_side must be PRHS_UNITS_ALL, _RETRIEVING or _SHARING");
+  if (units_side != PRHS_UNITS_ALL && kv && kv->batch > 0 && !unit_gate)
+    return fail(PRHS_E_INVALID, "unit_gate must be non-NULL with a units_side filter");
   return attention_common(kv, q, pool_idx, pool_len, set_cap, nullptr, unit_row, unit_tail,
-                          pool_rows, psaw, scale, out, lse, ws, ws_bytes, stream, false,
-                          "prhs_pool_decode_attn launch");
+                          pool_rows, unit_gate, units_side, psaw, scale, out, lse, ws, ws_bytes,
+                          stream, false, "prhs_pool_decode_attn launch");
 }
 
-prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                      int32_t dtype, const void* q, const int32_t* seq_lens, double tau,
-                      int32_t num_slots, int32_t slot, void* ref_q, int32_t* ref_valid,
-                      int32_t* slot_lens, int32_t* choice, int32_t* row_anchor,
-                      int32_t* row_other, int32_t* tail, void* stream) {
+static prhs_status gate_args(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t head_dim, int32_t dtype, const void* q,
+                             const int32_t* seq_lens, double tau, int32_t num_slots, int32_t slot,
+                             void* ref_q, int32_t* ref_valid, int32_t* slot_lens, int32_t* choice,
+                             int32_t* row_anchor, int32_t* row_other, int32_t* tail,
+                             int32_t record, prhs::GateLaunch* a) {
   if (batch < 0) return fail(PRHS_E_INVALID, "batch must be >= 0");
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0)
     return fail(PRHS_E_INVALID, "num_q_heads must be a positive multiple of num_kv_heads");
@@ -457,26 +469,58 @@ prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, 
   if (batch > 0 && (!q || !seq_lens || !ref_q || !ref_valid || !slot_lens || !choice ||
                     !row_anchor || !row_other || !tail))
     return fail(PRHS_E_INVALID, "device arrays must be non-NULL");
-  if (batch == 0) return PRHS_OK;
+  a->batch = batch;
+  a->hq = num_q_heads;
+  a->hkv = num_kv_heads;
+  a->d = head_dim;
+  a->dtype = dtype;
+  a->q = q;
+  a->seq_lens = seq_lens;
+  a->tau = tau;
+  a->num_slots = num_slots;
+  a->slot = slot;
+  a->ref_q = ref_q;
+  a->ref_valid = ref_valid;
+  a->slot_lens = slot_lens;
+  a->choice = choice;
+  a->row_anchor = row_anchor;
+  a->row_other = row_other;
+  a->tail = tail;
+  a->record = record ? 1 : 0;
+  return PRHS_OK;
+}
+
+prhs_status prhs_gate(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t dtype, const void* q, const int32_t* seq_lens, double tau,
+                      int32_t num_slots, int32_t slot, void* ref_q, int32_t* ref_valid,
+                      int32_t* slot_lens, int32_t* choice, int32_t* row_anchor,
+                      int32_t* row_other, int32_t* tail, int32_t record, void* stream) {
   prhs::GateLaunch a;
-  a.batch = batch;
-  a.hq = num_q_heads;
-  a.hkv = num_kv_heads;
-  a.d = head_dim;
-  a.dtype = dtype;
-  a.q = q;
-  a.seq_lens = seq_lens;
-  a.tau = tau;
-  a.num_slots = num_slots;
-  a.slot = slot;
-  a.ref_q = ref_q;
-  a.ref_valid = ref_valid;
-  a.slot_lens = slot_lens;
-  a.choice = choice;
-  a.row_anchor = row_anchor;
-  a.row_other = row_other;
-  a.tail = tail;
+  prhs_status st = gate_args(batch, num_q_heads, num_kv_heads, head_dim, dtype, q, seq_lens, tau,
+                             num_slots, slot, ref_q, ref_valid, slot_lens, choice, row_anchor,
+                             row_other, tail, record, &a);
+  if (st != PRHS_OK || batch == 0) return st;
   return device_status(prhs::launch_gate(a, (hipStream_t)stream), "prhs_gate launch");
+}
+
+prhs_status prhs_gate_select(const prhs_kv* kv, const void* q, const prhs_params* params,
+                             double tau, int32_t num_slots, int32_t slot, void* ref_q,
+                             int32_t* ref_valid, int32_t* slot_lens, int32_t* choice,
+                             int32_t* row_anchor, int32_t* row_other, int32_t* tail,
+                             int32_t* topk_idx, int32_t* topk_len, int32_t k_cap,
+                             int32_t* set_idx, int32_t* set_len, int32_t set_cap,
+                             int32_t* shared_idx, int32_t* shared_len, void* ws, size_t ws_bytes,
+                             void* stream) {
+  prhs_status st = check_kv_shape(kv);
+  if (st != PRHS_OK) return st;
+  prhs::GateLaunch g;
+  st = gate_args(kv->batch, kv->num_q_heads, kv->num_kv_heads, kv->head_dim, kv->dtype, q,
+                 kv->seq_lens, tau, num_slots, slot, ref_q, ref_valid, slot_lens, choice,
+                 row_anchor, row_other, tail, 1, &g);
+  if (st != PRHS_OK) return st;
+  return select_common(kv, q, params, topk_idx, topk_len, k_cap, set_idx, set_len, set_cap,
+                       shared_idx, shared_len, true, nullptr, &g, ws, ws_bytes, stream,
+                       "prhs_gate_select launch");
 }
 
 prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
@@ -511,8 +555,8 @@ prhs_status prhs_prefill_attn(const prhs_kv* kv, const void* q, int32_t q_len,
 
 prhs_status prhs_dense_decode_attn(const prhs_kv* kv, const void* q, float scale, float* out,
                                    float* lse, void* ws, size_t ws_bytes, void* stream) {
-  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr,
-                          scale, out, lse, ws, ws_bytes, stream, true,
+  return attention_common(kv, q, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0, nullptr, 0,
+                          nullptr, scale, out, lse, ws, ws_bytes, stream, true,
                           "prhs_dense_decode_attn launch");
 }
 

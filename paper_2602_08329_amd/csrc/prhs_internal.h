@@ -135,6 +135,8 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
 // ---------------------------------------------------------------------------
 // Host launch functions (defined next to their kernels).
 
+struct GateLaunch;
+
 struct SelectLaunch {
   KvView kv;
   const void* q;
@@ -150,6 +152,7 @@ struct SelectLaunch {
   int32_t* shared_idx;  // optional: dilated shared set at the anchor length
   int32_t* shared_len;
   const int32_t* row_choice;  // optional [rows]: only rows with a negative entry are selected
+  const GateLaunch* gate;     // optional: take the similarity gate first, select the retrieving rows
   void* ws;
   int max_topk;   // host bound on the clamped budget (sort size)
 };
@@ -180,6 +183,8 @@ struct AttnLaunch {
   const int32_t* unit_row;    // [B*Hkv] or null: pool row each unit attends
   const int32_t* unit_tail;   // [B*Hkv] with unit_row: first position of the unit's tail
   int pool_rows;              // rows of set_idx when unit_row is given
+  const int32_t* unit_gate;   // [B*Hkv] or null: the gate's choice per unit, for units_side
+  int units_side;             // 0 all units; 1 only units with unit_gate < 0; 2 only >= 0
   int psaw;                   // nonzero: positions in [psaw_sink, first visible) are masked
   double psaw_f;              // the layer's factor 1 - phi^e of Eq. psaw
   int psaw_sink;
@@ -215,6 +220,7 @@ struct GateLaunch {
   int32_t* row_anchor;  // [B*Hkv]
   int32_t* row_other;   // [B*Hkv]
   int32_t* tail;        // [B*Hkv]
+  int record;           // nonzero: also record the step (ref_q, ref_valid, slot_lens)
 };
 hipError_t launch_gate(const GateLaunch& a, hipStream_t stream);
 

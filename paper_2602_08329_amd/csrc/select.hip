@@ -30,6 +30,7 @@
 #include <stdlib.h>
 
 #include "prhs.h"
+#include "gate.h"
 #include "prhs_internal.h"
 #include "setops.h"
 
@@ -76,6 +77,8 @@ struct SelArgs {
   int32_t* shared_len;
   int balance_cus;      // fused refresh: > 0 = CU count to balance rows over, 0 = off
   const int32_t* row_choice;  // optional [rows]: rows with an entry >= 0 are left untouched
+  int gate_fused;       // fused refresh: wave 0 takes the similarity gate of its row first
+  GateLaunch gate;      // (with gate_fused) and the workgroup selects only a retrieving row
 };
 
 // Rows the similarity gate lets share are not selected again.
@@ -1058,8 +1061,19 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   __shared__ int s_len[kBalanceMaxBatch];
   __shared__ int s_row;
   __shared__ u32x4_t s_kst[BLOCK / 64][16 * (D / 8)];
+  __shared__ int s_choice;
   const int row = fused_row(a, blockIdx.x, s_len, &s_row);
-  if (row_skipped(a, row)) return;
+  if (a.gate_fused) {
+    // the gate of this row's unit (recording the step); a sharing row is done
+    if (threadIdx.x < 64) {
+      const int c = gate_unit<__bf16>(a.gate, row, threadIdx.x);
+      if (threadIdx.x == 0) s_choice = c;
+    }
+    __syncthreads();
+    if (s_choice >= 0) return;
+  } else if (row_skipped(a, row)) {
+    return;
+  }
   const int b = row / a.kv.hkv, g = row % a.kv.hkv;
   const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
@@ -1275,8 +1289,20 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.shared_len = s.shared_len;
   a.balance_cus = 0;
   a.row_choice = s.row_choice;
+  a.gate_fused = 0;
 
   const SelPath path = select_path(s.dtype, s.kv.paged != 0, rows, a.mcap);
+  if (s.gate) {
+    if (path == SelPath::kFused) {
+      a.gate_fused = 1;   // the gate runs inside the refresh launch
+      a.gate = *s.gate;
+    } else {
+      // a launch of its own, then the path's kernels on the retrieving rows
+      const hipError_t e = launch_gate(*s.gate, stream);
+      if (e != hipSuccess) return e;
+      a.row_choice = s.gate->choice;
+    }
+  }
   // many short contiguous bf16 rows: the whole refresh in one launch
   if (path == SelPath::kFused) {
     const size_t dyn = (size_t)a.mcap * 4;

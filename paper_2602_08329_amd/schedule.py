@@ -215,16 +215,30 @@ class DecodeRunner:
 class GatedDecodeRunner(DecodeRunner):
     """The decode schedule with the similarity gate (Sec. 4.1, Similarity
     Criteria): blocks of s steps; at every step each group's anchor layer
-    runs prhs_gate, the units it sends to retrieval run prhs_select_gated,
-    and every layer attends its pool row plus the decoded tail through
+    takes the gate and refreshes its retrieving units (prhs_gate_select: the
+    gate inside the refresh launch where that is one fused kernel), and every
+    layer attends its pool row plus the decoded tail through
     prhs_pool_decode_attn.  Per group the state is the block's reference
     queries, retrieval flags and lengths per slot, and the set pool
-    [2][s][B][Hkv][set_cap] (kind 0 critical sets, kind 1 shared sets)."""
+    [2][s][B][Hkv][set_cap] (kind 0 critical sets, kind 1 shared sets).
 
-    def __init__(self, inp, device="cuda", tau=0.8, psaw=None):
+    With concurrent=True, step() runs the two kinds of unit concurrently
+    (Sec. 4.4: shared heads need no retrieval, so their attention does not
+    wait for it): the current stream takes the gate, the refresh and then
+    the retrieving units' attention; a second stream of the same priority
+    takes the same gate decisions without recording them (prhs_gate, record
+    off, into arrays of its own) and attends the sharing units.  The two
+    launches of a layer write disjoint units and use separate workspaces.
+    Otherwise step() is selection_step() and every layer's attend(), one
+    launch after another (the faster order on this GPU: a launch restricted
+    to half the units keeps half the workgroups busy for about as long as a
+    full launch takes)."""
+
+    def __init__(self, inp, device="cuda", tau=0.8, psaw=None, concurrent=False):
         super().__init__(inp, device, psaw=psaw)
         w = self.w
         self.tau = float(tau)
+        self.concurrent = concurrent
         dev, i32 = self.device, torch.int32
         G_, S, U = self.groups, w.s, w.batch * w.hkv
         q = inp.q
@@ -237,22 +251,31 @@ class GatedDecodeRunner(DecodeRunner):
         self.row_anchor = torch.zeros(G_, U, dtype=i32, device=dev)
         self.row_other = torch.zeros(G_, U, dtype=i32, device=dev)
         self.tail = torch.zeros(G_, U, dtype=i32, device=dev)
+        # the sharing branch's own copy of the decisions and its workspace
+        self.side_choice = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.side_row_anchor = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.side_row_other = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.side_tail = torch.zeros(G_, U, dtype=i32, device=dev)
+        self.ws_attn_side = torch.zeros_like(self.ws_attn)
+        self.side_stream = None
         self.gated_step = [None] * G_
+
+    def _gate_order(self, gi, j):
+        if j % self.w.s != 0 and self.gated_step[gi] != j - 1:
+            raise RuntimeError(f"group {gi}: the gate runs at every step of a block in order")
 
     def selection_step(self, j):
         w = self.w
         slot = j % w.s
         for gi in range(self.groups):
-            if slot != 0 and self.gated_step[gi] != j - 1:
-                raise RuntimeError(f"group {gi}: the gate runs at every step of a block in order")
+            self._gate_order(gi, j)
             l = gi * w.G
-            B.prhs_gate(self.inp.q[l, j], self.seq_lens[j], self.tau, slot, self.ref_q[gi],
-                        self.ref_valid[gi], self.slot_lens[gi], self.choice[gi],
-                        self.row_anchor[gi], self.row_other[gi], self.tail[gi], w.hkv)
-            B.prhs_select_gated(self.kv[l][j], self.inp.q[l, j], self.params, self.choice[gi],
-                                self.topk_idx[gi], self.topk_len[gi], self.pool[gi, 0, slot],
-                                self.pool_len[gi, 0, slot], self.pool[gi, 1, slot],
-                                self.pool_len[gi, 1, slot], self.ws_select)
+            B.prhs_gate_select(self.kv[l][j], self.inp.q[l, j], self.params, self.tau, slot,
+                               self.ref_q[gi], self.ref_valid[gi], self.slot_lens[gi],
+                               self.choice[gi], self.row_anchor[gi], self.row_other[gi],
+                               self.tail[gi], self.topk_idx[gi], self.topk_len[gi],
+                               self.pool[gi, 0, slot], self.pool_len[gi, 0, slot],
+                               self.pool[gi, 1, slot], self.pool_len[gi, 1, slot], self.ws_select)
             self.gated_step[gi] = j
 
     def set_for(self, l, j):
@@ -269,6 +292,53 @@ class GatedDecodeRunner(DecodeRunner):
                                 self.scale, self.out if out is None else out,
                                 self.lse if lse is None else lse, self.ws_attn,
                                 psaw=self.psaw_desc.get(l))
+
+    def step(self, j, outs=None):
+        """One gated decode step over every layer; outs[l] receives layer
+        l's (out, lse) when given."""
+        if not self.concurrent:
+            return DecodeRunner.step(self, j, outs)
+        w = self.w
+        slot = j % w.s
+        main = torch.cuda.current_stream(self.device)
+        if self.side_stream is None:
+            self.side_stream = torch.cuda.Stream(self.device)   # default priority
+        side = self.side_stream
+
+        def dest(l):
+            o = None if outs is None else outs[l]
+            return (self.out, self.lse) if o is None else o
+
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            for gi in range(self.groups):
+                self._gate_order(gi, j)
+                l0 = gi * w.G
+                B.prhs_gate(self.inp.q[l0, j], self.seq_lens[j], self.tau, slot, self.ref_q[gi],
+                            self.ref_valid[gi], self.slot_lens[gi], self.side_choice[gi],
+                            self.side_row_anchor[gi], self.side_row_other[gi],
+                            self.side_tail[gi], w.hkv, stream=side, record=False)
+                for l in range(l0, min(l0 + w.G, self.L)):
+                    rows = self.side_row_anchor[gi] if l == l0 else self.side_row_other[gi]
+                    out, lse = dest(l)
+                    B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], self.pool[gi],
+                                            self.pool_len[gi], rows, self.side_tail[gi],
+                                            self.scale, out, lse, self.ws_attn_side,
+                                            stream=side, psaw=self.psaw_desc.get(l),
+                                            unit_gate=self.side_choice[gi],
+                                            units_side=B.PRHS_UNITS_SHARING)
+        self.selection_step(j)
+        for gi in range(self.groups):
+            l0 = gi * w.G
+            for l in range(l0, min(l0 + w.G, self.L)):
+                rows = self.row_anchor[gi] if l == l0 else self.row_other[gi]
+                out, lse = dest(l)
+                B.prhs_pool_decode_attn(self.kv[l][j], self.inp.q[l, j], self.pool[gi],
+                                        self.pool_len[gi], rows, self.tail[gi], self.scale, out,
+                                        lse, self.ws_attn, psaw=self.psaw_desc.get(l),
+                                        unit_gate=self.choice[gi],
+                                        units_side=B.PRHS_UNITS_RETRIEVING)
+        main.wait_stream(side)
 
     def retrieving_units(self):
         """Units of every group that retrieved at the last gated step."""

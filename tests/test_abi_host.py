@@ -220,7 +220,7 @@ def test_select_shared_validation(L):
 def test_gate_validation(L):
     def gate(batch=2, hq=8, hkv=2, d=128, dtype=B.PRHS_BF16, tau=0.8, S=4, slot=1, ptr=0x10):
         return L.prhs_gate(batch, hq, hkv, d, dtype, ptr, ptr, tau, S, slot, ptr, ptr, ptr, ptr, ptr,
-                           ptr, ptr, None)
+                           ptr, ptr, 1, None)
     assert gate(tau=1.5) == B.PRHS_E_INVALID
     assert gate(tau=-0.1) == B.PRHS_E_INVALID
     assert gate(tau=float("nan")) == B.PRHS_E_INVALID
@@ -246,14 +246,43 @@ def test_select_gated_and_pool_attention_validation(L):
     assert st == B.PRHS_E_CAPACITY
     L.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, ctypes.byref(kv), None, 300, ctypes.byref(n))
     good = B.psaw(7, 8, 6, 0.7, 1.0, 4)
-    pool = lambda rows, urow, ps, wsb: L.prhs_pool_decode_attn(  # noqa: E731
-        ctypes.byref(kv), 0x1, 0x2, 0x3, rows, 300, urow, 0x5, None if ps is None else ctypes.byref(ps),
-        0.1, 0x6, None, 0x7, wsb, None)
+    pool = lambda rows, urow, ps, wsb, gate=None, side=0: L.prhs_pool_decode_attn(  # noqa: E731
+        ctypes.byref(kv), 0x1, 0x2, 0x3, rows, 300, urow, 0x5, gate, side,
+        None if ps is None else ctypes.byref(ps), 0.1, 0x6, None, 0x7, wsb, None)
     assert pool(-1, 0x4, None, n.value) == B.PRHS_E_INVALID
     assert pool(8, None, None, n.value) == B.PRHS_E_INVALID
     assert pool(8, 0x4, B.psaw(7, 8, 6, 0.7, 1.0, -2), n.value) == B.PRHS_E_INVALID
     assert pool(8, 0x4, B.psaw(8, 8, 6, 0.7, 1.0, 4), n.value) == B.PRHS_E_INVALID
     assert pool(8, 0x4, good, n.value - 1) == B.PRHS_E_WORKSPACE
+    # the unit filter: a known side, and the gate's choice with a filter
+    assert pool(8, 0x4, None, n.value, gate=0x9, side=3) == B.PRHS_E_INVALID
+    assert pool(8, 0x4, None, n.value, gate=None, side=B.PRHS_UNITS_SHARING) == B.PRHS_E_INVALID
+    assert b"unit_gate" in L.prhs_last_error()
+    assert pool(8, 0x4, None, n.value - 1, gate=0x9,
+                side=B.PRHS_UNITS_RETRIEVING) == B.PRHS_E_WORKSPACE
+
+
+def test_gate_select_validation(L):
+    kv = _kv()
+    p = B.params(k=8, window=4, refresh_every=4)
+    cap = L.prhs_set_capacity(ctypes.byref(p), kv.max_seq_len)
+    n = ctypes.c_size_t(0)
+    L.prhs_workspace_size(B.PRHS_OP_SELECT, ctypes.byref(kv), ctypes.byref(p), 0, ctypes.byref(n))
+
+    def gs(kv=kv, tau=0.8, S=4, slot=1, ptr=0x10, set_cap=cap, wsb=n.value):
+        return L.prhs_gate_select(ctypes.byref(kv), 0x1, ctypes.byref(p), tau, S, slot, ptr, ptr,
+                                  ptr, ptr, ptr, ptr, ptr, 0x2, 0x3, 64, 0x4, 0x5, set_cap, 0x6,
+                                  0x7, 0x8, wsb, None)
+    assert gs(tau=1.2) == B.PRHS_E_INVALID and b"tau" in L.prhs_last_error()
+    assert gs(slot=4) == B.PRHS_E_INVALID
+    assert gs(ptr=None) == B.PRHS_E_INVALID
+    assert gs(set_cap=cap - 1) == B.PRHS_E_CAPACITY
+    assert gs(wsb=0) == B.PRHS_E_WORKSPACE
+    assert gs(kv=_kv(head_dim=96)) == B.PRHS_E_UNSUPPORTED
+    kv0 = _kv(batch=0, k=None, v=None, seq_lens=None)
+    assert L.prhs_gate_select(ctypes.byref(kv0), None, ctypes.byref(p), 0.8, 4, 0, None, None,
+                              None, None, None, None, None, None, None, 8, None, None, cap, None,
+                              None, None, 0, None) == B.PRHS_OK
 
 
 def test_dilate_validation_and_empty_batch(L):

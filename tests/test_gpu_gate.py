@@ -290,3 +290,44 @@ def test_gate_decisions_off_grid(dtype, hq, hkv, tau):
                     assert margin <= 1e-4, f"slot {t} unit {u} anchor {st}: margin {margin:.2e}"
             if c == -1:
                 anchors[u].append((t, Qg))
+
+
+@pytest.mark.parametrize("case", ["fused-rows", "radix-paged", "psaw"])
+def test_concurrent_step_equals_sequential(case):
+    # GatedDecodeRunner.step runs the sharing units' attention on a second
+    # stream beside the gate + refresh + retrieving units' attention: every
+    # layer's outputs equal, bit for bit, those of the same work run one
+    # launch after another, at every step of two blocks (the gate in the
+    # refresh launch on the fused path; a gate launch first otherwise)
+    psaw = None
+    if case == "fused-rows":
+        w = synth.workload(1).replace(layers=4, batch=5, n_ctx=(1500, 900, 1200, 700, 1100), steps=8)
+    elif case == "radix-paged":
+        w = synth.workload(3).replace(layers=2, n_ctx=(30000,), heavy=100, steps=16)
+    else:
+        w = synth.workload(1).replace(layers=8, batch=2, n_ctx=(2048, 1500), steps=8)
+        psaw = (6, 0.3, 1.0)
+    inp = synth.generate(w, device=DEV)
+    L = len(inp.K)
+    seq = GatedDecodeRunner(inp, DEV, tau=0.8, psaw=psaw)
+    con = GatedDecodeRunner(inp, DEV, tau=0.8, psaw=psaw, concurrent=True)
+    mk = lambda: [(torch.full((w.batch, w.hq, w.d), float("nan"), device=DEV),  # noqa: E731
+                   torch.full((w.batch, w.hq), float("nan"), device=DEV)) for _ in range(L)]
+    mixed = False
+    for j in range(w.steps):
+        a, b = mk(), mk()
+        seq.selection_step(j)
+        for l in range(L):
+            seq.attend(l, j, *a[l])
+        con.step(j, b)
+        torch.cuda.synchronize()
+        c = seq.choice.cpu().numpy()
+        assert np.array_equal(c, con.choice.cpu().numpy()), f"step {j}: decisions differ"
+        assert np.array_equal(c, con.side_choice.cpu().numpy()), f"step {j}: side decisions differ"
+        mixed |= bool((c < 0).any() and (c >= 0).any())
+        for l in range(L):
+            for x, y in zip(a[l], b[l]):
+                xh, yh = x.cpu().numpy(), y.cpu().numpy()
+                assert not np.isnan(yh).any(), f"step {j} layer {l}: unit not attended"
+                assert np.array_equal(xh, yh), f"step {j} layer {l}: outputs differ"
+    assert mixed, "the case should mix sharing and retrieving units"

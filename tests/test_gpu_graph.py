@@ -67,12 +67,18 @@ def _check_graph(w, runner, replays=3):
     del g
 
 
-@pytest.mark.parametrize("mode", ["shared", "per_step", "psaw", "gated"])
+@pytest.mark.parametrize("mode", ["shared", "per_step", "psaw", "gated", "gated_fused",
+                                  "gated_concurrent"])
 def test_graph_replay_config1_cut(mode):
-    # fused refresh path; 4 layers in one group of 4, blocks of 4 steps
+    # 4 layers in one group of 4, blocks of 4 steps; the gated step runs its
+    # sharing units on a second stream inside the graph; with 5 sequences
+    # (160 rows) the gate runs inside the fused refresh launch
     w = synth.workload(1).replace(layers=4, batch=2, n_ctx=(2048, 1500), steps=8)
-    if mode == "gated":
-        runner = lambda inp: GatedDecodeRunner(inp, DEV, tau=0.8)  # noqa: E731
+    if mode in ("gated_fused", "gated_concurrent"):
+        w = w.replace(batch=5, n_ctx=(2048, 1500, 900, 1700, 1200))
+    if mode.startswith("gated"):
+        conc = mode == "gated_concurrent"
+        runner = lambda inp: GatedDecodeRunner(inp, DEV, tau=0.8, concurrent=conc)  # noqa: E731
     elif mode == "psaw":
         runner = lambda inp: DecodeRunner(inp, DEV, psaw=(2, 0.3, 1.0))  # noqa: E731
     else:
