@@ -84,6 +84,18 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Workgroup barrier that orders LDS accesses only: it waits for this wave's
+// LDS operations, not for its outstanding global stores, so a workgroup that
+// has written results to global memory (which it never reads back) does not
+// stall on their acknowledgement at every later barrier.  Global memory
+// exchanged between the workgroup's threads needs __syncthreads() (or
+// block_publish) instead.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave with DPP lane moves:
 // shifts by 1, 2, 4, 8 inside each row of 16 lanes (a lane without a source
 // adds 0), then lane 15 of each row into the next row (rows 1, 3) and lane
@@ -107,7 +119,8 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan(uint64_t x) {
 }
 
 // Exclusive prefix sum over a workgroup of BLOCK threads; `scratch` holds
-// BLOCK/64 + 1 elements of LDS.  Returns this thread's exclusive prefix and
+// BLOCK/64 + 1 elements of LDS (exchanged through LDS only: the barriers do
+// not order global memory).  Returns this thread's exclusive prefix and
 // the block total in *total.  Must be reached by every thread.  With T =
 // uint64_t, several narrow counters packed into one word scan together as
 // long as no field overflows (and none straddles bit 32).
@@ -118,7 +131,7 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
   const int wave = threadIdx.x >> 6;
   const T x = wave_inclusive_scan(v);
   if (lane == 63) scratch[wave] = x;
-  __syncthreads();
+  lds_barrier();
   // every thread adds up the wave totals itself (broadcast LDS reads)
   T before = 0, tot = 0;
 #pragma unroll
@@ -128,7 +141,7 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
     tot += s;
   }
   *total = tot;
-  __syncthreads();  // scratch may be written again after return
+  lds_barrier();  // scratch may be written again after return
   return before + x - v;
 }
 

@@ -151,7 +151,7 @@ __device__ void find_threshold(const uint32_t* h, uint32_t kk, uint32_t* scan, i
     }
     cum += c;
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 __global__ __launch_bounds__(256) void select_clear(SelArgs a) {
@@ -770,7 +770,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       bt[w] = 0u;
       bd[w] = 0u;
     }
-    __syncthreads();
+    lds_barrier();
     for (uint32_t i = tid; i < total; i += kFinishBlock) {
       const uint64_t x = dyn[i];
       if (x < c_k) continue;
@@ -830,7 +830,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     pos_r += (int)((tot >> 16) & 0xFFFFu);
     pos_w += (int)((tot >> 32) & 0xFFFFu);
     pos_s += (int)(tot >> 48);
-    __syncthreads();
+    lds_barrier();
   }
   if (tid == 0) a.topk_len[row] = (int32_t)kout;
   // then the window, after the winners (and after the dilated middle)
@@ -881,16 +881,16 @@ __device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t
       const int psh = key_level_shift(lv - 1);
       const uint32_t dmask = lv == 1 ? 0x7FFu : 0x3FFu;
       for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
-      __syncthreads();
+      lds_barrier();
       for (uint32_t i = tid; i < n; i += BLOCK) {
         const uint32_t key = keys[i];
         if ((key >> psh) == t.p) atomicAdd(&h[(key >> sh) & dmask], 1u);
       }
-      __syncthreads();
+      lds_barrier();
     }
     find_threshold<BLOCK>(lv == 0 ? h0 : h, kk, scan, s_bin, s_krem, s_cnt);
     const uint32_t bin = (uint32_t)*s_bin, krem = *s_krem, cnt = *s_cnt;
-    __syncthreads();
+    lds_barrier();
     t.p = lv == 0 ? bin : ((t.p << (key_level_shift(lv - 1) - sh)) | bin);
     t.sh = sh;
     if (cnt == krem) {  // the whole bin is taken
@@ -965,7 +965,7 @@ __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, 
       key_threshold<BLOCK>(s_keys, (uint32_t)M, m, h, h, scan, s_bin, s_krem, s_cnt);
 #pragma unroll
   for (int j = 0; j < kBinsPerThread; ++j) h[tid + j * BLOCK] = h_keep[j];
-  __syncthreads();
+  lds_barrier();
   const KeyThreshold tk =
       key_threshold<BLOCK>(s_keys, (uint32_t)M, kout, h, h, scan, s_bin, s_krem, s_cnt);
   // h becomes the bitmap of the dilated shared set over the middle indices
@@ -1037,7 +1037,7 @@ __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, 
     a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
   }
   if (shared) {
-    __syncthreads();
+    lds_barrier();
     int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
     for (int i = tid; i < se; i += BLOCK)
       if (i < a.set_cap) sh[i] = i;
@@ -1069,7 +1069,7 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
       const int c = gate_unit<__bf16>(a.gate, row, threadIdx.x);
       if (threadIdx.x == 0) s_choice = c;
     }
-    __syncthreads();
+    lds_barrier();
     if (s_choice >= 0) return;
   } else if (row_skipped(a, row)) {
     return;

@@ -62,11 +62,11 @@ __device__ int compact_marked(int lo, int hi, int seg_bits, Mark mark, int32_t* 
     const int seg_hi = min(hi, seg_lo + seg_bits);
     const int nwords = (seg_hi - seg_lo + 31) >> 5;
     for (int w = tid; w < nwords; w += BLOCK) bm[w] = 0u;
-    __syncthreads();
+    lds_barrier();
     mark(seg_lo, seg_hi, bm);
-    __syncthreads();
+    lds_barrier();
     pos = compact_bitmap<BLOCK>(bm, nwords, seg_lo, out, cap, pos, scan);
-    __syncthreads();
+    lds_barrier();
   }
   return pos;
 }
