@@ -52,6 +52,12 @@ constexpr int kFinishTies = 4096;    // level-1 ties the finish kernel keeps in 
 // positions per bitmap segment of the finish kernel (3 bitmaps of 8 KB): whole
 // words, and below 2^16 so that per-segment counts fit 16-bit fields
 constexpr int kFinishSegBits = 65504;
+// output staging of the finish kernel: a bitmap segment's outputs up to this
+// many entries (or what LDS has room for) are gathered in LDS and copied out
+// with whole-wave stores
+constexpr int kFinishStage = 8192;
+// candidates few enough for one wave to rank them directly
+constexpr int kSmallRank = 64;
 
 struct SelArgs {
   KvView kv;
@@ -59,6 +65,8 @@ struct SelArgs {
   int k, k_num, k_den, sink, window, dilate_m;
   int mcap, selcap;
   int sortcap;         // LDS sort buffer entries of select_finish (>= selcap)
+  int stagecap;        // LDS output staging entries of select_finish
+  int woff;            // select_finish has LDS for per-word output offsets
   uint32_t* keys;      // [rows][mcap]
   uint32_t* hist0;     // [rows][2048]
   uint32_t* hist1;     // [rows][2048]
@@ -588,34 +596,79 @@ __device__ void radix_global(const SelArgs& a, uint32_t* nsel, uint2* sel, uint2
   }
 }
 
+// The k-th largest (1 <= k <= c) of the c <= kSmallRank composites among
+// get(0..n-1) whose bits under pmask equal prefix: one pass gathers them into
+// `small` (LDS), then each lane of wave 0 counts the gathered values above
+// its own.  The values are distinct, so exactly one lane has k - 1 above it.
+// Every thread must call it.
+template <typename Get>
+__device__ uint64_t lds_kth_small(Get get, uint32_t n, uint32_t k, uint64_t prefix, uint64_t pmask,
+                                  uint64_t* small, uint32_t* s_n, uint64_t* s_out) {
+  const int tid = threadIdx.x;
+  if (tid == 0) *s_n = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < n; i += kFinishBlock) {
+    const uint64_t x = get(i);
+    if ((x & pmask) == prefix) {
+      const uint32_t slot = atomicAdd(s_n, 1u);
+      if (slot < (uint32_t)kSmallRank) small[slot] = x;
+    }
+  }
+  __syncthreads();
+  const uint32_t c = min(*s_n, (uint32_t)kSmallRank);
+  if (tid < kSmallRank) {
+    const uint64_t x = (uint32_t)tid < c ? small[tid] : 0ull;
+    uint32_t above = 0;
+    for (uint32_t j = 0; j < c; ++j) above += small[j] > x ? 1u : 0u;
+    if ((uint32_t)tid < c && above == k - 1u) *s_out = x;
+  }
+  __syncthreads();
+  return *s_out;
+}
+
+// LDS scratch of the threshold searches.
+struct KthScratch {
+  uint32_t* h;
+  uint32_t* scan;
+  int* s_bin;
+  uint32_t *s_krem, *s_cnt, *s_n;
+  uint64_t *small, *s_out;
+};
+
 // Threshold T with exactly k of the n distinct composites get(0..n-1) at or
 // above it (1 <= k <= n): radix select over 11-bit digits of the 54-bit
-// values, stopping as soon as a whole bin is taken.  With lv0 > 0 the digits
-// of levels below lv0 are already known: `prefix` (under `pmask`) holds them,
-// and k counts within the composites that share them.  The values must be
+// values, stopping as soon as a whole bin is taken, and ranking the
+// candidates directly once at most kSmallRank remain.  With lv0 > 0 the
+// digits of levels below lv0 are already known: `prefix` (under `pmask`)
+// holds them, and k counts within the `count` composites that share them
+// (count may exceed the true number when unknown).  The values must be
 // readable from LDS.  Every thread must call it.
 template <typename Get>
-__device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, uint32_t* h, uint32_t* scan,
-                                    int* s_bin, uint32_t* s_krem, uint32_t* s_cnt, int lv0 = 0,
-                                    uint64_t prefix = 0, uint64_t pmask = 0) {
+__device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, const KthScratch& ks,
+                                    int lv0 = 0, uint64_t prefix = 0, uint64_t pmask = 0,
+                                    uint32_t count = 0xFFFFFFFFu) {
   const int tid = threadIdx.x;
   uint32_t krem = k;
+  if (lv0 == 0 && count > n) count = n;
   for (int lv = lv0; lv < 5; ++lv) {
+    if (count <= (uint32_t)kSmallRank)
+      return lds_kth_small(get, n, krem, prefix, pmask, ks.small, ks.s_n, ks.s_out);
     const int sh = lv < 4 ? 43 - 11 * lv : 0;
     const uint64_t dmask = lv < 4 ? 0x7FFull : 0x3FFull;
-    for (int i = tid; i < kHistBins; i += kFinishBlock) h[i] = 0u;
+    for (int i = tid; i < kHistBins; i += kFinishBlock) ks.h[i] = 0u;
     __syncthreads();
     for (uint32_t i = tid; i < n; i += kFinishBlock) {
       const uint64_t x = get(i);
-      if ((x & pmask) == prefix) atomicAdd(&h[(uint32_t)((x >> sh) & dmask)], 1u);
+      if ((x & pmask) == prefix) atomicAdd(&ks.h[(uint32_t)((x >> sh) & dmask)], 1u);
     }
     __syncthreads();
-    find_threshold<kFinishBlock>(h, krem, scan, s_bin, s_krem, s_cnt);
-    const uint32_t bin = (uint32_t)*s_bin, krem2 = *s_krem, cnt = *s_cnt;
+    find_threshold<kFinishBlock>(ks.h, krem, ks.scan, ks.s_bin, ks.s_krem, ks.s_cnt);
+    const uint32_t bin = (uint32_t)*ks.s_bin, krem2 = *ks.s_krem, cnt = *ks.s_cnt;
     prefix |= (uint64_t)bin << sh;
     pmask |= dmask << sh;
     if (cnt == krem2) break;
     krem = krem2;
+    count = cnt;
   }
   return prefix;
 }
@@ -636,6 +689,10 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt, s_base;
   __shared__ uint32_t s_nsel;  // entries in the row's output list sel (only this workgroup appends)
+  __shared__ uint64_t s_small[kSmallRank];
+  __shared__ uint64_t s_out;
+  __shared__ uint32_t s_n;
+  const KthScratch ks{h, scan, &s_bin, &s_krem, &s_cnt, &s_n, s_small, &s_out};
   const int row = blockIdx.x;
   if (row_skipped(a, row)) return;
   const int b = row / a.kv.hkv;
@@ -725,19 +782,18 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   uint64_t c_k = 0ull;
   if (kout < total) {
     if (b1 >= 0 && n_lds > 0 && n_sel + krem1 == kout)  // among the ties, from level 2
-      c_k = lds_kth_largest(get, n_lds, krem1, h, scan, &s_bin, &s_krem, &s_cnt, 2,
-                            ((uint64_t)b0 << 43) | ((uint64_t)b1 << 32), kD0 | kD1);
+      c_k = lds_kth_largest(get, n_lds, krem1, ks, 2,
+                            ((uint64_t)b0 << 43) | ((uint64_t)b1 << 32), kD0 | kD1, n_lds);
     else
-      c_k = lds_kth_largest(get, total, kout, h, scan, &s_bin, &s_krem, &s_cnt);
+      c_k = lds_kth_largest(get, total, kout, ks);
   }
   uint64_t c_m = ~0ull;
   if (m > 0) {
     if (bm0 >= 0 && m == m0)  // level-0 digit from the global histogram
       c_m = m_resolved0 ? (uint64_t)bm0 << 43
-                        : lds_kth_largest(get, total, kremm0, h, scan, &s_bin, &s_krem, &s_cnt, 1,
-                                          (uint64_t)bm0 << 43, kD0);
+                        : lds_kth_largest(get, total, kremm0, ks, 1, (uint64_t)bm0 << 43, kD0);
     else
-      c_m = lds_kth_largest(get, total, m, h, scan, &s_bin, &s_krem, &s_cnt);
+      c_m = lds_kth_largest(get, total, m, ks);
   }
   // One ordered pass over the middle range writes all outputs: per bitmap
   // segment the winners W (x >= c_k), the top m T (x >= c_m) and the +-r
@@ -752,6 +808,9 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   uint32_t* bw = (uint32_t*)(dyn + a.sortcap);
   uint32_t* bt = bw + kSegW;
   uint32_t* bd = bt + kSegW;
+  // optional per-word output offsets [kSegW], then the output staging
+  uint64_t* woff = a.woff ? (uint64_t*)(bd + kSegW + 1) : nullptr;
+  int32_t* stage = a.woff ? (int32_t*)(woff + kSegW) : (int32_t*)(bd + kSegW);  // a.stagecap entries
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
   int32_t* sh = shared ? a.shared_idx + (size_t)row * a.set_cap : nullptr;
@@ -798,37 +857,114 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     }
     uint64_t tot;
     const uint64_t off = block_exclusive_scan<kFinishBlock, uint64_t>(cnt, scan64, &tot);
-    int ot = pos_t + (int)(off & 0xFFFFu), orr = pos_r + (int)((off >> 16) & 0xFFFFu);
-    int ow = pos_w + (int)((off >> 32) & 0xFFFFu), os = pos_s + (int)(off >> 48);
-    for (int w = w_begin; w < w_end; ++w) {
-      const uint32_t W = bw[w], T = bt[w];
-      uint32_t bits = shared ? (W | bd[w]) : W;
-      const int base = seg_lo + (w << 5);
-      while (bits) {
-        const int bit = __ffs(bits) - 1;
-        const uint32_t one = 1u << bit;
-        bits &= bits - 1u;
-        const int p = base + bit;
-        if (W & one) {
-          if (T & one) {
-            if (ot < a.k_cap) topk[ot] = p;
-            ++ot;
-          } else {
-            if (orr < a.k_cap) topk[orr] = p;
-            ++orr;
-          }
-          if (ow < a.set_cap) out[ow] = p;
-          ++ow;
+    // the segment's outputs: top m, other winners, anchor set, shared set
+    const int n_t = (int)(tot & 0xFFFFu), n_r = (int)((tot >> 16) & 0xFFFFu);
+    const int n_w = (int)((tot >> 32) & 0xFFFFu), n_s = shared ? (int)(tot >> 48) : 0;
+    // Staged in LDS when they fit, then copied out with whole-wave stores
+    // (scattered stores from the bit loop below leave most lanes idle and
+    // cost the CU one store instruction per few entries); else written
+    // directly.
+    const bool staged = n_t + n_r + n_w + n_s <= a.stagecap;
+    int32_t* dt = staged ? stage : topk + pos_t;
+    int32_t* dr = staged ? stage + n_t : topk + pos_r;
+    int32_t* dw = staged ? stage + n_t + n_r : out + pos_w;
+    int32_t* ds = staged ? stage + n_t + n_r + n_w : (shared ? sh + pos_s : nullptr);
+    const int lim_t = staged ? n_t : a.k_cap - pos_t, lim_r = staged ? n_r : a.k_cap - pos_r;
+    const int lim_w = staged ? n_w : a.set_cap - pos_w, lim_s = staged ? n_s : a.set_cap - pos_s;
+    if (woff) {
+      // Per-entry writes: with each word's output offsets in LDS, every
+      // winner places itself (word offset + set bits below it), so clustered
+      // winners do not serialise on the thread owning their words; the
+      // dilation-only positions of the shared set, sparse by comparison,
+      // are walked per word.
+      uint64_t run = off;
+      for (int w = w_begin; w < w_end; ++w) {
+        woff[w] = run;
+        const uint32_t W = bw[w], T = bt[w], S = W | bd[w];
+        run += (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
+               ((uint64_t)__popc(W) << 32) | ((uint64_t)__popc(S) << 48);
+      }
+      lds_barrier();
+      for (uint32_t i = tid; i < total; i += kFinishBlock) {
+        const uint64_t x = dyn[i];
+        if (x < c_k) continue;
+        const int p = composite_pos(x);
+        if (p < seg_lo || p >= seg_hi) continue;
+        const int rel = p - seg_lo, w = rel >> 5;
+        const uint32_t below = (1u << (rel & 31)) - 1u;
+        const uint64_t o = woff[w];
+        const uint32_t W = bw[w], T = bt[w];
+        if (x >= c_m) {
+          const int j = (int)(o & 0xFFFFu) + __popc(T & below);
+          if (j < lim_t) dt[j] = p;
+        } else {
+          const int j = (int)((o >> 16) & 0xFFFFu) + __popc(W & ~T & below);
+          if (j < lim_r) dr[j] = p;
         }
+        const int jw = (int)((o >> 32) & 0xFFFFu) + __popc(W & below);
+        if (jw < lim_w) dw[jw] = p;
         if (shared) {
-          if (os < a.set_cap) sh[os] = p;
-          ++os;
+          const int js = (int)(o >> 48) + __popc((W | bd[w]) & below);
+          if (js < lim_s) ds[js] = p;
+        }
+      }
+      if (shared) {
+        for (int w = w_begin; w < w_end; ++w) {
+          const uint32_t W = bw[w], S = W | bd[w];
+          uint32_t bits = S & ~W;
+          const int js0 = (int)(woff[w] >> 48);
+          while (bits) {
+            const int bit = __ffs(bits) - 1;
+            bits &= bits - 1u;
+            const int js = js0 + __popc(S & ((1u << bit) - 1u));
+            if (js < lim_s) ds[js] = seg_lo + (w << 5) + bit;
+          }
+        }
+      }
+    } else {
+      int ot = (int)(off & 0xFFFFu), orr = (int)((off >> 16) & 0xFFFFu);
+      int ow = (int)((off >> 32) & 0xFFFFu), os = (int)(off >> 48);
+      for (int w = w_begin; w < w_end; ++w) {
+        const uint32_t W = bw[w], T = bt[w];
+        uint32_t bits = shared ? (W | bd[w]) : W;
+        const int base = seg_lo + (w << 5);
+        while (bits) {
+          const int bit = __ffs(bits) - 1;
+          const uint32_t one = 1u << bit;
+          bits &= bits - 1u;
+          const int p = base + bit;
+          if (W & one) {
+            if (T & one) {
+              if (ot < lim_t) dt[ot] = p;
+              ++ot;
+            } else {
+              if (orr < lim_r) dr[orr] = p;
+              ++orr;
+            }
+            if (ow < lim_w) dw[ow] = p;
+            ++ow;
+          }
+          if (shared) {
+            if (os < lim_s) ds[os] = p;
+            ++os;
+          }
         }
       }
     }
-    pos_t += (int)(tot & 0xFFFFu);
-    pos_r += (int)((tot >> 16) & 0xFFFFu);
-    pos_w += (int)((tot >> 32) & 0xFFFFu);
+    if (staged) {
+      lds_barrier();
+      for (int i = tid; i < n_t; i += kFinishBlock)
+        if (pos_t + i < a.k_cap) topk[pos_t + i] = stage[i];
+      for (int i = tid; i < n_r; i += kFinishBlock)
+        if (pos_r + i < a.k_cap) topk[pos_r + i] = stage[n_t + i];
+      for (int i = tid; i < n_w; i += kFinishBlock)
+        if (pos_w + i < a.set_cap) out[pos_w + i] = stage[n_t + n_r + i];
+      for (int i = tid; i < n_s; i += kFinishBlock)
+        if (pos_s + i < a.set_cap) sh[pos_s + i] = stage[n_t + n_r + n_w + i];
+    }
+    pos_t += n_t;
+    pos_r += n_r;
+    pos_w += n_w;
     pos_s += (int)(tot >> 48);
     lds_barrier();
   }
@@ -1377,19 +1513,26 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   hipLaunchKernelGGL(select_filter, fgrid, dim3(kFilterBlock), 0, stream, a);
   // LDS buffer: the k winners plus up to kFinishTies level-1 ties, as far as
   // the CU's LDS holds them beside the kernel's static LDS and the bitmap
-  // segment; the host bound PRHS_MAX_TOPK keeps the winners alone inside it
+  // segment (the host bound PRHS_MAX_TOPK keeps the winners alone inside
+  // it); the output staging takes what remains, up to kFinishStage entries
   static const long long finish_static = [] {
     hipFuncAttributes fa;
     return hipFuncGetAttributes(&fa, (const void*)select_finish) == hipSuccess
                ? (long long)fa.sharedSizeBytes : -1LL;
   }();
   if (finish_static < 0) return hipErrorInvalidDeviceFunction;
-  const long long lds_cap = ((long long)kLdsBytes - finish_static - 3LL * kFinishSegBits / 8) / 8;
+  const long long avail = (long long)kLdsBytes - finish_static - 3LL * kFinishSegBits / 8;
   long long cap = (long long)a.selcap + kFinishTies;
-  if (cap > lds_cap) cap = lds_cap;
+  if (cap > avail / 8) cap = avail / 8;
   if (cap < a.selcap) return hipErrorInvalidValue;  // unreachable for k_b <= PRHS_MAX_TOPK
   a.sortcap = (int)cap;
-  const size_t dyn = (size_t)a.sortcap * 8 + 3 * kFinishSegBits / 8;
+  long long rest = avail - cap * 8;
+  constexpr long long kWoffBytes = (kFinishSegBits / 32 + 1) * 8LL;  // with 4 bytes of alignment
+  a.woff = rest >= kWoffBytes ? 1 : 0;
+  if (a.woff) rest -= kWoffBytes;
+  a.stagecap = (int)(rest / 4 < kFinishStage ? rest / 4 : kFinishStage);
+  const size_t dyn = (size_t)a.sortcap * 8 + 3 * kFinishSegBits / 8 + (a.woff ? kWoffBytes : 0) +
+                     (size_t)a.stagecap * 4;
   if (dyn > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)select_finish,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
