@@ -17,6 +17,12 @@
  * - The caller owns every buffer.  The library allocates no device memory and
  *   keeps no state between calls; calls on different streams with different
  *   buffers may run concurrently.  Calls sharing a workspace must be ordered.
+ * - Workspaces need no initialisation, with one exception: a selection
+ *   workspace (PRHS_OP_SELECT) begins with per-row histograms and counters,
+ *   2 x align256(R x 8192) + align256(R x 16) bytes for R = batch x
+ *   num_kv_heads rows, which must be zero when a call starts and which every
+ *   call leaves zero.  Zero-fill a selection workspace before its first use,
+ *   and again before a call with more rows than the calls it served so far.
  * - Every call is asynchronous on `stream`; results are valid once the stream
  *   has synchronised.  No call synchronises internally.
  * - Positions are 0-based.  A sequence of current length n attends keys
@@ -192,8 +198,8 @@ int32_t prhs_psaw_first_visible(const prhs_psaw* psaw, int32_t n);
  * topk_len: [batch][num_kv_heads] int32.
  * set_idx: [batch][num_kv_heads][set_cap] int32, set_cap >= min(max_seq_len,
  *   sink + prhs_max_topk() + window).  set_len: [batch][num_kv_heads] int32.
- * ws: >= prhs_workspace_size(PRHS_OP_SELECT) bytes, contents need no
- *   initialisation and are clobbered.
+ * ws: >= prhs_workspace_size(PRHS_OP_SELECT) bytes; its leading histogram
+ *   region zero (see the conventions above), the rest clobbered.
  * -0.0 scores rank equal to +0.0; NaN or infinite inputs are a precondition
  * violation. */
 prhs_status prhs_select(const prhs_kv* kv, const void* q, const prhs_params* params,

@@ -285,9 +285,21 @@ def prhs_workspace_size(op, kv=None, p=None, set_cap=0):
 
 
 def workspace(nbytes, device):
-    """A zero-filled device workspace.  No entry point needs its workspace
-    initialised; zeros keep runs reproducible."""
+    """A zero-filled device workspace: a selection workspace needs its
+    leading histogram region (select_zero_bytes) zero before its first use;
+    the other workspaces need no initialisation."""
     return torch.zeros(max(1, nbytes), dtype=torch.uint8, device=device)
+
+
+def select_zero_bytes(kv):
+    """Bytes at the front of a selection workspace that must be zero when a
+    call starts and that every call leaves zero (per-row histograms and
+    counters of batch x num_kv_heads rows)."""
+    rows = kv.c.batch * kv.c.num_kv_heads
+
+    def a256(x):
+        return (x + 255) // 256 * 256
+    return 2 * a256(rows * 8192) + a256(rows * 16)
 
 
 def _q(kv, q):

@@ -17,7 +17,6 @@
 //                  runs select_fused's selection half, one workgroup per row
 //                  -- two launches;
 //   radix path     longer middle ranges, one launch each:
-//     select_clear   zero the per-row histograms and counters
 //     score_*        sigma_i = max_h q_h . k_i (raw, fp32) -> order-preserving
 //                    u32 key; fused histogram of the top 11 key bits
 //     select_filter  locate the threshold bin of level 0; keys above it are
@@ -27,6 +26,11 @@
 //                    composites (key, kIdxMax - pos), distinct, so ties go to
 //                    the lower position; one segmented bitmap pass writes the
 //                    ordered outputs.
+//                  The per-row histograms and counters the score and filter
+//                  kernels accumulate into sit at the front of the workspace;
+//                  they are zero when a call starts (the caller zero-fills a
+//                  new workspace) and select_finish zeroes each row's again
+//                  once it has read them, so no clearing launch is needed.
 #include <stdlib.h>
 
 #include "prhs.h"
@@ -160,16 +164,6 @@ __device__ void find_threshold(const uint32_t* h, uint32_t kk, uint32_t* scan, i
     cum += c;
   }
   lds_barrier();
-}
-
-__global__ __launch_bounds__(256) void select_clear(SelArgs a) {
-  const int row = blockIdx.x;
-  if (row_skipped(a, row)) return;
-  for (int i = threadIdx.x; i < kHistBins; i += 256) {
-    a.hist0[(size_t)row * kHistBins + i] = 0u;
-    a.hist1[(size_t)row * kHistBins + i] = 0u;
-  }
-  if (threadIdx.x < 4) a.counters[row * 4 + threadIdx.x] = 0u;
 }
 
 __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
@@ -983,6 +977,13 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     a.set_len[row] = pos_w < a.set_cap ? pos_w : a.set_cap;
     if (shared) a.shared_len[row] = pos_s < a.set_cap ? pos_s : a.set_cap;
   }
+  // leave the row's histograms and counters zero for the next call (every
+  // thread read its own histogram entries and the counters long before)
+  for (int i = tid; i < kHistBins; i += kFinishBlock) {
+    a.hist0[(size_t)row * kHistBins + i] = 0u;
+    a.hist1[(size_t)row * kHistBins + i] = 0u;
+  }
+  if (tid < 4) cnt[tid] = 0u;
 }
 
 // Exact threshold of one selection target over the LDS key array: a key
@@ -1369,13 +1370,15 @@ struct SelLayout {
   size_t keys, hist0, hist1, counters, sel, cand, cand2, total;
 };
 
+// The zero-between-calls region (histograms, counters) comes first, so a
+// workspace keeps it in place for calls with fewer rows too.
 SelLayout select_layout(int rows, int mcap, int selcap) {
   SelLayout L;
   size_t off = 0;
-  L.keys = off;     off += align256((size_t)rows * mcap * 4);
   L.hist0 = off;    off += align256((size_t)rows * kHistBins * 4);
   L.hist1 = off;    off += align256((size_t)rows * kHistBins * 4);
   L.counters = off; off += align256((size_t)rows * 16);
+  L.keys = off;     off += align256((size_t)rows * mcap * 4);
   L.sel = off;      off += align256((size_t)rows * selcap * 8);
   L.cand = off;     off += align256((size_t)rows * mcap * 8);
   L.cand2 = off;    off += align256((size_t)rows * mcap * 8);
@@ -1476,7 +1479,6 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   // the middle range is shorter than max_seq_len; size grids by max_seq_len
   const int mid_max = a.mcap;
   const bool radix = path == SelPath::kRadix;
-  if (radix) hipLaunchKernelGGL(select_clear, dim3(rows), dim3(256), 0, stream, a);
   const dim3 sgrid((mid_max + kScoreChunk - 1) / kScoreChunk, rows);
 #define PRHS_SCORE_LAUNCH(HIST)                                                               \
   if (s.dtype == 1) {                                                                         \

@@ -204,9 +204,12 @@ def run_select(inp, lens, p, layer=0, step=0):
     sidx = torch.full((w.batch, w.hkv, set_cap), -7, dtype=torch.int32, device=DEV)
     slen = torch.full((w.batch, w.hkv), -7, dtype=torch.int32, device=DEV)
     ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv, p), DEV)
-    ws.fill_(0xAB)   # the workspace needs no initialisation
+    zb = B.select_zero_bytes(kv)
+    ws.fill_(0xAB)   # beyond the histogram region the workspace needs no initialisation
+    ws[:zb].zero_()
     B.prhs_select(kv, inp.q[layer, step], p, topk, tlen, sidx, slen, ws)
     torch.cuda.synchronize()
+    assert not ws[:zb].any(), "the histogram region is not left zero"
     return topk.cpu().numpy(), tlen.cpu().numpy(), sidx.cpu().numpy(), slen.cpu().numpy()
 
 
@@ -313,9 +316,12 @@ def check_select_shared(inp, lens, p):
     hidx = torch.full(shape + (set_cap,), -7, dtype=torch.int32, device=DEV)
     hlen = torch.full(shape, -7, dtype=torch.int32, device=DEV)
     ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SELECT, kv, p), DEV)
+    zb = B.select_zero_bytes(kv)
     ws.fill_(0xCD)
+    ws[:zb].zero_()
     B.prhs_select_shared(kv, inp.q[0, 0], p, topk, tlen, sidx, slen, hidx, hlen, ws)
     torch.cuda.synchronize()
+    assert not ws[:zb].any(), "the histogram region is not left zero"
     topk, tlen, sidx, slen = (t.cpu().numpy() for t in (topk, tlen, sidx, slen))
     hidx, hlen = hidx.cpu().numpy(), hlen.cpu().numpy()
     for (b, g), (S, C) in oracle_select(inp, lens, p).items():
