@@ -1113,8 +1113,9 @@ __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, 
     for (int i = tid; i < mwords; i += BLOCK) h[i] = 0u;
   // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept); one
   // scan of four 16-bit counts gives every thread its output offsets (the
-  // middle range is below 2^16 keys here)
-  const int ept = (M + BLOCK - 1) / BLOCK;
+  // middle range is below 2^16 keys here).  ept is odd, so the lanes' LDS
+  // reads at stride ept fall in distinct banks.
+  const int ept = ((M + BLOCK - 1) / BLOCK) | 1;
   const int i_begin = min(M, tid * ept), i_end = min(M, i_begin + ept);
   uint32_t gm = 0, em = 0, gk = 0, ek = 0;
   for (int i = i_begin; i < i_end; ++i) {

@@ -68,8 +68,12 @@ def run_schedule(w, steps, units_out, units_set=None, layers=None, per_step_sets
     out = torch.empty(w.batch, w.hq, w.d, device=DEV)
     lse = torch.empty(w.batch, w.hq, device=DEV)
     worst = 0.0
+    zero = B.select_zero_bytes(run.kv[0][0])
     for j in steps:
         run.selection_step(j)
+        torch.cuda.synchronize()
+        # the histogram region and the refresh's row queue are left zero
+        assert not run.ws_select[:zero].any(), f"step {j}: selection zero region not left zero"
         for l in range(L):
             out.fill_(float("nan"))
             run.attend(l, j, out, lse)
