@@ -542,7 +542,7 @@ def selection_kernels(w, cus):
         return "select_fused", 1
     if fits:
         return "score + select_keyed", 2
-    return "select_clear + score + select_filter + select_finish", 4
+    return "score + select_filter + select_finish", 3
 
 
 def measure(w, args, dev, K_steps, W_steps, psaw=None, gated=False, tau=None):
