@@ -1447,11 +1447,21 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   if (path == SelPath::kFused) {
     const size_t dyn = (size_t)a.mcap * 4;
     a.balance_cus = balance_cus();
-    // one 1024-thread workgroup per CU while the rows fit the CUs and its
-    // LDS (static part plus the key array) fits the CU's 160 KB; otherwise
-    // 512-thread workgroups, two to a CU where they fit, so that one's
-    // selection overlaps the other's scoring
+    // 1024-thread workgroups (one per CU) when the rows fit the CUs, or when
+    // two 512-thread ones would not fit one CU's LDS either (long middle
+    // ranges: more waves stream each row); otherwise 512-thread workgroups,
+    // two to a CU, so that one's selection overlaps the other's scoring.
+    // Either way only while the workgroup's LDS (static part plus the key
+    // array) fits the CU's 160 KB.
     bool wide = a.balance_cus <= 0 || rows <= a.balance_cus;
+    if (!wide) {
+      hipFuncAttributes fb;
+      const hipError_t eb =
+          s.kv.d == 128 ? hipFuncGetAttributes(&fb, (const void*)select_fused<128, 512>)
+                        : hipFuncGetAttributes(&fb, (const void*)select_fused<64, 512>);
+      if (eb != hipSuccess) return eb;
+      wide = 2 * (fb.sharedSizeBytes + dyn) > (size_t)kLdsBytes;
+    }
     if (wide) {
       hipFuncAttributes fa;
       const hipError_t ea =
