@@ -302,7 +302,7 @@ def test_golden_paper_budgets():
     assert C_star <= lb["cis_star_avg_budget"] <= C_star + 2 * (lb["k_cis_star"] // 3)
 
 
-# ---------------------------------------------------------------- invariants of the benchmark spec
+# ---------------------------------------------------------------- invariant: a full budget is dense attention
 
 def test_full_budget_reproduces_dense():
     # k >= |middle| (or window >= n) gives R = [0, n): sparse == dense
