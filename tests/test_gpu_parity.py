@@ -179,6 +179,65 @@ def test_sparse_attention_unsplit_boundary(dtype, set_cap):
                          f"b{b} g{g} |S|={len(S)}")
 
 
+def test_attention_skips_entries_and_pages_outside_the_cache():
+    """Device arrays the host cannot check: set entries outside [0, n) (negative,
+    at or past n, huge), block-table entries outside the page pool (-1, past
+    the last page) and a sequence length beyond max_seq_len.  The kernels skip
+    such entries and pages and clamp the length, so the outputs are attention
+    over the remaining valid positions."""
+    lens = (300, 200)
+    inp = synth.random_inputs(2, 8, 2, 128, lens, paged=True, seed=61, grid=False,
+                              key_scale=1.5, device=DEV)
+    w = inp.w
+    ps = w.page_size
+    table = inp.block_table.clone()
+    P = inp.K[0].shape[0]
+    bad = {(0, 1): -1, (1, 0): P + 7, (0, 3): 1 << 30}
+    for (b, pg), v in bad.items():
+        table[b, pg] = v
+    kv = B.KV(inp.K[0], inp.V[0], lens_tensor(lens), w.capacity, w.hq, table)
+    rng = np.random.default_rng(17)
+    set_cap = 160
+    idx = torch.zeros(2, 2, set_cap, dtype=torch.int32)
+    ln = torch.zeros(2, 2, dtype=torch.int32)
+    sets = {}
+    for b, n in enumerate(lens):
+        for g in range(2):
+            S = sorted(rng.choice(n, size=120, replace=False).tolist())
+            S = [-5, -1] + S + [n, n + 100, w.capacity + 5, 1 << 30]
+            idx[b, g, : len(S)] = torch.tensor(S, dtype=torch.int32)
+            ln[b, g] = len(S)
+            sets[(b, g)] = [i for i in S if 0 <= i < n and (b, i // ps) not in bad]
+    out = torch.full((2, 8, 128), float("nan"), device=DEV)
+    lse = torch.full((2, 8), float("nan"), device=DEV)
+    ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv, None, set_cap), DEV)
+    B.prhs_sparse_decode_attn(kv, inp.q[0, 0], idx.to(DEV), ln.to(DEV), 1 / math.sqrt(128), out,
+                              lse, ws)
+    torch.cuda.synchronize()
+    y, ls = out.cpu().numpy(), lse.cpu().numpy()
+    for (b, g), S in sets.items():
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, 0, b, g)
+        for j in range(4):
+            yr, lr = O.sparse_attention(Qg[j], K, V, S)
+            assert_close(y[b, g * 4 + j], ls[b, g * 4 + j], yr, lr, TOL["bf16"], f"b{b} g{g}")
+    # a length beyond max_seq_len is clamped to it: dense attention over the
+    # whole cache of the longest sequence (every row of it is valid)
+    big = torch.tensor([w.capacity + 1000, lens[1]], dtype=torch.int32, device=DEV)
+    kvc = B.KV(inp.K[0], inp.V[0], big, w.capacity, w.hq, inp.block_table)
+    out.fill_(float("nan"))
+    wsd = B.workspace(B.prhs_workspace_size(B.PRHS_OP_DENSE_ATTN, kvc), DEV)
+    B.prhs_dense_decode_attn(kvc, inp.q[0, 0], 1 / math.sqrt(128), out, lse, wsd)
+    torch.cuda.synchronize()
+    y, ls = out.cpu().numpy(), lse.cpu().numpy()
+    for g in range(2):
+        K, V = synth.gather_unit(inp, 0, 0, g, w.capacity)
+        Qg = synth.query_group(inp, 0, 0, 0, g)
+        for j in range(4):
+            yr, lr = O.dense_attention(Qg[j], K, V)
+            assert_close(y[0, g * 4 + j], ls[0, g * 4 + j], yr, lr, TOL["bf16"], f"clamped g{g}")
+
+
 def test_sparse_full_set_matches_dense_kernel():
     lens = (1500, 333)
     inp = synth.random_inputs(2, 8, 2, 128, lens, seed=31, grid=False, device=DEV)
