@@ -36,7 +36,10 @@
  *   max_seq_len, anchor_lens[b] <= seq_lens[b], block-table entries in
  *   [0, num_pages), set indices < seq_lens[b].  Kernels clamp lengths to the
  *   host-declared bounds and skip out-of-range rows instead of reading out of
- *   bounds; results for inputs that break a precondition are unspecified.
+ *   bounds.  The attention entry points then attend exactly the remaining
+ *   valid positions (set entries outside [0, n) and positions on pages
+ *   outside the pool are left out); selection results for inputs that break
+ *   a precondition are unspecified.
  */
 #ifndef PRHS_H_
 #define PRHS_H_
