@@ -313,7 +313,7 @@ SELECT_CASES = [
     ("big-k", "bf16", 128, False, 4, 1, (20000,), dict(k=9000, sink=4, window=64)),
     ("keyed-128-rows", "bf16", 128, False, 32, 8, tuple(300 + (i * 997) % 5000 for i in range(16)),
      dict(k=150, sink=4, window=32)),
-    # middle ranges beyond LDS: the radix path (clear, score, filter, finish),
+    # middle ranges beyond LDS: the radix path (score, filter, finish),
     # including a k whose level-1 ties overflow the LDS buffer
     ("radix-ragged-gqa", "bf16", 128, False, 8, 2, (30000, 26000, 70), dict(k=300, sink=4, window=64)),
     ("radix-paged-d64", "bf16", 64, True, 4, 4, (27000,), dict(k=100, sink=4, window=32)),
@@ -345,6 +345,13 @@ SELECT_CASES = [
      dict(k=1000, sink=4, window=128)),
     ("fused-narrow-24k", "bf16", 128, False, 32, 8, (24000, 23000) * 8 + (20000,),
      dict(k_num=1, k_den=20, sink=4, window=128)),
+    # more rows than CUs with long middle ranges: two 512-thread workgroups
+    # would not share a CU's LDS, so 1024-thread ones take the rows by length
+    ("fused-wide-many-rows", "bf16", 128, False, 32, 8, tuple(15000 + 31 * i for i in range(33)),
+     dict(k_num=1, k_den=20, sink=4, window=128)),
+    # more than 256 sequences: no length ranking, one row per workgroup in order
+    ("fused-many-seqs", "bf16", 128, False, 4, 1, tuple(100 + (i * 131) % 1200 for i in range(260)),
+     dict(k=40, sink=4, window=16)),
     # the largest query group (16 heads per kv head) on each path
     ("g16-keyed", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
     ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(136)),
