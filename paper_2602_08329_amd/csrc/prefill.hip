@@ -148,7 +148,6 @@ constexpr int vrow_bytes() { return D * 2 + 32; }
 template <int D, int NT>
 __device__ __forceinline__ void tile_store(const TileRegs<D, NT>& R, u32x4_t* sk, u32x4_t* sv) {
   constexpr int CH = D / 8;
-  unsigned char* vt = (unsigned char*)sv;
 #pragma unroll
   for (int j = 0; j < TileRegs<D, NT>::RPL; ++j) {
     const int e = (int)threadIdx.x + j * NT;
