@@ -999,45 +999,285 @@ struct KeyThreshold {
 // Radix levels over the 32-bit key: bits [31:21], [20:10], [9:0].
 __device__ __forceinline__ int key_level_shift(int lv) { return lv == 0 ? 21 : (lv == 1 ? 10 : 0); }
 
-// Threshold for the kk largest of the n LDS keys (kk = 0 selects nothing,
-// kk >= n everything).  h0 holds the level-0 histogram (key >> 21) of all n
-// keys; h (which may be h0) is overwritten when a deeper level is needed.
-// Reached by every thread.
+// The crossing bins of two targets in one pass over two histograms: for
+// target j (ka for ha, kb for hb; 0 = no search), the bin where the count
+// taken from the top reaches the target, the remainder taken inside it and
+// its count, into res[3j .. 3j + 2].  One packed scan serves both.  Every
+// thread must call it.
 template <int BLOCK>
-__device__ KeyThreshold key_threshold(const uint32_t* keys, uint32_t n, uint32_t kk,
-                                      const uint32_t* h0, uint32_t* h, uint32_t* scan, int* s_bin,
-                                      uint32_t* s_krem, uint32_t* s_cnt) {
-  if (kk == 0) return {0, 0xFFFFFFFFu, 0u};        // nothing: key > max never holds
-  if (kk >= n) return {0, 0u, 0xFFFFFFFFu};        // everything
+__device__ void find_threshold_pair(const uint32_t* ha, const uint32_t* hb, uint32_t ka,
+                                    uint32_t kb, uint64_t* scan64, uint32_t* res) {
+  constexpr int BPT = kHistBins / BLOCK;
+  const int t = threadIdx.x;
+  uint32_t la = 0, lb = 0;
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int bin = kHistBins - 1 - (t * BPT + i);
+    la += ha[bin];
+    lb += hb[bin];
+  }
+  uint64_t total;
+  const uint64_t cum = block_exclusive_scan<BLOCK, uint64_t>(
+      (uint64_t)la | ((uint64_t)lb << 32), scan64, &total);
+  uint32_t ca = (uint32_t)cum, cb = (uint32_t)(cum >> 32);
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int bin = kHistBins - 1 - (t * BPT + i);
+    const uint32_t c = ha[bin], d = hb[bin];
+    if (ca < ka && ca + c >= ka) {
+      res[0] = (uint32_t)bin;
+      res[1] = ka - ca;
+      res[2] = c;
+    }
+    if (cb < kb && cb + d >= kb) {
+      res[3] = (uint32_t)bin;
+      res[4] = kb - cb;
+      res[5] = d;
+    }
+    ca += c;
+    cb += d;
+  }
+  lds_barrier();
+}
+
+// Thresholds for the ka and the kb largest of the n LDS keys at once (a
+// target of 0 selects nothing, one of n or more everything): radix levels
+// in lockstep, one pass over the keys per level building both targets'
+// next-digit histograms (h for ka, h2 for kb), one scan finding both bins.
+// h holds the level-0 histogram (key >> 21) of all n keys on entry; h and h2
+// are overwritten.  res: 6 words of LDS.  Reached by every thread.
+template <int BLOCK>
+__device__ void key_threshold_pair(const uint32_t* keys, uint32_t n, uint32_t ka, uint32_t kb,
+                                   uint32_t* h, uint32_t* h2, uint64_t* scan64, uint32_t* res,
+                                   KeyThreshold* out) {
   const int tid = threadIdx.x;
-  KeyThreshold t = {21, 0u, 0u};
-  for (int lv = 0; lv < 3; ++lv) {
+  KeyThreshold t[2];
+  uint32_t kk[2] = {ka, kb};
+  bool live[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    live[j] = kk[j] > 0 && kk[j] < n;
+    if (kk[j] == 0) t[j] = {0, 0xFFFFFFFFu, 0u};       // nothing: key > max never holds
+    else if (kk[j] >= n) t[j] = {0, 0u, 0xFFFFFFFFu};  // everything
+    else t[j] = {21, 0u, 0u};
+  }
+  for (int lv = 0; lv < 3 && (live[0] || live[1]); ++lv) {
     const int sh = key_level_shift(lv);
     if (lv > 0) {
-      // histogram of the next digit over the keys that share the prefix
+      // next-digit histograms over the keys that share each live prefix (a
+      // finished target's prefix is replaced by a value no key shift reaches)
       const int psh = key_level_shift(lv - 1);
       const uint32_t dmask = lv == 1 ? 0x7FFu : 0x3FFu;
-      for (int i = tid; i < kHistBins; i += BLOCK) h[i] = 0u;
+      const uint32_t pa = live[0] ? t[0].p : 0xFFFFFFFFu, pb = live[1] ? t[1].p : 0xFFFFFFFFu;
+      for (int i = tid; i < kHistBins; i += BLOCK) {
+        if (live[0]) h[i] = 0u;
+        if (live[1]) h2[i] = 0u;
+      }
       lds_barrier();
-      for (uint32_t i = tid; i < n; i += BLOCK) {
-        const uint32_t key = keys[i];
-        if ((key >> psh) == t.p) atomicAdd(&h[(key >> sh) & dmask], 1u);
+      // four keys per thread in flight (reads clamped into the array)
+      for (uint32_t i0 = tid; i0 < n; i0 += 4 * BLOCK) {
+        uint32_t kv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kv[u] = keys[min(i0 + u * BLOCK, n - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool in = i0 + u * BLOCK < n;
+          const uint32_t x = kv[u] >> psh, d = (kv[u] >> sh) & dmask;
+          if (in && x == pa) atomicAdd(&h[d], 1u);
+          if (in && x == pb) atomicAdd(&h2[d], 1u);
+        }
       }
       lds_barrier();
     }
-    find_threshold<BLOCK>(lv == 0 ? h0 : h, kk, scan, s_bin, s_krem, s_cnt);
-    const uint32_t bin = (uint32_t)*s_bin, krem = *s_krem, cnt = *s_cnt;
-    lds_barrier();
-    t.p = lv == 0 ? bin : ((t.p << (key_level_shift(lv - 1) - sh)) | bin);
-    t.sh = sh;
-    if (cnt == krem) {  // the whole bin is taken
-      t.take = 0xFFFFFFFFu;
-      return t;
+    find_threshold_pair<BLOCK>(h, lv == 0 ? h : h2, live[0] ? kk[0] : 0u, live[1] ? kk[1] : 0u,
+                               scan64, res);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (!live[j]) continue;
+      const uint32_t bin = res[3 * j], krem = res[3 * j + 1], cnt = res[3 * j + 2];
+      t[j].p = lv == 0 ? bin : ((t[j].p << (key_level_shift(lv - 1) - sh)) | bin);
+      t[j].sh = sh;
+      if (cnt == krem) {  // the whole bin is taken
+        t[j].take = 0xFFFFFFFFu;
+        live[j] = false;
+      } else {
+        kk[j] = krem;
+      }
     }
-    kk = krem;
   }
-  t.take = kk;  // the first kk keys equal to the full 32-bit threshold
-  return t;
+  // the first kk keys equal to the full 32-bit threshold
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (live[j]) t[j].take = kk[j];
+    out[j] = t[j];
+  }
+}
+
+// The t lowest set bits of x (all of them when x has t or fewer).
+__device__ __forceinline__ uint64_t lowest_bits(uint64_t x, uint32_t t) {
+  if (t >= (uint32_t)__popcll(x)) return x;
+  uint64_t r = 0;
+  for (uint32_t j = 0; j < t; ++j) {
+    const uint64_t b = x & (~x + 1u);
+    r |= b;
+    x ^= b;
+  }
+  return r;
+}
+
+constexpr int kFusedMaxKeys = 24576;         // middle range held in LDS (96 KB)
+constexpr int kBmWords = kFusedMaxKeys / 32;  // words of a bitmap over the middle range
+static_assert(2 * kBmWords <= kHistBins, "two selection bitmaps in the histogram");
+static_assert(kFusedMaxKeys % 64 == 0, "whole 64-key chunks");
+// LDS scratch of the selection half beside the histogram: the second
+// threshold histogram, then the shared-set bitmap and two tie bitmaps
+constexpr int kTailScratchWords = 3 * kBmWords > kHistBins ? 3 * kBmWords : kHistBins;
+
+// x with the value of lane L replaced by the wave-uniform v.
+template <int L>
+__device__ __forceinline__ uint32_t put_lane(uint32_t x, uint32_t v) {
+  asm("v_writelane_b32 %0, %1, %2" : "+v"(x) : "s"(v), "i"(L));
+  return x;
+}
+
+// A value every lane of the wave holds, moved to a scalar register.
+__device__ __forceinline__ uint32_t wave_uniform(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
+}
+__device__ __forceinline__ uint64_t wave_uniform(uint64_t x) {
+  return (uint64_t)wave_uniform((uint32_t)x) | ((uint64_t)wave_uniform((uint32_t)(x >> 32)) << 32);
+}
+
+// Lanes of chunk c (middle indices 64c + lane) that lie below M.
+__device__ __forceinline__ uint64_t chunk_lanes(int c, int M) {
+  const int rem = M - (c << 6);
+  return rem >= 64 ? ~0ull : (rem <= 0 ? 0ull : (1ull << rem) - 1ull);
+}
+
+// Thresholds of the two selections as compare bounds: keys above G are
+// taken and keys in [E, G] are ties, of which `take` are taken in position
+// order (all when unbounded).  A selection's candidates are the keys at or
+// above C: C = E, except without ties taken (take = 0), where C = G + 1 (no
+// key at all when G is the largest key: cnone).  split: a bounded, nonzero
+// take, where the keys above G are kept apart.
+struct SelBounds {
+  uint32_t Gm, Cm, Gk, Ck;
+  bool cnone_m, cnone_k;
+};
+
+// Lane masks of chunk c's 64 keys (key of this lane in kv), kept in lane J
+// of the wave's registers: w[0..1] the top-m candidates, w[2..3] those of
+// k_b, and with SPLIT w[4..7] the keys above G of each.
+template <int J, bool SPLIT>
+__device__ __forceinline__ void chunk_masks(uint32_t kv, int c, int M, const SelBounds& sb,
+                                            uint32_t (&w)[8]) {
+  const uint64_t vm = chunk_lanes(c, M);
+  const uint64_t cm = __builtin_amdgcn_ballot_w64(kv >= sb.Cm) & (sb.cnone_m ? 0ull : vm);
+  const uint64_t ck = __builtin_amdgcn_ballot_w64(kv >= sb.Ck) & (sb.cnone_k ? 0ull : vm);
+  w[0] = put_lane<J>(w[0], (uint32_t)cm);
+  w[1] = put_lane<J>(w[1], (uint32_t)(cm >> 32));
+  w[2] = put_lane<J>(w[2], (uint32_t)ck);
+  w[3] = put_lane<J>(w[3], (uint32_t)(ck >> 32));
+  if (SPLIT) {
+    const uint64_t gtm = __builtin_amdgcn_ballot_w64(kv > sb.Gm) & vm;
+    const uint64_t gtk = __builtin_amdgcn_ballot_w64(kv > sb.Gk) & vm;
+    w[4] = put_lane<J>(w[4], (uint32_t)gtm);
+    w[5] = put_lane<J>(w[5], (uint32_t)(gtm >> 32));
+    w[6] = put_lane<J>(w[6], (uint32_t)gtk);
+    w[7] = put_lane<J>(w[7], (uint32_t)(gtk >> 32));
+  }
+}
+
+// Four chunks from J0 of block blk (chunks 16 blk + j), their loads first.
+template <int J0, bool SPLIT>
+__device__ __forceinline__ void chunk_masks4(const uint32_t* s_keys, int blk, int M, int lane,
+                                             const SelBounds& sb, uint32_t (&w)[8]) {
+  const int c = (blk << 4) + J0;
+  uint32_t kv[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) kv[u] = s_keys[min(((c + u) << 6) + lane, M - 1)];
+  chunk_masks<J0 + 0, SPLIT>(kv[0], c + 0, M, sb, w);
+  chunk_masks<J0 + 1, SPLIT>(kv[1], c + 1, M, sb, w);
+  chunk_masks<J0 + 2, SPLIT>(kv[2], c + 2, M, sb, w);
+  chunk_masks<J0 + 3, SPLIT>(kv[3], c + 3, M, sb, w);
+}
+
+// Four whole chunks from J0 of a block of 16 inside the middle range (keys
+// of this lane at kp[64 j]): candidates are the keys above Tm and Tk.
+template <int J0>
+__device__ __forceinline__ void chunk_masks4_inner(const uint32_t* kp, uint32_t Tm, uint32_t Tk,
+                                                   uint32_t (&w)[4]) {
+  uint32_t kv[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) kv[u] = kp[(J0 + u) << 6];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint64_t cm = __builtin_amdgcn_ballot_w64(kv[u] > Tm);
+    const uint64_t ck = __builtin_amdgcn_ballot_w64(kv[u] > Tk);
+    // lane J0 + u (the unrolled index is a constant)
+    switch (u) {
+      case 0:
+        w[0] = put_lane<J0 + 0>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 0>(w[1], (uint32_t)(cm >> 32));
+        w[2] = put_lane<J0 + 0>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 0>(w[3], (uint32_t)(ck >> 32));
+        break;
+      case 1:
+        w[0] = put_lane<J0 + 1>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 1>(w[1], (uint32_t)(cm >> 32));
+        w[2] = put_lane<J0 + 1>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 1>(w[3], (uint32_t)(ck >> 32));
+        break;
+      case 2:
+        w[0] = put_lane<J0 + 2>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 2>(w[1], (uint32_t)(cm >> 32));
+        w[2] = put_lane<J0 + 2>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 2>(w[3], (uint32_t)(ck >> 32));
+        break;
+      default:
+        w[0] = put_lane<J0 + 3>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 3>(w[1], (uint32_t)(cm >> 32));
+        w[2] = put_lane<J0 + 3>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 3>(w[3], (uint32_t)(ck >> 32));
+        break;
+    }
+  }
+}
+
+// The candidate and strict bitmaps of the middle range (words 2c, 2c + 1
+// for chunk c): wave w takes blocks of 16 chunks from block w in steps of
+// W; lane j collects chunk j's words, then lanes 0..15 store them.  With
+// `inner` (every tie or none taken, and no candidate bound at 0, so that
+// "above T" expresses each selection), blocks wholly inside the middle
+// range take the short path.
+template <int W, bool SPLIT>
+__device__ __forceinline__ void build_bitmaps(const uint32_t* s_keys, int M, int wave, int lane,
+                                              const SelBounds& sb, bool inner, uint32_t Tm,
+                                              uint32_t Tk, uint32_t* wm, uint32_t* wk,
+                                              uint32_t* wgm, uint32_t* wgk) {
+  const int nch = (M + 63) >> 6;
+  const int nblk = (nch + 15) >> 4;
+  for (int blk = wave; blk < nblk; blk += W) {
+    if (!SPLIT && inner && ((blk + 1) << 10) <= M) {
+      uint32_t w4[4] = {0u, 0u, 0u, 0u};
+      const uint32_t* kp = s_keys + (blk << 10) + lane;
+      chunk_masks4_inner<0>(kp, Tm, Tk, w4);
+      chunk_masks4_inner<4>(kp, Tm, Tk, w4);
+      chunk_masks4_inner<8>(kp, Tm, Tk, w4);
+      chunk_masks4_inner<12>(kp, Tm, Tk, w4);
+      if (lane < 16) {
+        ((uint2*)wm)[(blk << 4) + lane] = make_uint2(w4[0], w4[1]);
+        ((uint2*)wk)[(blk << 4) + lane] = make_uint2(w4[2], w4[3]);
+      }
+      continue;
+    }
+    uint32_t w8[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    chunk_masks4<0, SPLIT>(s_keys, blk, M, lane, sb, w8);
+    chunk_masks4<4, SPLIT>(s_keys, blk, M, lane, sb, w8);
+    chunk_masks4<8, SPLIT>(s_keys, blk, M, lane, sb, w8);
+    chunk_masks4<12, SPLIT>(s_keys, blk, M, lane, sb, w8);
+    const int c = (blk << 4) + lane;
+    if (lane < 16 && c < nch) {
+      ((uint2*)wm)[c] = make_uint2(w8[0], w8[1]);
+      ((uint2*)wk)[c] = make_uint2(w8[2], w8[3]);
+      if (SPLIT) {
+        ((uint2*)wgm)[c] = make_uint2(w8[4], w8[5]);
+        ((uint2*)wgk)[c] = make_uint2(w8[6], w8[7]);
+      }
+    }
+  }
 }
 
 // Whole refresh of one row in one workgroup, for many short rows: MFMA
@@ -1079,111 +1319,171 @@ __device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
 // histogram (key >> 21) in h: exact thresholds for the k_b and m largest,
 // one ordered compaction in position order (which also settles ties) into
 // top m, other winners and the anchor set, and with a shared-set output the
-// dilated shared set.  Reached by every thread of the workgroup.
+// dilated shared set.  h2: kTailScratchWords words of LDS scratch; res: 6
+// words.  Reached by every thread of the workgroup.
 template <int BLOCK>
 __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, uint32_t* s_keys,
-                                  uint32_t* h, uint32_t* scan, uint64_t* scan64, int* s_bin,
-                                  uint32_t* s_krem, uint32_t* s_cnt) {
-  const int tid = threadIdx.x;
+                                  uint32_t* h, uint32_t* h2, uint64_t* scan64, uint32_t* res) {
+  constexpr int W = BLOCK / 64;
+  static_assert(kHistBins % BLOCK == 0, "whole histogram bins per thread");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int M = rg.m;
   const int se = rg.sink_end;
   const uint32_t kout = (uint32_t)rg.kb;
   const long long kraw = a.k_den > 0 ? ((long long)a.k_num * rg.n0) / a.k_den : (long long)a.k;
   long long mm = a.dilate_m < 0 ? (kraw < 0 ? 0 : kraw) / 3 : a.dilate_m;
   const uint32_t m = (uint32_t)(mm > (long long)kout ? kout : mm);
-  // both searches start from the scoring histogram; each thread keeps its
-  // bins in registers while the first search reuses h
-  constexpr int kBinsPerThread = kHistBins / BLOCK;
-  static_assert(kHistBins % BLOCK == 0, "whole histogram bins per thread");
-  uint32_t h_keep[kBinsPerThread];
-#pragma unroll
-  for (int j = 0; j < kBinsPerThread; ++j) h_keep[j] = h[tid + j * BLOCK];
-  const KeyThreshold tm =
-      key_threshold<BLOCK>(s_keys, (uint32_t)M, m, h, h, scan, s_bin, s_krem, s_cnt);
-#pragma unroll
-  for (int j = 0; j < kBinsPerThread; ++j) h[tid + j * BLOCK] = h_keep[j];
-  lds_barrier();
-  const KeyThreshold tk =
-      key_threshold<BLOCK>(s_keys, (uint32_t)M, kout, h, h, scan, s_bin, s_krem, s_cnt);
-  // h becomes the bitmap of the dilated shared set over the middle indices
-  // (M <= 32 * kHistBins); the scan below orders the clearing before marking
+  KeyThreshold th[2];
+  key_threshold_pair<BLOCK>(s_keys, (uint32_t)M, m, kout, h, h2, scan64, res, th);
+  const KeyThreshold tm = th[0], tk = th[1];
+  // The selections as bitmaps over the middle indices (bit i % 32 of word
+  // i / 32 for middle index i), built a chunk of 64 keys per wave step from
+  // lane masks of the compares: a threshold (sh, p) splits the keys into
+  // those above G = (p << sh) | (2^sh - 1), the ties in [p << sh, G], and
+  // the rest.  Every tie is taken when take is unbounded, none when it is 0;
+  // otherwise the first `take` ties in position order (pass below).
   const bool shared = a.shared_idx != nullptr;
-  const int mwords = (M + 31) >> 5;
-  if (shared)
-    for (int i = tid; i < mwords; i += BLOCK) h[i] = 0u;
-  // ordered compaction: thread t owns middle indices [t*ept, (t+1)*ept); one
-  // scan of four 16-bit counts gives every thread its output offsets (the
-  // middle range is below 2^16 keys here).  ept is odd, so the lanes' LDS
-  // reads at stride ept fall in distinct banks.
-  const int ept = ((M + BLOCK - 1) / BLOCK) | 1;
-  const int i_begin = min(M, tid * ept), i_end = min(M, i_begin + ept);
-  uint32_t gm = 0, em = 0, gk = 0, ek = 0;
-  for (int i = i_begin; i < i_end; ++i) {
-    const uint32_t xm = s_keys[i] >> tm.sh, xk = s_keys[i] >> tk.sh;
-    gm += xm > tm.p ? 1u : 0u;
-    em += xm == tm.p ? 1u : 0u;
-    gk += xk > tk.p ? 1u : 0u;
-    ek += xk == tk.p ? 1u : 0u;
+  const int nwords = (M + 31) >> 5;
+  uint32_t* wm = h;                   // top m
+  uint32_t* wk = h + kBmWords;        // top k_b
+  uint32_t* wsh = h2;                 // dilated shared set
+  uint32_t* wgm = h2 + kBmWords;      // keys above the m threshold (split ties only)
+  uint32_t* wgk = h2 + 2 * kBmWords;  // keys above the k_b threshold (split ties only)
+  const uint32_t take_m = wave_uniform(tm.take), take_k = wave_uniform(tk.take);
+  const bool split_m = take_m != 0xFFFFFFFFu && take_m != 0u;
+  const bool split_k = take_k != 0xFFFFFFFFu && take_k != 0u;
+  SelBounds sb;
+  sb.Gm = wave_uniform((tm.p << tm.sh) | ((1u << tm.sh) - 1u));
+  sb.Gk = wave_uniform((tk.p << tk.sh) | ((1u << tk.sh) - 1u));
+  sb.Cm = take_m == 0u ? sb.Gm + 1u : wave_uniform(tm.p << tm.sh);
+  sb.Ck = take_k == 0u ? sb.Gk + 1u : wave_uniform(tk.p << tk.sh);
+  sb.cnone_m = take_m == 0u && sb.Gm == 0xFFFFFFFFu;
+  sb.cnone_k = take_k == 0u && sb.Gk == 0xFFFFFFFFu;
+  // "above T" forms: T = C - 1, or G where no tie is taken
+  const uint32_t Tm = take_m == 0u ? sb.Gm : sb.Cm - 1u, Tk = take_k == 0u ? sb.Gk : sb.Ck - 1u;
+  const bool inner = !split_m && !split_k && (take_m == 0u || sb.Cm > 0u) && (take_k == 0u || sb.Ck > 0u);
+  if (split_m || split_k)
+    build_bitmaps<W, true>(s_keys, M, wave, lane, sb, inner, Tm, Tk, wm, wk, wgm, wgk);
+  else
+    build_bitmaps<W, false>(s_keys, M, wave, lane, sb, inner, Tm, Tk, wm, wk, wgm, wgk);
+  lds_barrier();
+  // thread t owns words [t * wpt, (t + 1) * wpt)
+  const int wpt = (nwords + BLOCK - 1) / BLOCK;
+  const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
+  if (split_m || split_k) {
+    // split ties: keep the first `take` of them in position order
+    uint32_t em = 0, ek = 0;
+    for (int w = w_begin; w < w_end; ++w) {
+      if (split_m) em += (uint32_t)__popc(wm[w] & ~wgm[w]);
+      if (split_k) ek += (uint32_t)__popc(wk[w] & ~wgk[w]);
+    }
+    uint64_t tt;
+    const uint64_t pe = block_exclusive_scan<BLOCK, uint64_t>((uint64_t)em | ((uint64_t)ek << 32), scan64, &tt);
+    uint32_t rm = (uint32_t)pe, rk = (uint32_t)(pe >> 32);
+    for (int w = w_begin; w < w_end; ++w) {
+      if (split_m) {
+        const uint32_t eq = wm[w] & ~wgm[w];
+        wm[w] = wgm[w] | (uint32_t)lowest_bits(eq, take_m > rm ? take_m - rm : 0u);
+        rm += (uint32_t)__popc(eq);
+      }
+      if (split_k) {
+        const uint32_t eq = wk[w] & ~wgk[w];
+        wk[w] = wgk[w] | (uint32_t)lowest_bits(eq, take_k > rk ? take_k - rk : 0u);
+        rk += (uint32_t)__popc(eq);
+      }
+    }
+    lds_barrier();
+  }
+  const int r = a.dilate_r;
+  if (shared) {
+    // the winners and the +-r neighbours of the top m that stay in the
+    // middle range; radii below one word by shifts of neighbouring words
+    const uint32_t last = (M & 31) ? (1u << (M & 31)) - 1u : 0xFFFFFFFFu;
+    for (int w = w_begin; w < w_end; ++w) {
+      uint32_t acc = wk[w];
+      if (r < 32) {
+        const uint32_t c0 = wm[w], cp = w > 0 ? wm[w - 1] : 0u, cn = w + 1 < nwords ? wm[w + 1] : 0u;
+        for (int d = 1; d <= r; ++d) acc |= (c0 << d) | (cp >> (32 - d)) | (c0 >> d) | (cn << (32 - d));
+      }
+      wsh[w] = w == nwords - 1 ? acc & last : acc;
+    }
+    if (r >= 32) {
+      lds_barrier();
+      for (int w = w_begin; w < w_end; ++w) {
+        uint32_t bits = wm[w];
+        while (bits) {
+          const int i = (w << 5) + __ffs(bits) - 1;
+          bits &= bits - 1u;
+          const int lo = max(0, i - r), hi = min(M - 1, i + r);
+          for (int x = lo >> 5; x <= hi >> 5; ++x) {
+            const int b0 = max(lo - (x << 5), 0), b1 = min(hi - (x << 5), 31);
+            const uint32_t span = (b1 - b0 == 31) ? 0xFFFFFFFFu : (((1u << (b1 - b0 + 1)) - 1u) << b0);
+            atomicOr(&wsh[x], span);
+          }
+        }
+      }
+    }
+    lds_barrier();
+  }
+  // output offsets: one scan of four 16-bit counts per thread (top m, the
+  // other winners, all winners, the shared set), over 16-bit units of the
+  // bitmaps so that every wave takes part: thread t owns units
+  // [t * upt, (t + 1) * upt)
+  const int nunits = (M + 15) >> 4;
+  const int upt = (nunits + BLOCK - 1) / BLOCK;
+  const int u_begin = min(nunits, tid * upt), u_end = min(nunits, u_begin + upt);
+  uint32_t cm = 0, co = 0, ck = 0, cs = 0;
+  for (int u = u_begin; u < u_end; ++u) {
+    const int sh16 = (u & 1) << 4;
+    const uint32_t x = (wm[u >> 1] >> sh16) & 0xFFFFu, y = (wk[u >> 1] >> sh16) & 0xFFFFu;
+    cm += (uint32_t)__popc(x);
+    co += (uint32_t)__popc(y & ~x);
+    ck += (uint32_t)__popc(y);
+    if (shared) cs += (uint32_t)__popc((wsh[u >> 1] >> sh16) & 0xFFFFu);
   }
   uint64_t tot;
   const uint64_t pre = block_exclusive_scan<BLOCK, uint64_t>(
-      (uint64_t)gm | ((uint64_t)em << 16) | ((uint64_t)gk << 32) | ((uint64_t)ek << 48), scan64,
-      &tot);
-  uint32_t rm = (uint32_t)(pre >> 16) & 0xFFFFu, rk = (uint32_t)(pre >> 48) & 0xFFFFu;
-  // winners before this thread's range: strictly above plus the earlier ties taken
-  const uint32_t before_m = ((uint32_t)pre & 0xFFFFu) + min(rm, tm.take);
-  const uint32_t before_k = ((uint32_t)(pre >> 32) & 0xFFFFu) + min(rk, tk.take);
+      (uint64_t)cm | ((uint64_t)co << 16) | ((uint64_t)ck << 32) | ((uint64_t)cs << 48), scan64, &tot);
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
-  uint32_t oa = before_m, ob = m + (before_k - before_m), os = se + before_k;
-  for (int i = i_begin; i < i_end; ++i) {
-    const uint32_t key = s_keys[i];
-    const uint32_t xm = key >> tm.sh, xk = key >> tk.sh;
-    const bool in_m = xm > tm.p || (xm == tm.p && rm < tm.take);
-    const bool in_k = xk > tk.p || (xk == tk.p && rk < tk.take);
-    rm += xm == tm.p ? 1u : 0u;
-    rk += xk == tk.p ? 1u : 0u;
-    const int p = se + i;
-    if (in_m) {
-      if (oa < (uint32_t)a.k_cap) topk[oa] = p;
-      ++oa;
-    } else if (in_k) {
-      if (ob < (uint32_t)a.k_cap) topk[ob] = p;
-      ++ob;
-    }
-    if (in_k) {
-      if (os < (uint32_t)a.set_cap) out[os] = p;
-      ++os;
-    }
-    if (shared && in_k) {
-      // a top-m winner brings its +-r neighbours that stay in the middle range
-      const int lo = in_m ? max(0, i - a.dilate_r) : i;
-      const int hi = in_m ? min(M - 1, i + a.dilate_r) : i;
-      for (int j = lo; j <= hi; ++j) atomicOr(&h[j >> 5], 1u << (j & 31));
-    }
+  int32_t* shv = shared ? a.shared_idx + (size_t)row * a.set_cap : nullptr;
+  uint32_t oa = (uint32_t)pre & 0xFFFFu, ob = m + ((uint32_t)(pre >> 16) & 0xFFFFu);
+  uint32_t os = se + ((uint32_t)(pre >> 32) & 0xFFFFu), ss = se + (uint32_t)(pre >> 48);
+  const uint32_t kcap = (uint32_t)a.k_cap, scap = (uint32_t)a.set_cap;
+  for (int u = u_begin; u < u_end; ++u) {
+    const int base = se + (u << 4), sh16 = (u & 1) << 4;
+    const uint32_t x = (wm[u >> 1] >> sh16) & 0xFFFFu, y = (wk[u >> 1] >> sh16) & 0xFFFFu;
+    for (uint32_t bits = x; bits; bits &= bits - 1u, ++oa)
+      if (oa < kcap) topk[oa] = base + __ffs(bits) - 1;
+    for (uint32_t bits = y & ~x; bits; bits &= bits - 1u, ++ob)
+      if (ob < kcap) topk[ob] = base + __ffs(bits) - 1;
+    for (uint32_t bits = y; bits; bits &= bits - 1u, ++os)
+      if (os < scap) out[os] = base + __ffs(bits) - 1;
+    if (shared)
+      for (uint32_t bits = (wsh[u >> 1] >> sh16) & 0xFFFFu; bits; bits &= bits - 1u, ++ss)
+        if (ss < scap) shv[ss] = base + __ffs(bits) - 1;
   }
-  const uint32_t total_k = ((uint32_t)(tot >> 32) & 0xFFFFu) + min((uint32_t)(tot >> 48) & 0xFFFFu, tk.take);
-  for (int i = tid; i < se; i += BLOCK)
-    if (i < a.set_cap) out[i] = i;
-  int pos = se + (int)total_k;
+  const uint32_t total_k = (uint32_t)(tot >> 32) & 0xFFFFu;
+  const uint32_t total_s = (uint32_t)(tot >> 48);
   const int nw = rg.n0 - rg.win_start;
-  for (int i = tid; i < nw; i += BLOCK)
+  int pos = se + (int)total_k, pos2 = se + (int)total_s;
+  for (int i = tid; i < se; i += BLOCK) {
+    if (i < a.set_cap) out[i] = i;
+    if (shared && i < a.set_cap) shv[i] = i;
+  }
+  for (int i = tid; i < nw; i += BLOCK) {
     if (pos + i < a.set_cap) out[pos + i] = rg.win_start + i;
-  if (nw > 0) pos += nw;
+    if (shared && pos2 + i < a.set_cap) shv[pos2 + i] = rg.win_start + i;
+  }
+  if (nw > 0) {
+    pos += nw;
+    pos2 += nw;
+  }
   if (tid == 0) {
     a.topk_len[row] = (int32_t)kout;
     a.set_len[row] = pos < a.set_cap ? pos : a.set_cap;
-  }
-  if (shared) {
-    lds_barrier();
-    int32_t* sh = a.shared_idx + (size_t)row * a.set_cap;
-    for (int i = tid; i < se; i += BLOCK)
-      if (i < a.set_cap) sh[i] = i;
-    int pos2 = compact_bitmap<BLOCK>(h, mwords, se, sh, a.set_cap, se, scan);
-    for (int i = tid; i < nw; i += BLOCK)
-      if (pos2 + i < a.set_cap) sh[pos2 + i] = rg.win_start + i;
-    if (nw > 0) pos2 += nw;
-    if (tid == 0) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
+    if (shared) a.shared_len[row] = pos2 < a.set_cap ? pos2 : a.set_cap;
   }
 }
 
@@ -1192,13 +1492,13 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   constexpr int KS = D / 32;
   extern __shared__ uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
-  __shared__ uint32_t scan[BLOCK / 64 + 1];
   __shared__ uint64_t scan64[BLOCK / 64 + 1];
-  __shared__ int s_bin;
-  __shared__ uint32_t s_krem, s_cnt;
+  __shared__ uint32_t s_res[6];
   __shared__ int s_len[kBalanceMaxBatch];
   __shared__ int s_row;
   __shared__ u32x4_t s_kst[BLOCK / 64][16 * (D / 8)];
+  static_assert(sizeof(s_kst) >= kTailScratchWords * sizeof(uint32_t),
+                "the selection's scratch in the staging tiles");
   __shared__ int s_choice;
   const int row = fused_row(a, blockIdx.x, s_len, &s_row);
   if (a.gate_fused) {
@@ -1258,7 +1558,8 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
     }
   }
   __syncthreads();
-  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, scan, scan64, &s_bin, &s_krem, &s_cnt);
+  // the staging tiles are free now: they hold the selection's scratch
+  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, (uint32_t*)&s_kst[0][0], scan64, s_res);
 }
 
 // Selection of one row whose middle-range keys a scoring kernel (without
@@ -1272,10 +1573,9 @@ __global__ __launch_bounds__(BLOCK) void select_keyed(SelArgs a) {
   constexpr int kPer = 16;  // keys per thread per batch
   extern __shared__ uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
-  __shared__ uint32_t scan[BLOCK / 64 + 1];
+  __shared__ uint32_t h2[kTailScratchWords];
   __shared__ uint64_t scan64[BLOCK / 64 + 1];
-  __shared__ int s_bin;
-  __shared__ uint32_t s_krem, s_cnt;
+  __shared__ uint32_t s_res[6];
   const int row = blockIdx.x;
   if (row_skipped(a, row)) return;
   const RowGeom rg = row_geom(a, row / a.kv.hkv);
@@ -1302,14 +1602,12 @@ __global__ __launch_bounds__(BLOCK) void select_keyed(SelArgs a) {
     }
   }
   __syncthreads();
-  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, scan, scan64, &s_bin, &s_krem, &s_cnt);
+  fused_select_tail<BLOCK>(a, row, rg, s_keys, h, h2, scan64, s_res);
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-constexpr int kFusedMaxKeys = 24576;  // middle range held in LDS (96 KB)
 constexpr int kLdsBytes = 160 * 1024;  // LDS of one CU
-static_assert(kFusedMaxKeys <= 32 * kHistBins, "the shared-set bitmap reuses the histogram");
 
 }  // namespace
 

@@ -412,6 +412,22 @@ def test_select_shared_bit_exact(name, dtype, d, paged, hq, hkv, lens, pk):
         check_select_shared(inp, lens, B.params(refresh_every=4, **pk, **var))
 
 
+WIDE_DILATION_CASES = [c for c in SELECT_CASES
+                       if c[0] in ("ragged-gqa", "fused-ragged", "fused-mha-d64", "keyed-128-rows",
+                                   "radix-ragged-gqa")]
+
+
+@pytest.mark.parametrize("r", [31, 32, 40, 63, 64, 70])
+@pytest.mark.parametrize("name,dtype,d,paged,hq,hkv,lens,pk", WIDE_DILATION_CASES,
+                         ids=[c[0] for c in WIDE_DILATION_CASES])
+def test_select_shared_wide_dilation(name, dtype, d, paged, hq, hkv, lens, pk, r):
+    """Dilation radii around one and two bitmap words (neighbours that reach
+    past the next 32 and 64 middle positions)."""
+    inp = synth.random_inputs(len(lens), hq, hkv, d, lens, dtype=dtype, paged=paged,
+                              seed=7 + r, grid=True, device=DEV)
+    check_select_shared(inp, lens, B.params(refresh_every=4, **pk, dilate_r=r, dilate_m=25))
+
+
 def test_select_shared_window_zero_edges():
     # no window: a top-m winner at the last middle position has its right
     # neighbour at n0, outside [0, n0); a winner at the first has its left
