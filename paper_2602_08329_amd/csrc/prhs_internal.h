@@ -76,6 +76,39 @@ __host__ __device__ __forceinline__ int psaw_first_visible(double f, int sink, i
   return se > P - 1 ? se : P - 1;
 }
 
+// Length rank of workgroup w of a grid of U workgroups placed on C CUs, when
+// the workgroups w = c, c + C, c + 2C, ... run side by side on CU c (the
+// order in which this chip fills its CUs when they all fit at once): rounds
+// of C ranks, every other round reversed, so that the units of one CU pair
+// long with short.  A permutation of [0, U).
+__host__ __device__ __forceinline__ int serpentine_rank(int w, int C, int U) {
+  const int k = w / C, c = w - k * C;
+  const int p = min(C, U - k * C);  // workgroups in this round
+  return k * C + ((k & 1) ? p - 1 - c : c);
+}
+
+// Unit b * heads + h of length rank t (0 = longest): sequences ordered by
+// decreasing cached length, ties by index; the heads of a sequence share its
+// length and take consecutive ranks.  s_len holds kv.batch ints of LDS,
+// s_out one.  Every thread of the workgroup must call it.
+__device__ __forceinline__ int unit_of_length_rank(const KvView& kv, int heads, int t, int* s_len,
+                                                   int* s_out) {
+  const int B = kv.batch, tb = t / heads;
+  for (int b = threadIdx.x; b < B; b += blockDim.x) s_len[b] = kv_seq_len(kv, b);
+  __syncthreads();
+  for (int b = threadIdx.x; b < B; b += blockDim.x) {
+    const int nb = s_len[b];
+    int r = 0;
+    for (int b2 = 0; b2 < B; ++b2) {
+      const int n2 = s_len[b2];
+      r += (n2 > nb || (n2 == nb && b2 < b)) ? 1 : 0;
+    }
+    if (r == tb) *s_out = b * heads + (t - tb * heads);
+  }
+  __syncthreads();
+  return *s_out;
+}
+
 // Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
 // -0.0 is mapped like +0.0.
 __device__ __forceinline__ uint32_t score_key(float f) {

@@ -88,6 +88,7 @@ struct SelArgs {
   int32_t* shared_idx;  // optional [rows][set_cap]: the dilated shared set at n0
   int32_t* shared_len;
   int balance_cus;      // fused refresh: > 0 = CU count to balance rows over, 0 = off
+  int balance_serpentine;  // with balance_cus: workgroups share CUs side by side
   const int32_t* row_choice;  // optional [rows]: rows with an entry >= 0 are left untouched
   int gate_fused;       // fused refresh: wave 0 takes the similarity gate of its row first
   GateLaunch gate;      // (with gate_fused) and the workgroup selects only a retrieving row
@@ -1297,21 +1298,10 @@ __device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
   const int ncu = a.balance_cus;
   const int B = a.kv.batch, H = a.kv.hkv, rows = B * H;
   if (ncu <= 0 || rows <= ncu || B > kBalanceMaxBatch) return w;
-  const int t = w;  // target length rank
-  const int tb = t / H;
-  for (int b = threadIdx.x; b < B; b += blockDim.x) s_len[b] = kv_seq_len(a.kv, b);
-  __syncthreads();
-  for (int b = threadIdx.x; b < B; b += blockDim.x) {
-    const int nb = s_len[b];
-    int r = 0;
-    for (int b2 = 0; b2 < B; ++b2) {
-      const int n2 = s_len[b2];
-      r += (n2 > nb || (n2 == nb && b2 < b)) ? 1 : 0;
-    }
-    if (r == tb) *s_row = b * H + (t - tb * H);
-  }
-  __syncthreads();
-  return *s_row;
+  // one workgroup per CU: later workgroups start as earlier ones finish, so
+  // rank order is longest first; several per CU side by side: serpentine
+  const int t = a.balance_serpentine ? serpentine_rank(w, ncu, rows) : w;
+  return unit_of_length_rank(a.kv, H, t, s_len, s_row);
 }
 
 // Selection half of the fused refresh, after the row's middle-range keys
@@ -1726,6 +1716,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.shared_idx = s.shared_idx;
   a.shared_len = s.shared_len;
   a.balance_cus = 0;
+  a.balance_serpentine = 0;
   a.row_choice = s.row_choice;
   a.gate_fused = 0;
 
@@ -1768,6 +1759,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
       if (ea != hipSuccess) return ea;
       wide = fa.sharedSizeBytes + dyn <= (size_t)kLdsBytes;
     }
+    a.balance_serpentine = wide ? 0 : 1;
     hipError_t e = hipSuccess;
 #define PRHS_FUSED_LAUNCH(DV, BL)                                                           \
   {                                                                                         \

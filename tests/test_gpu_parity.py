@@ -152,6 +152,31 @@ def test_sparse_attention_oracle_sets(dtype, d, paged, hq, hkv, lens):
                          f"b{b} g{g} |S|={len(S)}")
 
 
+@pytest.mark.parametrize("paged", [False, True])
+def test_sparse_attention_more_units_than_cus(paged):
+    """More unsplit units than CUs (several workgroups per CU), with varied
+    lengths and set sizes: every unit's output lands in its own place."""
+    lens = tuple(100 + (i * 379) % 1100 for i in range(150))
+    hq, hkv = 8, 2
+    inp = synth.random_inputs(len(lens), hq, hkv, 128, lens, paged=paged, seed=91,
+                              grid=False, key_scale=1.5, device=DEV)
+    rng = np.random.default_rng(11)
+    sets = {}
+    for b, n in enumerate(lens):
+        for g in range(hkv):
+            size = int(rng.integers(1, min(n, 400) + 1))
+            sets[(b, g)] = sorted(rng.choice(n, size=size, replace=False).tolist())
+    y, lse = run_sparse(inp, lens, sets, 400)
+    gq = hq // hkv
+    for (b, g), S in sets.items():
+        K, V = synth.gather_unit(inp, 0, b, g, lens[b])
+        Qg = synth.query_group(inp, 0, 0, b, g)
+        for j in range(gq):
+            yr, lr = O.sparse_attention(Qg[j], K, V, S)
+            assert_close(y[b, g * gq + j], lse[b, g * gq + j], yr, lr, TOL["bf16"],
+                         f"b{b} g{g} |S|={len(S)}")
+
+
 @pytest.mark.parametrize("dtype,set_cap", [("bf16", 512), ("bf16", 513), ("f32", 512), ("f32", 513)])
 def test_sparse_attention_unsplit_boundary(dtype, set_cap):
     """Sets of at most 512 rows per unit run in one launch without a merge,
