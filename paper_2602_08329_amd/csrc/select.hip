@@ -1283,15 +1283,17 @@ __device__ __forceinline__ void build_bitmaps(const uint32_t* s_keys, int M, int
 
 // Whole refresh of one row in one workgroup, for many short rows: MFMA
 // scores of the middle range into LDS as order-preserving keys with their
-// level-0 histogram, exact thresholds for the k_b and m largest, and one
-// ordered compaction in position order (the key array is already in position
-// order, which also settles ties): top m, other winners, anchor set.
+// level-0 histogram, then the selection half below (exact thresholds for
+// the k_b and m largest, the selections as position-ordered bitmaps, which
+// also settle ties): top m, other winners, anchor set, shared set.
 // Contiguous bf16 caches whose middle range fits LDS.
 // Row of fused-refresh workgroup w when there are more rows than CUs: rows
-// in order of decreasing length, so the workgroups that start last, as
-// earlier ones finish, carry the shortest rows (longest-first scheduling).
-// Sequences rank by length, ties by index; all kv heads of a sequence have
-// its length.  A mapping only: every row is taken exactly once.
+// by decreasing length.  One workgroup per CU: the workgroups that start
+// last, as earlier ones finish, carry the shortest rows (longest-first
+// scheduling); several side by side on a CU: serpentine ranks pair long
+// rows with short ones.  Sequences rank by length, ties by index; all kv
+// heads of a sequence have its length.  A mapping only: every row is taken
+// exactly once.
 constexpr int kBalanceMaxBatch = 256;
 
 __device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
@@ -1307,10 +1309,11 @@ __device__ int fused_row(const SelArgs& a, int w, int* s_len, int* s_row) {
 // Selection half of the fused refresh, after the row's middle-range keys
 // (order-preserving u32, position order) are in s_keys and their level-0
 // histogram (key >> 21) in h: exact thresholds for the k_b and m largest,
-// one ordered compaction in position order (which also settles ties) into
-// top m, other winners and the anchor set, and with a shared-set output the
-// dilated shared set.  h2: kTailScratchWords words of LDS scratch; res: 6
-// words.  Reached by every thread of the workgroup.
+// the selections as bitmaps over the middle positions (whose order settles
+// ties), and from them the top m, the other winners, the anchor set and,
+// with a shared-set output, the dilated shared set.  h2: kTailScratchWords
+// words of LDS scratch; res: 6 words.  Reached by every thread of the
+// workgroup.
 template <int BLOCK>
 __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, uint32_t* s_keys,
                                   uint32_t* h, uint32_t* h2, uint64_t* scan64, uint32_t* res) {
