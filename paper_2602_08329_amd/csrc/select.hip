@@ -71,6 +71,8 @@ struct SelArgs {
   int sortcap;         // LDS sort buffer entries of select_finish (>= selcap)
   int stagecap;        // LDS output staging entries of select_finish
   int woff;            // select_finish has LDS for per-word output offsets
+  int seg_bits;        // select_finish: positions per bitmap segment (a multiple of 32)
+  int seg_shift;       // select_finish: one segment, the dilation by shifts of the top-m bitmap
   uint32_t* keys;      // [rows][mcap]
   uint32_t* hist0;     // [rows][2048]
   uint32_t* hist1;     // [rows][2048]
@@ -488,6 +490,19 @@ __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   }
 }
 
+// Whether bitmap bm has a set bit at any position in [lo, hi).
+__device__ __forceinline__ bool any_bits(const uint32_t* bm, int lo, int hi) {
+  if (lo >= hi) return false;
+  const int w0 = lo >> 5, w1 = (hi - 1) >> 5;
+  for (int w = w0; w <= w1; ++w) {
+    uint32_t m = bm[w];
+    if (w == w0) m &= ~0u << (lo & 31);
+    if (w == w1) m &= 0xFFFFFFFFu >> (31 - ((hi - 1) & 31));
+    if (m) return true;
+  }
+  return false;
+}
+
 __device__ __forceinline__ uint32_t coherent_load(uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -798,14 +813,20 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   // range fall in the sink, the window or outside [0, n0).
   const bool shared = a.shared_idx != nullptr;
   const int r = a.dilate_r;
-  const int seg_bits = kFinishSegBits;
-  constexpr int kSegW = kFinishSegBits / 32;
+  const int seg_bits = a.seg_bits;
+  const int segw = seg_bits >> 5;
+  // With seg_shift the middle range is one segment and the neighbours of the
+  // top m come from shifts of its bitmap (r < 32), so there is no third
+  // bitmap.
+  const bool shiftd = a.seg_shift != 0;
   uint32_t* bw = (uint32_t*)(dyn + a.sortcap);
-  uint32_t* bt = bw + kSegW;
-  uint32_t* bd = bt + kSegW;
-  // optional per-word output offsets [kSegW], then the output staging
-  uint64_t* woff = a.woff ? (uint64_t*)(bd + kSegW + 1) : nullptr;
-  int32_t* stage = a.woff ? (int32_t*)(woff + kSegW) : (int32_t*)(bd + kSegW);  // a.stagecap entries
+  uint32_t* bt = bw + segw;
+  uint32_t* bd = shiftd ? nullptr : bt + segw;
+  uint32_t* bend = bt + (shiftd ? 1 : 2) * segw;
+  // optional per-word output offsets [segw] (8-byte aligned: bw is), then
+  // the output staging
+  uint64_t* woff = a.woff ? (uint64_t*)(bend + ((bend - bw) & 1)) : nullptr;
+  int32_t* stage = a.woff ? (int32_t*)(woff + segw) : (int32_t*)bend;  // a.stagecap entries
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
   int32_t* sh = shared ? a.shared_idx + (size_t)row * a.set_cap : nullptr;
@@ -819,12 +840,22 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   for (int seg_lo = rg.sink_end; seg_lo < rg.win_start; seg_lo += seg_bits) {
     const int seg_hi = min(rg.win_start, seg_lo + seg_bits);
     const int nwords = (seg_hi - seg_lo + 31) >> 5;
+    const uint32_t lastw = ((seg_hi - seg_lo) & 31) ? (1u << ((seg_hi - seg_lo) & 31)) - 1u : ~0u;
     for (int w = tid; w < nwords; w += kFinishBlock) {
       bw[w] = 0u;
       bt[w] = 0u;
-      bd[w] = 0u;
+      if (!shiftd) bd[w] = 0u;
     }
     lds_barrier();
+    // the dilation-only neighbours D of word w: marked, or shifted from the
+    // top-m words around it
+    auto dil = [&](int w) -> uint32_t {
+      if (!shiftd) return bd[w];
+      const uint32_t c0 = bt[w], cp = w > 0 ? bt[w - 1] : 0u, cn = w + 1 < nwords ? bt[w + 1] : 0u;
+      uint32_t acc = 0u;
+      for (int d = 1; d <= r; ++d) acc |= (c0 << d) | (cp >> (32 - d)) | (c0 >> d) | (cn << (32 - d));
+      return w == nwords - 1 ? acc & lastw : acc;
+    };
     for (uint32_t i = tid; i < total; i += kFinishBlock) {
       const uint64_t x = dyn[i];
       if (x < c_k) continue;
@@ -834,24 +865,56 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
         mark_bit(bw, seg_lo, p);
         if (top) mark_bit(bt, seg_lo, p);
       }
-      if (shared && top) {
+      if (shared && top && !shiftd) {
         const int lo = max(p - r, seg_lo), hi = min(p + r, seg_hi - 1);
         for (int q = lo; q <= hi; ++q) mark_bit(bd, seg_lo, q);
       }
     }
     __syncthreads();
-    // thread t owns words [t*wpt, (t+1)*wpt); a segment holds fewer than
-    // 2^16 positions, so each packed 16-bit count fits
-    const int wpt = (nwords + kFinishBlock - 1) / kFinishBlock;
-    const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
-    uint64_t cnt = 0;
-    for (int w = w_begin; w < w_end; ++w) {
-      const uint32_t W = bw[w], T = bt[w], S = W | bd[w];
-      cnt += (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
+    // Packed counts of a word's top m, other winners, all winners and shared
+    // set; each 16-bit field of a segment's totals fits (fewer than 2^16
+    // positions, or the host's bound on the outputs of one segment).
+    auto word_counts = [&](int w) -> uint64_t {
+      const uint32_t W = bw[w], T = bt[w], S = W | (shared ? dil(w) : 0u);
+      return (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
              ((uint64_t)__popc(W) << 32) | ((uint64_t)__popc(S) << 48);
+    };
+    const int wpt = (nwords + kFinishBlock - 1) / kFinishBlock;
+    const int lane = tid & 63, wv = tid >> 6;
+    const int wbase = wv * 64 * wpt;  // with woff: wave wv's words, lane l at wbase + 64 j + l
+    // without woff: thread t owns words [t*wpt, (t+1)*wpt)
+    const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
+    uint64_t tot = 0, off = 0;
+    if (woff) {
+      // every word's output offsets, in word order: a wave scan per row of
+      // 64 consecutive words (conflict-free LDS reads), then one scan of the
+      // waves' totals
+      uint64_t carry = 0;
+      for (int j = 0; j < wpt; ++j) {
+        const int w = wbase + 64 * j + lane;
+        const uint64_t c = w < nwords ? word_counts(w) : 0u;
+        const uint64_t inc = wave_inclusive_scan(c);
+        if (w < nwords) woff[w] = carry + inc - c;
+        carry += (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)inc, 63) |
+                 ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(inc >> 32), 63) << 32);
+      }
+      if (lane == 0) scan64[wv] = carry;
+      lds_barrier();
+      uint64_t before = 0;
+      for (int v = 0; v < kFinishBlock / 64; ++v) {
+        const uint64_t x = scan64[v];
+        before += v < wv ? x : 0u;
+        tot += x;
+      }
+      for (int j = 0; j < wpt; ++j) {
+        const int w = wbase + 64 * j + lane;
+        if (w < nwords) woff[w] += before;
+      }
+    } else {
+      uint64_t cnt = 0;
+      for (int w = w_begin; w < w_end; ++w) cnt += word_counts(w);
+      off = block_exclusive_scan<kFinishBlock, uint64_t>(cnt, scan64, &tot);
     }
-    uint64_t tot;
-    const uint64_t off = block_exclusive_scan<kFinishBlock, uint64_t>(cnt, scan64, &tot);
     // the segment's outputs: top m, other winners, anchor set, shared set
     const int n_t = (int)(tot & 0xFFFFu), n_r = (int)((tot >> 16) & 0xFFFFu);
     const int n_w = (int)((tot >> 32) & 0xFFFFu), n_s = shared ? (int)(tot >> 48) : 0;
@@ -870,15 +933,8 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       // Per-entry writes: with each word's output offsets in LDS, every
       // winner places itself (word offset + set bits below it), so clustered
       // winners do not serialise on the thread owning their words; the
-      // dilation-only positions of the shared set, sparse by comparison,
-      // are walked per word.
-      uint64_t run = off;
-      for (int w = w_begin; w < w_end; ++w) {
-        woff[w] = run;
-        const uint32_t W = bw[w], T = bt[w], S = W | bd[w];
-        run += (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
-               ((uint64_t)__popc(W) << 32) | ((uint64_t)__popc(S) << 48);
-      }
+      // dilation-only positions of the shared set are placed by the top-m
+      // winners that reach them (shifted dilation) or walked per word.
       lds_barrier();
       for (uint32_t i = tid; i < total; i += kFinishBlock) {
         const uint64_t x = dyn[i];
@@ -899,13 +955,29 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
         const int jw = (int)((o >> 32) & 0xFFFFu) + __popc(W & below);
         if (jw < lim_w) dw[jw] = p;
         if (shared) {
-          const int js = (int)(o >> 48) + __popc((W | bd[w]) & below);
+          const int js = (int)(o >> 48) + __popc((W | dil(w)) & below);
           if (js < lim_s) ds[js] = p;
         }
+        if (shared && shiftd && x >= c_m) {
+          // the dilation-only neighbours of this top-m winner that no lower
+          // top-m winner reaches (each is written by the lowest one in reach)
+          for (int d = -r; d <= r; ++d) {
+            const int q = rel + d;
+            if (d == 0 || q < 0 || q >= seg_hi - seg_lo) continue;
+            const int wq = q >> 5;
+            const uint32_t bq = 1u << (q & 31);
+            const uint32_t Wq = bw[wq];
+            if ((Wq & bq) || any_bits(bt, max(0, q - r), rel)) continue;
+            const int js = (int)(woff[wq] >> 48) + __popc((Wq | dil(wq)) & (bq - 1u));
+            if (js < lim_s) ds[js] = seg_lo + q;
+          }
+        }
       }
-      if (shared) {
-        for (int w = w_begin; w < w_end; ++w) {
-          const uint32_t W = bw[w], S = W | bd[w];
+      if (shared && !shiftd) {
+        for (int j = 0; j < wpt; ++j) {
+          const int w = wbase + 64 * j + lane;
+          if (w >= nwords) continue;
+          const uint32_t W = bw[w], S = W | dil(w);
           uint32_t bits = S & ~W;
           const int js0 = (int)(woff[w] >> 48);
           while (bits) {
@@ -921,7 +993,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       int ow = (int)((off >> 32) & 0xFFFFu), os = (int)(off >> 48);
       for (int w = w_begin; w < w_end; ++w) {
         const uint32_t W = bw[w], T = bt[w];
-        uint32_t bits = shared ? (W | bd[w]) : W;
+        uint32_t bits = shared ? (W | dil(w)) : W;
         const int base = seg_lo + (w << 5);
         while (bits) {
           const int bit = __ffs(bits) - 1;
@@ -1720,6 +1792,8 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   a.shared_len = s.shared_len;
   a.balance_cus = 0;
   a.balance_serpentine = 0;
+  a.seg_bits = kFinishSegBits;
+  a.seg_shift = 0;
   a.row_choice = s.row_choice;
   a.gate_fused = 0;
 
@@ -1827,18 +1901,47 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
                ? (long long)fa.sharedSizeBytes : -1LL;
   }();
   if (finish_static < 0) return hipErrorInvalidDeviceFunction;
-  const long long avail = (long long)kLdsBytes - finish_static - 3LL * kFinishSegBits / 8;
-  long long cap = (long long)a.selcap + kFinishTies;
-  if (cap > avail / 8) cap = avail / 8;
-  if (cap < a.selcap) return hipErrorInvalidValue;  // unreachable for k_b <= PRHS_MAX_TOPK
-  a.sortcap = (int)cap;
-  long long rest = avail - cap * 8;
-  constexpr long long kWoffBytes = (kFinishSegBits / 32 + 1) * 8LL;  // with 4 bytes of alignment
-  a.woff = rest >= kWoffBytes ? 1 : 0;
-  if (a.woff) rest -= kWoffBytes;
-  a.stagecap = (int)(rest / 4 < kFinishStage ? rest / 4 : kFinishStage);
-  const size_t dyn = (size_t)a.sortcap * 8 + 3 * kFinishSegBits / 8 + (a.woff ? kWoffBytes : 0) +
-                     (size_t)a.stagecap * 4;
+  // LDS plan for segments of seg_bits positions with nbm bitmaps each
+  struct FinishPlan {
+    int sortcap, woff, stagecap;
+    size_t dyn;
+  };
+  auto plan = [&](long long seg_bits, long long nbm, FinishPlan* fp) {
+    const long long bm_bytes = nbm * seg_bits / 8;
+    const long long avail = (long long)kLdsBytes - finish_static - bm_bytes;
+    long long cap = (long long)a.selcap + kFinishTies;
+    if (cap > avail / 8) cap = avail / 8;
+    if (cap < a.selcap) return false;
+    long long rest = avail - cap * 8;
+    const long long woff_bytes = seg_bits / 32 * 8 + 4;  // with 4 bytes of alignment
+    fp->sortcap = (int)cap;
+    fp->woff = rest >= woff_bytes ? 1 : 0;
+    if (fp->woff) rest -= woff_bytes;
+    fp->stagecap = (int)(rest / 4 < kFinishStage ? rest / 4 : kFinishStage);
+    fp->dyn = (size_t)(cap * 8 + bm_bytes + (fp->woff ? woff_bytes : 0) + (long long)fp->stagecap * 4);
+    return true;
+  };
+  // the whole middle range as one segment when its outputs keep the packed
+  // counts below 2^16 (at most max_topk winners, each with at most 2r
+  // neighbours), the radius is below a word (the neighbours then come from
+  // shifts of the top-m bitmap, two bitmaps instead of three) and the full
+  // tie buffer and the per-word offsets still fit LDS
+  FinishPlan fp{};
+  const long long one_bits = ((long long)a.mcap + 31) / 32 * 32;
+  bool one = s.dilate_r < 32 && (long long)a.selcap * (2LL * s.dilate_r + 1) < 65536 &&
+             plan(one_bits, 2, &fp) && fp.sortcap == a.selcap + kFinishTies && fp.woff;
+  if (one) {
+    a.seg_bits = (int)one_bits;
+    a.seg_shift = 1;
+  } else {
+    if (!plan(kFinishSegBits, 3, &fp)) return hipErrorInvalidValue;  // unreachable for k_b <= PRHS_MAX_TOPK
+    a.seg_bits = kFinishSegBits;
+    a.seg_shift = 0;
+  }
+  a.sortcap = fp.sortcap;
+  a.woff = fp.woff;
+  a.stagecap = fp.stagecap;
+  const size_t dyn = fp.dyn;
   if (dyn > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)select_finish,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
