@@ -157,7 +157,7 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan(uint64_t x) {
 // the block total in *total.  Must be reached by every thread.  With T =
 // uint64_t, several narrow counters packed into one word scan together as
 // long as no field overflows (and none straddles bit 32).
-template <int BLOCK, typename T = uint32_t>
+template <int BLOCK, typename T = uint32_t, bool REUSE_BARRIER = true>
 __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
   constexpr int W = BLOCK / 64;
   const int lane = threadIdx.x & 63;
@@ -174,7 +174,9 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T* scratch, T* total) {
     tot += s;
   }
   *total = tot;
-  lds_barrier();  // scratch may be written again after return
+  // scratch may be written again after return (without REUSE_BARRIER the
+  // caller reaches a barrier before it writes scratch again)
+  if (REUSE_BARRIER) lds_barrier();
   return before + x - v;
 }
 

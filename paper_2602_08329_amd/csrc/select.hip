@@ -1090,7 +1090,8 @@ __device__ void find_threshold_pair(const uint32_t* ha, const uint32_t* hb, uint
     lb += hb[bin];
   }
   uint64_t total;
-  const uint64_t cum = block_exclusive_scan<BLOCK, uint64_t>(
+  // the barrier below comes before scan64 is written again
+  const uint64_t cum = block_exclusive_scan<BLOCK, uint64_t, false>(
       (uint64_t)la | ((uint64_t)lb << 32), scan64, &total);
   uint32_t ca = (uint32_t)cum, cb = (uint32_t)(cum >> 32);
 #pragma unroll
@@ -1147,14 +1148,24 @@ __device__ void key_threshold_pair(const uint32_t* keys, uint32_t n, uint32_t ka
         if (live[1]) h2[i] = 0u;
       }
       lds_barrier();
-      // four keys per thread in flight (reads clamped into the array)
-      for (uint32_t i0 = tid; i0 < n; i0 += 4 * BLOCK) {
+      // four consecutive keys per thread and read (16-byte LDS reads of
+      // consecutive lanes; the array is 16-byte aligned), the last partial
+      // group element by element
+      for (uint32_t i0 = 4 * tid; i0 < n; i0 += 4 * BLOCK) {
         uint32_t kv[4];
+        if (i0 + 4 <= n) {
+          const uint4 v = *(const uint4*)(keys + i0);
+          kv[0] = v.x;
+          kv[1] = v.y;
+          kv[2] = v.z;
+          kv[3] = v.w;
+        } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) kv[u] = keys[min(i0 + u * BLOCK, n - 1)];
+          for (int u = 0; u < 4; ++u) kv[u] = keys[min(i0 + u, n - 1)];
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const bool in = i0 + u * BLOCK < n;
+          const bool in = i0 + u < n;
           const uint32_t x = kv[u] >> psh, d = (kv[u] >> sh) & dmask;
           if (in && x == pa) atomicAdd(&h[d], 1u);
           if (in && x == pb) atomicAdd(&h2[d], 1u);
@@ -1555,7 +1566,7 @@ __device__ void fused_select_tail(const SelArgs& a, int row, const RowGeom& rg, 
 template <int D, int BLOCK>
 __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
   constexpr int KS = D / 32;
-  extern __shared__ uint32_t s_keys[];  // [middle length]
+  extern __shared__ __attribute__((aligned(16))) uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
   __shared__ uint64_t scan64[BLOCK / 64 + 1];
   __shared__ uint32_t s_res[6];
@@ -1636,7 +1647,7 @@ __global__ __launch_bounds__(BLOCK) void select_fused(SelArgs a) {
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void select_keyed(SelArgs a) {
   constexpr int kPer = 16;  // keys per thread per batch
-  extern __shared__ uint32_t s_keys[];  // [middle length]
+  extern __shared__ __attribute__((aligned(16))) uint32_t s_keys[];  // [middle length]
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t h2[kTailScratchWords];
   __shared__ uint64_t scan64[BLOCK / 64 + 1];
