@@ -463,9 +463,14 @@ __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   uint32_t total;
   const uint32_t pre = block_exclusive_scan<kFilterBlock>(packed, scan, &total);
   uint32_t* cnt = a.counters + row * 4;
-  if (tid == 0) {
-    s_base[0] = (total >> 16) ? atomicAdd(&cnt[0], total >> 16) : 0u;
-    s_base[1] = (total & 0xFFFFu) ? atomicAdd(&cnt[1], total & 0xFFFFu) : 0u;
+  if (tid == 0 && total != 0u) {
+    // both list offsets in one 64-bit atomic: cnt[0] (selected) is the low
+    // word, cnt[1] (candidates) the high one; neither count reaches 2^32
+    const unsigned long long add =
+        (unsigned long long)(total >> 16) | ((unsigned long long)(total & 0xFFFFu) << 32);
+    const unsigned long long old = atomicAdd((unsigned long long*)cnt, add);
+    s_base[0] = (uint32_t)old;
+    s_base[1] = (uint32_t)(old >> 32);
   }
   __syncthreads();
   uint32_t ot = s_base[0] + (pre >> 16), ok = s_base[1] + (pre & 0xFFFFu);
