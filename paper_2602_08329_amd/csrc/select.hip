@@ -169,10 +169,14 @@ __device__ void find_threshold(const uint32_t* h, uint32_t kk, uint32_t* scan, i
   lds_barrier();
 }
 
+// Adds an LDS histogram (8-byte aligned) into a global one, two bins per
+// 64-bit atomic (a bin's count stays below 2^32, so no carry crosses into
+// its neighbour), skipping empty pairs.
 __device__ __forceinline__ void flush_hist(const uint32_t* h, uint32_t* dst) {
-  for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
-    const uint32_t c = h[i];
-    if (c) atomicAdd(&dst[i], c);
+  for (int i = threadIdx.x; i < kHistBins / 2; i += blockDim.x) {
+    const uint2 c = ((const uint2*)h)[i];
+    if (c.x | c.y)
+      atomicAdd((unsigned long long*)dst + i, (unsigned long long)c.x | ((unsigned long long)c.y << 32));
   }
 }
 
@@ -292,7 +296,7 @@ __device__ __forceinline__ void score_consume(const ScoreStep<D, SUB>& S, const 
 template <int D, bool PAGED, bool HIST>
 __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(4))) void score_bf16(SelArgs a) {
   constexpr int KS = D / 32;
-  __shared__ uint32_t hist[kHistBins];
+  __shared__ __attribute__((aligned(8))) uint32_t hist[kHistBins];
   __shared__ int32_t s_page[kScoreChunk + 1];
   __shared__ u32x4_t s_kst[kScoreBlock / 64][16 * (D / 8)];
   const int row = blockIdx.y;
@@ -368,7 +372,7 @@ __global__ __launch_bounds__(kScoreBlock) __attribute__((amdgpu_waves_per_eu(4))
 // staged in LDS, sequential fp32 fused multiply-adds over d.
 template <int D, bool HIST>
 __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
-  __shared__ uint32_t hist[kHistBins];
+  __shared__ __attribute__((aligned(8))) uint32_t hist[kHistBins];
   __shared__ float qs[16 * D];
   const int row = blockIdx.y;
   if (row_skipped(a, row)) return;
@@ -416,7 +420,7 @@ __global__ __launch_bounds__(kScoreBlock) void score_f32(SelArgs a) {
 // Each thread holds 16 keys; one workgroup prefix sum and one atomic per
 // output list place them.
 __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
-  __shared__ uint32_t h[kHistBins];
+  __shared__ __attribute__((aligned(8))) uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFilterBlock / 64 + 1];
   __shared__ int s_bin;
   __shared__ uint32_t s_krem, s_cnt;
