@@ -1226,7 +1226,8 @@ static_assert(kFusedMaxKeys % 64 == 0, "whole 64-key chunks");
 // threshold histogram, then the shared-set bitmap and two tie bitmaps
 constexpr int kTailScratchWords = 3 * kBmWords > kHistBins ? 3 * kBmWords : kHistBins;
 
-// x with the value of lane L replaced by the wave-uniform v.
+// x with the value of lane L replaced by the wave-uniform v (v_writelane
+// writes that lane whatever the execution mask).
 template <int L>
 __device__ __forceinline__ uint32_t put_lane(uint32_t x, uint32_t v) {
   asm("v_writelane_b32 %0, %1, %2" : "+v"(x) : "s"(v), "i"(L));
@@ -1251,8 +1252,8 @@ __device__ __forceinline__ uint64_t chunk_lanes(int c, int M) {
 // taken and keys in [E, G] are ties, of which `take` are taken in position
 // order (all when unbounded).  A selection's candidates are the keys at or
 // above C: C = E, except without ties taken (take = 0), where C = G + 1 (no
-// key at all when G is the largest key: cnone).  split: a bounded, nonzero
-// take, where the keys above G are kept apart.
+// key at all when G is the largest key: cnone).  Where a bounded, nonzero
+// number of ties is taken, the keys above G are kept apart as well.
 struct SelBounds {
   uint32_t Gm, Cm, Gk, Ck;
   bool cnone_m, cnone_k;
@@ -1295,6 +1296,15 @@ __device__ __forceinline__ void chunk_masks4(const uint32_t* s_keys, int blk, in
   chunk_masks<J0 + 3, SPLIT>(kv[3], c + 3, M, sb, w);
 }
 
+// Candidate masks cm (top m) and ck (top k_b) of one chunk into lane J of w.
+template <int J>
+__device__ __forceinline__ void put_masks(uint32_t (&w)[4], uint64_t cm, uint64_t ck) {
+  w[0] = put_lane<J>(w[0], (uint32_t)cm);
+  w[1] = put_lane<J>(w[1], (uint32_t)(cm >> 32));
+  w[2] = put_lane<J>(w[2], (uint32_t)ck);
+  w[3] = put_lane<J>(w[3], (uint32_t)(ck >> 32));
+}
+
 // Four whole chunks from J0 of a block of 16 inside the middle range (keys
 // of this lane at kp[64 j]): candidates are the keys above Tm and Tk.
 template <int J0>
@@ -1303,30 +1313,10 @@ __device__ __forceinline__ void chunk_masks4_inner(const uint32_t* kp, uint32_t 
   uint32_t kv[4];
 #pragma unroll
   for (int u = 0; u < 4; ++u) kv[u] = kp[(J0 + u) << 6];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const uint64_t cm = __builtin_amdgcn_ballot_w64(kv[u] > Tm);
-    const uint64_t ck = __builtin_amdgcn_ballot_w64(kv[u] > Tk);
-    // lane J0 + u (the unrolled index is a constant)
-    switch (u) {
-      case 0:
-        w[0] = put_lane<J0 + 0>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 0>(w[1], (uint32_t)(cm >> 32));
-        w[2] = put_lane<J0 + 0>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 0>(w[3], (uint32_t)(ck >> 32));
-        break;
-      case 1:
-        w[0] = put_lane<J0 + 1>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 1>(w[1], (uint32_t)(cm >> 32));
-        w[2] = put_lane<J0 + 1>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 1>(w[3], (uint32_t)(ck >> 32));
-        break;
-      case 2:
-        w[0] = put_lane<J0 + 2>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 2>(w[1], (uint32_t)(cm >> 32));
-        w[2] = put_lane<J0 + 2>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 2>(w[3], (uint32_t)(ck >> 32));
-        break;
-      default:
-        w[0] = put_lane<J0 + 3>(w[0], (uint32_t)cm); w[1] = put_lane<J0 + 3>(w[1], (uint32_t)(cm >> 32));
-        w[2] = put_lane<J0 + 3>(w[2], (uint32_t)ck); w[3] = put_lane<J0 + 3>(w[3], (uint32_t)(ck >> 32));
-        break;
-    }
-  }
+  put_masks<J0 + 0>(w, __builtin_amdgcn_ballot_w64(kv[0] > Tm), __builtin_amdgcn_ballot_w64(kv[0] > Tk));
+  put_masks<J0 + 1>(w, __builtin_amdgcn_ballot_w64(kv[1] > Tm), __builtin_amdgcn_ballot_w64(kv[1] > Tk));
+  put_masks<J0 + 2>(w, __builtin_amdgcn_ballot_w64(kv[2] > Tm), __builtin_amdgcn_ballot_w64(kv[2] > Tk));
+  put_masks<J0 + 3>(w, __builtin_amdgcn_ballot_w64(kv[3] > Tm), __builtin_amdgcn_ballot_w64(kv[3] > Tk));
 }
 
 // The candidate and strict bitmaps of the middle range (words 2c, 2c + 1
