@@ -377,6 +377,10 @@ SELECT_CASES = [
     # more than 256 sequences: no length ranking, one row per workgroup in order
     ("fused-many-seqs", "bf16", 128, False, 4, 1, tuple(100 + (i * 131) % 1200 for i in range(260)),
      dict(k=40, sink=4, window=16)),
+    # short rows, two workgroups side by side per CU, more than two rounds of
+    # rows over the CUs (serpentine length order)
+    ("fused-three-rounds", "bf16", 128, False, 8, 4, tuple(50 + (i * 97) % 700 for i in range(150)),
+     dict(k=30, sink=4, window=16)),
     # the largest query group (16 heads per kv head) on each path
     ("g16-keyed", "bf16", 128, True, 32, 2, (6000, 2500), dict(k=200, sink=4, window=64)),
     ("g16-fused", "bf16", 128, False, 16, 1, tuple(900 + 37 * i for i in range(136)),
