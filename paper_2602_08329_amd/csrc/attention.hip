@@ -684,10 +684,14 @@ __global__ __launch_bounds__(256) void attn_split_f32(AttnArgs a) {
 }
 
 // Combines the split partials of one query head (grid: batch * num_q_heads,
-// 256 threads).  Every thread first loads all it needs (its splits' m, l and
-// numerators, for 256 / d split groups), so the kernel costs one memory
-// latency; the max, the weights and the sums follow in registers and LDS.
-// Units that fit one split were written by the split kernel and are skipped.
+// 256 threads).  Every thread first loads all it may need (the m, l and
+// numerators of its first kMergePerThread split slots, for 256 / d split
+// groups) together with the unit's lengths, before the number of splits in
+// use is known, so the kernel costs one memory latency; slots past that
+// number (stale values of earlier calls) are masked, never used in
+// arithmetic.  The max, the weights and the sums follow in registers and
+// LDS.  Units that fit one split were written by the split kernel and are
+// skipped.
 constexpr int kMergePerThread = 16;
 
 template <int D, bool DENSE>
@@ -699,14 +703,25 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   const int bh = blockIdx.x;
   const int hkv = a.kv.hkv, hq = a.kv.hq, G = hq / hkv;
   const int b = bh / hq, h = bh % hq, u = b * hkv + h / G;
-  if (!DENSE && unit_excluded(a, u)) return;
-  const int L = unit_span<DENSE>(a, u, b, kv_seq_len(a.kv, b)).L;
-  const int nsp = (L + a.chunk - 1) / a.chunk;
-  if (nsp <= 1) return;
   const float* ml = a.part_ml + (size_t)bh * a.nsplit * 2;
   const float* po = a.part_o + (size_t)bh * a.nsplit * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sg = tid / D, dim = tid - sg * D;
+  // the first batch of slots, loaded unconditionally (every slot index is
+  // below nsplit, inside the workspace)
+  float m0[kMergePerThread], l0[kMergePerThread], o0[kMergePerThread];
+#pragma unroll
+  for (int k = 0; k < kMergePerThread; ++k) {
+    const int s = sg + k * SG;
+    const int sl = s < a.nsplit ? s : 0;
+    m0[k] = ml[2 * sl];
+    l0[k] = ml[2 * sl + 1];
+    o0[k] = po[(size_t)sl * D + dim];
+  }
+  if (!DENSE && unit_excluded(a, u)) return;
+  const int L = unit_span<DENSE>(a, u, b, kv_seq_len(a.kv, b)).L;
+  const int nsp = (L + a.chunk - 1) / a.chunk;
+  if (nsp <= 1) return;
   float mx = -INFINITY, num = 0.f, den = 0.f;
   for (int s0 = sg; s0 < nsp; s0 += SG * kMergePerThread) {
     float m[kMergePerThread], l[kMergePerThread], o[kMergePerThread];
@@ -714,9 +729,15 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
     for (int k = 0; k < kMergePerThread; ++k) {
       const int s = s0 + k * SG;
       const bool ok = s < nsp;
-      m[k] = ok ? ml[2 * s] : -INFINITY;
-      l[k] = ok ? ml[2 * s + 1] : 0.f;
-      o[k] = ok ? po[(size_t)s * D + dim] : 0.f;
+      if (s0 == sg) {
+        m[k] = ok ? m0[k] : -INFINITY;
+        l[k] = ok ? l0[k] : 0.f;
+        o[k] = ok ? o0[k] : 0.f;
+      } else {
+        m[k] = ok ? ml[2 * s] : -INFINITY;
+        l[k] = ok ? ml[2 * s + 1] : 0.f;
+        o[k] = ok ? po[(size_t)s * D + dim] : 0.f;
+      }
     }
     // rescale the running sums to the new maximum of this thread
     float bm = mx;

@@ -457,6 +457,29 @@ def test_select_shared_wide_dilation(name, dtype, d, paged, hq, hkv, lens, pk, r
     check_select_shared(inp, lens, B.params(refresh_every=4, **pk, dilate_r=r, dilate_m=25))
 
 
+def test_select_shared_clustered_top_m_long_middle():
+    """Top-m winners packed in bands (stride 5) at 1/4, 1/3, 1/2, 2/3 and 3/4
+    of middle ranges beyond LDS (the radix path): neighbours of winners on
+    either side of any split of the range into equal parts must all land in
+    the shared set."""
+    lens = (30000, 40000)
+    hq, hkv = 4, 2
+    G = hq // hkv
+    inp = synth.random_inputs(2, hq, hkv, 128, lens, seed=21, grid=True, device=DEV)
+    K = inp.K[0]
+    for b, n in enumerate(lens):
+        lo, hi = 4, n - 64
+        for f in (1 / 4, 1 / 3, 1 / 2, 2 / 3, 3 / 4):
+            c = lo + int((hi - lo) * f)
+            pos = torch.arange(c - 80, c + 80, 5, device=DEV)
+            for g in range(hkv):
+                # 4 q of the group's first head: far above every random score
+                K[b, g, pos] = (4 * inp.q[0, 0, b, g * G]).to(K.dtype)
+    for r in (1, 5, 31):
+        check_select_shared(inp, lens, B.params(refresh_every=4, k=600, sink=4, window=64,
+                                                dilate_r=r))
+
+
 def test_select_shared_window_zero_edges():
     # no window: a top-m winner at the last middle position has its right
     # neighbour at n0, outside [0, n0); a winner at the first has its left
