@@ -54,8 +54,9 @@ constexpr int kFinishBlock = 1024;
 constexpr int kFinishPerThread = 8;  // candidates per thread per pass
 constexpr int kFinishTies = 4096;    // level-1 ties the finish kernel keeps in LDS
 // positions per bitmap segment of the finish kernel (3 bitmaps of 8 KB): whole
-// words, and below 2^16 so that per-segment counts fit 16-bit fields
-constexpr int kFinishSegBits = 65504;
+// groups of four words, and below 2^16 so that per-segment counts fit 16-bit
+// fields
+constexpr int kFinishSegBits = 65408;
 // output staging of the finish kernel: a bitmap segment's outputs up to this
 // many entries (or what LDS has room for) are gathered in LDS and copied out
 // with whole-wave stores
@@ -701,7 +702,7 @@ __device__ uint64_t lds_kth_largest(Get get, uint32_t n, uint32_t k, const KthSc
 // m, the other winners, the anchor set and the shared set, each ascending by
 // position.
 __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
-  extern __shared__ uint64_t dyn[];  // sort buffer: a.sortcap entries
+  extern __shared__ __attribute__((aligned(16))) uint64_t dyn[];  // sort buffer: a.sortcap entries
   __shared__ uint32_t h[kHistBins];
   __shared__ uint32_t scan[kFinishBlock / 64 + 1];
   __shared__ uint64_t scan64[kFinishBlock / 64 + 1];
@@ -828,13 +829,16 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   // top m come from shifts of its bitmap (r < 32), so there is no third
   // bitmap.
   const bool shiftd = a.seg_shift != 0;
-  uint32_t* bw = (uint32_t*)(dyn + a.sortcap);
+  // The bitmaps start 16-byte aligned after the sort buffer, segw is a
+  // multiple of 4 (whole groups of four words), and 16 bytes of slack follow
+  // the last bitmap, so that every word read below (a group of four, a word
+  // before or after one) stays inside the buffer.
+  uint32_t* bw = (uint32_t*)(dyn + ((a.sortcap + 1) & ~1));
   uint32_t* bt = bw + segw;
   uint32_t* bd = shiftd ? nullptr : bt + segw;
-  uint32_t* bend = bt + (shiftd ? 1 : 2) * segw;
-  // optional per-word output offsets [segw] (8-byte aligned: bw is), then
-  // the output staging
-  uint64_t* woff = a.woff ? (uint64_t*)(bend + ((bend - bw) & 1)) : nullptr;
+  uint32_t* bend = bt + (shiftd ? 1 : 2) * segw + 4;
+  // optional per-word output offsets [segw], then the output staging
+  uint64_t* woff = a.woff ? (uint64_t*)bend : nullptr;
   int32_t* stage = a.woff ? (int32_t*)(woff + segw) : (int32_t*)bend;  // a.stagecap entries
   int32_t* topk = a.topk_idx + (size_t)row * a.k_cap;
   int32_t* out = a.set_idx + (size_t)row * a.set_cap;
@@ -849,21 +853,28 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   for (int seg_lo = rg.sink_end; seg_lo < rg.win_start; seg_lo += seg_bits) {
     const int seg_hi = min(rg.win_start, seg_lo + seg_bits);
     const int nwords = (seg_hi - seg_lo + 31) >> 5;
+    const int ngrp = (nwords + 3) >> 2;  // groups of four words (the last one padded with zeros)
     const uint32_t lastw = ((seg_hi - seg_lo) & 31) ? (1u << ((seg_hi - seg_lo) & 31)) - 1u : ~0u;
-    for (int w = tid; w < nwords; w += kFinishBlock) {
+    for (int w = tid; w < 4 * ngrp; w += kFinishBlock) {
       bw[w] = 0u;
       bt[w] = 0u;
       if (!shiftd) bd[w] = 0u;
     }
     lds_barrier();
-    // the dilation-only neighbours D of word w: marked, or shifted from the
-    // top-m words around it
-    auto dil = [&](int w) -> uint32_t {
-      if (!shiftd) return bd[w];
-      const uint32_t c0 = bt[w], cp = w > 0 ? bt[w - 1] : 0u, cn = w + 1 < nwords ? bt[w + 1] : 0u;
+    // the dilation-only neighbours of word w given the top-m words c0 (its
+    // own), cp and cn (before and after it, zero outside the segment)
+    auto spread = [&](int w, uint32_t c0, uint32_t cp, uint32_t cn) -> uint32_t {
       uint32_t acc = 0u;
       for (int d = 1; d <= r; ++d) acc |= (c0 << d) | (cp >> (32 - d)) | (c0 >> d) | (cn << (32 - d));
       return w == nwords - 1 ? acc & lastw : acc;
+    };
+    // the same for any word w < nwords: marked, or shifted from the top-m
+    // words around it (all three read unconditionally: bt[-1] and bt[nwords]
+    // lie inside the buffer)
+    auto dil = [&](int w) -> uint32_t {
+      if (!shiftd) return bd[w];
+      const uint32_t c0 = bt[w], cp = bt[w - 1], cn = bt[w + 1];
+      return spread(w, c0, w > 0 ? cp : 0u, w + 1 < nwords ? cn : 0u);
     };
     for (uint32_t i = tid; i < total; i += kFinishBlock) {
       const uint64_t x = dyn[i];
@@ -890,20 +901,48 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
     };
     const int wpt = (nwords + kFinishBlock - 1) / kFinishBlock;
     const int lane = tid & 63, wv = tid >> 6;
-    const int wbase = wv * 64 * wpt;  // with woff: wave wv's words, lane l at wbase + 64 j + l
     // without woff: thread t owns words [t*wpt, (t+1)*wpt)
     const int w_begin = min(nwords, tid * wpt), w_end = min(nwords, w_begin + wpt);
     uint64_t tot = 0, off = 0;
     if (woff) {
-      // every word's output offsets, in word order: a wave scan per row of
-      // 64 consecutive words (conflict-free LDS reads), then one scan of the
-      // waves' totals
+      // Every word's output offsets, in word order.  Each lane takes groups
+      // of four consecutive words (16-byte reads of each bitmap and the two
+      // words around the group, all issued together), its group's total
+      // goes through a wave scan per row of 64 groups, then one scan of the
+      // waves' totals.
+      const int gpt = (ngrp + kFinishBlock - 1) / kFinishBlock;
+      const int gbase = wv * 64 * gpt;  // wave wv's groups, lane l at gbase + 64 j + l
       uint64_t carry = 0;
-      for (int j = 0; j < wpt; ++j) {
-        const int w = wbase + 64 * j + lane;
-        const uint64_t c = w < nwords ? word_counts(w) : 0u;
-        const uint64_t inc = wave_inclusive_scan(c);
-        if (w < nwords) woff[w] = carry + inc - c;
+      for (int j = 0; j < gpt; ++j) {
+        const int gi = gbase + 64 * j + lane;
+        const int w0 = 4 * gi;
+        uint64_t c[4] = {0u, 0u, 0u, 0u};
+        if (gi < ngrp) {
+          const uint4 W4 = *(const uint4*)(bw + w0), T4 = *(const uint4*)(bt + w0);
+          const uint4 D4 = shiftd ? make_uint4(0u, 0u, 0u, 0u) : *(const uint4*)(bd + w0);
+          const uint32_t tp = bt[w0 - 1], tn = bt[w0 + 4];
+          const uint32_t Wv[4] = {W4.x, W4.y, W4.z, W4.w}, Tv[4] = {T4.x, T4.y, T4.z, T4.w};
+          const uint32_t Dv[4] = {D4.x, D4.y, D4.z, D4.w};
+          // neighbours of the group's words (pad words past nwords are zero)
+          const uint32_t Pv[4] = {w0 > 0 ? tp : 0u, Tv[0], Tv[1], Tv[2]};
+          const uint32_t Nv[4] = {Tv[1], Tv[2], Tv[3], w0 + 4 < nwords ? tn : 0u};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t W = Wv[i], T = Tv[i];
+            const uint32_t S = W | (shared ? (shiftd ? spread(w0 + i, T, Pv[i], Nv[i]) : Dv[i]) : 0u);
+            c[i] = w0 + i < nwords ? (uint64_t)__popc(T) | ((uint64_t)__popc(W & ~T) << 16) |
+                                         ((uint64_t)__popc(W) << 32) | ((uint64_t)__popc(S) << 48)
+                                   : 0u;
+          }
+        }
+        const uint64_t gsum = c[0] + c[1] + c[2] + c[3];
+        const uint64_t inc = wave_inclusive_scan(gsum);
+        if (gi < ngrp) {
+          const uint64_t o0 = carry + inc - gsum, o1 = o0 + c[0], o2 = o1 + c[1], o3 = o2 + c[2];
+          ulonglong2* wo = (ulonglong2*)(woff + w0);
+          wo[0] = make_ulonglong2(o0, o1);
+          wo[1] = make_ulonglong2(o2, o3);
+        }
         carry += (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)inc, 63) |
                  ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(inc >> 32), 63) << 32);
       }
@@ -915,9 +954,16 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
         before += v < wv ? x : 0u;
         tot += x;
       }
-      for (int j = 0; j < wpt; ++j) {
-        const int w = wbase + 64 * j + lane;
-        if (w < nwords) woff[w] += before;
+      if (before != 0u) {
+        for (int j = 0; j < gpt; ++j) {
+          const int gi = gbase + 64 * j + lane;
+          if (gi >= ngrp) continue;
+          ulonglong2* wo = (ulonglong2*)(woff + 4 * gi);
+          ulonglong2 x0 = wo[0], x1 = wo[1];
+          x0.x += before; x0.y += before; x1.x += before; x1.y += before;
+          wo[0] = x0;
+          wo[1] = x1;
+        }
       }
     } else {
       uint64_t cnt = 0;
@@ -983,9 +1029,7 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
         }
       }
       if (shared && !shiftd) {
-        for (int j = 0; j < wpt; ++j) {
-          const int w = wbase + 64 * j + lane;
-          if (w >= nwords) continue;
+        for (int w = tid; w < nwords; w += kFinishBlock) {
           const uint32_t W = bw[w], S = W | dil(w);
           uint32_t bits = S & ~W;
           const int js0 = (int)(woff[w] >> 48);
@@ -1916,19 +1960,24 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
     int sortcap, woff, stagecap;
     size_t dyn;
   };
+  // (seg_bits a multiple of 128: bitmaps of whole 16-byte groups of words)
   auto plan = [&](long long seg_bits, long long nbm, FinishPlan* fp) {
-    const long long bm_bytes = nbm * seg_bits / 8;
-    const long long avail = (long long)kLdsBytes - finish_static - bm_bytes;
+    // the bitmaps start 16-byte aligned after the sort buffer (one entry of
+    // padding when sortcap is odd) and end with 16 bytes of slack; 16 bytes
+    // more cover the dynamic buffer's alignment after the static LDS
+    const long long bm_bytes = nbm * seg_bits / 8 + 16;
+    const long long avail = (long long)kLdsBytes - finish_static - 16 - bm_bytes - 8;
     long long cap = (long long)a.selcap + kFinishTies;
     if (cap > avail / 8) cap = avail / 8;
     if (cap < a.selcap) return false;
     long long rest = avail - cap * 8;
-    const long long woff_bytes = seg_bits / 32 * 8 + 4;  // with 4 bytes of alignment
+    const long long woff_bytes = seg_bits / 32 * 8;
     fp->sortcap = (int)cap;
     fp->woff = rest >= woff_bytes ? 1 : 0;
     if (fp->woff) rest -= woff_bytes;
     fp->stagecap = (int)(rest / 4 < kFinishStage ? rest / 4 : kFinishStage);
-    fp->dyn = (size_t)(cap * 8 + bm_bytes + (fp->woff ? woff_bytes : 0) + (long long)fp->stagecap * 4);
+    fp->dyn = (size_t)(((cap + 1) & ~1LL) * 8 + bm_bytes + (fp->woff ? woff_bytes : 0) +
+                       (long long)fp->stagecap * 4);
     return true;
   };
   // the whole middle range as one segment when its outputs keep the packed
@@ -1937,7 +1986,7 @@ hipError_t launch_select(const SelectLaunch& s, hipStream_t stream) {
   // shifts of the top-m bitmap, two bitmaps instead of three) and the full
   // tie buffer and the per-word offsets still fit LDS
   FinishPlan fp{};
-  const long long one_bits = ((long long)a.mcap + 31) / 32 * 32;
+  const long long one_bits = ((long long)a.mcap + 127) / 128 * 128;
   bool one = s.dilate_r < 32 && (long long)a.selcap * (2LL * s.dilate_r + 1) < 65536 &&
              plan(one_bits, 2, &fp) && fp.sortcap == a.selcap + kFinishTies && fp.woff;
   if (one) {
