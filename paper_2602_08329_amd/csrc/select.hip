@@ -63,6 +63,8 @@ constexpr int kFinishSegBits = 65408;
 constexpr int kFinishStage = 8192;
 // candidates few enough for one wave to rank them directly
 constexpr int kSmallRank = 64;
+// winners per thread of the finish kernel loaded with its histograms
+constexpr int kSelPrefetch = 2;
 
 struct SelArgs {
   KvView kv;
@@ -427,25 +429,33 @@ __global__ __launch_bounds__(kFilterBlock) void select_filter(SelArgs a) {
   __shared__ uint32_t s_krem, s_cnt;
   __shared__ uint32_t s_base[2];
   const int row = blockIdx.y;
-  if (row_skipped(a, row)) return;
-  const int b = row / a.kv.hkv;
-  const RowGeom rg = row_geom(a, b);
   const int base = blockIdx.x * kFilterChunk;
-  if (base >= rg.m || rg.kb <= 0) return;
-  const int end = min(rg.m, base + kFilterChunk);
-  const bool all = rg.kb >= rg.m;
   const int tid = threadIdx.x;
+  // The key chunk and the level-0 histogram load before the row's length
+  // (and the gate's choice) are known, so that all of them share one memory
+  // latency: every key index below mcap lies inside the row's key array.
   const uint32_t* keys = a.keys + (size_t)row * a.mcap;
   uint32_t key[kFilterPerThread];
 #pragma unroll
   for (int k = 0; k < kFilterPerThread; ++k) {
     const int i = base + tid + k * kFilterBlock;
-    key[k] = i < end ? keys[i] : 0u;
+    key[k] = i < a.mcap ? keys[i] : 0u;
   }
+  constexpr int HPT = kHistBins / kFilterBlock;
+  uint32_t hv[HPT];
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) hv[j] = a.hist0[(size_t)row * kHistBins + tid + j * kFilterBlock];
+  if (row_skipped(a, row)) return;
+  const int b = row / a.kv.hkv;
+  const RowGeom rg = row_geom(a, b);
+  if (base >= rg.m || rg.kb <= 0) return;
+  const int end = min(rg.m, base + kFilterChunk);
+  const bool all = rg.kb >= rg.m;
   int bin = 0;
   bool resolved = true;
   if (!all) {
-    for (int i = tid; i < kHistBins; i += kFilterBlock) h[i] = a.hist0[(size_t)row * kHistBins + i];
+#pragma unroll
+    for (int j = 0; j < HPT; ++j) h[tid + j * kFilterBlock] = hv[j];
     __syncthreads();
     find_threshold<kFilterBlock>(h, (uint32_t)rg.kb, scan, &s_bin, &s_krem, &s_cnt);
     bin = s_bin;
@@ -529,11 +539,17 @@ __device__ __forceinline__ void block_publish() {
 // digit above bl (or equal, when the bin is taken whole) goes to the output
 // list sel; digit equal to bl is kept, either as a 64-bit composite in the LDS
 // buffer `keep_lds` or in the global list `keep_glb`.  Returns the number
-// kept.  Every thread of the workgroup must call it.
-__device__ uint32_t split_candidates(const SelArgs& a, uint32_t* nsel, uint2* sel, const uint2* src,
-                                     uint32_t count, int level, uint32_t bl, bool resolved,
-                                     uint64_t* keep_lds, uint2* keep_glb, uint32_t* scan,
-                                     uint32_t* s_base) {
+// kept.  Every thread of the workgroup must call it.  The first pass of
+// candidates may come loaded already (`first`; values past count unused).
+struct CandPass {  // one pass of candidates: src[tid + k * kFinishBlock]
+  uint2 x[kFinishPerThread];
+};
+__device__ __forceinline__ uint32_t split_candidates(const SelArgs& a, uint32_t* nsel, uint2* sel,
+                                                     const uint2* src, uint32_t count, int level,
+                                                     uint32_t bl, bool resolved, uint64_t* keep_lds,
+                                                     uint2* keep_glb, uint32_t* scan,
+                                                     uint32_t* s_base,
+                                                     const CandPass* first = nullptr) {
   const int tid = threadIdx.x;
   uint32_t kept = 0;
   for (uint32_t e0 = 0; e0 < count; e0 += kFinishBlock * kFinishPerThread) {
@@ -542,7 +558,7 @@ __device__ uint32_t split_candidates(const SelArgs& a, uint32_t* nsel, uint2* se
 #pragma unroll
     for (int k = 0; k < kFinishPerThread; ++k) {
       const uint32_t e = e0 + tid + k * kFinishBlock;
-      x[k] = e < count ? src[e] : make_uint2(0u, 0u);
+      x[k] = first && e0 == 0 ? first->x[k] : (e < count ? src[e] : make_uint2(0u, 0u));
     }
 #pragma unroll
     for (int k = 0; k < kFinishPerThread; ++k) {
@@ -714,13 +730,39 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   __shared__ uint32_t s_n;
   const KthScratch ks{h, scan, &s_bin, &s_krem, &s_cnt, &s_n, s_small, &s_out};
   const int row = blockIdx.x;
-  if (row_skipped(a, row)) return;
-  const int b = row / a.kv.hkv;
-  const RowGeom rg = row_geom(a, b);
   const int tid = threadIdx.x;
   uint32_t* cnt = a.counters + row * 4;
   uint2* sel = a.sel + (size_t)row * a.selcap;
+  const uint2* cand = a.cand + (size_t)row * a.mcap;
+  // The counters, both histograms, the first pass of level-0 candidates and
+  // the first kSelPrefetch winners per thread load before the row's length
+  // (and the gate's choice) are known, so that they share one memory
+  // latency.  Every index stays inside the row's lists (mcap candidates,
+  // selcap winners); values past the counts are loaded and never used.
   const uint32_t nsel0 = coherent_load(&cnt[0]);  // the filter's winners
+  const uint32_t count0_all = coherent_load(&cnt[1]);
+  constexpr int HPT = kHistBins / kFinishBlock;
+  uint32_t h0[HPT], h1[HPT];
+#pragma unroll
+  for (int j = 0; j < HPT; ++j) {
+    h0[j] = a.hist0[(size_t)row * kHistBins + tid + j * kFinishBlock];
+    h1[j] = a.hist1[(size_t)row * kHistBins + tid + j * kFinishBlock];
+  }
+  CandPass cp0;
+#pragma unroll
+  for (int k = 0; k < kFinishPerThread; ++k) {
+    const int e = tid + k * kFinishBlock;
+    cp0.x[k] = e < a.mcap ? cand[e] : make_uint2(0u, 0u);
+  }
+  uint2 sp0[kSelPrefetch];
+#pragma unroll
+  for (int k = 0; k < kSelPrefetch; ++k) {
+    const int j = tid + k * kFinishBlock;
+    sp0[k] = j < a.selcap ? sel[j] : make_uint2(0u, 0u);
+  }
+  if (row_skipped(a, row)) return;
+  const int b = row / a.kv.hkv;
+  const RowGeom rg = row_geom(a, b);
   uint32_t n_lds = 0;  // staged ties in dyn[0, n_lds)
   // m from the budget before clamping to the middle range (floor(k / 3) by
   // default), clamped to the winners
@@ -736,15 +778,6 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
   bool m_resolved0 = false;
 
   if (rg.kb > 0 && rg.kb < rg.m) {
-    // both histograms and the candidate count in one memory latency
-    constexpr int HPT = kHistBins / kFinishBlock;
-    uint32_t h0[HPT], h1[HPT];
-#pragma unroll
-    for (int j = 0; j < HPT; ++j) {
-      h0[j] = a.hist0[(size_t)row * kHistBins + tid + j * kFinishBlock];
-      h1[j] = a.hist1[(size_t)row * kHistBins + tid + j * kFinishBlock];
-    }
-    const uint32_t count0_all = coherent_load(&cnt[1]);
     if (tid == 0) s_nsel = nsel0;
 #pragma unroll
     for (int j = 0; j < HPT; ++j) h[tid + j * kFinishBlock] = h0[j];
@@ -772,9 +805,8 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
       const bool in_lds = !resolved1 && c1 + (uint32_t)rg.kb <= (uint32_t)a.sortcap;
       const uint32_t count0 = min(count0_all, (uint32_t)a.mcap);
       uint2* cand2 = a.cand2 + (size_t)row * a.mcap;
-      const uint32_t kept = split_candidates(a, &s_nsel, sel, a.cand + (size_t)row * a.mcap, count0, 1,
-                                             b1, resolved1, in_lds ? dyn : nullptr, cand2, scan,
-                                             &s_base);
+      const uint32_t kept = split_candidates(a, &s_nsel, sel, cand, count0, 1, b1, resolved1,
+                                             in_lds ? dyn : nullptr, cand2, scan, &s_base, &cp0);
       block_publish();
       if (in_lds) {
         n_lds = kept;
@@ -792,7 +824,15 @@ __global__ __launch_bounds__(kFinishBlock) void select_finish(SelArgs a) {
 
   const uint32_t n_sel = rg.kb > 0 ? min(s_nsel, (uint32_t)a.selcap) : 0u;
   const uint32_t total = n_sel + n_lds;
-  for (uint32_t i = n_lds + tid; i < total; i += kFinishBlock) dyn[i] = composite(sel[i - n_lds]);
+  // winner j is sel[j]: the filter's ones (j < nsel0) prefetched for the
+  // first kSelPrefetch passes, the ones appended here read back
+#pragma unroll
+  for (int k = 0; k < kSelPrefetch; ++k) {
+    const uint32_t j = tid + k * kFinishBlock;
+    if (j < n_sel) dyn[n_lds + j] = composite(j < nsel0 ? sp0[k] : sel[j]);
+  }
+  for (uint32_t j = tid + kSelPrefetch * kFinishBlock; j < n_sel; j += kFinishBlock)
+    dyn[n_lds + j] = composite(sel[j]);
   __syncthreads();
   // winners: the kout largest composites; top: the m largest of them
   const uint32_t kout = min(total, kb_u);
