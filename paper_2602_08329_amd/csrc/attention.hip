@@ -707,16 +707,16 @@ __global__ __launch_bounds__(256) void attn_merge(AttnArgs a) {
   const float* po = a.part_o + (size_t)bh * a.nsplit * D;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sg = tid / D, dim = tid - sg * D;
-  // the first batch of slots, loaded unconditionally (every slot index is
-  // below nsplit, inside the workspace)
+  // the first batch of slots below nsplit (a launch argument: no load
+  // waits for another)
   float m0[kMergePerThread], l0[kMergePerThread], o0[kMergePerThread];
 #pragma unroll
   for (int k = 0; k < kMergePerThread; ++k) {
     const int s = sg + k * SG;
-    const int sl = s < a.nsplit ? s : 0;
-    m0[k] = ml[2 * sl];
-    l0[k] = ml[2 * sl + 1];
-    o0[k] = po[(size_t)sl * D + dim];
+    const bool in = s < a.nsplit;
+    m0[k] = in ? ml[2 * s] : -INFINITY;
+    l0[k] = in ? ml[2 * s + 1] : 0.f;
+    o0[k] = in ? po[(size_t)s * D + dim] : 0.f;
   }
   if (!DENSE && unit_excluded(a, u)) return;
   const int L = unit_span<DENSE>(a, u, b, kv_seq_len(a.kv, b)).L;
