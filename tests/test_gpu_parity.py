@@ -346,6 +346,10 @@ SELECT_CASES = [
     ("radix-f32-paged", "f32", 128, True, 8, 2, (26000,), dict(k=50, sink=2, window=8)),
     ("radix-ratio", "bf16", 128, True, 8, 2, (40000, 25000), dict(k_num=1, k_den=20, sink=4, window=128)),
     ("radix-g16", "bf16", 128, True, 32, 2, (30000,), dict(k=200, sink=4, window=64)),
+    # odd budget (an odd sort buffer: the finish kernel's bitmaps start one
+    # entry further to stay 16-byte aligned) and a cache capacity that is not
+    # a whole number of 128-position groups
+    ("radix-odd-k", "bf16", 128, False, 8, 2, (30007, 26001), dict(k=301, sink=3, window=61)),
     # 17 sequences x 8 kv heads = 136 rows, more than half the CUs: the
     # single-launch refresh path
     ("fused-ragged", "bf16", 128, False, 32, 8,
@@ -704,11 +708,14 @@ def test_split_merge_workspace_reused_across_calls():
     # one attention workspace for consecutive calls whose units split a
     # different number of ways (including one split and empty units): the
     # merge of every call is complete and the workspace is left reusable.
+    # The workspace starts as NaN bytes, so a merge that let a split slot
+    # no call wrote into its arithmetic would give NaN.
     inp = synth.random_inputs(2, 32, 8, 128, (9000, 3000), seed=53, grid=False, device=DEV)
     rng = np.random.default_rng(53)
     cap = 8200
     kv, _ = kv_for(inp, (9000, 3000))
     ws = B.workspace(B.prhs_workspace_size(B.PRHS_OP_SPARSE_ATTN, kv, None, cap), DEV)
+    ws.fill_(0xFF)
     for call in range(4):
         lens = (9000 - 1000 * call, 3000 - 700 * call)
         sets = {}
