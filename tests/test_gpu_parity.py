@@ -461,6 +461,28 @@ def test_select_shared_wide_dilation(name, dtype, d, paged, hq, hkv, lens, pk, r
     check_select_shared(inp, lens, B.params(refresh_every=4, **pk, dilate_r=r, dilate_m=25))
 
 
+@pytest.mark.parametrize("r", [33, 64])
+def test_select_shared_two_bitmap_segments(r):
+    """A radius of a word or more keeps the radix finish in its segmented
+    form (a marked neighbour bitmap); a middle range of about 70k positions
+    then spans two segments, with top-m winners placed on both sides of the
+    boundary whose neighbours cross it."""
+    lens = (70100, 20000)
+    hq, hkv = 4, 1
+    inp = synth.random_inputs(2, hq, hkv, 128, lens, seed=31 + r, grid=True, device=DEV)
+    K = inp.K[0]
+    for b, n in enumerate(lens):
+        # bands around the segment boundaries a 65,408-position segment
+        # would have (4 + 65408 from the sink), and at the middle
+        for c in (4 + 65408, n // 2):
+            if c + 200 >= n - 64:
+                continue
+            pos = torch.arange(c - 150, c + 150, 7, device=DEV)
+            K[b, 0, pos] = (4 * inp.q[0, 0, b, 0]).to(K.dtype)
+    check_select_shared(inp, lens, B.params(refresh_every=4, k=400, sink=4, window=64,
+                                            dilate_r=r))
+
+
 def test_select_shared_clustered_top_m_long_middle():
     """Top-m winners packed in bands (stride 5) at 1/4, 1/3, 1/2, 2/3 and 3/4
     of middle ranges beyond LDS (the radix path): neighbours of winners on
